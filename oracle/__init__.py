@@ -1,0 +1,18 @@
+"""CPU oracle of the paper's hot path: masking compressor and spectral corrector.
+
+TEST INFRASTRUCTURE ONLY.  Plain, slow, obviously correct definitions written
+from the paper (Sec. 3.1, Sec. 3.2, Alg. 1, App. D, App. F), used to check the
+HIP library.  Only the test suite, the smoke check and the benchmark's
+CPU-baseline leg may import it; the library never does, and the two share no
+code.
+
+Pins (tests run without a GPU) and their status:
+  mask.*       pinned: published SplitMix64 / MurmurHash3 vectors, bijection and
+               permutation brute force, subset-uniformity statistics,
+               unbiasedness and variance of the rescaled mask (App. F), the
+               paper's worked payload arithmetic (App. H), torch's bf16 rounding.
+  spectral.*   pinned: closed forms for G = U S V^T, alpha = 1 identity,
+               projector idempotence and self-adjointness at tau = 0,
+               Lemma 1 (non-expansive) and Lemma 2 (noise contraction, Monte
+               Carlo), EMA closed forms, SVD against eigh brute force.
+"""

@@ -1,0 +1,100 @@
+"""Spectral-correction oracle (paper Sec. 3.2; Alg. 1; App. D), float64 numpy.
+
+TEST INFRASTRUCTURE ONLY.  Plain definitions, one step per function, in the
+order and notation of the paper:
+
+  anchor EMA          M <- beta * M + (1 - beta) * G_anc          (Sec. 3.2 eq.)
+  SVD of the EMA      M = U S V^T, truncated to the top r triplets  (Sec. 3.2; App. D)
+  soft filter         d_i = s_i / (s_i + tau)                      (Sec. 3.2 eq.)
+  two-sided filter    X = U^T G V;  X_f = diag(d) X diag(d);
+                      G_filt = U X_f V^T                           (Sec. 3.2)
+  blend               G_proj = alpha * G + (1 - alpha) * G_filt    (Sec. 3.2 eq.)
+
+Readings of the paper taken here (the paper does not fix them):
+  * the top-r truncation of App. D, applied before the soft filter;
+  * tau acts on the raw singular values of the EMA;
+  * 0 / 0 in the filter (s_i = 0 with tau = 0) is taken as d_i = 0, so an
+    empty prior (M = 0) gives G_proj = alpha * G.
+The SVD is LAPACK's (numpy.linalg.svd), a library primitive.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def ema(M_prev: np.ndarray, G_anc: np.ndarray, beta: float) -> np.ndarray:
+    """Anchor-momentum EMA, one arrival (Sec. 3.2 eq.; Alg. 1)."""
+    return beta * np.asarray(M_prev, dtype=np.float64) + (1.0 - beta) * np.asarray(G_anc, dtype=np.float64)
+
+
+def top_r_svd(M: np.ndarray, r: int):
+    """Top-r singular triplets of M (Sec. 3.2; App. D truncation).
+
+    Returns U [m, r], s [r] (descending), V [n, r]."""
+    M = np.asarray(M, dtype=np.float64)
+    U, s, Vt = np.linalg.svd(M, full_matrices=False)
+    return U[:, :r].copy(), s[:r].copy(), Vt[:r, :].T.copy()
+
+
+def filter_weights(s: np.ndarray, tau: float) -> np.ndarray:
+    """d_i = s_i / (s_i + tau) (Sec. 3.2 eq.), with 0/0 read as 0."""
+    s = np.asarray(s, dtype=np.float64)
+    den = s + tau
+    d = np.zeros_like(s)
+    nz = den != 0
+    d[nz] = s[nz] / den[nz]
+    return d
+
+
+def two_sided_filter(G: np.ndarray, U: np.ndarray, d: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """G_filt = U diag(d) (U^T G V) diag(d) V^T (Sec. 3.2; App. D P_t)."""
+    G = np.asarray(G, dtype=np.float64)
+    X = U.T @ G @ V
+    Xf = d[:, None] * X * d[None, :]
+    return U @ Xf @ V.T
+
+
+def correct(G: np.ndarray, U: np.ndarray, d: np.ndarray, V: np.ndarray, alpha: float) -> np.ndarray:
+    """G_proj = alpha * G + (1 - alpha) * G_filt (Sec. 3.2 eq.; Alg. 1)."""
+    G = np.asarray(G, dtype=np.float64)
+    return alpha * G + (1.0 - alpha) * two_sided_filter(G, U, d, V)
+
+
+def build_prior(M_prev, G_anc, beta: float, r: int, tau: float):
+    """EMA (if an anchor gradient arrived), then top-r SVD and filter weights.
+
+    Returns (M, U, s, V, d)."""
+    M = ema(M_prev, G_anc, beta) if G_anc is not None else np.asarray(M_prev, dtype=np.float64)
+    U, s, V = top_r_svd(M, r)
+    d = filter_weights(s, tau)
+    return M, U, s, V, d
+
+
+def corrected_step(M_prev, G_anc, G_mask, beta: float, r: int, tau: float, alpha: float):
+    """One pass of the corrector for one matrix: build the prior, then correct."""
+    M, U, s, V, d = build_prior(M_prev, G_anc, beta, r, tau)
+    return M, U, s, V, d, correct(G_mask, U, d, V, alpha)
+
+
+def alignment(g: np.ndarray, U: np.ndarray, V: np.ndarray) -> float:
+    """eta_r = ||U^T g V||_F^2 / ||g||_F^2 (App. G)."""
+    g = np.asarray(g, dtype=np.float64)
+    num = np.linalg.norm(U.T @ g @ V) ** 2
+    den = np.linalg.norm(g) ** 2
+    return float(num / den) if den > 0 else 0.0
+
+
+def projector_distance(U1: np.ndarray, U2: np.ndarray) -> float:
+    """||U1 U1^T - U2 U2^T||_F / sqrt(2 r): basis-free subspace distance."""
+    r = U1.shape[1]
+    P1 = U1 @ U1.T
+    P2 = U2 @ U2.T
+    return float(np.linalg.norm(P1 - P2) / np.sqrt(2.0 * r))
+
+
+def rel_fro(a, b) -> float:
+    """||a - b||_F / ||b||_F."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / nb) if nb > 0 else float(np.linalg.norm(a - b))
