@@ -1,0 +1,343 @@
+#!/usr/bin/env python3
+"""Benchmark of one pipeline stage's hot path on one MI355X.
+
+One step = every row of the hot path once, over one batch of synthetic input
+resident in HBM (70B-class slice, four layers):
+  per layer: pack + unpack of the boundary activation (forward) and of the
+  activation gradient (backward, same mask key);
+  per weight matrix (3 per layer): anchor EMA + top-r SVD + filter
+  (sc_build_prior), then the spectral correction of the masked gradient
+  (sc_correct).
+
+Prints one JSON line.  `value` is the algorithmic HBM bytes of the step
+divided by the measured step time (GB/s); `roofline` reports the kernel that
+took the most time, measured live with HIP events on its own stream (library
+event timing); `cpu_baseline` times the CPU oracle on a bounded sample of the
+same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "mask pack/unpack GB/s + spectral-correction TFLOP/s, % of HBM/MFMA peak"
+PEAK_HBM = 8000.0          # GB/s
+PEAK_BF16 = 2500.0         # TFLOP/s dense
+PEAK_F32 = 157.3           # TFLOP/s (fp32 matrix and vector)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="approximate budget of the CPU-oracle sample")
+    return ap.parse_args()
+
+
+def touched_line_fraction(H: int, K: int, elem_bytes: int, line: int = 128) -> float:
+    """Expected share of 128-byte lines of a row that hold >= 1 kept entry:
+    1 - C(H - E, K) / C(H, K) with E elements per line."""
+    E = line // elem_bytes
+    if K > H - E:
+        return 1.0
+    lg = math.lgamma
+    log_ratio = (lg(H - E + 1) - lg(K + 1) - lg(H - E - K + 1)) - (lg(H + 1) - lg(K + 1) - lg(H - K + 1))
+    return 1.0 - math.exp(log_ratio)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path: every GPU box here has one GPU.", file=sys.stderr)
+        return 2
+
+    import torch
+    import workloads
+    import paper_2609_14339_amd as pk
+
+    cfg = workloads.CONFIGS[args.config]
+    act, gs = cfg.act, cfg.grad
+    dev = torch.device("cuda")
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    esz = 2 if act.dtype == torch.bfloat16 else 4
+    gsz = 2 if gs.dtype == torch.bfloat16 else 4
+    L = gs.layers
+    keep = act.keep[0]
+    H, rows = act.H, act.B * act.S
+    K = pk.ac_keep_count(H, keep)
+    scale = H / K
+    r = gs.r[0]
+    p, q = cfg.oversample, cfg.power_iters
+    t0 = time.time()
+
+    # ---------------- inputs, resident in HBM ----------------
+    xs, gxs, keys = [], [], []
+    for l in range(L):
+        xs.append(workloads.activation(act, cfg.cid, l, 0, dev))
+        gxs.append(workloads.activation(act, cfg.cid, l, 1, dev))
+        keys.append(pk.make_key(B=act.B, S=act.S, H=H, **workloads.mask_key_fields(cfg.cid, layer=l)))
+    vals = [[torch.empty(rows, K, dtype=act.dtype, device=dev) for _ in range(2)] for _ in range(L)]
+    idxs = [[torch.empty(rows, K, dtype=torch.int16, device=dev) for _ in range(2)] for _ in range(L)]
+    ys = [[torch.empty(rows, H, dtype=act.dtype, device=dev) for _ in range(2)] for _ in range(L)]
+    mats = []
+    ws_bytes = 0
+    for l in range(L):
+        for j, (m, n) in enumerate(gs.shapes):
+            G_anc, G_mask = workloads.grad_pair_fast(gs, cfg.cid, l, j, dev)
+            mats.append(dict(m=m, n=n, G_anc=G_anc, G_mask=G_mask,
+                             M=torch.zeros(m, n, device=dev),
+                             out=(torch.empty(m, r, device=dev), torch.empty(r, device=dev),
+                                  torch.empty(n, r, device=dev), torch.empty(r, device=dev)),
+                             Gp=torch.empty_like(G_mask)))
+            ws_bytes = max(ws_bytes, pk.sc_workspace_size(m, n, r, p, gs.dtype))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+    print(f"[bench] inputs ready in {setup_s:.1f} s; HBM in use "
+          f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB", file=sys.stderr, flush=True)
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    phase_ms = {"ac": 0.0, "build": 0.0, "correct": 0.0}
+
+    def step(record: bool):
+        e0, e1, e2, e3 = ev(), ev(), ev(), ev()
+        e0.record(stream)
+        for l in range(L):
+            for dirn, src in enumerate((xs[l], gxs[l])):      # forward, then backward
+                pk.ac_mask_pack(src, K, keys[l], vals=vals[l][dirn], idx=idxs[l][dirn])
+                pk.ac_unpack_scatter(vals[l][dirn], H, keys[l], scale, idx=idxs[l][dirn],
+                                     y=ys[l][dirn])
+        e1.record(stream)
+        for i, mt in enumerate(mats):
+            pk.sc_build_prior(mt["G_anc"], mt["M"], r, workloads.BETA, workloads.TAU, p, q,
+                              seed=1000 + i, ws=ws, out=mt["out"])
+        e2.record(stream)
+        for mt in mats:
+            U, s, V, d = mt["out"]
+            pk.sc_correct(mt["G_mask"], U, d, V, workloads.ALPHA, out=mt["Gp"], ws=ws)
+        e3.record(stream)
+        return (e0, e1, e2, e3) if record else None
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    print(f"[bench] {args.warmup} warmup steps done", file=sys.stderr, flush=True)
+
+    pk.acsc_stats_enable(True)
+    torch.cuda.synchronize()
+    start, stop = ev(), ev()
+    marks = []
+    start.record(stream)
+    for _ in range(args.steps):
+        marks.append(step(True))
+    stop.record(stream)
+    torch.cuda.synchronize()
+    stats = pk.acsc_stats_read()
+    pk.acsc_stats_enable(False)
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+    for e0, e1, e2, e3 in marks:
+        phase_ms["ac"] += e0.elapsed_time(e1) / args.steps
+        phase_ms["build"] += e1.elapsed_time(e2) / args.steps
+        phase_ms["correct"] += e2.elapsed_time(e3) / args.steps
+    print(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # ---------------- algorithmic work of one step ----------------
+    f_line = touched_line_fraction(H, K, esz)
+    pack_bytes = f_line * rows * H * esz + rows * K * (esz + 2)
+    unpack_bytes = rows * H * esz + rows * K * (esz + 2)
+    passes = 2 * q + 2
+    kk = min(r + p, min(gs.shapes[0]))
+    work = {"ac_pack": dict(bytes=2 * L * pack_bytes, calls=2 * L),
+            "ac_unpack": dict(bytes=2 * L * unpack_bytes, calls=2 * L),
+            "sc_ema": dict(bytes=0.0, calls=0), "sc_pass": dict(flops=0.0, bytes=0.0, calls=0),
+            "sc_correct": dict(bytes=0.0, flops=0.0, calls=0),
+            "sc_blend": dict(bytes=0.0, flops=0.0, calls=0), "sc_gv": dict(bytes=0.0, flops=0.0, calls=0)}
+    for mt in mats:
+        m, n = mt["m"], mt["n"]
+        k = min(r + p, m, n, pk.SC_KMAX)
+        work["sc_ema"]["bytes"] += m * n * (4 + 4 + gsz)
+        work["sc_ema"]["calls"] += 1
+        work["sc_pass"]["flops"] += passes * 2.0 * m * n * k
+        work["sc_pass"]["bytes"] += passes * 4.0 * m * n
+        work["sc_pass"]["calls"] += passes
+        work["sc_correct"]["bytes"] += 3.0 * m * n * gsz
+        work["sc_correct"]["flops"] += 4.0 * m * n * r + 3.0 * m * n
+        work["sc_correct"]["calls"] += 1
+        work["sc_blend"]["bytes"] += 2.0 * m * n * gsz
+        work["sc_blend"]["flops"] += 2.0 * m * n * r + 3.0 * m * n
+        work["sc_blend"]["calls"] += 1
+        work["sc_gv"]["bytes"] += 1.0 * m * n * gsz
+        work["sc_gv"]["flops"] += 2.0 * m * n * r
+        work["sc_gv"]["calls"] += 1
+    step_bytes = (work["ac_pack"]["bytes"] + work["ac_unpack"]["bytes"] + work["sc_ema"]["bytes"]
+                  + work["sc_pass"]["bytes"] + work["sc_correct"]["bytes"])
+    step_flops = work["sc_pass"]["flops"] + work["sc_correct"]["flops"]
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---------------- per-kernel view (library event timing) ----------------
+    per_step = {name: (n / args.steps, ms / args.steps) for name, (n, ms) in stats.items()}
+    groups = {"sc_pass": ("sc_pass_mz", "sc_pass_mtq")}
+    kern = {}
+    for name, (n, ms) in per_step.items():
+        kern[name] = dict(launches_per_step=n, ms_per_step=ms, avg_us=1e3 * ms / max(n, 1e-9))
+    # roofline models for the kernels whose work has a clean algorithmic count
+    def model(name):
+        if name in ("ac_pack", "ac_unpack", "sc_ema"):
+            return "hbm", work[name]["bytes"], work[name]["calls"]
+        if name == "sc_blend":
+            return "hbm", work["sc_blend"]["bytes"], work["sc_blend"]["calls"]
+        if name == "sc_gv":
+            return "hbm", work["sc_gv"]["bytes"], work["sc_gv"]["calls"]
+        if name in groups["sc_pass"]:
+            return "mfma", work["sc_pass"]["flops"], work["sc_pass"]["calls"]
+        return None
+    pass_ms = sum(per_step.get(t, (0, 0.0))[1] for t in groups["sc_pass"])
+    pass_n = sum(per_step.get(t, (0, 0.0))[0] for t in groups["sc_pass"])
+    candidates = {name: ms for name, (n, ms) in per_step.items() if name not in groups["sc_pass"]}
+    candidates["sc_pass"] = pass_ms
+    dom = max(candidates, key=candidates.get)
+    if dom == "sc_pass":
+        bound, amount, calls = "mfma", work["sc_pass"]["flops"], work["sc_pass"]["calls"]
+        dom_ms, dom_n = pass_ms, pass_n
+    else:
+        mm = model(dom)
+        dom_n, dom_ms = per_step[dom]
+        bound, amount, calls = mm if mm else ("latency", 0.0, dom_n)
+    avg_s = dom_ms * 1e-3 / max(dom_n, 1e-9)
+    per_launch = amount / max(calls, 1e-9)
+    if bound == "hbm":
+        achieved = per_launch / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM, 4)}
+    elif bound == "mfma":
+        achieved = per_launch / avg_s / 1e12
+        peak = PEAK_F32
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4)}
+    else:
+        roof = {"bound": "latency", "achieved": None, "peak": None, "unit": None, "frac": None}
+    roof.update({"kernel": dom, "avg_launch_us": round(avg_s * 1e6, 2),
+                 "launches_per_step": dom_n, "work_per_launch": per_launch, "traffic": None})
+
+    comp = {}
+    for name in ("ac_pack", "ac_unpack", "sc_ema", "sc_gv", "sc_blend"):
+        if name in per_step:
+            n, ms = per_step[name]
+            gbs = work[name]["bytes"] / (ms * 1e-3) / 1e9
+            comp[name] = {"GB/s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM, 4),
+                          "ms_per_step": round(ms, 4), "launches_per_step": n}
+    if pass_ms > 0:
+        tf = work["sc_pass"]["flops"] / (pass_ms * 1e-3) / 1e12
+        comp["sc_pass"] = {"TFLOP/s": round(tf, 2), "frac_fp32_mfma": round(tf / PEAK_F32, 4),
+                           "ms_per_step": round(pass_ms, 4), "launches_per_step": pass_n}
+    comp["phase_ms"] = {k: round(v, 4) for k, v in phase_ms.items()}
+    comp["sc_correct_step"] = {"GB/s": round(work["sc_correct"]["bytes"] / (phase_ms["correct"] * 1e-3) / 1e9, 1),
+                               "TFLOP/s": round(work["sc_correct"]["flops"] / (phase_ms["correct"] * 1e-3) / 1e12, 2)}
+    comp["ac_step"] = {"GB/s": round((work["ac_pack"]["bytes"] + work["ac_unpack"]["bytes"])
+                                     / (phase_ms["ac"] * 1e-3) / 1e9, 1)}
+    comp["kernels"] = {k: {kk_: round(v, 4) if isinstance(v, float) else v for kk_, v in d.items()}
+                       for k, d in sorted(kern.items())}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, args.cpu_seconds)
+
+    shapes = "+".join(f"{m}x{n}" for m, n in gs.shapes)
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: activation [{act.B},{act.S},{H}] keep {keep} (K={K}) "
+                               f"fwd+bwd x{L} layers; gradients {shapes} x{L} layers, rank-{gs.rank} "
+                               f"signal + noise; r={r}, k={kk}, power_iters={q}",
+                   "step_bytes": step_bytes, "step_flops": step_flops,
+                   "step_TFLOP/s": round(step_flops / (ms_per_step * 1e-3) / 1e12, 2)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "components": comp,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def cpu_baseline(cfg, budget_s: float):
+    """The oracle as it stands, on host cores, on a bounded sample of the same
+    workload: pack + unpack of a slice of layer-0 rows (C oracle, one thread),
+    and build_prior + correct of one gradient block (float64 numpy/LAPACK)."""
+    import numpy as np
+    import torch
+    import workloads
+    from oracle import mask as om
+    from oracle import spectral as osp
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    act, gs = cfg.act, cfg.grad
+    H = act.H
+    K = om.keep_count(H, act.keep[0])
+    esz = 2 if act.dtype == torch.bfloat16 else 4
+    gsz = 2 if gs.dtype == torch.bfloat16 else 4
+    # mask sample: rows of layer 0
+    rows = 2048
+    x = workloads.activation(act, cfg.cid, 0, 0, "cpu", rows=rows)
+    xh = x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
+    key = om.mask_key(**{k: v for k, v in workloads.mask_key_fields(cfg.cid).items()},
+                      B=act.B, S=act.S, H=H)
+    t = time.time()
+    vals, idx = om.pack(xh, K, key)
+    om.unpack(vals, H, key, H / K, idx=idx)
+    t_ac = time.time() - t
+    ac_bytes = (touched_line_fraction(H, K, esz) * rows * H * esz + rows * K * (esz + 2)
+                + rows * H * esz + rows * K * (esz + 2))
+    # spectral sample: leading block of the first gradient matrix, sized to the budget
+    m0, n0 = gs.shapes[0]
+    side = 1024
+    while side * 2 <= min(m0, n0) and (side * 2) ** 3 * 4 / 2e10 < budget_s:
+        side *= 2
+    m, n = min(side, m0), min(side, n0)
+    spec = workloads.GradSpec(((m, n),), min(gs.rank, m), gs.s_range, (min(gs.r[0], m),),
+                              gs.dtype, gs.anc_noise, gs.mask_noise)
+    gp = workloads.grad_pair(spec, cfg.cid, 0, 0, "cpu")
+    Ga = gp.G_anc.double().numpy()
+    Gm = gp.G_mask.double().numpy()
+    t = time.time()
+    osp.corrected_step(np.zeros((m, n)), Ga, Gm, workloads.BETA, spec.r[0], workloads.TAU,
+                       workloads.ALPHA)
+    t_sc = time.time() - t
+    sc_bytes = m * n * (4 + 4 + gsz) + 4 * m * n + 3 * m * n * gsz   # EMA + one read of M + correction
+    total = t_ac + t_sc
+    model = platform.processor()
+    try:
+        model = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
+        model = [l.split(":", 1)[1].strip() for l in model.splitlines() if l.startswith("Model name")][0]
+    except Exception:
+        pass
+    return {"value": round((ac_bytes + sc_bytes) / total / 1e9, 3), "unit": "GB/s",
+            "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"C oracle pack+unpack of {rows} rows x H={H} (1 thread, {t_ac:.2f} s); "
+                      f"float64 oracle EMA + LAPACK SVD + correction of a {m}x{n} block of the "
+                      f"{m0}x{n0} gradient ({blas_threads} BLAS threads, {t_sc:.2f} s)",
+            "cpu_model": model, "seconds": round(total, 2)}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

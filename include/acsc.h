@@ -1,0 +1,174 @@
+/*
+ * acsc.h — C ABI of the MI355X (gfx950) masking compressor and spectral
+ * corrector: the hot path of one pipeline stage of the fast compressed
+ * training circuit of "Communication-Efficient LLM Adaptation over
+ * Decentralized GPU Meshes".
+ *
+ * Conventions for every entry point:
+ *   - Pointers named as device buffers must be device memory of the current
+ *     HIP device; the caller owns every buffer.  The library allocates no
+ *     device memory and keeps no pointer after a call returns.
+ *   - Work is enqueued asynchronously on `stream` (NULL = the null stream).
+ *     Buffers must stay alive, and outputs unread, until the stream has
+ *     reached the enqueued work.  One workspace must not serve two calls
+ *     that may run concurrently.
+ *   - Matrices are row-major; `ld_*` is the row stride in elements.
+ *   - Every call returns ACSC_OK (0) or a negative error code, and
+ *     acsc_last_error() then describes the failure (per thread).  All argument
+ *     checks happen on the host before anything is enqueued, so a failed call
+ *     has no side effect.  No exception or abort crosses this boundary.
+ *   - bf16 data is passed as its 16-bit patterns (uint16_t storage).
+ */
+#ifndef ACSC_H
+#define ACSC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum acsc_dtype { ACSC_F32 = 0, ACSC_BF16 = 1 } acsc_dtype;
+
+#define ACSC_OK 0
+#define ACSC_EINVAL (-1)  /* null pointer, bad shape, K or r out of range   */
+#define ACSC_EDTYPE (-2)  /* unknown dtype                                  */
+#define ACSC_EALIGN (-3)  /* pointer or stride not aligned as required      */
+#define ACSC_EHIP (-4)    /* HIP launch or runtime failure                  */
+#define ACSC_ENOSPC (-5)  /* workspace too small                            */
+
+/* Text of the last error raised on the calling thread ("" if none). */
+const char *acsc_last_error(void);
+
+/* Library ABI version (increments on any signature change). */
+int acsc_version(void);
+
+/* Diagnostics, not part of the hot path.  acsc_stats_enable(1) resets the
+ * counters and starts timing: every kernel the library enqueues from then on
+ * is bracketed by a pair of HIP events recorded on its own stream, and its
+ * duration is added to the total of its kernel name.  acsc_stats_enable(0)
+ * stops timing.  acsc_stats_read waits for the recorded events, then returns
+ * the name (NUL-terminated, truncated to name_len), launch count and summed
+ * milliseconds of the index-th kernel name (alphabetical); ACSC_EINVAL past
+ * the last one.  Timing serialises nothing but adds two event records per
+ * launch. */
+int acsc_stats_enable(int on);
+int acsc_stats_read(int index, char *name, size_t name_len, int64_t *launches, double *total_ms);
+
+/* ------------------------------------------------------------------------
+ * Activation-masking compressor (paper Sec. 3.1; Alg. 1; App. F).
+ *
+ * The mask of a [B, S, H] hidden state at one pipeline boundary is the
+ * paper's shared pseudorandom function g(layer, step, B, S, H): sender and
+ * receiver rebuild it from this key, so only the kept values need to cross
+ * the link.  The backward pass uses the same key, so the activation gradient
+ * is packed at exactly the positions kept in the forward pass.  The key has
+ * no direction field on purpose.
+ *
+ * Per token row r = b*S + s the kept set I_r holds K distinct indices of
+ * [0, H) in ascending order; it is the image of [0, K) under a keyed Feistel
+ * permutation of [0, H) (cycle walking), keyed by mix64 over the fields
+ * below.  The full construction is specified in the project's design notes
+ * and implemented independently by the CPU oracle.
+ * ---------------------------------------------------------------------- */
+typedef struct ac_mask_key {
+    uint64_t seed;        /* run-wide secret shared by sender and receiver   */
+    uint64_t step;        /* optimisation step t                             */
+    uint32_t layer;       /* boundary layer index l                          */
+    uint32_t microbatch;  /* microbatch id within the step                   */
+    uint32_t B, S, H;     /* tensor shape: batch, sequence length, hidden    */
+} ac_mask_key;
+
+/* K = round(keep * H) kept dimensions per token (Sec. 3.1, keep = 1 - p),
+ * computed as floor(keep*H + 0.5) in double.  Requires 1 <= H <= 65536,
+ * 0 < keep <= 1 and a result in [1, H]; else ACSC_EINVAL. */
+int ac_keep_count(int H, double keep, int *K);
+
+/* Pack (Sec. 3.1 forward send; Alg. 1 backward send, same key):
+ *   vals[r, i] = x[r, I_r[i]]   (bit copy)     for 0 <= r < rows, 0 <= i < K
+ *   idx[r, i]  = I_r[i]         (if idx != NULL)
+ * x     device, [rows, ld_x] elements of `dt`, ld_x >= H.
+ * vals  device, [rows, K] contiguous, same dtype; must not overlap x.
+ * idx   device or NULL, [rows, K] uint16, ascending within each row.
+ * Requires rows == key->B * key->S, H == key->H, 1 <= K <= H <= 65536, and
+ * element-size alignment of x and vals (2-byte idx). */
+int ac_mask_pack(const void *x, acsc_dtype dt, int64_t rows, int H, int64_t ld_x, int K,
+                 const ac_mask_key *key, void *vals, uint16_t *idx, hipStream_t stream);
+
+/* Unpack and scatter (Sec. 3.1 receiver; App. F receiver-side rescale):
+ *   y[r, j] = round(scale * vals[r, i])  if j = I_r[i]
+ *   y[r, j] = +0                          otherwise,     for j < H
+ * The product is rounded once to `dt` (nearest even), so scale = 1 copies
+ * bits exactly (for bf16, products in the fp32 normal range).  scale = H/K
+ * makes the fixed-K mask unbiased; the paper's 1/(1-p) is within 0.5% of it.
+ * vals  device, [rows, K] contiguous.
+ * idx   device or NULL.  NULL: positions are rebuilt from `key` (the paper's
+ *       wire format).  Otherwise row r of idx must be strictly ascending, as
+ *       ac_mask_pack writes it; entries >= H are ignored.
+ * y     device, [rows, ld_y], ld_y >= H; columns >= H are not touched; must
+ *       not overlap vals or idx.
+ * Same shape and key requirements as ac_mask_pack. */
+int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int64_t rows, int H,
+                      int K, const ac_mask_key *key, float scale, void *y, int64_t ld_y,
+                      hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Spectral corrector (paper Sec. 3.2; Alg. 1; App. D).
+ * ---------------------------------------------------------------------- */
+
+/* Largest supported k = r + oversample (columns of the subspace iteration). */
+#define SC_KMAX 192
+
+/* Bytes of device workspace that sc_build_prior and sc_correct need for an
+ * m x n matrix, prior rank r and oversampling p (k = min(r + p, m, n)).
+ * Requires 1 <= r <= min(m, n, SC_KMAX), p >= 0. */
+int sc_workspace_size(int m, int n, int r, int oversample, acsc_dtype dt, size_t *bytes);
+
+/* Anchor prior (Sec. 3.2; Alg. 1 on anchor arrival; App. D):
+ *   1. if G_anc != NULL:  M <- beta * M + (1 - beta) * G_anc       (EMA)
+ *   2. (U, s, V) = the top-r singular triplets of M                 (SVD)
+ *   3. d_i = s_i / (s_i + tau), with 0/0 taken as 0                 (filter)
+ * The SVD is computed by randomised block subspace iteration on the device:
+ * k = min(r + oversample, m, n) columns, `power_iters` passes of M^T then M,
+ * CholeskyQR2 re-orthonormalisation, Rayleigh-Ritz via one-sided Jacobi.
+ * Starting block: V_warm (n x r, e.g. the previous V) padded with random
+ * columns drawn from `seed`, or all random when V_warm is NULL.
+ * G_anc  device or NULL, [m, n] of `dt`.
+ * M      device fp32 [m, n], in/out (the EMA state; start it at zero).
+ * U      device fp32 [m, r] out, orthonormal columns.
+ * s, d   device fp32 [r] out; s descending, d in [0, 1).
+ * V      device fp32 [n, r] out, orthonormal columns.
+ * Singular values at or below 1e-5 times the largest (the numerical rank of
+ * an fp32 iteration; M of rank < r) are returned as s_i = d_i = 0 with zero
+ * columns in U and V.
+ * Requires 0 <= beta <= 1, tau >= 0, power_iters >= 0, 1 <= r <= min(m,n,SC_KMAX),
+ * ws_bytes >= sc_workspace_size(...), 256-byte aligned ws. */
+int sc_build_prior(const void *G_anc, acsc_dtype dt, float *M, int m, int n, float beta, int r,
+                   int oversample, int power_iters, float tau, const float *V_warm, uint64_t seed,
+                   float *U, float *s, float *V, float *d, void *ws, size_t ws_bytes,
+                   hipStream_t stream);
+
+/* Spectral correction of one masked weight gradient (Sec. 3.2; Alg. 1):
+ *   X = U^T G V;  X_f = diag(d) X diag(d);  G_filt = U X_f V^T;
+ *   G_proj = alpha * G + (1 - alpha) * G_filt
+ * G       device [m, n] of `dt`.
+ * U, V    device fp32 [m, r], [n, r];  d device fp32 [r].
+ * G_proj  device [m, n] of `dt`; may equal G (in place), must not partially
+ *         overlap it.
+ * Accumulation is fp32.  For bf16 G the products run on bf16 matrix cores,
+ * with U X_f and V rounded to bf16 (relative error ~1e-3, well inside the
+ * 2e-2 budget of bf16 inputs); for fp32 G everything stays fp32.
+ * Requires 1 <= r <= SC_KMAX, r <= min(m, n), ws as for sc_build_prior,
+ * element-aligned pointers. */
+int sc_correct(const void *G, acsc_dtype dt, int m, int n, const float *U, const float *d,
+               const float *V, int r, float alpha, void *G_proj, void *ws, size_t ws_bytes,
+               hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACSC_H */

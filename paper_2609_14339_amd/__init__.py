@@ -1,0 +1,229 @@
+"""Python binding of libacsc.so (include/acsc.h): argument marshalling only.
+
+Every step of the hot path runs in the HIP library; this module turns torch
+tensors into device pointers and the current HIP stream, calls the C entry
+point of the same name, and raises ``AcscError`` on a non-zero return code.
+There is no fallback: if the library is not built, importing this package
+raises ``ImportError``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libacsc.so")
+
+F32, BF16 = 0, 1
+SC_KMAX = 192
+
+ACSC_OK, ACSC_EINVAL, ACSC_EDTYPE, ACSC_EALIGN, ACSC_EHIP, ACSC_ENOSPC = 0, -1, -2, -3, -4, -5
+
+
+class AcscError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"acsc error {code}: {msg}")
+        self.code = code
+
+
+class MaskKey(C.Structure):
+    """ac_mask_key: the fields of the paper's g(layer, step, B, S, H) plus a
+    seed and a microbatch id."""
+    _fields_ = [("seed", C.c_uint64), ("step", C.c_uint64), ("layer", C.c_uint32),
+                ("microbatch", C.c_uint32), ("B", C.c_uint32), ("S", C.c_uint32),
+                ("H", C.c_uint32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "(or python paper_2609_14339_amd/build.py)")
+    lib = C.CDLL(LIB_PATH)
+    vp, i32, i64, u64, f32, sz = C.c_void_p, C.c_int, C.c_int64, C.c_uint64, C.c_float, C.c_size_t
+    lib.acsc_last_error.restype = C.c_char_p
+    lib.acsc_last_error.argtypes = []
+    lib.acsc_version.restype = i32
+    lib.ac_keep_count.restype = i32
+    lib.ac_keep_count.argtypes = [i32, C.c_double, C.POINTER(i32)]
+    lib.ac_mask_pack.restype = i32
+    lib.ac_mask_pack.argtypes = [vp, i32, i64, i32, i64, i32, C.POINTER(MaskKey), vp, vp, vp]
+    lib.ac_unpack_scatter.restype = i32
+    lib.ac_unpack_scatter.argtypes = [vp, vp, i32, i64, i32, i32, C.POINTER(MaskKey), f32, vp,
+                                      i64, vp]
+    lib.sc_workspace_size.restype = i32
+    lib.sc_workspace_size.argtypes = [i32, i32, i32, i32, i32, C.POINTER(sz)]
+    lib.sc_build_prior.restype = i32
+    lib.sc_build_prior.argtypes = [vp, i32, vp, i32, i32, f32, i32, i32, i32, f32, vp, u64,
+                                   vp, vp, vp, vp, vp, sz, vp]
+    lib.sc_correct.restype = i32
+    lib.sc_correct.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, f32, vp, vp, sz, vp]
+    lib.acsc_stats_enable.restype = i32
+    lib.acsc_stats_enable.argtypes = [i32]
+    lib.acsc_stats_read.restype = i32
+    lib.acsc_stats_read.argtypes = [i32, C.c_char_p, sz, C.POINTER(i64), C.POINTER(C.c_double)]
+    return lib
+
+
+lib = _load()
+
+EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
+            "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
+            "sc_build_prior", "sc_correct")
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise AcscError(rc, lib.acsc_last_error().decode())
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise AcscError(ACSC_EDTYPE, f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise AcscError(ACSC_EINVAL, "tensors must live on the GPU")
+
+
+def _in(t: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    """Row-major copy of an input if it is not already contiguous."""
+    return None if t is None else t.contiguous()
+
+
+def _out(*ts):
+    for t in ts:
+        if t is not None and not t.is_contiguous():
+            raise AcscError(ACSC_EINVAL, "output and in/out tensors must be contiguous")
+
+
+def acsc_stats_enable(on: bool = True) -> None:
+    """Start (resetting the counters) or stop per-kernel event timing."""
+    _check(lib.acsc_stats_enable(1 if on else 0))
+
+
+def acsc_stats_read() -> dict:
+    """{kernel name: (launches, total milliseconds)} of the timed launches."""
+    out = {}
+    i = 0
+    buf = C.create_string_buffer(128)
+    n = C.c_int64(0)
+    ms = C.c_double(0.0)
+    while lib.acsc_stats_read(i, buf, 128, C.byref(n), C.byref(ms)) == 0:
+        out[buf.value.decode()] = (n.value, ms.value)
+        i += 1
+    return out
+
+
+def make_key(seed: int, layer: int, step: int, microbatch: int, B: int, S: int, H: int) -> MaskKey:
+    return MaskKey(seed=seed, step=step, layer=layer, microbatch=microbatch, B=B, S=S, H=H)
+
+
+def ac_keep_count(H: int, keep: float) -> int:
+    k = C.c_int(0)
+    _check(lib.ac_keep_count(H, keep, C.byref(k)))
+    return k.value
+
+
+def ac_mask_pack(x: torch.Tensor, K: int, key: MaskKey, vals: Optional[torch.Tensor] = None,
+                 idx: Optional[torch.Tensor] = None, with_idx: bool = True, stream=None):
+    """x: [rows, H] (row stride x.stride(0)).  Returns (vals [rows, K], idx
+    [rows, K] int16 holding uint16 patterns, or None)."""
+    _need_cuda(x)
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise AcscError(ACSC_EINVAL, "x must be 2-D with unit column stride")
+    rows, H = x.shape
+    if vals is None:
+        vals = torch.empty(rows, K, dtype=x.dtype, device=x.device)
+    if idx is None and with_idx:
+        idx = torch.empty(rows, K, dtype=torch.int16, device=x.device)
+    _need_cuda(vals, idx)
+    _check(lib.ac_mask_pack(_ptr(x), _dt(x), rows, H, x.stride(0), K, C.byref(key), _ptr(vals),
+                            _ptr(idx), _stream(stream)))
+    return vals, idx
+
+
+def ac_unpack_scatter(vals: torch.Tensor, H: int, key: MaskKey, scale: float = 1.0,
+                      idx: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """Dense [rows, H] output (or into ``y``, row stride y.stride(0))."""
+    _need_cuda(vals, idx)
+    rows, K = vals.shape
+    if y is None:
+        y = torch.empty(rows, H, dtype=vals.dtype, device=vals.device)
+    _need_cuda(y)
+    if y.dim() != 2 or y.stride(1) != 1 or not vals.is_contiguous():
+        raise AcscError(ACSC_EINVAL, "vals must be contiguous and y 2-D with unit column stride")
+    _check(lib.ac_unpack_scatter(_ptr(vals), _ptr(idx), _dt(vals), rows, H, K, C.byref(key),
+                                 float(scale), _ptr(y), y.stride(0), _stream(stream)))
+    return y
+
+
+def sc_workspace_size(m: int, n: int, r: int, oversample: int, dtype: torch.dtype) -> int:
+    b = C.c_size_t(0)
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(lib.sc_workspace_size(m, n, r, oversample, code, C.byref(b)))
+    return b.value
+
+
+def workspace(m: int, n: int, r: int, oversample: int, dtype: torch.dtype, device="cuda"):
+    nbytes = sc_workspace_size(m, n, r, oversample, dtype)
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def sc_build_prior(G_anc: Optional[torch.Tensor], M: torch.Tensor, r: int, beta: float,
+                   tau: float, oversample: int, power_iters: int, seed: int = 0,
+                   V_warm: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                   out=None, dtype: Optional[torch.dtype] = None, stream=None):
+    """EMA of G_anc into M (fp32, in place), then (U, s, V, d).  Returns them."""
+    _need_cuda(G_anc, M, V_warm)
+    G_anc, V_warm = _in(G_anc), _in(V_warm)
+    _out(M)
+    m, n = M.shape
+    dt = dtype if dtype is not None else (G_anc.dtype if G_anc is not None else torch.float32)
+    if out is None:
+        out = (torch.empty(m, r, device=M.device), torch.empty(r, device=M.device),
+               torch.empty(n, r, device=M.device), torch.empty(r, device=M.device))
+    U, s, V, d = out
+    _out(U, s, V, d)
+    if ws is None:
+        ws = workspace(m, n, r, oversample, dt, M.device)
+    code = BF16 if dt == torch.bfloat16 else F32
+    _check(lib.sc_build_prior(_ptr(G_anc), code, _ptr(M), m, n, float(beta), r, oversample,
+                              power_iters, float(tau), _ptr(V_warm), seed, _ptr(U), _ptr(s),
+                              _ptr(V), _ptr(d), _ptr(ws), ws.numel(), _stream(stream)))
+    return U, s, V, d
+
+
+def sc_correct(G: torch.Tensor, U: torch.Tensor, d: torch.Tensor, V: torch.Tensor, alpha: float,
+               out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+               stream=None) -> torch.Tensor:
+    """G_proj = alpha G + (1 - alpha) U diag(d) U^T G V diag(d) V^T."""
+    _need_cuda(G, U, d, V, out)
+    G, U, d, V = _in(G), _in(U), _in(d), _in(V)
+    _out(out)
+    m, n = G.shape
+    r = U.shape[1]
+    if out is None:
+        out = torch.empty_like(G)
+    if ws is None:
+        ws = workspace(m, n, r, 0, G.dtype, G.device)
+    _check(lib.sc_correct(_ptr(G), _dt(G), m, n, _ptr(U), _ptr(d), _ptr(V), r, float(alpha),
+                          _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+    return out

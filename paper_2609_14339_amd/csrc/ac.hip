@@ -1,0 +1,449 @@
+// Activation-masking compressor for gfx950 (paper Sec. 3.1; Alg. 1; App. F).
+//
+// One wavefront owns one token row; a workgroup holds up to four rows.
+//   pack:   keyed permutation -> kept-set bitmap in LDS -> wave prefix scan
+//           of word popcounts -> ascending index list in LDS -> gather of the
+//           kept values -> coalesced stores of vals (and uint16 idx).
+//   unpack: bitmap (from the key, or from transmitted indices) -> per-word
+//           exclusive prefix in LDS -> every lane writes whole 16-byte chunks
+//           of the dense row: zeros, or scale * vals[rank] at kept slots.
+// Rows are independent, so neither kernel needs more than wave-level and
+// workgroup-level synchronisation, and the dense side is touched exactly once.
+#include "common.h"
+
+namespace acsc {
+namespace {
+
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+constexpr int kMaxWavesPerBlock = 4;
+constexpr size_t kLdsBudget = 160 * 1024;
+
+// SplitMix64 output function (Steele, Lea & Flood 2014).
+__host__ __device__ __forceinline__ uint64_t mix64(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// MurmurHash3 32-bit finaliser (Appleby), the Feistel round function.
+__device__ __forceinline__ uint32_t fmix32(uint32_t h)
+{
+    h ^= h >> 16;
+    h *= 0x85EBCA6Bu;
+    h ^= h >> 13;
+    h *= 0xC2B2AE35u;
+    h ^= h >> 16;
+    return h;
+}
+
+// Key chain over the fields of g(layer, step, B, S, H), plus seed and microbatch.
+uint64_t chain_key(const ac_mask_key &k)
+{
+    const uint64_t f[6] = {k.layer, k.step, k.microbatch, k.B, k.S, k.H};
+    uint64_t z = k.seed;
+    for (int i = 0; i < 6; ++i)
+        z = mix64((z ^ f[i]) + kGamma);
+    return z;
+}
+
+int domain_bits(int H)
+{
+    int w = 2;
+    while ((1ll << w) < H)
+        w += 2;
+    return w;
+}
+
+// Keyed permutation of [0, H) for one row: a balanced Feistel network on
+// 2*hb bits, cycle-walked back into range.
+template <int ROUNDS>
+struct RowPerm {
+    uint32_t sk[ROUNDS];
+    uint32_t mask;
+    int hb;
+    uint32_t H;
+
+    __device__ __forceinline__ RowPerm(uint64_t key, uint64_t row, int w, uint32_t H_) : H(H_)
+    {
+        uint64_t c = mix64((key ^ row) + kGamma);
+#pragma unroll
+        for (int j = 0; j < ROUNDS / 2; ++j) {
+            sk[2 * j] = static_cast<uint32_t>(c);
+            sk[2 * j + 1] = static_cast<uint32_t>(c >> 32);
+            c = mix64(c + kGamma);
+        }
+        hb = w >> 1;
+        mask = (1u << hb) - 1u;
+    }
+
+    __device__ __forceinline__ uint32_t feistel(uint32_t x) const
+    {
+        uint32_t L = x >> hb, R = x & mask;
+#pragma unroll
+        for (int j = 0; j < ROUNDS; ++j) {
+            const uint32_t t = L ^ (fmix32(R ^ sk[j]) & mask);
+            L = R;
+            R = t;
+        }
+        return (L << hb) | R;
+    }
+
+    __device__ __forceinline__ uint32_t operator()(uint32_t i) const
+    {
+        uint32_t y = feistel(i);
+        while (y >= H)
+            y = feistel(y);
+        return y;
+    }
+};
+
+__device__ __forceinline__ int wave_exclusive_scan(int v, int lane)
+{
+    int incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(incl, off, 64);
+        if (lane >= off)
+            incl += t;
+    }
+    return incl - v;
+}
+
+// Per-wave LDS layout of the pack kernel: bitmap[nw] then uint16 kidx[K].
+__host__ __device__ __forceinline__ int pack_wave_words(int nw, int K) { return nw + (K + 1) / 2; }
+
+template <typename E, int ROUNDS>
+__global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, int64_t rows, int H,
+                                                      int64_t ld_x, int K, uint64_t key, int w,
+                                                      E *__restrict__ vals,
+                                                      uint16_t *__restrict__ idx)
+{
+    extern __shared__ uint32_t smem[];
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int wpb = blockDim.x >> 6;
+    const int nw = (H + 31) >> 5;
+    uint32_t *bm = smem + wid * pack_wave_words(nw, K);
+    uint16_t *kidx = reinterpret_cast<uint16_t *>(bm + nw);
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
+    const bool active = row < rows;
+
+    for (int i = lane; i < nw; i += 64)
+        bm[i] = 0u;
+    __syncthreads();
+    if (active) {
+        const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
+        for (int i = lane; i < K; i += 64) {
+            const uint32_t j = perm(static_cast<uint32_t>(i));
+            atomicOr(&bm[j >> 5], 1u << (j & 31));
+        }
+    }
+    __syncthreads();
+    if (active) {
+        const int per = (nw + 63) >> 6;
+        const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
+        int cnt = 0;
+        for (int i = w0; i < w1; ++i)
+            cnt += __popc(bm[i]);
+        int pos = wave_exclusive_scan(cnt, lane);
+        for (int i = w0; i < w1; ++i) {
+            uint32_t b = bm[i];
+            while (b) {
+                const int t = __ffs(b) - 1;
+                b &= b - 1u;
+                kidx[pos++] = static_cast<uint16_t>((i << 5) + t);
+            }
+        }
+    }
+    __syncthreads();
+    if (active) {
+        const E *xr = x + row * ld_x;
+        E *vr = vals + row * K;
+        uint16_t *ir = idx ? idx + row * K : nullptr;
+        for (int i = lane; i < K; i += 64) {
+            const uint16_t j = kidx[i];
+            vr[i] = xr[j];
+            if (ir)
+                ir[i] = j;
+        }
+    }
+}
+
+// scale * v rounded once to the output type.
+__device__ __forceinline__ uint32_t scaled(uint32_t vbits, float scale)
+{
+    return __float_as_uint(__uint_as_float(vbits) * scale);
+}
+
+// bf16: p = fl32(v * s) and e = v * s - p (exact, by fma) decide the rounding
+// of the exact product: only when p sits exactly on a bf16 tie does the sign
+// of e matter; otherwise rounding p to nearest even equals rounding v * s.
+__device__ __forceinline__ uint16_t scaled(uint16_t vbits, float scale)
+{
+    const float v = bf16_to_f32(vbits);
+    const float p = v * scale;
+    const float e = __builtin_fmaf(v, scale, -p);
+    uint32_t u = __float_as_uint(p);
+    if ((u & 0x7F800000u) == 0x7F800000u)
+        return (u & 0x007FFFFFu) ? static_cast<uint16_t>((u >> 16) | 0x0040u)
+                                 : static_cast<uint16_t>(u >> 16);
+    if ((u & 0xFFFFu) == 0x8000u && e != 0.0f) {
+        const bool away = (e > 0.0f) == (p > 0.0f);
+        u = away ? u + 0x8000u : (u & 0xFFFF0000u);
+        return static_cast<uint16_t>(u >> 16);
+    }
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+template <typename E>
+struct Vec16;
+template <>
+struct Vec16<uint16_t> {
+    static constexpr int N = 8;
+};
+template <>
+struct Vec16<uint32_t> {
+    static constexpr int N = 4;
+};
+
+// Per-wave LDS layout of the unpack kernel: bitmap[nw] then prefix[nw].
+template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
+__global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ vals,
+                                                        const uint16_t *__restrict__ idx,
+                                                        int64_t rows, int H, int K, uint64_t key,
+                                                        int w, float scale, E *__restrict__ y,
+                                                        int64_t ld_y)
+{
+    extern __shared__ uint32_t smem[];
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int wpb = blockDim.x >> 6;
+    const int nw = (H + 31) >> 5;
+    uint32_t *bm = smem + wid * 2 * nw;
+    uint32_t *pre = bm + nw;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
+    const bool active = row < rows;
+
+    for (int i = lane; i < nw; i += 64)
+        bm[i] = 0u;
+    __syncthreads();
+    if (active) {
+        if (FROM_IDX) {
+            const uint16_t *ir = idx + row * K;
+            for (int i = lane; i < K; i += 64) {
+                const uint32_t j = ir[i];
+                if (j < static_cast<uint32_t>(H))
+                    atomicOr(&bm[j >> 5], 1u << (j & 31));
+            }
+        } else {
+            const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w,
+                                       static_cast<uint32_t>(H));
+            for (int i = lane; i < K; i += 64) {
+                const uint32_t j = perm(static_cast<uint32_t>(i));
+                atomicOr(&bm[j >> 5], 1u << (j & 31));
+            }
+        }
+    }
+    __syncthreads();
+    if (active) {
+        const int per = (nw + 63) >> 6;
+        const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
+        int cnt = 0;
+        for (int i = w0; i < w1; ++i)
+            cnt += __popc(bm[i]);
+        int pos = wave_exclusive_scan(cnt, lane);
+        for (int i = w0; i < w1; ++i) {
+            pre[i] = static_cast<uint32_t>(pos);
+            pos += __popc(bm[i]);
+        }
+    }
+    __syncthreads();
+    if (!active)
+        return;
+    const E *vr = vals + row * K;
+    E *yr = y + row * ld_y;
+    int jtail = 0;
+    if (VEC) {
+        constexpr int N = Vec16<E>::N;
+        const int nch = H / N;
+        for (int c = lane; c < nch; c += 64) {
+            const int j0 = c * N;
+            const uint32_t word = bm[j0 >> 5];
+            const int sh = j0 & 31;
+            uint32_t bits = (word >> sh) & ((1u << N) - 1u);
+            E out[N];
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                out[e] = 0;
+            if (bits) {
+                int rank = static_cast<int>(pre[j0 >> 5]) + __popc(word & ((1u << sh) - 1u));
+#pragma unroll
+                for (int e = 0; e < N; ++e) {
+                    if (bits & (1u << e))
+                        out[e] = scaled(vr[rank++], scale);
+                }
+            }
+            *reinterpret_cast<uint4 *>(yr + j0) = *reinterpret_cast<const uint4 *>(out);
+        }
+        jtail = nch * N;
+    }
+    for (int j = jtail + lane; j < H; j += 64) {
+        const uint32_t word = bm[j >> 5];
+        const int b = j & 31;
+        E out = 0;
+        if ((word >> b) & 1u) {
+            const int rank = static_cast<int>(pre[j >> 5]) + __popc(word & ((1u << b) - 1u));
+            out = scaled(vr[rank], scale);
+        }
+        yr[j] = out;
+    }
+}
+
+int common_checks(acsc_dtype dt, int64_t rows, int H, int K, const ac_mask_key *key)
+{
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(key != nullptr, ACSC_EINVAL, "key is NULL");
+    ACSC_CHECK_ARG(H >= 1 && H <= 65536, ACSC_EINVAL, "H=%d outside [1, 65536]", H);
+    ACSC_CHECK_ARG(K >= 1 && K <= H, ACSC_EINVAL, "K=%d outside [1, H=%d]", K, H);
+    ACSC_CHECK_ARG(rows >= 0, ACSC_EINVAL, "rows=%lld < 0", (long long)rows);
+    ACSC_CHECK_ARG(key->H == static_cast<uint32_t>(H), ACSC_EINVAL, "key.H=%u != H=%d", key->H, H);
+    ACSC_CHECK_ARG(static_cast<int64_t>(key->B) * key->S == rows, ACSC_EINVAL,
+                   "rows=%lld != key.B*key.S=%llu", (long long)rows,
+                   (unsigned long long)key->B * key->S);
+    return ACSC_OK;
+}
+
+// Waves per workgroup such that the per-wave LDS fits the budget.
+int waves_for(size_t per_wave_bytes)
+{
+    int wpb = kMaxWavesPerBlock;
+    while (wpb > 1 && per_wave_bytes * wpb > kLdsBudget)
+        --wpb;
+    return wpb;
+}
+
+template <typename E, int ROUNDS>
+void launch_pack(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
+                 void *vals, uint16_t *idx, hipStream_t st)
+{
+    const int nw = (H + 31) / 32;
+    const size_t per = static_cast<size_t>(pack_wave_words(nw, K)) * 4;
+    const int wpb = waves_for(per);
+    const int64_t blocks = (rows + wpb - 1) / wpb;
+    ACSC_LAUNCH("ac_pack", (ac_pack_kernel<E, ROUNDS>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(64 * wpb), per * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K,
+                       key, w, static_cast<E *>(vals), idx);
+}
+
+template <typename E, int ROUNDS, bool FROM_IDX>
+void launch_unpack(const void *vals, const uint16_t *idx, int64_t rows, int H, int K, uint64_t key,
+                   int w, float scale, void *y, int64_t ld_y, bool vec, hipStream_t st)
+{
+    const int nw = (H + 31) / 32;
+    const size_t per = static_cast<size_t>(2 * nw) * 4;
+    const int wpb = waves_for(per);
+    const int64_t blocks = (rows + wpb - 1) / wpb;
+    if (vec)
+        ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, true>),
+                           dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
+                           static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
+                           static_cast<E *>(y), ld_y);
+    else
+        ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, false>),
+                           dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
+                           static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
+                           static_cast<E *>(y), ld_y);
+}
+
+}  // namespace
+}  // namespace acsc
+
+using namespace acsc;
+
+extern "C" int ac_keep_count(int H, double keep, int *K)
+{
+    clear_error();
+    ACSC_CHECK_ARG(K != nullptr, ACSC_EINVAL, "K is NULL");
+    ACSC_CHECK_ARG(H >= 1 && H <= 65536, ACSC_EINVAL, "H=%d outside [1, 65536]", H);
+    ACSC_CHECK_ARG(keep > 0.0 && keep <= 1.0, ACSC_EINVAL, "keep=%g outside (0, 1]", keep);
+    const double k = std::floor(keep * static_cast<double>(H) + 0.5);
+    ACSC_CHECK_ARG(k >= 1.0 && k <= static_cast<double>(H), ACSC_EINVAL,
+                   "round(keep*H)=%g outside [1, H]", k);
+    *K = static_cast<int>(k);
+    return ACSC_OK;
+}
+
+extern "C" int ac_mask_pack(const void *x, acsc_dtype dt, int64_t rows, int H, int64_t ld_x, int K,
+                            const ac_mask_key *key, void *vals, uint16_t *idx, hipStream_t stream)
+{
+    clear_error();
+    int rc = common_checks(dt, rows, H, K, key);
+    if (rc)
+        return rc;
+    ACSC_CHECK_ARG(ld_x >= H, ACSC_EINVAL, "ld_x=%lld < H=%d", (long long)ld_x, H);
+    if (rows == 0)
+        return ACSC_OK;
+    ACSC_CHECK_ARG(x && vals, ACSC_EINVAL, "x or vals is NULL");
+    const size_t es = dtype_size(dt);
+    ACSC_CHECK_ARG(aligned(x, es) && aligned(vals, es), ACSC_EALIGN,
+                   "x and vals must be %zu-byte aligned", es);
+    ACSC_CHECK_ARG(!idx || aligned(idx, 2), ACSC_EALIGN, "idx must be 2-byte aligned");
+    const uint64_t k = chain_key(*key);
+    const int w = domain_bits(H);
+    if (dt == ACSC_BF16) {
+        if (w <= 4)
+            launch_pack<uint16_t, 12>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
+        else
+            launch_pack<uint16_t, 8>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
+    } else {
+        if (w <= 4)
+            launch_pack<uint32_t, 12>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
+        else
+            launch_pack<uint32_t, 8>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
+    }
+    return check_launch("ac_mask_pack");
+}
+
+extern "C" int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int64_t rows,
+                                 int H, int K, const ac_mask_key *key, float scale, void *y,
+                                 int64_t ld_y, hipStream_t stream)
+{
+    clear_error();
+    int rc = common_checks(dt, rows, H, K, key);
+    if (rc)
+        return rc;
+    ACSC_CHECK_ARG(ld_y >= H, ACSC_EINVAL, "ld_y=%lld < H=%d", (long long)ld_y, H);
+    ACSC_CHECK_ARG(std::isfinite(scale), ACSC_EINVAL, "scale must be finite");
+    if (rows == 0)
+        return ACSC_OK;
+    ACSC_CHECK_ARG(vals && y, ACSC_EINVAL, "vals or y is NULL");
+    const size_t es = dtype_size(dt);
+    ACSC_CHECK_ARG(aligned(vals, es) && aligned(y, es), ACSC_EALIGN,
+                   "vals and y must be %zu-byte aligned", es);
+    ACSC_CHECK_ARG(!idx || aligned(idx, 2), ACSC_EALIGN, "idx must be 2-byte aligned");
+    const bool vec = aligned(y, 16) && (static_cast<size_t>(ld_y) * es) % 16 == 0;
+    const uint64_t k = chain_key(*key);
+    const int w = domain_bits(H);
+#define ACSC_UNPACK(E, R)                                                                        \
+    do {                                                                                         \
+        if (idx)                                                                                 \
+            launch_unpack<E, R, true>(vals, idx, rows, H, K, k, w, scale, y, ld_y, vec, stream); \
+        else                                                                                     \
+            launch_unpack<E, R, false>(vals, idx, rows, H, K, k, w, scale, y, ld_y, vec, stream); \
+    } while (0)
+    if (dt == ACSC_BF16) {
+        if (w <= 4)
+            ACSC_UNPACK(uint16_t, 12);
+        else
+            ACSC_UNPACK(uint16_t, 8);
+    } else {
+        if (w <= 4)
+            ACSC_UNPACK(uint32_t, 12);
+        else
+            ACSC_UNPACK(uint32_t, 8);
+    }
+#undef ACSC_UNPACK
+    return check_launch("ac_unpack_scatter");
+}

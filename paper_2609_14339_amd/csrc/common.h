@@ -1,0 +1,71 @@
+// Internal helpers shared by the library's translation units: error state,
+// argument checks and bf16 bit conversions.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+
+#include "../../include/acsc.h"
+
+namespace acsc {
+
+// Per-thread text of the last error; set_error returns its code so that
+// entry points can `return set_error(...)`.
+int set_error(int code, const char *fmt, ...);
+void clear_error();
+
+#define ACSC_CHECK_ARG(cond, code, ...)            \
+    do {                                           \
+        if (!(cond))                               \
+            return ::acsc::set_error(code, __VA_ARGS__); \
+    } while (0)
+
+// Optional per-kernel timing (acsc_stats_enable): ACSC_LAUNCH brackets a
+// launch with HIP events on its stream when timing is on.
+bool stats_on();
+void *stats_begin(hipStream_t st, const char *tag);
+void stats_end(hipStream_t st, void *token);
+
+#define ACSC_LAUNCH(tag, kernel, grid, block, lds, st, ...)                         \
+    do {                                                                          \
+        void *acsc_tok_ = ::acsc::stats_on() ? ::acsc::stats_begin(st, tag) : nullptr; \
+        hipLaunchKernelGGL(kernel, grid, block, lds, st, __VA_ARGS__);            \
+        if (acsc_tok_)                                                            \
+            ::acsc::stats_end(st, acsc_tok_);                                     \
+    } while (0)
+
+// Enqueue-time HIP error check; hipGetLastError also clears sticky launch
+// errors left by this library's own launch.
+inline int check_launch(const char *what)
+{
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return set_error(ACSC_EHIP, "%s: %s", what, hipGetErrorString(e));
+    return ACSC_OK;
+}
+
+inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+inline size_t dtype_size(acsc_dtype dt) { return dt == ACSC_BF16 ? 2 : 4; }
+
+// bf16 <-> fp32 on bit patterns.
+__device__ __forceinline__ float bf16_to_f32(uint16_t h)
+{
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Round to nearest even; NaN stays a quiet NaN of the same sign.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
+        return static_cast<uint16_t>((u >> 16) | 0x0040u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+}  // namespace acsc

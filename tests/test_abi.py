@@ -1,0 +1,97 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/acsc.h declares, and rejects bad arguments on the host (before any
+HIP call, so these run on a machine without a GPU)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "acsc.h")
+LIB = os.path.join(ROOT, "paper_2609_14339_amd", "libacsc.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z][a-z0-9_]*)\s*\([^;{]*\)\s*;", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail("libacsc.so is not built (run __graft_entry__.build())")
+    return C.CDLL(LIB)
+
+
+def test_header_declares_the_four_hot_path_calls():
+    fns = declared_functions()
+    for name in ("ac_mask_pack", "ac_unpack_scatter", "sc_build_prior", "sc_correct"):
+        assert name in fns
+
+
+def test_library_exports_every_declared_function(lib):
+    fns = declared_functions()
+    assert len(fns) >= 8
+    for name in fns:
+        assert hasattr(lib, name), name
+
+
+def test_python_binding_names_match_the_header():
+    import paper_2609_14339_amd as pk
+    assert set(pk.EXPORTED) == set(declared_functions())
+    for name in pk.EXPORTED:
+        if not name.startswith("acsc_"):
+            assert callable(getattr(pk, name)), name
+
+
+class Key(C.Structure):
+    _fields_ = [("seed", C.c_uint64), ("step", C.c_uint64), ("layer", C.c_uint32),
+                ("microbatch", C.c_uint32), ("B", C.c_uint32), ("S", C.c_uint32),
+                ("H", C.c_uint32)]
+
+
+def _err(lib):
+    lib.acsc_last_error.restype = C.c_char_p
+    return lib.acsc_last_error().decode()
+
+
+def test_keep_count_on_host(lib):
+    k = C.c_int(0)
+    lib.ac_keep_count.argtypes = [C.c_int, C.c_double, C.POINTER(C.c_int)]
+    assert lib.ac_keep_count(2048, 0.05, C.byref(k)) == 0 and k.value == 102
+    assert lib.ac_keep_count(8192, 0.02, C.byref(k)) == 0 and k.value == 164
+    assert lib.ac_keep_count(10, 0.01, C.byref(k)) == -1 and "outside" in _err(lib)
+    assert lib.ac_keep_count(70000, 0.5, C.byref(k)) == -1
+
+
+def test_pack_and_unpack_reject_bad_arguments_before_launch(lib):
+    vp = C.c_void_p
+    lib.ac_mask_pack.argtypes = [vp, C.c_int, C.c_int64, C.c_int, C.c_int64, C.c_int,
+                                 C.POINTER(Key), vp, vp, vp]
+    lib.ac_unpack_scatter.argtypes = [vp, vp, C.c_int, C.c_int64, C.c_int, C.c_int,
+                                      C.POINTER(Key), C.c_float, vp, C.c_int64, vp]
+    key = Key(seed=1, step=1, layer=0, microbatch=0, B=2, S=4, H=64)
+    fake = vp(0x1000)
+    # wrong dtype, K out of range, shape mismatch with the key, ld too small,
+    # null pointers, misaligned pointers
+    assert lib.ac_mask_pack(fake, 7, 8, 64, 64, 4, C.byref(key), fake, None, None) == -2
+    assert lib.ac_mask_pack(fake, 1, 8, 64, 64, 0, C.byref(key), fake, None, None) == -1
+    assert lib.ac_mask_pack(fake, 1, 8, 64, 64, 65, C.byref(key), fake, None, None) == -1
+    assert lib.ac_mask_pack(fake, 1, 9, 64, 64, 4, C.byref(key), fake, None, None) == -1
+    assert "key.B*key.S" in _err(lib)
+    assert lib.ac_mask_pack(fake, 1, 8, 64, 63, 4, C.byref(key), fake, None, None) == -1
+    assert lib.ac_mask_pack(None, 1, 8, 64, 64, 4, C.byref(key), fake, None, None) == -1
+    assert lib.ac_mask_pack(fake, 1, 8, 64, 64, 4, None, fake, None, None) == -1
+    assert lib.ac_mask_pack(vp(0x1001), 1, 8, 64, 64, 4, C.byref(key), fake, None, None) == -3
+    assert lib.ac_mask_pack(vp(0x1002), 0, 8, 64, 64, 4, C.byref(key), fake, None, None) == -3
+    assert lib.ac_unpack_scatter(fake, None, 1, 8, 64, 4, C.byref(key), 1.0, fake, 32, None) == -1
+    assert lib.ac_unpack_scatter(fake, None, 1, 8, 64, 4, C.byref(key), float("inf"), fake, 64,
+                                 None) == -1
+    assert lib.ac_unpack_scatter(fake, vp(0x1003), 1, 8, 64, 4, C.byref(key), 1.0, fake, 64,
+                                 None) == -3
+    # zero rows is a no-op that succeeds without touching any pointer
+    key0 = Key(seed=1, step=1, layer=0, microbatch=0, B=0, S=4, H=64)
+    assert lib.ac_mask_pack(None, 1, 0, 64, 64, 4, C.byref(key0), None, None, None) == 0
+    assert lib.ac_unpack_scatter(None, None, 1, 0, 64, 4, C.byref(key0), 1.0, None, 64, None) == 0

@@ -71,7 +71,7 @@ CONFIGS = {
     1: Config(1, "tiny-fp32",
               ActSpec(2, 64, 256, torch.float32, (0.1,), "normal"),
               GradSpec(((256, 256),), 8, (1.0, 10.0), (8,), torch.float32, 0.01, 0.1),
-              oversample=8, power_iters=4),
+              oversample=8, power_iters=6),
     2: Config(2, "1b-bf16",
               ActSpec(8, 2048, 2048, torch.bfloat16, (0.05,), "normal"),
               GradSpec(((2048, 2048),) * 4 + ((2048, 8192), (8192, 2048)), 32, (1.0, 100.0),
