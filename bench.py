@@ -95,7 +95,6 @@ def main():
     idxs = [[torch.empty(rows, K, dtype=torch.int16, device=dev) for _ in range(2)] for _ in range(L)]
     ys = [[torch.empty(rows, H, dtype=act.dtype, device=dev) for _ in range(2)] for _ in range(L)]
     mats = []
-    ws_bytes = 0
     for l in range(L):
         for j, (m, n) in enumerate(gs.shapes):
             G_anc, G_mask = workloads.grad_pair_fast(gs, cfg.cid, l, j, dev)
@@ -103,9 +102,12 @@ def main():
                              M=torch.zeros(m, n, device=dev),
                              out=(torch.empty(m, r, device=dev), torch.empty(r, device=dev),
                                   torch.empty(n, r, device=dev), torch.empty(r, device=dev)),
-                             Gp=torch.empty_like(G_mask)))
-            ws_bytes = max(ws_bytes, pk.sc_workspace_size(m, n, r, p, gs.dtype))
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+                             Gp=torch.empty_like(G_mask),
+                             ws=pk.workspace(m, n, r, p, gs.dtype)))
+    # one batched call per phase over every matrix of the stage
+    build_items = [dict(G_anc=mt["G_anc"], M=mt["M"], out=mt["out"], ws=mt["ws"]) for mt in mats]
+    corr_items = [dict(G=mt["G_mask"], prior=(mt["out"][0], mt["out"][3], mt["out"][2]), out=mt["Gp"],
+                       ws=mt["ws"]) for mt in mats]
     torch.cuda.synchronize()
     setup_s = time.time() - t0
     print(f"[bench] inputs ready in {setup_s:.1f} s; HBM in use "
@@ -123,13 +125,10 @@ def main():
                 pk.ac_unpack_scatter(vals[l][dirn], H, keys[l], scale, idx=idxs[l][dirn],
                                      y=ys[l][dirn])
         e1.record(stream)
-        for i, mt in enumerate(mats):
-            pk.sc_build_prior(mt["G_anc"], mt["M"], r, workloads.BETA, workloads.TAU, p, q,
-                              seed=1000 + i, ws=ws, out=mt["out"])
+        pk.sc_build_prior_batched(build_items, r, workloads.BETA, workloads.TAU, p, q, seed=1000,
+                                  dtype=gs.dtype)
         e2.record(stream)
-        for mt in mats:
-            U, s, V, d = mt["out"]
-            pk.sc_correct(mt["G_mask"], U, d, V, workloads.ALPHA, out=mt["Gp"], ws=ws)
+        pk.sc_correct_batched(corr_items, r, workloads.ALPHA, dtype=gs.dtype)
         e3.record(stream)
         return (e0, e1, e2, e3) if record else None
 
@@ -171,10 +170,10 @@ def main():
     for mt in mats:
         m, n = mt["m"], mt["n"]
         k = min(r + p, m, n, pk.SC_KMAX)
-        work["sc_ema"]["bytes"] += m * n * (4 + 4 + gsz)
+        work["sc_ema"]["bytes"] += m * n * (4 + 4 + gsz + (2 if gsz == 2 else 0))   # + bf16 shadow
         work["sc_ema"]["calls"] += 1
         work["sc_pass"]["flops"] += passes * 2.0 * m * n * k
-        work["sc_pass"]["bytes"] += passes * 4.0 * m * n
+        work["sc_pass"]["bytes"] += passes * float(gsz) * m * n     # the shadow (bf16) or M (fp32)
         work["sc_pass"]["calls"] += passes
         work["sc_correct"]["bytes"] += 3.0 * m * n * gsz
         work["sc_correct"]["flops"] += 4.0 * m * n * r + 3.0 * m * n
@@ -219,21 +218,25 @@ def main():
         mm = model(dom)
         dom_n, dom_ms = per_step[dom]
         bound, amount, calls = mm if mm else ("latency", 0.0, dom_n)
+    # achieved = algorithmic work of every launch of the kernel in the timed
+    # region / the summed event-measured duration of those launches
     avg_s = dom_ms * 1e-3 / max(dom_n, 1e-9)
-    per_launch = amount / max(calls, 1e-9)
+    total_s = dom_ms * 1e-3
+    per_launch = amount / max(dom_n, 1e-9)
     if bound == "hbm":
-        achieved = per_launch / avg_s / 1e9
+        achieved = amount / total_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM, 4)}
     elif bound == "mfma":
-        achieved = per_launch / avg_s / 1e12
-        peak = PEAK_F32
+        achieved = amount / total_s / 1e12
+        peak = PEAK_BF16 if gs.dtype == torch.bfloat16 else PEAK_F32
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4)}
     else:
         roof = {"bound": "latency", "achieved": None, "peak": None, "unit": None, "frac": None}
     roof.update({"kernel": dom, "avg_launch_us": round(avg_s * 1e6, 2),
-                 "launches_per_step": dom_n, "work_per_launch": per_launch, "traffic": None})
+                 "launches_per_step": dom_n, "work_per_launch": per_launch,
+                 "work_unit": "bytes" if bound == "hbm" else "flops", "traffic": None})
 
     comp = {}
     for name in ("ac_pack", "ac_unpack", "sc_ema", "sc_gv", "sc_blend"):
@@ -244,7 +247,9 @@ def main():
                           "ms_per_step": round(ms, 4), "launches_per_step": n}
     if pass_ms > 0:
         tf = work["sc_pass"]["flops"] / (pass_ms * 1e-3) / 1e12
-        comp["sc_pass"] = {"TFLOP/s": round(tf, 2), "frac_fp32_mfma": round(tf / PEAK_F32, 4),
+        pk_ = PEAK_BF16 if gs.dtype == torch.bfloat16 else PEAK_F32
+        comp["sc_pass"] = {"TFLOP/s": round(tf, 2), "frac_mfma": round(tf / pk_, 4),
+                           "GB/s": round(work["sc_pass"]["bytes"] / (pass_ms * 1e-3) / 1e9, 1),
                            "ms_per_step": round(pass_ms, 4), "launches_per_step": pass_n}
     comp["phase_ms"] = {k: round(v, 4) for k, v in phase_ms.items()}
     comp["sc_correct_step"] = {"GB/s": round(work["sc_correct"]["bytes"] / (phase_ms["correct"] * 1e-3) / 1e9, 1),

@@ -167,6 +167,37 @@ int sc_correct(const void *G, acsc_dtype dt, int m, int n, const float *U, const
                const float *V, int r, float alpha, void *G_proj, void *ws, size_t ws_bytes,
                hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Batched forms: the same operations on several weight matrices (e.g. all
+ * targeted matrices of the layers a pipeline stage holds) in one call.  Every
+ * kernel is launched once for up to 16 matrices, so the latency-bound small
+ * steps (Cholesky, Jacobi) of different matrices run side by side, and the
+ * streaming passes of small matrices fill the GPU together.
+ * ---------------------------------------------------------------------- */
+typedef struct sc_matrix {
+    const void *G;          /* build: G_anc [m, n] of dt, or NULL (no arrival);
+                               correct: the masked gradient G [m, n] of dt     */
+    float *M;               /* build: EMA state, fp32 [m, n], in/out; unused by correct */
+    int m, n;               /* shape of this matrix                              */
+    float *U, *s, *V, *d;   /* build: outputs; correct: the prior (s unused)     */
+    const float *V_warm;    /* build: optional [n, r] start block, or NULL       */
+    void *G_proj;           /* correct: output [m, n] of dt (may equal G); unused by build */
+    void *ws;               /* device workspace of this matrix (256-byte aligned) */
+    size_t ws_bytes;        /* >= sc_workspace_size(m, n, r, oversample, dt)     */
+} sc_matrix;
+
+/* sc_build_prior on each of mats[0 .. count-1] with shared dt, beta, r,
+ * oversample, power_iters and tau; matrix i starts from the random block of
+ * seed + i.  Matrices must not share M, outputs or workspaces.  All arguments
+ * of all matrices are checked before anything is enqueued. */
+int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                           int oversample, int power_iters, float tau, uint64_t seed,
+                           hipStream_t stream);
+
+/* sc_correct on each of mats[0 .. count-1] with shared dt, r and alpha. */
+int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,
+                       hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -37,6 +37,14 @@ class MaskKey(C.Structure):
                 ("H", C.c_uint32)]
 
 
+class ScMatrix(C.Structure):
+    """sc_matrix: one weight matrix of a batched sc_* call."""
+    _fields_ = [("G", C.c_void_p), ("M", C.c_void_p), ("m", C.c_int), ("n", C.c_int),
+                ("U", C.c_void_p), ("s", C.c_void_p), ("V", C.c_void_p), ("d", C.c_void_p),
+                ("V_warm", C.c_void_p), ("G_proj", C.c_void_p), ("ws", C.c_void_p),
+                ("ws_bytes", C.c_size_t)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -60,6 +68,10 @@ def _load():
                                    vp, vp, vp, vp, vp, sz, vp]
     lib.sc_correct.restype = i32
     lib.sc_correct.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, f32, vp, vp, sz, vp]
+    lib.sc_build_prior_batched.restype = i32
+    lib.sc_build_prior_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, f32, i32, i32, i32, f32, u64, vp]
+    lib.sc_correct_batched.restype = i32
+    lib.sc_correct_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, i32, f32, vp]
     lib.acsc_stats_enable.restype = i32
     lib.acsc_stats_enable.argtypes = [i32]
     lib.acsc_stats_read.restype = i32
@@ -71,7 +83,7 @@ lib = _load()
 
 EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
-            "sc_build_prior", "sc_correct")
+            "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched")
 
 
 def _check(rc: int):
@@ -227,3 +239,46 @@ def sc_correct(G: torch.Tensor, U: torch.Tensor, d: torch.Tensor, V: torch.Tenso
     _check(lib.sc_correct(_ptr(G), _dt(G), m, n, _ptr(U), _ptr(d), _ptr(V), r, float(alpha),
                           _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
     return out
+
+
+def _p(t):
+    return None if t is None else t.data_ptr()
+
+
+def sc_build_prior_batched(items, r: int, beta: float, tau: float, oversample: int,
+                           power_iters: int, seed: int = 0, dtype: torch.dtype = torch.bfloat16,
+                           stream=None):
+    """items: list of dicts with G_anc (or None), M, out=(U, s, V, d), ws, and
+    optionally V_warm.  Matrix i starts from the random block of seed + i."""
+    arr = (ScMatrix * max(len(items), 1))()
+    keep = []
+    for i, it in enumerate(items):
+        G, M, (U, s, V, d), ws = _in(it.get("G_anc")), it["M"], it["out"], it["ws"]
+        Vw = _in(it.get("V_warm"))
+        _need_cuda(G, M, U, s, V, d, ws, Vw)
+        _out(M, U, s, V, d)
+        keep += [G, Vw]
+        m, n = M.shape
+        arr[i] = ScMatrix(_p(G), _p(M), m, n, _p(U), _p(s), _p(V), _p(d), _p(Vw), None, _p(ws),
+                          ws.numel())
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(lib.sc_build_prior_batched(len(items), arr, code, float(beta), r, oversample, power_iters,
+                                      float(tau), seed, _stream(stream)))
+
+
+def sc_correct_batched(items, r: int, alpha: float, dtype: torch.dtype = torch.bfloat16,
+                       stream=None):
+    """items: list of dicts with G, prior=(U, d, V), out (G_proj) and ws."""
+    arr = (ScMatrix * max(len(items), 1))()
+    keep = []
+    for i, it in enumerate(items):
+        G, (U, d, V), out, ws = _in(it["G"]), it["prior"], it["out"], it["ws"]
+        U, d, V = _in(U), _in(d), _in(V)
+        _need_cuda(G, U, d, V, out, ws)
+        _out(out)
+        keep += [G, U, d, V]
+        m, n = G.shape
+        arr[i] = ScMatrix(_p(G), None, m, n, _p(U), _p(d), _p(V), _p(d), None, _p(out), _p(ws),
+                          ws.numel())
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(lib.sc_correct_batched(len(items), arr, code, r, float(alpha), _stream(stream)))

@@ -9,6 +9,7 @@
 #include "common.h"
 
 #include <algorithm>
+#include <vector>
 
 namespace acsc {
 namespace {
@@ -20,11 +21,22 @@ constexpr int kKMax = SC_KMAX;
 constexpr int kBM = 64;   // rows of the output per workgroup in the tall GEMM
 constexpr int kBK = 32;   // depth of one K step
 constexpr int kNTMax = kKMax / 16;
+// Rows of a Jacobi column pair held by each of its 16 lanes.
+constexpr int kRowsPerLane = (kKMax + 15) / 16;
 // Singular values of the prior at or below this fraction of the largest are
 // returned as zero (numerical rank of an fp32 subspace iteration).
 constexpr double kRankCutoff = 1e-5;
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+
+// A launch works on up to kMaxBatch matrices: blockIdx.z selects the job,
+// whose pointers and sizes travel by value in the kernel arguments.
+constexpr int kMaxBatch = 16;
+template <class Job>
+struct Batch {
+    int count;
+    Job j[kMaxBatch];
+};
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------------------
@@ -72,12 +84,34 @@ struct GemmLds<float> {
     static constexpr int BPITCH = kBK + 1;
 };
 
+template <typename TA, typename TO>
+struct GemmJob {
+    const TA *A;
+    int64_t lda;
+    const float *B;
+    int64_t ldb;
+    TO *C;
+    int64_t ldc, split_stride;
+    int M, K, nvalid, nwrite, kchunk, splits;
+    uint16_t *Ct16;
+    int64_t ldct;
+};
+
 template <typename TA, bool TRANS, typename TO>
-__global__ __launch_bounds__(256) void gemm_tall_kernel(const TA *A, int64_t lda, const float *B,
-                                                        int64_t ldb, TO *C, int64_t ldc,
-                                                        int64_t split_stride, int M, int K,
-                                                        int nvalid, int nwrite, int kchunk)
+__global__ __launch_bounds__(256) void gemm_tall_kernel(const Batch<GemmJob<TA, TO>> jb)
 {
+    const GemmJob<TA, TO> &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.y) >= J.splits || static_cast<int>(blockIdx.x) * kBM >= J.M)
+        return;
+    const TA *A = J.A;
+    const int64_t lda = J.lda;
+    const float *B = J.B;
+    const int64_t ldb = J.ldb;
+    TO *C = J.C;
+    const int64_t ldc = J.ldc, split_stride = J.split_stride;
+    const int M = J.M, K = J.K, nvalid = J.nvalid, nwrite = J.nwrite, kchunk = J.kchunk;
+    uint16_t *Ct16 = J.Ct16;
+    const int64_t ldct = J.ldct;
     using L = GemmLds<TA>;
     __shared__ __attribute__((aligned(16))) TA As[kBM * L::APITCH];
     __shared__ __attribute__((aligned(16))) TA Bs[kKMax * L::BPITCH];
@@ -168,19 +202,339 @@ __global__ __launch_bounds__(256) void gemm_tall_kernel(const TA *A, int64_t lda
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int row = row0 + wave * 16 + (lane >> 4) * 4 + e;
-                if (row < M && col < nwrite)
+                if (row < M && col < nwrite) {
                     Cs[static_cast<int64_t>(row) * ldc + col] = from_f32<TO>(acc[t][e]);
+                    if (Ct16)
+                        Ct16[static_cast<int64_t>(col) * ldct + row] = f32_to_bf16(acc[t][e]);
+                }
             }
         }
     }
 }
 
+// ---------------------------------------------------------------------------
+// Streaming pass over a large bf16 matrix with a thin right factor:
+//   C[s][i, c] = sum_{k in split s} opA[i, k] * B[k, c],   c < NP (<= SC_KMAX)
+// opA = A ([M, K] row-major, lda) or A^T (A stored [K, M], lda).  The thin
+// factor comes transposed and in bf16, Bt[c][k] (row stride ldbt, a multiple
+// of 8), so both tiles load as 16-byte chunks that go straight into LDS rows
+// with k contiguous, as v_mfma_f32_16x16x32_bf16 reads them.  BM rows per
+// workgroup (4 waves of BM/4 rows), 64-deep K steps, the next step's tiles
+// loaded into registers while the current one is multiplied.  Block b works
+// on split b % splits: workgroups are dealt to the XCDs round-robin, so with
+// splits a power of two up to 8 every XCD keeps to one slice of Bt in its L2.
+// ---------------------------------------------------------------------------
+constexpr int kPBK = 64;
+constexpr int kPPitch = kPBK + 8;   // 144-byte LDS rows: 16-byte aligned, staggered banks
+constexpr int kPBChunks = (kKMax * (kPBK / 8) + 255) / 256;
+
+struct PassJob {
+    const uint16_t *A;
+    int64_t lda;
+    const uint16_t *Bt;
+    int64_t ldbt;
+    float *C;
+    int64_t ldc, split_stride;
+    int M, K, NP, kchunk, splits, avec, nblocks;
+};
+
+template <bool TRANS, int BM>
+__global__ __launch_bounds__(256) void pass_kernel(const Batch<PassJob> jb)
+{
+    const PassJob &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.x) >= J.nblocks)
+        return;
+    const uint16_t *__restrict__ A = J.A;
+    const int64_t lda = J.lda;
+    const uint16_t *__restrict__ Bt = J.Bt;
+    const int64_t ldbt = J.ldbt;
+    float *__restrict__ C = J.C;
+    const int64_t ldc = J.ldc, split_stride = J.split_stride;
+    const int M = J.M, K = J.K, NP = J.NP, kchunk = J.kchunk, splits = J.splits, avec = J.avec;
+    constexpr int RT = BM / 64;                    // 16-row MFMA tiles per wave
+    constexpr int ACH = BM * (kPBK / 8) / 256;     // 16-byte A chunks per thread
+    // A^T tiles stay in their loaded [k][i] order (row pitch BM + 4: 8-byte
+    // aligned rows, conflict-free column reads); A tiles are [i][k].
+    constexpr int TPITCH = BM + 4;
+    __shared__ __attribute__((aligned(16))) uint16_t As[TRANS ? kPBK * TPITCH : BM * kPPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[kKMax * kPPitch];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int split = static_cast<int>(blockIdx.x % splits);
+    const int row0 = static_cast<int>(blockIdx.x / splits) * BM;
+    const int kbeg = split * kchunk;
+    const int kend = min(K, kbeg + kchunk);
+    const int NT = NP / 16;
+    const int nbch = NP * (kPBK / 8);
+
+    f32x4 acc[RT][kNTMax];
+#pragma unroll
+    for (int a = 0; a < RT; ++a)
+#pragma unroll
+        for (int t = 0; t < kNTMax; ++t)
+            acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    uint4 ra[ACH];
+    uint4 rb[kPBChunks];
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int j = 0; j < ACH; ++j) {
+            const int q = tid + 256 * j;
+            int gi, gk;
+            if (!TRANS) {
+                gi = row0 + q / (kPBK / 8);
+                gk = k0 + (q % (kPBK / 8)) * 8;
+            } else {
+                gk = k0 + q / (BM / 8);
+                gi = row0 + (q % (BM / 8)) * 8;
+            }
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (!TRANS) {
+                if (gi < M) {
+                    const uint16_t *src = A + static_cast<int64_t>(gi) * lda + gk;
+                    if (avec && gk + 8 <= kend) {
+                        v = *reinterpret_cast<const uint4 *>(src);
+                    } else {
+                        uint16_t e8[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            e8[e] = (gk + e < kend) ? src[e] : uint16_t(0);
+                        v = *reinterpret_cast<const uint4 *>(e8);
+                    }
+                }
+            } else {
+                if (gk < kend) {
+                    const uint16_t *src = A + static_cast<int64_t>(gk) * lda + gi;
+                    if (avec && gi + 8 <= M) {
+                        v = *reinterpret_cast<const uint4 *>(src);
+                    } else {
+                        uint16_t e8[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            e8[e] = (gi + e < M) ? src[e] : uint16_t(0);
+                        v = *reinterpret_cast<const uint4 *>(e8);
+                    }
+                }
+            }
+            ra[j] = v;
+        }
+#pragma unroll
+        for (int j = 0; j < kPBChunks; ++j) {
+            const int q = tid + 256 * j;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (q < nbch) {
+                const int c = q / (kPBK / 8);
+                const int gk = k0 + (q % (kPBK / 8)) * 8;
+                const uint16_t *src = Bt + static_cast<int64_t>(c) * ldbt + gk;
+                if (gk + 8 <= kend) {
+                    v = *reinterpret_cast<const uint4 *>(src);
+                } else {
+                    uint16_t e8[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        e8[e] = (gk + e < kend) ? src[e] : uint16_t(0);
+                    v = *reinterpret_cast<const uint4 *>(e8);
+                }
+            }
+            rb[j] = v;
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int j = 0; j < ACH; ++j) {
+            const int q = tid + 256 * j;
+            if (!TRANS) {
+                const int r = q / (kPBK / 8), c8 = (q % (kPBK / 8)) * 8;
+                *reinterpret_cast<uint4 *>(&As[r * kPPitch + c8]) = ra[j];
+            } else {
+                const int kk = q / (BM / 8), i8 = (q % (BM / 8)) * 8;
+                uint2 *dst = reinterpret_cast<uint2 *>(&As[kk * TPITCH + i8]);
+                dst[0] = make_uint2(ra[j].x, ra[j].y);
+                dst[1] = make_uint2(ra[j].z, ra[j].w);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kPBChunks; ++j) {
+            const int q = tid + 256 * j;
+            if (q < nbch) {
+                const int c = q / (kPBK / 8), k8 = (q % (kPBK / 8)) * 8;
+                *reinterpret_cast<uint4 *>(&Bs[c * kPPitch + k8]) = rb[j];
+            }
+        }
+    };
+
+    if (kbeg < kend)
+        load(kbeg);
+    for (int k0 = kbeg; k0 < kend; k0 += kPBK) {
+        __syncthreads();
+        store();
+        __syncthreads();
+        if (k0 + kPBK < kend)
+            load(k0 + kPBK);
+#pragma unroll
+        for (int ks = 0; ks < kPBK / 32; ++ks) {
+            bf16x8 af[RT];
+#pragma unroll
+            for (int a = 0; a < RT; ++a) {
+                const int ii = wave * RT * 16 + a * 16 + (lane & 15);
+                if (!TRANS) {
+                    af[a] = *reinterpret_cast<const bf16x8 *>(&As[ii * kPPitch + ks * 32 + (lane >> 4) * 8]);
+                } else {
+                    const uint16_t *col = &As[(ks * 32 + (lane >> 4) * 8) * TPITCH + ii];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        af[a][e] = static_cast<short>(col[e * TPITCH]);
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < kNTMax; ++t) {
+                if (t < NT) {
+                    const bf16x8 b = *reinterpret_cast<const bf16x8 *>(
+                        &Bs[(t * 16 + (lane & 15)) * kPPitch + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+                    for (int a = 0; a < RT; ++a)
+                        acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b, acc[a][t], 0, 0, 0);
+                }
+            }
+        }
+    }
+    float *Cs = C + static_cast<int64_t>(split) * split_stride;
+#pragma unroll
+    for (int a = 0; a < RT; ++a)
+#pragma unroll
+        for (int t = 0; t < kNTMax; ++t) {
+            if (t < NT) {
+                const int col = t * 16 + (lane & 15);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int row = row0 + wave * RT * 16 + a * 16 + (lane >> 4) * 4 + e;
+                    if (row < M)
+                        Cs[static_cast<int64_t>(row) * ldc + col] = acc[a][t][e];
+                }
+            }
+        }
+}
+
+// Anchor EMA with a bf16 shadow for the streaming passes (one thread per 8
+// consecutive elements of a row; 16-byte accesses when rows are aligned):
+//   M <- beta * M + (1 - beta) * G;  M16 <- bf16(M).   With G == NULL only the
+// shadow is written.
+template <typename GT>
+struct EmaJob {
+    float *M;
+    const GT *G;
+    int m, n, vec;
+    uint16_t *M16;
+    int64_t ld16;
+};
+
+template <typename GT>
+__global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>> jb, float beta, float omb)
+{
+    const EmaJob<GT> &J = jb.j[blockIdx.z];
+    float *M = J.M;
+    const GT *G = J.G;
+    const int m = J.m, n = J.n;
+    const bool VEC = J.vec != 0;
+    uint16_t *M16 = J.M16;
+    const int64_t ld16 = J.ld16;
+    const int nch = (n + 7) / 8;
+    const int64_t total = static_cast<int64_t>(m) * nch;
+    for (int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; q < total;
+         q += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t i = q / nch;
+        const int j0 = static_cast<int>(q - i * nch) * 8;
+        float *mr = M + i * n + j0;
+        const GT *gr = G ? G + i * n + j0 : nullptr;
+        float v[8];
+        if (VEC && j0 + 8 <= n) {
+            const float4 m0 = *reinterpret_cast<const float4 *>(mr);
+            const float4 m1 = *reinterpret_cast<const float4 *>(mr + 4);
+            v[0] = m0.x; v[1] = m0.y; v[2] = m0.z; v[3] = m0.w;
+            v[4] = m1.x; v[5] = m1.y; v[6] = m1.z; v[7] = m1.w;
+            if (gr) {
+                float g[8];
+                if constexpr (sizeof(GT) == 2) {
+                    const uint4 gb = *reinterpret_cast<const uint4 *>(gr);
+                    const uint32_t w4[4] = {gb.x, gb.y, gb.z, gb.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        g[2 * e] = __uint_as_float(w4[e] << 16);
+                        g[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
+                    }
+                } else {
+                    const float4 g0 = *reinterpret_cast<const float4 *>(gr);
+                    const float4 g1 = *reinterpret_cast<const float4 *>(gr + 4);
+                    g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
+                    g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    v[e] = beta * v[e] + omb * g[e];
+                *reinterpret_cast<float4 *>(mr) = make_float4(v[0], v[1], v[2], v[3]);
+                *reinterpret_cast<float4 *>(mr + 4) = make_float4(v[4], v[5], v[6], v[7]);
+            }
+            uint16_t h[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                h[e] = f32_to_bf16(v[e]);
+            *reinterpret_cast<uint4 *>(M16 + i * ld16 + j0) = *reinterpret_cast<const uint4 *>(h);
+        } else {
+            for (int e = 0; e < 8 && j0 + e < n; ++e) {
+                float x = mr[e];
+                if (gr) {
+                    x = beta * x + omb * to_f32<GT>(gr[e]);
+                    mr[e] = x;
+                }
+                M16[i * ld16 + j0 + e] = f32_to_bf16(x);
+            }
+        }
+    }
+}
+
+// Xt[c][i] = bf16(X[i][c]) for c < cols (zero for cols <= c < CP), i < rows;
+// Xt has row stride ldt.
+struct TrJob {
+    const float *X;
+    int64_t ldx;
+    int rows, cols, CP;
+    uint16_t *Xt;
+    int64_t ldt;
+};
+
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const Batch<TrJob> jb)
+{
+    const TrJob &J = jb.j[blockIdx.z];
+    const float *X = J.X;
+    const int64_t ldx = J.ldx, ldt = J.ldt;
+    const int rows = J.rows, cols = J.cols, CP = J.CP;
+    uint16_t *Xt = J.Xt;
+    const int64_t total = static_cast<int64_t>(CP) * rows;
+    for (int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; q < total;
+         q += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int c = static_cast<int>(q / rows);
+        const int64_t i = q - static_cast<int64_t>(c) * rows;
+        Xt[static_cast<int64_t>(c) * ldt + i] = c < cols ? f32_to_bf16(X[i * ldx + c]) : uint16_t(0);
+    }
+}
+
 // C[i, c] = sum_s P[s][i, c] for c < nwrite (P has row stride ldp).
 template <typename TO>
-__global__ __launch_bounds__(256) void reduce_splits_kernel(const float *P, int64_t ldp,
-                                                            int64_t split_stride, int splits,
-                                                            int M, int nwrite, TO *C, int64_t ldc)
+struct ReduceJob {
+    const float *P;
+    int64_t ldp, split_stride;
+    int splits, M, nwrite;
+    TO *C;
+    int64_t ldc;
+};
+
+template <typename TO>
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const Batch<ReduceJob<TO>> jb)
 {
+    const ReduceJob<TO> &J = jb.j[blockIdx.z];
+    const float *P = J.P;
+    const int64_t ldp = J.ldp, split_stride = J.split_stride, ldc = J.ldc;
+    const int splits = J.splits, M = J.M, nwrite = J.nwrite;
+    TO *C = J.C;
     const int64_t total = static_cast<int64_t>(M) * nwrite;
     for (int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
          idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
@@ -201,10 +555,22 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float *P, int6
 constexpr int kGT = 64;
 constexpr int kGRows = 32;
 
-__global__ __launch_bounds__(256) void gram_partial_kernel(const float *A, int64_t lda, int rows,
-                                                           int KP, int rows_per_block,
-                                                           double *part)
+struct GramJob {
+    const float *A;
+    int64_t lda;
+    int rows, rows_per_block, blocks;
+    double *part;
+};
+
+__global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> jb, int KP)
 {
+    const GramJob &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.y) >= J.blocks)
+        return;
+    const float *A = J.A;
+    const int64_t lda = J.lda;
+    const int rows = J.rows, rows_per_block = J.rows_per_block;
+    double *part = J.part;
     __shared__ float Ai[kGRows][kGT + 1];
     __shared__ float Aj[kGRows][kGT + 1];
     const int nt = static_cast<int>(cdiv(KP, kGT));
@@ -262,9 +628,18 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const float *A, int64
     }
 }
 
-__global__ __launch_bounds__(256) void gram_reduce_kernel(const double *part, int blocks, int KP,
-                                                          double *G)
+struct GramRedJob {
+    const double *part;
+    int blocks;
+    double *G;
+};
+
+__global__ __launch_bounds__(256) void gram_reduce_kernel(const Batch<GramRedJob> jb, int KP)
 {
+    const GramRedJob &J = jb.j[blockIdx.z];
+    const double *part = J.part;
+    const int blocks = J.blocks;
+    double *G = J.G;
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= KP * KP)
         return;
@@ -282,88 +657,113 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const double *part, in
 
 // ---------------------------------------------------------------------------
 // Cholesky G = L L^T of a k x k Gram matrix in LDS (fp64, packed lower
-// triangle), one workgroup.  Pivots below tiny * max(diag) are taken as zero
-// (the column of L becomes zero: a rank-deficient block).
-//   INVERT: write T = L^{-T} (k x k, fp32, zero-padded to KP x KP) so that
-//           Q = Y T has orthonormal columns (CholeskyQR).
-//   else:   write L itself (fp64, KP x KP, zero upper part).
+// triangle), one workgroup of 32 x 32 threads, one barrier per column:
+// right-looking elimination on the unscaled columns (a_ic -= a_ij a_cj / d_j),
+// scaled at the end (l_ij = a_ij / sqrt(d_j)).  Pivots d_j at or below
+// 1e-15 * k * max(diag) are taken as zero: that column of L is zero (a
+// rank-deficient block).
+//   INVERT: then X = L^{-1} in place (right-looking forward elimination, one
+//           barrier per row) and T = X^T (fp32, zero-padded to KP x KP), so
+//           that Q = Y T has orthonormal columns (CholeskyQR).
+//   else:   write L itself (fp64, KP x KP, zero upper part) over G.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int tri(int i) { return i * (i + 1) / 2; }
 
+struct CholJob {
+    double *G;
+    float *Tout;
+};
+
 template <bool INVERT>
-__global__ __launch_bounds__(1024) void chol_kernel(double *G, int k, int KP, float *Tout)
+__global__ __launch_bounds__(1024) void chol_kernel(const Batch<CholJob> jb, int k, int KP)
 {
+    double *G = jb.j[blockIdx.z].G;
+    float *Tout = jb.j[blockIdx.z].Tout;
     extern __shared__ double Lp[];
-    double *tmp = Lp + tri(k);
-    __shared__ double sh_max;
+    double *buf0 = Lp + tri(k);
+    double *buf1 = buf0 + k;
+    __shared__ double sh_thresh;
     const int tid = threadIdx.x;
-    const int nth = blockDim.x;
-    for (int idx = tid; idx < k * k; idx += nth) {
-        const int i = idx / k, j = idx % k;
-        if (j <= i)
-            Lp[tri(i) + j] = G[static_cast<int64_t>(i) * KP + j];
-    }
+    const int tx = tid & 31, ty = tid >> 5;
+    for (int i = ty; i < k; i += 32)
+        for (int c = tx; c <= i; c += 32)
+            Lp[tri(i) + c] = G[static_cast<int64_t>(i) * KP + c];
     __syncthreads();
     if (tid == 0) {
         double mx = 0.0;
         for (int i = 0; i < k; ++i)
             mx = fmax(mx, Lp[tri(i) + i]);
-        sh_max = mx;
+        sh_thresh = 1e-15 * k * mx;
     }
     __syncthreads();
-    const double thresh = 1e-15 * sh_max * k;
+    const double thresh = sh_thresh;
     for (int j = 0; j < k; ++j) {
-        if (tid == 0) {
-            const double dj = Lp[tri(j) + j];
-            Lp[tri(j) + j] = (dj > thresh) ? sqrt(dj) : 0.0;
-        }
-        __syncthreads();
-        const double piv = Lp[tri(j) + j];
-        const double inv = piv > 0.0 ? 1.0 / piv : 0.0;
-        for (int i = j + 1 + tid; i < k; i += nth)
-            Lp[tri(i) + j] *= inv;
-        __syncthreads();
-        const int w = k - j - 1;
-        for (int p = tid; p < w * w; p += nth) {
-            const int i = j + 1 + p / w;
-            const int c = j + 1 + p % w;
-            if (c <= i)
-                Lp[tri(i) + c] -= Lp[tri(i) + j] * Lp[tri(c) + j];
+        const double dj = Lp[tri(j) + j];
+        if (dj > thresh) {
+            const double inv = 1.0 / dj;
+            for (int i = j + 1 + ty; i < k; i += 32) {
+                const double aij = Lp[tri(i) + j] * inv;
+                for (int c = j + 1 + tx; c <= i; c += 32)
+                    Lp[tri(i) + c] -= aij * Lp[tri(c) + j];
+            }
         }
         __syncthreads();
     }
-    if (INVERT) {
-        // in-place inverse of the lower-triangular factor, last column first
-        for (int j = k - 1; j >= 0; --j) {
-            const double ljj = Lp[tri(j) + j];
-            const double ij = ljj > 0.0 ? 1.0 / ljj : 0.0;
-            for (int i = j + 1 + tid; i < k; i += nth)
-                tmp[i] = Lp[tri(i) + j];
-            __syncthreads();
-            for (int i = j + 1 + tid; i < k; i += nth) {
-                double s = 0.0;
-                for (int c = j + 1; c <= i; ++c)
-                    s += Lp[tri(i) + c] * tmp[c];
-                Lp[tri(i) + j] = -ij * s;
-            }
-            __syncthreads();
-            if (tid == 0)
-                Lp[tri(j) + j] = ij;
-            __syncthreads();
-        }
-        // T[c][i] = Linv[i][c]
-        for (int idx = tid; idx < KP * KP; idx += nth) {
-            const int c = idx / KP, i = idx % KP;
-            float v = 0.f;
-            if (i < k && c < k && c <= i)
-                v = static_cast<float>(Lp[tri(i) + c]);
-            Tout[idx] = v;
-        }
-    } else {
-        for (int idx = tid; idx < KP * KP; idx += nth) {
+    for (int j = tid; j < k; j += 1024) {
+        const double dj = Lp[tri(j) + j];
+        buf0[j] = dj > thresh ? 1.0 / sqrt(dj) : 0.0;
+    }
+    __syncthreads();
+    for (int i = ty; i < k; i += 32)
+        for (int c = tx; c <= i; c += 32)
+            Lp[tri(i) + c] = (i == c) ? (buf0[c] > 0.0 ? 1.0 / buf0[c] : 0.0) : Lp[tri(i) + c] * buf0[c];
+    __syncthreads();
+    if (!INVERT) {
+        for (int idx = tid; idx < KP * KP; idx += 1024) {
             const int i = idx / KP, c = idx % KP;
             G[idx] = (i < k && c < k && c <= i) ? Lp[tri(i) + c] : 0.0;
         }
+        return;
+    }
+    // X = L^{-1}:  row j of X is (e_j - sum_{c<j} L[j][c] X[c][:]) / L[j][j].
+    // Entries (i, c), c < i, hold L[i][c] until column c is consumed, then the
+    // running residual of row i; row j is final once scaled.
+    {
+        const double l00 = Lp[0];
+        for (int i = 1 + tid; i < k; i += 1024)
+            buf0[i] = Lp[tri(i)];
+        __syncthreads();
+        if (tid == 0)
+            Lp[0] = l00 > 0.0 ? 1.0 / l00 : 0.0;
+        __syncthreads();
+    }
+    for (int j = 0; j + 1 < k; ++j) {
+        double *cur = (j & 1) ? buf1 : buf0;
+        double *nxt = (j & 1) ? buf0 : buf1;
+        const double l1 = Lp[tri(j + 1) + j + 1];
+        const double inv1 = l1 > 0.0 ? 1.0 / l1 : 0.0;
+        for (int i = j + 1 + ty; i < k; i += 32) {
+            const double li = cur[i];
+            for (int c = tx; c <= j; c += 32) {
+                double v = (c == j ? 0.0 : Lp[tri(i) + c]) - li * Lp[tri(j) + c];
+                if (i == j + 1)
+                    v *= inv1;
+                Lp[tri(i) + c] = v;
+            }
+        }
+        for (int i = j + 2 + tid; i < k; i += 1024)
+            nxt[i] = Lp[tri(i) + j + 1];
+        if (tid == 0)
+            Lp[tri(j + 1) + j + 1] = inv1;
+        __syncthreads();
+    }
+    // T[c][i] = X[i][c]
+    for (int idx = tid; idx < KP * KP; idx += 1024) {
+        const int c = idx / KP, i = idx % KP;
+        float v = 0.f;
+        if (i < k && c < k && c <= i)
+            v = static_cast<float>(Lp[tri(i) + c]);
+        Tout[idx] = v;
     }
 }
 
@@ -375,12 +775,20 @@ __global__ __launch_bounds__(1024) void chol_kernel(double *G, int k, int KP, fl
 // products are written:  Bu[:, t] = u_(t), Bv[:, t] = u_(t) / sigma_(t),
 // s[t] = sigma_(t), d[t] = s / (s + tau) for t < r.
 // ---------------------------------------------------------------------------
+struct JacJob {
+    const double *Lf;
+    float *Bu, *Bv, *s_out, *d_out;
+    int *info;
+};
+
 template <typename T>
-__global__ __launch_bounds__(1024) void jacobi_kernel(const double *Lf, int k, int KP, int r,
-                                                      int RP, float tau, T tol, int max_sweeps,
-                                                      float *Bu, float *Bv, float *s_out,
-                                                      float *d_out)
+__global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, int k, int KP, int r,
+                                                      int RP, float tau, T tol, int max_sweeps)
 {
+    const JacJob &J = jb.j[blockIdx.z];
+    const double *Lf = J.Lf;
+    float *Bu = J.Bu, *Bv = J.Bv, *s_out = J.s_out, *d_out = J.d_out;
+    int *info = J.info;
     extern __shared__ __attribute__((aligned(16))) unsigned char jsm[];
     T *A = reinterpret_cast<T *>(jsm);   // column c at A[c * k]
     __shared__ unsigned int sh_off;
@@ -394,13 +802,18 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const double *Lf, int k, i
     }
     const int n2 = k + (k & 1);
     const int npairs = n2 / 2;
+    // four column pairs per wave, 16 lanes each
+    const int grp = lane >> 4, gl = lane & 15;
+    const int slots = nwave * 4;
+    int sweeps_used = 0;
+    float last_off = 0.f;
     for (int sweep = 0; sweep < max_sweeps; ++sweep) {
         if (tid == 0)
             sh_off = 0u;
         __syncthreads();
         float wmax = 0.f;
         for (int round = 0; round < n2 - 1; ++round) {
-            for (int p = wave; p < npairs; p += nwave) {
+            for (int p = wave * 4 + grp; p < npairs; p += slots) {
                 auto pos = [&](int x) { return x == 0 ? 0 : ((x - 1 + round) % (n2 - 1)) + 1; };
                 int cp = pos(p), cq = pos(n2 - 1 - p);
                 if (cp >= k || cq >= k)
@@ -412,18 +825,27 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const double *Lf, int k, i
                 }
                 T *ap = A + cp * k;
                 T *aq = A + cq * k;
+                // the pair's columns stay in registers: 16 lanes x kRowsPerLane rows
+                T xv[kRowsPerLane], yv[kRowsPerLane];
+#pragma unroll
+                for (int e = 0; e < kRowsPerLane; ++e) {
+                    const int i = gl + 16 * e;
+                    xv[e] = i < k ? ap[i] : T(0);
+                    yv[e] = i < k ? aq[i] : T(0);
+                }
                 double al = 0.0, be = 0.0, ga = 0.0;
-                for (int i = lane; i < k; i += 64) {
-                    const double x = ap[i], y = aq[i];
+#pragma unroll
+                for (int e = 0; e < kRowsPerLane; ++e) {
+                    const double x = xv[e], y = yv[e];
                     al += x * x;
                     be += y * y;
                     ga += x * y;
                 }
 #pragma unroll
-                for (int off = 32; off >= 1; off >>= 1) {
-                    al += __shfl_xor(al, off, 64);
-                    be += __shfl_xor(be, off, 64);
-                    ga += __shfl_xor(ga, off, 64);
+                for (int off = 8; off >= 1; off >>= 1) {
+                    al += __shfl_xor(al, off, 16);
+                    be += __shfl_xor(be, off, 16);
+                    ga += __shfl_xor(ga, off, 16);
                 }
                 const double nrm = sqrt(al * be);
                 if (ga == 0.0 || nrm == 0.0)
@@ -436,21 +858,35 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const double *Lf, int k, i
                 const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
                 const double c = 1.0 / sqrt(1.0 + t * t);
                 const double sn = c * t;
-                for (int i = lane; i < k; i += 64) {
-                    const double x = ap[i], y = aq[i];
-                    ap[i] = static_cast<T>(c * x - sn * y);
-                    aq[i] = static_cast<T>(sn * x + c * y);
+#pragma unroll
+                for (int e = 0; e < kRowsPerLane; ++e) {
+                    const int i = gl + 16 * e;
+                    if (i < k) {
+                        const double x = xv[e], y = yv[e];
+                        ap[i] = static_cast<T>(c * x - sn * y);
+                        aq[i] = static_cast<T>(sn * x + c * y);
+                    }
                 }
             }
             __syncthreads();
         }
+        // reduce the sweep's largest off-diagonal ratio over the workgroup
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1)
+            wmax = fmaxf(wmax, __shfl_xor(wmax, off, 64));
         if (lane == 0)
             atomicMax(&sh_off, __float_as_uint(wmax));
         __syncthreads();
         const float off = __uint_as_float(sh_off);
         __syncthreads();
+        sweeps_used = sweep + 1;
+        last_off = off;
         if (off <= static_cast<float>(tol))
             break;
+    }
+    if (tid == 0 && info) {
+        info[0] = sweeps_used;
+        info[1] = __float_as_int(last_off);
     }
     // norms (one wave per column)
     for (int c = wave; c < k; c += nwave) {
@@ -517,9 +953,20 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const double *Lf, int k, i
 // ---------------------------------------------------------------------------
 // M <- beta * M + (1 - beta) * G  (fp32 state)
 template <typename GT>
-__global__ __launch_bounds__(256) void ema_kernel(float *M, const GT *G, int64_t count, float beta,
-                                                  float omb)
+struct Ema32Job {
+    float *M;
+    const GT *G;
+    int64_t count;
+};
+
+template <typename GT>
+__global__ __launch_bounds__(256) void ema_kernel(const Batch<Ema32Job<GT>> jb, float beta, float omb)
 {
+    float *M = jb.j[blockIdx.z].M;
+    const GT *G = jb.j[blockIdx.z].G;
+    const int64_t count = jb.j[blockIdx.z].count;
+    if (!G)
+        return;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x * 4;
     for (int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 4; i < count;
          i += stride) {
@@ -554,9 +1001,20 @@ __global__ __launch_bounds__(256) void ema_kernel(float *M, const GT *G, int64_t
 // Starting block Z0 [n, KP]: V_warm columns first (if given), then uniform
 // random values in [-1, 1) from a counter-based hash of (seed, i, c); zero
 // beyond k.
-__global__ __launch_bounds__(256) void init_block_kernel(float *Z, int n, int k, int KP,
-                                                         const float *Vw, int rw, uint64_t seed)
+struct InitJob {
+    float *Z;
+    int n;
+    const float *Vw;
+    uint64_t seed;
+};
+
+__global__ __launch_bounds__(256) void init_block_kernel(const Batch<InitJob> jb, int k, int KP, int r)
 {
+    float *Z = jb.j[blockIdx.z].Z;
+    const int n = jb.j[blockIdx.z].n;
+    const float *Vw = jb.j[blockIdx.z].Vw;
+    const int rw = Vw ? r : 0;
+    const uint64_t seed = jb.j[blockIdx.z].seed;
     const int64_t total = static_cast<int64_t>(n) * KP;
     for (int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
          idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
@@ -579,9 +1037,18 @@ __global__ __launch_bounds__(256) void init_block_kernel(float *Z, int n, int k,
 }
 
 // Xf[i][j] = d_i * X[i][j] * d_j for i, j < r; zero elsewhere (RP x RP).
-__global__ __launch_bounds__(256) void filter_x_kernel(const float *X, int64_t ldx, const float *d,
-                                                       int r, int RP, float *Xf)
+struct FilterJob {
+    const float *X;
+    const float *d;
+    float *Xf;
+};
+
+__global__ __launch_bounds__(256) void filter_x_kernel(const Batch<FilterJob> jb, int r, int RP)
 {
+    const float *X = jb.j[blockIdx.z].X;
+    const float *d = jb.j[blockIdx.z].d;
+    float *Xf = jb.j[blockIdx.z].Xf;
+    const int64_t ldx = RP;
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= RP * RP)
         return;
@@ -591,9 +1058,18 @@ __global__ __launch_bounds__(256) void filter_x_kernel(const float *X, int64_t l
 
 // Vc[i][c] = V[i][c] for c < r, zero up to RP, converted to the compute type.
 template <typename CT>
-__global__ __launch_bounds__(256) void pad_convert_kernel(const float *V, int n, int r, int RP,
-                                                          CT *Vc)
+struct PadJob {
+    const float *V;
+    int n;
+    CT *Vc;
+};
+
+template <typename CT>
+__global__ __launch_bounds__(256) void pad_convert_kernel(const Batch<PadJob<CT>> jb, int r, int RP)
 {
+    const float *V = jb.j[blockIdx.z].V;
+    const int n = jb.j[blockIdx.z].n;
+    CT *Vc = jb.j[blockIdx.z].Vc;
     const int64_t total = static_cast<int64_t>(n) * RP;
     for (int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
          idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
@@ -609,9 +1085,23 @@ __global__ __launch_bounds__(256) void pad_convert_kernel(const float *V, int n,
 // 32, zero padded).  Four waves, each a 32 x 32 quarter of the tile.
 // ---------------------------------------------------------------------------
 template <typename GT>
-__global__ __launch_bounds__(256) void blend_kernel(const GT *G, GT *out, int m, int n, const GT *P,
-                                                    const GT *Vc, int RP, float alpha)
+struct BlendJob {
+    const GT *G;
+    GT *out;
+    int m, n;
+    const GT *P, *Vc;
+};
+
+template <typename GT>
+__global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb, int RP, float alpha)
 {
+    const BlendJob<GT> &J = jb.j[blockIdx.z];
+    const GT *G = J.G;
+    GT *out = J.out;
+    const int m = J.m, n = J.n;
+    const GT *P = J.P, *Vc = J.Vc;
+    if (static_cast<int>(blockIdx.x) * 64 >= n || static_cast<int>(blockIdx.y) * 64 >= m)
+        return;
     extern __shared__ __attribute__((aligned(16))) unsigned char bsm[];
     constexpr int PAD = sizeof(GT) == 2 ? 8 : 1;
     const int pitch = RP + PAD;
@@ -683,6 +1173,128 @@ __global__ __launch_bounds__(256) void blend_kernel(const GT *G, GT *out, int m,
 }
 
 // ---------------------------------------------------------------------------
+// Fused correction pass for bf16 G, 128 x 128 output tiles:
+//   out = alpha * G + (1 - alpha) * P V^T,  P [m, RP], Vc [n, RP] (bf16, RP a
+// multiple of 32, zero padded).
+// The G tile is staged in LDS with 16-byte coalesced loads issued before the
+// products, blended in place in LDS, and written back with 16-byte coalesced
+// stores.  P and V stream through LDS in 32-deep slices.  Four waves, each a
+// 64 x 64 quarter (4 x 4 MFMA tiles).  Tile order: block b runs on XCD b % 8,
+// and XCD x takes the row blocks congruent to x, walking their column blocks,
+// so a row block's slice of P stays in one L2.
+// ---------------------------------------------------------------------------
+constexpr int kBT = 128;              // tile edge
+constexpr int kGPitch = kBT + 8;      // bf16 elements per staged G row (272 bytes)
+constexpr int kKPitch = 32 + 8;       // P / V slice rows (80 bytes)
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint16_t>> jb, int RP, float alpha,
+                                                      int col_blocks_max)
+{
+    const BlendJob<uint16_t> &J = jb.j[blockIdx.z];
+    const int m = J.m, n = J.n;
+    const int rb_n = (m + kBT - 1) / kBT, cb_n = (n + kBT - 1) / kBT;
+    // XCD-aware tile order
+    const int b = blockIdx.x;
+    const int xcd = b & 7, t = b >> 3;
+    const int rb = xcd + 8 * (t / cb_n);
+    const int cb = t % cb_n;
+    (void)col_blocks_max;
+    if (rb >= rb_n)
+        return;
+    const int row0 = rb * kBT, col0 = cb * kBT;
+    __shared__ __attribute__((aligned(16))) uint16_t Gs[kBT * kGPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t Ps[kBT * kKPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[kBT * kKPitch];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint16_t *G = J.G;
+    uint16_t *out = J.out;
+    // stage G: 128 rows x 16 chunks of 8
+    for (int q = tid; q < kBT * (kBT / 8); q += 256) {
+        const int rr = q >> 4, c8 = (q & 15) * 8;
+        const int gi = row0 + rr, gj = col0 + c8;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (gi < m) {
+            const uint16_t *src = G + static_cast<int64_t>(gi) * n + gj;
+            if (VEC && gj + 8 <= n) {
+                v = *reinterpret_cast<const uint4 *>(src);
+            } else {
+                uint16_t e8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    e8[e] = (gj + e < n) ? src[e] : uint16_t(0);
+                v = *reinterpret_cast<const uint4 *>(e8);
+            }
+        }
+        *reinterpret_cast<uint4 *>(&Gs[rr * kGPitch + c8]) = v;
+    }
+    const int wr = wave >> 1, wc = wave & 1;
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < RP; k0 += 32) {
+        __syncthreads();
+        // P and V slices: 128 rows x 4 chunks each
+        for (int q = tid; q < 2 * kBT * 4; q += 256) {
+            const bool isV = q >= kBT * 4;
+            const int qq = isV ? q - kBT * 4 : q;
+            const int rr = qq >> 2, c8 = (qq & 3) * 8;
+            const int g = (isV ? col0 : row0) + rr;
+            const int lim = isV ? n : m;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (g < lim)
+                v = *reinterpret_cast<const uint4 *>((isV ? J.Vc : J.P) + static_cast<int64_t>(g) * RP + k0 + c8);
+            *reinterpret_cast<uint4 *>(&(isV ? Vs : Ps)[rr * kKPitch + c8]) = v;
+        }
+        __syncthreads();
+        bf16x8 af[4], bfr[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+            af[a] = *reinterpret_cast<const bf16x8 *>(&Ps[(wr * 64 + a * 16 + (lane & 15)) * kKPitch + (lane >> 4) * 8]);
+            bfr[a] = *reinterpret_cast<const bf16x8 *>(&Vs[(wc * 64 + a * 16 + (lane & 15)) * kKPitch + (lane >> 4) * 8]);
+        }
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                acc[a][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[c], acc[a][c], 0, 0, 0);
+    }
+    // blend in place in the staged tile
+    const float oma = 1.0f - alpha;
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int cc = wc * 64 + c * 16 + (lane & 15);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int rr = wr * 64 + a * 16 + (lane >> 4) * 4 + e;
+                uint16_t &gv = Gs[rr * kGPitch + cc];
+                gv = f32_to_bf16(alpha * bf16_to_f32(gv) + oma * acc[a][c][e]);
+            }
+        }
+    __syncthreads();
+    for (int q = tid; q < kBT * (kBT / 8); q += 256) {
+        const int rr = q >> 4, c8 = (q & 15) * 8;
+        const int gi = row0 + rr, gj = col0 + c8;
+        if (gi >= m)
+            continue;
+        uint16_t *dst = out + static_cast<int64_t>(gi) * n + gj;
+        const uint4 v = *reinterpret_cast<const uint4 *>(&Gs[rr * kGPitch + c8]);
+        if (VEC && gj + 8 <= n) {
+            *reinterpret_cast<uint4 *>(dst) = v;
+        } else {
+            const uint16_t *e8 = reinterpret_cast<const uint16_t *>(&v);
+            for (int e = 0; e < 8 && gj + e < n; ++e)
+                dst[e] = e8[e];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
 struct Carve {
@@ -709,6 +1321,22 @@ int split_count(int64_t Mdim, int64_t Kdim)
 
 int64_t split_chunk(int64_t Kdim, int splits) { return round_up(cdiv(Kdim, splits), kBK); }
 
+constexpr int kPassBM = 128;
+
+// Splits of the K range for a streaming pass: a power of two up to 8 (so the
+// round-robin XCD placement keeps each split on its own XCDs), enough to give
+// the chip about two workgroups per CU, and at least 512 of K per split.
+int pass_splits(int64_t Mdim, int64_t Kdim)
+{
+    const int64_t mb = cdiv(Mdim, kPassBM);
+    int s = 1;
+    while (s < 8 && mb * s < 512 && Kdim / (2 * s) >= 512)
+        s *= 2;
+    return s;
+}
+
+int64_t pass_chunk(int64_t Kdim, int splits) { return round_up(cdiv(Kdim, splits), kPBK); }
+
 int gram_blocks(int64_t rows) { return static_cast<int>(std::min<int64_t>(64, cdiv(rows, 512))); }
 
 struct Dims {
@@ -729,17 +1357,31 @@ Dims dims_of(int m, int n, int r, int oversample)
 
 // Buffers of sc_build_prior (carved in this order).
 struct PriorWs {
+    int *info;   // [0] Jacobi sweeps used, [1] last sweep's largest off-diagonal ratio (float bits)
     float *Y, *Z, *part, *T, *Bu, *Bv;
     double *gpart, *gram;
+    uint16_t *M16, *Yt16, *Zt16;   // bf16 path: shadow of M, transposed thin factors
+    int64_t ld16, ldy16, ldz16;
 };
 
-size_t carve_prior(const Dims &d, void *base, PriorWs *w)
+size_t carve_prior(const Dims &d, bool use16, void *base, PriorWs *w)
 {
     Carve c(base);
     const int64_t mx = std::max(d.m, d.n);
-    const int s1 = split_count(d.m, d.n), s2 = split_count(d.n, d.m);
-    const int64_t part = std::max<int64_t>(static_cast<int64_t>(s1) * d.m, static_cast<int64_t>(s2) * d.n) * d.KP;
+    int64_t s1 = split_count(d.m, d.n), s2 = split_count(d.n, d.m);
+    if (use16) {
+        s1 = std::max<int64_t>(s1, pass_splits(d.m, d.n));
+        s2 = std::max<int64_t>(s2, pass_splits(d.n, d.m));
+    }
+    const int64_t part = std::max<int64_t>(s1 * d.m, s2 * d.n) * d.KP;
     PriorWs t;
+    t.info = c.take<int>(64);
+    t.ld16 = round_up(d.n, 8);
+    t.ldy16 = round_up(d.m, 8);
+    t.ldz16 = round_up(d.n, 8);
+    t.M16 = use16 ? c.take<uint16_t>(static_cast<size_t>(d.m) * t.ld16) : nullptr;
+    t.Yt16 = use16 ? c.take<uint16_t>(static_cast<size_t>(d.KP) * t.ldy16) : nullptr;
+    t.Zt16 = use16 ? c.take<uint16_t>(static_cast<size_t>(d.KP) * t.ldz16) : nullptr;
     t.Y = c.take<float>(static_cast<size_t>(d.m) * d.KP);
     t.Z = c.take<float>(static_cast<size_t>(d.n) * d.KP);
     t.part = c.take<float>(static_cast<size_t>(part));
@@ -757,14 +1399,18 @@ size_t carve_prior(const Dims &d, void *base, PriorWs *w)
 struct CorrWs {
     float *Tm, *part, *xpart, *X, *Xf;
     void *Pc, *Vc;
+    uint16_t *Vt16;
+    int64_t ldv16;
 };
 
 size_t carve_correct(const Dims &d, size_t esize, void *base, CorrWs *w)
 {
     Carve c(base);
-    const int s1 = split_count(d.m, d.n);
+    const int s1 = std::max(split_count(d.m, d.n), esize == 2 ? pass_splits(d.m, d.n) : 1);
     const int s2 = split_count(d.r, d.m);
     CorrWs t;
+    t.ldv16 = round_up(d.n, 8);
+    t.Vt16 = esize == 2 ? c.take<uint16_t>(static_cast<size_t>(d.RP) * t.ldv16) : nullptr;
     t.Tm = c.take<float>(static_cast<size_t>(d.m) * d.RP);
     t.part = c.take<float>(static_cast<size_t>(s1) * d.m * d.RP);
     t.xpart = c.take<float>(static_cast<size_t>(s2) * d.r * d.RP);
@@ -782,26 +1428,18 @@ unsigned grid1d(int64_t total, int per = 256)
     return static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>(cdiv(total, per), 65536)));
 }
 
-// C = opA * B with split-K through `part` when more than one split pays off.
-template <typename TA, bool TRANS, typename TO>
-void tall_gemm(const char *tag, const TA *A, int64_t lda, const float *B, int64_t ldb, TO *C,
-               int64_t ldc, int M, int K, int nvalid, int nwrite, float *part, int splits,
-               hipStream_t st)
+// Enqueue `kernel` over `jobs`, kMaxBatch jobs per launch (grid.z = job).
+template <class Job, class K, class... Args>
+void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 grid, dim3 block, size_t lds,
+                 hipStream_t st, Args... args)
 {
-    const int NP = static_cast<int>(round_up(nwrite, 16));
-    const int64_t chunk = split_chunk(K, splits);
-    splits = static_cast<int>(cdiv(K, chunk));
-    const dim3 grid(static_cast<unsigned>(cdiv(M, kBM)), static_cast<unsigned>(splits));
-    if (splits == 1) {
-        ACSC_LAUNCH(tag, (gemm_tall_kernel<TA, TRANS, TO>), grid, dim3(256), 0, st, A, lda, B,
-                           ldb, C, ldc, int64_t(0), M, K, nvalid, nwrite, static_cast<int>(chunk));
-        return;
+    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxBatch) {
+        Batch<Job> b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxBatch, jobs.size() - c0));
+        for (int i = 0; i < b.count; ++i)
+            b.j[i] = jobs[c0 + i];
+        ACSC_LAUNCH(tag, kernel, dim3(grid.x, grid.y, b.count), block, lds, st, b, args...);
     }
-    const int64_t ss = static_cast<int64_t>(M) * NP;
-    ACSC_LAUNCH(tag, (gemm_tall_kernel<TA, TRANS, float>), grid, dim3(256), 0, st, A, lda, B, ldb,
-                       part, int64_t(NP), ss, M, K, nvalid, NP, static_cast<int>(chunk));
-    ACSC_LAUNCH("sc_split_reduce", (reduce_splits_kernel<TO>), dim3(grid1d(static_cast<int64_t>(M) * nwrite)),
-                       dim3(256), 0, st, part, int64_t(NP), ss, splits, M, nwrite, C, ldc);
 }
 
 // Raise a kernel's dynamic-LDS limit (needed above the default 64 KiB).
@@ -822,24 +1460,390 @@ int allow_lds(F kernel, size_t bytes)
     return ACSC_OK;
 }
 
-size_t chol_lds(int k) { return (static_cast<size_t>(k) * (k + 1) / 2 + k) * sizeof(double); }
+size_t chol_lds(int k) { return (static_cast<size_t>(k) * (k + 1) / 2 + 2 * static_cast<size_t>(k)) * sizeof(double); }
 
-// Q <- Y L^{-T} twice (CholeskyQR2) for Y [rows, KP] (first k columns live).
-void orthonormalise(float *Y, int rows, const Dims &d, PriorWs &w, hipStream_t st)
+// One tall-skinny product per job (opA * B), split-K through the job's
+// partial buffer `part` (nullptr: one split, straight into C).
+template <typename TA, typename TO>
+struct GemmReq {
+    const TA *A;
+    int64_t lda;
+    const float *B;
+    int64_t ldb;
+    TO *C;
+    int64_t ldc;
+    int M, K, nvalid, nwrite;
+    float *part;
+    uint16_t *Ct16;
+    int64_t ldct;
+};
+
+template <typename TA, bool TRANS, typename TO>
+void tall_gemm(const char *tag, const std::vector<GemmReq<TA, TO>> &reqs, hipStream_t st)
 {
-    const int gb = gram_blocks(rows);
-    const int rpb = static_cast<int>(round_up(cdiv(rows, gb), kGRows));
-    const int nt = static_cast<int>(cdiv(d.KP, kGT));
-    for (int pass = 0; pass < 2; ++pass) {
-        ACSC_LAUNCH("sc_gram", gram_partial_kernel, dim3(nt * (nt + 1) / 2, gb), dim3(256), 0, st, Y,
-                           int64_t(d.KP), rows, d.KP, rpb, w.gpart);
-        ACSC_LAUNCH("sc_gram_reduce", gram_reduce_kernel, dim3(grid1d(int64_t(d.KP) * d.KP)), dim3(256), 0, st,
-                           w.gpart, gb, d.KP, w.gram);
-        ACSC_LAUNCH("sc_chol_inv", (chol_kernel<true>), dim3(1), dim3(1024), chol_lds(d.k), st, w.gram, d.k,
-                           d.KP, w.T);
-        tall_gemm<float, false, float>("sc_orth_apply", Y, d.KP, w.T, d.KP, Y, d.KP, rows, d.KP, d.KP, d.KP, nullptr,
-                                       1, st);
+    std::vector<GemmJob<TA, TO>> direct;
+    std::vector<GemmJob<TA, float>> split;
+    std::vector<ReduceJob<TO>> red;
+    int gx = 1, gy = 1, sx = 1, sy = 1;
+    int64_t rtot = 1;
+    for (const auto &q : reqs) {
+        const int NP = static_cast<int>(round_up(q.nwrite, 16));
+        int splits = q.part ? split_count(q.M, q.K) : 1;
+        const int64_t chunk = split_chunk(q.K, splits);
+        splits = static_cast<int>(cdiv(q.K, chunk));
+        const int mb = static_cast<int>(cdiv(q.M, kBM));
+        if (splits == 1) {
+            direct.push_back(GemmJob<TA, TO>{q.A, q.lda, q.B, q.ldb, q.C, q.ldc, 0, q.M, q.K, q.nvalid, q.nwrite,
+                                             static_cast<int>(chunk), 1, q.Ct16, q.ldct});
+            gx = std::max(gx, mb);
+        } else {
+            const int64_t ss = static_cast<int64_t>(q.M) * NP;
+            split.push_back(GemmJob<TA, float>{q.A, q.lda, q.B, q.ldb, q.part, NP, ss, q.M, q.K, q.nvalid, NP,
+                                               static_cast<int>(chunk), splits, nullptr, 0});
+            red.push_back(ReduceJob<TO>{q.part, NP, ss, splits, q.M, q.nwrite, q.C, q.ldc});
+            sx = std::max(sx, mb);
+            sy = std::max(sy, splits);
+            rtot = std::max<int64_t>(rtot, static_cast<int64_t>(q.M) * q.nwrite);
+        }
     }
+    if (!direct.empty())
+        launch_jobs(tag, gemm_tall_kernel<TA, TRANS, TO>, direct, dim3(gx, gy), dim3(256), 0, st);
+    if (!split.empty()) {
+        launch_jobs(tag, gemm_tall_kernel<TA, TRANS, float>, split, dim3(sx, sy), dim3(256), 0, st);
+        launch_jobs("sc_split_reduce", reduce_splits_kernel<TO>, red, dim3(grid1d(rtot)), dim3(256), 0, st);
+    }
+}
+
+// One streaming pass per job: C[M, NP] (fp32) = opA * B for a bf16 matrix
+// A and the thin factor given transposed in bf16 (Bt[NP][ldbt]).
+struct PassReq {
+    const uint16_t *A;
+    int64_t lda;
+    bool avec;
+    const uint16_t *Bt;
+    int64_t ldbt;
+    float *C;
+    int64_t ldc;
+    int M, K, NP;
+    float *part;
+};
+
+template <bool TRANS>
+void stream_pass(const char *tag, const std::vector<PassReq> &reqs, hipStream_t st)
+{
+    std::vector<PassJob> jobs;
+    std::vector<ReduceJob<float>> red;
+    int gx = 1;
+    int64_t rtot = 1;
+    for (const auto &q : reqs) {
+        int splits = pass_splits(q.M, q.K);
+        const int64_t chunk = pass_chunk(q.K, splits);
+        splits = static_cast<int>(cdiv(q.K, chunk));
+        const int nb = static_cast<int>(cdiv(q.M, kPassBM) * splits);
+        gx = std::max(gx, nb);
+        if (splits == 1) {
+            jobs.push_back(PassJob{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, 0, q.M, q.K, q.NP, static_cast<int>(chunk),
+                                   1, q.avec ? 1 : 0, nb});
+        } else {
+            const int64_t ss = static_cast<int64_t>(q.M) * q.NP;
+            jobs.push_back(PassJob{q.A, q.lda, q.Bt, q.ldbt, q.part, q.NP, ss, q.M, q.K, q.NP,
+                                   static_cast<int>(chunk), splits, q.avec ? 1 : 0, nb});
+            red.push_back(ReduceJob<float>{q.part, q.NP, ss, splits, q.M, q.NP, q.C, q.ldc});
+            rtot = std::max<int64_t>(rtot, ss);
+        }
+    }
+    gx = static_cast<int>(round_up(gx, 8));   // keeps block -> XCD placement per job
+    launch_jobs(tag, pass_kernel<TRANS, kPassBM>, jobs, dim3(gx), dim3(256), 0, st);
+    if (!red.empty())
+        launch_jobs("sc_split_reduce", reduce_splits_kernel<float>, red, dim3(grid1d(rtot)), dim3(256), 0, st);
+}
+
+// Per-matrix state of a batched call.
+struct Mat {
+    const sc_matrix *in;
+    Dims D;
+    PriorWs pw;
+    CorrWs cw;
+    uint64_t seed;
+};
+
+// Gram matrices (fp64) of the first KP columns of one block per matrix.
+void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const std::vector<int> &rows,
+          hipStream_t st)
+{
+    const int KP = ms[0].D.KP;
+    const int nt = static_cast<int>(cdiv(KP, kGT));
+    std::vector<GramJob> gj;
+    std::vector<GramRedJob> rj;
+    int gy = 1;
+    for (size_t i = 0; i < ms.size(); ++i) {
+        const int gb = gram_blocks(rows[i]);
+        const int rpb = static_cast<int>(round_up(cdiv(rows[i], gb), kGRows));
+        gj.push_back(GramJob{A[i], KP, rows[i], rpb, gb, ms[i].pw.gpart});
+        rj.push_back(GramRedJob{ms[i].pw.gpart, gb, ms[i].pw.gram});
+        gy = std::max(gy, gb);
+    }
+    launch_jobs("sc_gram", gram_partial_kernel, gj, dim3(nt * (nt + 1) / 2, gy), dim3(256), 0, st, KP);
+    launch_jobs("sc_gram_reduce", gram_reduce_kernel, rj, dim3(grid1d(int64_t(KP) * KP)), dim3(256), 0, st, KP);
+}
+
+// Q <- Y L^{-T}, `passes` times (CholeskyQR; two passes = CholeskyQR2), for
+// one block Y [rows, KP] per matrix (first k columns live; `which` selects
+// the Y or the Z block).  The Gram matrix is accumulated in fp64 from the
+// fp32 block, so one pass already leaves the columns orthonormal to about
+// 1e-7 * cond(Y); the iteration only needs a well-conditioned basis, and the
+// final basis gets the second pass.  The last pass also writes the bf16
+// transposed copy that the next streaming pass reads.
+void orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipStream_t st)
+{
+    const Dims &d0 = ms[0].D;
+    std::vector<const float *> A;
+    std::vector<int> rows;
+    for (auto &m : ms) {
+        A.push_back(onY ? m.pw.Y : m.pw.Z);
+        rows.push_back(onY ? m.D.m : m.D.n);
+    }
+    for (int pass = 0; pass < passes; ++pass) {
+        gram(ms, A, rows, st);
+        std::vector<CholJob> cj;
+        for (auto &m : ms)
+            cj.push_back(CholJob{m.pw.gram, m.pw.T});
+        launch_jobs("sc_chol_inv", chol_kernel<true>, cj, dim3(1), dim3(1024), chol_lds(d0.k), st, d0.k, d0.KP);
+        std::vector<GemmReq<float, float>> g;
+        for (size_t i = 0; i < ms.size(); ++i) {
+            float *Y = const_cast<float *>(A[i]);
+            uint16_t *t16 = (use16 && pass + 1 == passes) ? (onY ? ms[i].pw.Yt16 : ms[i].pw.Zt16) : nullptr;
+            const int64_t ldt = onY ? ms[i].pw.ldy16 : ms[i].pw.ldz16;
+            g.push_back(GemmReq<float, float>{Y, d0.KP, ms[i].pw.T, d0.KP, Y, d0.KP, rows[i], d0.KP, d0.KP, d0.KP,
+                                              nullptr, t16, ldt});
+        }
+        tall_gemm<float, false, float>("sc_orth_apply", g, st);
+    }
+}
+
+// EMA + top-r SVD + filter for a group of matrices with the same k.
+void build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int power_iters, float tau,
+                 hipStream_t st)
+{
+    const Dims &d0 = ms[0].D;
+    const int k = d0.k, KP = d0.KP, RP = d0.RP;
+    const bool use16 = dt == ACSC_BF16;
+    const float omb = 1.0f - beta;
+    if (use16) {
+        std::vector<EmaJob<uint16_t>> j;
+        int64_t tot = 1;
+        for (auto &m : ms) {
+            j.push_back(EmaJob<uint16_t>{m.in->M, static_cast<const uint16_t *>(m.in->G), m.D.m, m.D.n,
+                                         (m.D.n % 8) == 0 ? 1 : 0, m.pw.M16, m.pw.ld16});
+            tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.m) * cdiv(m.D.n, 8));
+        }
+        launch_jobs("sc_ema", ema_shadow_kernel<uint16_t>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
+    } else {
+        std::vector<Ema32Job<float>> j;
+        int64_t tot = 1;
+        for (auto &m : ms) {
+            const int64_t c = static_cast<int64_t>(m.D.m) * m.D.n;
+            j.push_back(Ema32Job<float>{m.in->M, static_cast<const float *>(m.in->G), c});
+            tot = std::max(tot, cdiv(c, 4));
+        }
+        bool any = false;
+        for (auto &m : ms)
+            any = any || m.in->G;
+        if (any)
+            launch_jobs("sc_ema", ema_kernel<float>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
+    }
+    {
+        std::vector<InitJob> j;
+        std::vector<TrJob> t;
+        int64_t tot = 1;
+        for (auto &m : ms) {
+            j.push_back(InitJob{m.pw.Z, m.D.n, m.in->V_warm, m.seed});
+            t.push_back(TrJob{m.pw.Z, KP, m.D.n, KP, KP, m.pw.Zt16, m.pw.ldz16});
+            tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * KP);
+        }
+        launch_jobs("sc_init", init_block_kernel, j, dim3(grid1d(tot)), dim3(256), 0, st, k, KP, r);
+        if (use16)
+            launch_jobs("sc_transpose", transpose_bf16_kernel, t, dim3(grid1d(tot)), dim3(256), 0, st);
+    }
+    // one pass Y = M Z  /  Z = M^T Y over every EMA (bf16 shadow on matrix cores, or fp32)
+    auto pass = [&](bool mz) {
+        if (use16) {
+            std::vector<PassReq> q;
+            for (auto &m : ms) {
+                if (mz)
+                    q.push_back(PassReq{m.pw.M16, m.pw.ld16, true, m.pw.Zt16, m.pw.ldz16, m.pw.Y, KP, m.D.m, m.D.n,
+                                        KP, m.pw.part});
+                else
+                    q.push_back(PassReq{m.pw.M16, m.pw.ld16, true, m.pw.Yt16, m.pw.ldy16, m.pw.Z, KP, m.D.n, m.D.m,
+                                        KP, m.pw.part});
+            }
+            if (mz)
+                stream_pass<false>("sc_pass_mz", q, st);
+            else
+                stream_pass<true>("sc_pass_mtq", q, st);
+        } else {
+            std::vector<GemmReq<float, float>> q;
+            for (auto &m : ms) {
+                if (mz)
+                    q.push_back(GemmReq<float, float>{m.in->M, m.D.n, m.pw.Z, KP, m.pw.Y, KP, m.D.m, m.D.n, k, KP,
+                                                      m.pw.part, nullptr, 0});
+                else
+                    q.push_back(GemmReq<float, float>{m.in->M, m.D.n, m.pw.Y, KP, m.pw.Z, KP, m.D.n, m.D.m, k, KP,
+                                                      m.pw.part, nullptr, 0});
+            }
+            if (mz)
+                tall_gemm<float, false, float>("sc_pass_mz", q, st);
+            else
+                tall_gemm<float, true, float>("sc_pass_mtq", q, st);
+        }
+    };
+    pass(true);
+    orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st);
+    for (int it = 0; it < power_iters; ++it) {
+        pass(false);
+        orthonormalise(ms, false, 1, use16, st);
+        pass(true);
+        orthonormalise(ms, true, it + 1 == power_iters ? 2 : 1, use16, st);
+    }
+    // Rayleigh-Ritz: Z = M^T Q (= B^T), B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
+    pass(false);
+    {
+        std::vector<const float *> A;
+        std::vector<int> rows;
+        std::vector<CholJob> cj;
+        std::vector<JacJob> jj;
+        for (auto &m : ms) {
+            A.push_back(m.pw.Z);
+            rows.push_back(m.D.n);
+            cj.push_back(CholJob{m.pw.gram, nullptr});
+            jj.push_back(JacJob{m.pw.gram, m.pw.Bu, m.pw.Bv, m.in->s, m.in->d, m.pw.info});
+        }
+        gram(ms, A, rows, st);
+        launch_jobs("sc_chol", chol_kernel<false>, cj, dim3(1), dim3(1024), chol_lds(k), st, k, KP);
+        if (k <= 128)
+            launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(1024),
+                        static_cast<size_t>(k) * k * sizeof(double), st, k, KP, r, RP, tau, 1e-13, 40);
+        else
+            launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(1024),
+                        static_cast<size_t>(k) * k * sizeof(float), st, k, KP, r, RP, tau, 1e-5f, 40);
+    }
+    // U = Q Bu, V = Z Bv (first r columns)
+    std::vector<GemmReq<float, float>> g;
+    for (auto &m : ms) {
+        g.push_back(GemmReq<float, float>{m.pw.Y, KP, m.pw.Bu, RP, m.in->U, r, m.D.m, KP, r, r, nullptr, nullptr, 0});
+        g.push_back(GemmReq<float, float>{m.pw.Z, KP, m.pw.Bv, RP, m.in->V, r, m.D.n, KP, r, r, nullptr, nullptr, 0});
+    }
+    tall_gemm<float, false, float>("sc_basis", g, st);
+}
+
+// X = U^T G V, X_f = d X d, P = U X_f, then G_proj = alpha G + (1 - alpha) P V^T.
+template <typename GT>
+void correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
+{
+    const int RP = ms[0].D.RP;
+    const bool b16 = sizeof(GT) == 2;
+    // T = G V   [m, RP]
+    if (b16) {
+        std::vector<TrJob> t;
+        std::vector<PassReq> q;
+        int64_t tot = 1;
+        for (auto &m : ms) {
+            t.push_back(TrJob{m.in->V, r, m.D.n, r, RP, m.cw.Vt16, m.cw.ldv16});
+            tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * RP);
+            const bool avec = aligned(m.in->G, 16) && (m.D.n % 8) == 0;
+            q.push_back(PassReq{static_cast<const uint16_t *>(m.in->G), m.D.n, avec, m.cw.Vt16, m.cw.ldv16, m.cw.Tm,
+                                RP, m.D.m, m.D.n, RP, m.cw.part});
+        }
+        launch_jobs("sc_transpose", transpose_bf16_kernel, t, dim3(grid1d(tot)), dim3(256), 0, st);
+        stream_pass<false>("sc_gv", q, st);
+    } else {
+        std::vector<GemmReq<float, float>> q;
+        for (auto &m : ms)
+            q.push_back(GemmReq<float, float>{static_cast<const float *>(m.in->G), m.D.n, m.in->V, r, m.cw.Tm, RP,
+                                              m.D.m, m.D.n, r, RP, m.cw.part, nullptr, 0});
+        tall_gemm<float, false, float>("sc_gv", q, st);
+    }
+    // X = U^T T   [r, RP]
+    {
+        std::vector<GemmReq<float, float>> q;
+        for (auto &m : ms)
+            q.push_back(GemmReq<float, float>{m.in->U, r, m.cw.Tm, RP, m.cw.X, RP, r, m.D.m, RP, RP, m.cw.xpart,
+                                              nullptr, 0});
+        tall_gemm<float, true, float>("sc_utt", q, st);
+    }
+    {
+        std::vector<FilterJob> f;
+        for (auto &m : ms)
+            f.push_back(FilterJob{m.cw.X, m.in->d, m.cw.Xf});
+        launch_jobs("sc_filter", filter_x_kernel, f, dim3(grid1d(int64_t(RP) * RP)), dim3(256), 0, st, r, RP);
+    }
+    // P = U X_f  [m, RP] in the compute type; V in the compute type [n, RP]
+    {
+        std::vector<GemmReq<float, GT>> q;
+        std::vector<PadJob<GT>> pj;
+        int64_t tot = 1;
+        for (auto &m : ms) {
+            q.push_back(GemmReq<float, GT>{m.in->U, r, m.cw.Xf, RP, static_cast<GT *>(m.cw.Pc), RP, m.D.m, r, RP, RP,
+                                           nullptr, nullptr, 0});
+            pj.push_back(PadJob<GT>{m.in->V, m.D.n, static_cast<GT *>(m.cw.Vc)});
+            tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * RP);
+        }
+        tall_gemm<float, false, GT>("sc_ux", q, st);
+        launch_jobs("sc_vconvert", pad_convert_kernel<GT>, pj, dim3(grid1d(tot)), dim3(256), 0, st, r, RP);
+    }
+    {
+        std::vector<BlendJob<GT>> bj;
+        int gx = 1, gy = 1;
+        for (auto &m : ms) {
+            bj.push_back(BlendJob<GT>{static_cast<const GT *>(m.in->G), static_cast<GT *>(m.in->G_proj), m.D.m, m.D.n,
+                                      static_cast<const GT *>(m.cw.Pc), static_cast<const GT *>(m.cw.Vc)});
+            gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, 64)));
+            gy = std::max<int>(gy, static_cast<int>(cdiv(m.D.m, 64)));
+        }
+        if constexpr (sizeof(GT) == 2) {
+            // 128 x 128 tiles, XCD-aware order (see blend16_kernel)
+            int tiles = 1, cbm = 1;
+            bool vec = true;
+            for (auto &m : ms) {
+                const int rbn = static_cast<int>(cdiv(m.D.m, kBT)), cbn = static_cast<int>(cdiv(m.D.n, kBT));
+                tiles = std::max(tiles, static_cast<int>(round_up(rbn, 8)) * cbn);
+                cbm = std::max(cbm, cbn);
+                vec = vec && (m.D.n % 8) == 0 && aligned(m.in->G, 16) && aligned(m.in->G_proj, 16);
+            }
+            if (vec)
+                launch_jobs("sc_blend", blend16_kernel<true>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm);
+            else
+                launch_jobs("sc_blend", blend16_kernel<false>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm);
+        } else {
+            const size_t pitch = RP + 1;
+            const size_t blds = 2 * 64 * pitch * sizeof(GT);
+            launch_jobs("sc_blend", blend_kernel<GT>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha);
+        }
+    }
+}
+
+int check_matrix(const sc_matrix &a, int r, int oversample, acsc_dtype dt, bool build, size_t *need)
+{
+    ACSC_CHECK_ARG(a.m >= 1 && a.n >= 1, ACSC_EINVAL, "m=%d, n=%d must be >= 1", a.m, a.n);
+    ACSC_CHECK_ARG(r >= 1 && r <= std::min(std::min(a.m, a.n), kKMax), ACSC_EINVAL,
+                   "r=%d outside [1, min(m, n, %d)] for a %d x %d matrix", r, kKMax, a.m, a.n);
+    const Dims d = dims_of(a.m, a.n, r, oversample);
+    *need = build ? carve_prior(d, dt == ACSC_BF16, nullptr, nullptr) : carve_correct(d, dtype_size(dt), nullptr, nullptr);
+    ACSC_CHECK_ARG(a.ws != nullptr && a.U && a.s && a.V && a.d, ACSC_EINVAL, "null pointer argument");
+    ACSC_CHECK_ARG(a.ws_bytes >= *need, ACSC_ENOSPC, "workspace %zu bytes < %zu needed", a.ws_bytes, *need);
+    ACSC_CHECK_ARG(aligned(a.ws, 256), ACSC_EALIGN, "workspace must be 256-byte aligned");
+    ACSC_CHECK_ARG(aligned(a.U, 4) && aligned(a.V, 4) && aligned(a.s, 4) && aligned(a.d, 4), ACSC_EALIGN,
+                   "U, s, V, d must be 4-byte aligned");
+    const size_t es = dtype_size(dt);
+    if (build) {
+        ACSC_CHECK_ARG(a.M != nullptr, ACSC_EINVAL, "M is NULL");
+        ACSC_CHECK_ARG(aligned(a.M, 16), ACSC_EALIGN, "M must be 16-byte aligned");
+        ACSC_CHECK_ARG(!a.G || aligned(a.G, 16), ACSC_EALIGN, "G_anc must be 16-byte aligned");
+    } else {
+        ACSC_CHECK_ARG(a.G && a.G_proj, ACSC_EINVAL, "G or G_proj is NULL");
+        ACSC_CHECK_ARG(aligned(a.G, es) && aligned(a.G_proj, es), ACSC_EALIGN, "G, G_proj must be element-aligned");
+    }
+    return ACSC_OK;
 }
 
 }  // namespace
@@ -857,146 +1861,135 @@ extern "C" int sc_workspace_size(int m, int n, int r, int oversample, acsc_dtype
                    "r=%d outside [1, min(m, n, %d)]", r, kKMax);
     ACSC_CHECK_ARG(oversample >= 0, ACSC_EINVAL, "oversample=%d < 0", oversample);
     const Dims d = dims_of(m, n, r, oversample);
-    *bytes = std::max(carve_prior(d, nullptr, nullptr), carve_correct(d, dtype_size(dt), nullptr, nullptr));
+    *bytes = std::max(carve_prior(d, dt == ACSC_BF16, nullptr, nullptr),
+                      carve_correct(d, dtype_size(dt), nullptr, nullptr));
     return ACSC_OK;
 }
 
-extern "C" int sc_build_prior(const void *G_anc, acsc_dtype dt, float *M, int m, int n, float beta,
-                              int r, int oversample, int power_iters, float tau,
-                              const float *V_warm, uint64_t seed, float *U, float *s, float *V,
-                              float *d, void *ws, size_t ws_bytes, hipStream_t stream)
+extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                                      int oversample, int power_iters, float tau, uint64_t seed,
+                                      hipStream_t stream)
 {
-    size_t need = 0;
-    int rc = sc_workspace_size(m, n, r, oversample, dt, &need);
-    if (rc)
-        return rc;
-    ACSC_CHECK_ARG(M && U && s && V && d && ws, ACSC_EINVAL, "null pointer argument");
+    clear_error();
+    ACSC_CHECK_ARG(count >= 0, ACSC_EINVAL, "count=%d < 0", count);
+    ACSC_CHECK_ARG(count == 0 || mats != nullptr, ACSC_EINVAL, "mats is NULL");
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
     ACSC_CHECK_ARG(beta >= 0.f && beta <= 1.f, ACSC_EINVAL, "beta=%g outside [0, 1]", beta);
     ACSC_CHECK_ARG(tau >= 0.f && std::isfinite(tau), ACSC_EINVAL, "tau=%g must be finite, >= 0", tau);
     ACSC_CHECK_ARG(power_iters >= 0 && power_iters <= 64, ACSC_EINVAL, "power_iters=%d outside [0, 64]",
                    power_iters);
-    ACSC_CHECK_ARG(ws_bytes >= need, ACSC_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
-    ACSC_CHECK_ARG(aligned(ws, 256), ACSC_EALIGN, "workspace must be 256-byte aligned");
-    ACSC_CHECK_ARG(aligned(M, 16), ACSC_EALIGN, "M must be 16-byte aligned");
-    ACSC_CHECK_ARG(!G_anc || aligned(G_anc, 16), ACSC_EALIGN, "G_anc must be 16-byte aligned");
-    const Dims D = dims_of(m, n, r, oversample);
-    rc = allow_lds(chol_kernel<true>, chol_lds(D.k));
-    if (!rc)
-        rc = allow_lds(chol_kernel<false>, chol_lds(D.k));
-    if (!rc)
-        rc = D.k <= 128 ? allow_lds(jacobi_kernel<double>, static_cast<size_t>(D.k) * D.k * sizeof(double))
-                        : allow_lds(jacobi_kernel<float>, static_cast<size_t>(D.k) * D.k * sizeof(float));
+    ACSC_CHECK_ARG(oversample >= 0, ACSC_EINVAL, "oversample=%d < 0", oversample);
+    std::vector<Mat> all;
+    for (int i = 0; i < count; ++i) {
+        size_t need = 0;
+        int rc = check_matrix(mats[i], r, oversample, dt, true, &need);
+        if (rc)
+            return rc;
+        Mat m;
+        m.in = &mats[i];
+        m.D = dims_of(mats[i].m, mats[i].n, r, oversample);
+        carve_prior(m.D, dt == ACSC_BF16, mats[i].ws, &m.pw);
+        m.seed = seed + static_cast<uint64_t>(i);
+        all.push_back(m);
+    }
+    if (all.empty())
+        return ACSC_OK;
+    // LDS of the one-workgroup kernels, for every k in the batch
+    for (const Mat &m : all) {
+        int rc = allow_lds(chol_kernel<true>, chol_lds(m.D.k));
+        if (!rc)
+            rc = allow_lds(chol_kernel<false>, chol_lds(m.D.k));
+        if (!rc)
+            rc = m.D.k <= 128 ? allow_lds(jacobi_kernel<double>, static_cast<size_t>(m.D.k) * m.D.k * sizeof(double))
+                              : allow_lds(jacobi_kernel<float>, static_cast<size_t>(m.D.k) * m.D.k * sizeof(float));
+        if (rc)
+            return rc;
+    }
+    // matrices with the same k (= min(r + oversample, m, n)) share every launch
+    std::vector<bool> done(all.size(), false);
+    for (size_t i = 0; i < all.size(); ++i) {
+        if (done[i])
+            continue;
+        std::vector<Mat> group;
+        for (size_t j = i; j < all.size(); ++j)
+            if (!done[j] && all[j].D.k == all[i].D.k) {
+                group.push_back(all[j]);
+                done[j] = true;
+            }
+        build_group(group, dt, beta, r, power_iters, tau, stream);
+    }
+    return check_launch("sc_build_prior");
+}
+
+extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,
+                                  hipStream_t stream)
+{
+    clear_error();
+    ACSC_CHECK_ARG(count >= 0, ACSC_EINVAL, "count=%d < 0", count);
+    ACSC_CHECK_ARG(count == 0 || mats != nullptr, ACSC_EINVAL, "mats is NULL");
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(std::isfinite(alpha), ACSC_EINVAL, "alpha must be finite");
+    std::vector<Mat> all;
+    for (int i = 0; i < count; ++i) {
+        size_t need = 0;
+        int rc = check_matrix(mats[i], r, 0, dt, false, &need);
+        if (rc)
+            return rc;
+        Mat m;
+        m.in = &mats[i];
+        m.D = dims_of(mats[i].m, mats[i].n, r, 0);
+        carve_correct(m.D, dtype_size(dt), mats[i].ws, &m.cw);
+        m.seed = 0;
+        all.push_back(m);
+    }
+    if (all.empty())
+        return ACSC_OK;
+    const size_t es = dtype_size(dt);
+    const size_t blds = 2 * 64 * (all[0].D.RP + (dt == ACSC_BF16 ? 8 : 1)) * es;
+    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t>, blds) : allow_lds(blend_kernel<float>, blds);
     if (rc)
         return rc;
-    PriorWs w;
-    carve_prior(D, ws, &w);
-    hipStream_t st = stream;
-    const int64_t count = static_cast<int64_t>(m) * n;
-    if (G_anc) {
-        if (dt == ACSC_BF16)
-            ACSC_LAUNCH("sc_ema", (ema_kernel<uint16_t>), dim3(grid1d(cdiv(count, 4))), dim3(256), 0, st, M,
-                               static_cast<const uint16_t *>(G_anc), count, beta, 1.0f - beta);
-        else
-            ACSC_LAUNCH("sc_ema", (ema_kernel<float>), dim3(grid1d(cdiv(count, 4))), dim3(256), 0, st, M,
-                               static_cast<const float *>(G_anc), count, beta, 1.0f - beta);
-    }
-    ACSC_LAUNCH("sc_init", init_block_kernel, dim3(grid1d(int64_t(n) * D.KP)), dim3(256), 0, st, w.Z, n, D.k,
-                       D.KP, V_warm, V_warm ? r : 0, seed);
-    const int sY = split_count(m, n), sZ = split_count(n, m);
-    // Y = M Z0
-    tall_gemm<float, false, float>("sc_pass_mz", M, n, w.Z, D.KP, w.Y, D.KP, m, n, D.k, D.KP, w.part, sY, st);
-    orthonormalise(w.Y, m, D, w, st);
-    for (int it = 0; it < power_iters; ++it) {
-        tall_gemm<float, true, float>("sc_pass_mtq", M, n, w.Y, D.KP, w.Z, D.KP, n, m, D.k, D.KP, w.part, sZ, st);
-        orthonormalise(w.Z, n, D, w, st);
-        tall_gemm<float, false, float>("sc_pass_mz", M, n, w.Z, D.KP, w.Y, D.KP, m, n, D.k, D.KP, w.part, sY, st);
-        orthonormalise(w.Y, m, D, w, st);
-    }
-    // Rayleigh-Ritz: Z = M^T Q (= B^T), B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
-    tall_gemm<float, true, float>("sc_pass_mtq", M, n, w.Y, D.KP, w.Z, D.KP, n, m, D.k, D.KP, w.part, sZ, st);
-    {
-        const int gb = gram_blocks(n);
-        const int rpb = static_cast<int>(round_up(cdiv(n, gb), kGRows));
-        const int nt = static_cast<int>(cdiv(D.KP, kGT));
-        ACSC_LAUNCH("sc_gram", gram_partial_kernel, dim3(nt * (nt + 1) / 2, gb), dim3(256), 0, st, w.Z,
-                           int64_t(D.KP), n, D.KP, rpb, w.gpart);
-        ACSC_LAUNCH("sc_gram_reduce", gram_reduce_kernel, dim3(grid1d(int64_t(D.KP) * D.KP)), dim3(256), 0, st,
-                           w.gpart, gb, D.KP, w.gram);
-        ACSC_LAUNCH("sc_chol", (chol_kernel<false>), dim3(1), dim3(1024), chol_lds(D.k), st, w.gram, D.k,
-                           D.KP, static_cast<float *>(nullptr));
-    }
-    if (D.k <= 128)
-        ACSC_LAUNCH("sc_jacobi", (jacobi_kernel<double>), dim3(1), dim3(1024),
-                           static_cast<size_t>(D.k) * D.k * sizeof(double), st, w.gram, D.k, D.KP, r,
-                           D.RP, tau, 1e-13, 60, w.Bu, w.Bv, s, d);
+    if (dt == ACSC_BF16)
+        correct_group<uint16_t>(all, r, alpha, stream);
     else
-        ACSC_LAUNCH("sc_jacobi", (jacobi_kernel<float>), dim3(1), dim3(1024),
-                           static_cast<size_t>(D.k) * D.k * sizeof(float), st, w.gram, D.k, D.KP, r,
-                           D.RP, tau, 2e-6f, 60, w.Bu, w.Bv, s, d);
-    // U = Q Bu, V = Z Bv (first r columns)
-    tall_gemm<float, false, float>("sc_basis", w.Y, D.KP, w.Bu, D.RP, U, r, m, D.KP, r, r, nullptr, 1, st);
-    tall_gemm<float, false, float>("sc_basis", w.Z, D.KP, w.Bv, D.RP, V, r, n, D.KP, r, r, nullptr, 1, st);
-    return check_launch("sc_build_prior");
+        correct_group<float>(all, r, alpha, stream);
+    return check_launch("sc_correct");
+}
+
+extern "C" int sc_build_prior(const void *G_anc, acsc_dtype dt, float *M, int m, int n, float beta, int r,
+                              int oversample, int power_iters, float tau, const float *V_warm, uint64_t seed,
+                              float *U, float *s, float *V, float *d, void *ws, size_t ws_bytes,
+                              hipStream_t stream)
+{
+    sc_matrix a{};
+    a.G = G_anc;
+    a.M = M;
+    a.m = m;
+    a.n = n;
+    a.U = U;
+    a.s = s;
+    a.V = V;
+    a.d = d;
+    a.V_warm = V_warm;
+    a.ws = ws;
+    a.ws_bytes = ws_bytes;
+    return sc_build_prior_batched(1, &a, dt, beta, r, oversample, power_iters, tau, seed, stream);
 }
 
 extern "C" int sc_correct(const void *G, acsc_dtype dt, int m, int n, const float *U, const float *d,
                           const float *V, int r, float alpha, void *G_proj, void *ws, size_t ws_bytes,
                           hipStream_t stream)
 {
-    size_t need = 0;
-    int rc = sc_workspace_size(m, n, r, 0, dt, &need);
-    if (rc)
-        return rc;
-    ACSC_CHECK_ARG(G && U && d && V && G_proj && ws, ACSC_EINVAL, "null pointer argument");
-    ACSC_CHECK_ARG(std::isfinite(alpha), ACSC_EINVAL, "alpha must be finite");
-    ACSC_CHECK_ARG(ws_bytes >= need, ACSC_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
-    ACSC_CHECK_ARG(aligned(ws, 256), ACSC_EALIGN, "workspace must be 256-byte aligned");
-    const size_t es = dtype_size(dt);
-    ACSC_CHECK_ARG(aligned(G, es) && aligned(G_proj, es) && aligned(U, 4) && aligned(V, 4) && aligned(d, 4),
-                   ACSC_EALIGN, "G, G_proj, U, d, V must be aligned to their element size");
-    const Dims D = dims_of(m, n, r, 0);
-    {
-        const size_t pitch = D.RP + (dt == ACSC_BF16 ? 8 : 1);
-        const size_t blds = 2 * 64 * pitch * es;
-        rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t>, blds) : allow_lds(blend_kernel<float>, blds);
-        if (rc)
-            return rc;
-    }
-    CorrWs w;
-    carve_correct(D, es, ws, &w);
-    hipStream_t st = stream;
-    const int s1 = split_count(m, n), s2 = split_count(r, m);
-    // T = G V   [m, RP]
-    if (dt == ACSC_BF16)
-        tall_gemm<uint16_t, false, float>("sc_gv", static_cast<const uint16_t *>(G), n, V, r, w.Tm, D.RP, m, n, r,
-                                          D.RP, w.part, s1, st);
-    else
-        tall_gemm<float, false, float>("sc_gv", static_cast<const float *>(G), n, V, r, w.Tm, D.RP, m, n, r, D.RP,
-                                       w.part, s1, st);
-    // X = U^T T   [r, RP]
-    tall_gemm<float, true, float>("sc_utt", U, r, w.Tm, D.RP, w.X, D.RP, r, m, D.RP, D.RP, w.xpart, s2, st);
-    ACSC_LAUNCH("sc_filter", filter_x_kernel, dim3(grid1d(int64_t(D.RP) * D.RP)), dim3(256), 0, st, w.X,
-                       int64_t(D.RP), d, r, D.RP, w.Xf);
-    const dim3 bgrid(static_cast<unsigned>(cdiv(n, 64)), static_cast<unsigned>(cdiv(m, 64)));
-    const size_t pitch = D.RP + (dt == ACSC_BF16 ? 8 : 1);
-    const size_t blds = 2 * 64 * pitch * es;
-    if (dt == ACSC_BF16) {
-        uint16_t *Pc = static_cast<uint16_t *>(w.Pc), *Vc = static_cast<uint16_t *>(w.Vc);
-        // P = U X_f  [m, RP] in bf16
-        tall_gemm<float, false, uint16_t>("sc_ux", U, r, w.Xf, D.RP, Pc, D.RP, m, r, D.RP, D.RP, nullptr, 1, st);
-        ACSC_LAUNCH("sc_vconvert", (pad_convert_kernel<uint16_t>), dim3(grid1d(int64_t(n) * D.RP)), dim3(256), 0,
-                           st, V, n, r, D.RP, Vc);
-        ACSC_LAUNCH("sc_blend", (blend_kernel<uint16_t>), bgrid, dim3(256), blds, st,
-                           static_cast<const uint16_t *>(G), static_cast<uint16_t *>(G_proj), m, n, Pc,
-                           Vc, D.RP, alpha);
-    } else {
-        float *Pc = static_cast<float *>(w.Pc), *Vc = static_cast<float *>(w.Vc);
-        tall_gemm<float, false, float>("sc_ux", U, r, w.Xf, D.RP, Pc, D.RP, m, r, D.RP, D.RP, nullptr, 1, st);
-        ACSC_LAUNCH("sc_vconvert", (pad_convert_kernel<float>), dim3(grid1d(int64_t(n) * D.RP)), dim3(256), 0, st,
-                           V, n, r, D.RP, Vc);
-        ACSC_LAUNCH("sc_blend", (blend_kernel<float>), bgrid, dim3(256), blds, st,
-                           static_cast<const float *>(G), static_cast<float *>(G_proj), m, n, Pc, Vc,
-                           D.RP, alpha);
-    }
-    return check_launch("sc_correct");
+    sc_matrix a{};
+    a.G = G;
+    a.m = m;
+    a.n = n;
+    a.U = const_cast<float *>(U);
+    a.s = const_cast<float *>(d);   // unused by the correction; only checked non-null
+    a.V = const_cast<float *>(V);
+    a.d = const_cast<float *>(d);
+    a.G_proj = G_proj;
+    a.ws = ws;
+    a.ws_bytes = ws_bytes;
+    return sc_correct_batched(1, &a, dt, r, alpha, stream);
 }

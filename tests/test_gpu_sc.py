@@ -203,3 +203,43 @@ def test_errors_raise_before_any_work(pk):
     with pytest.raises(pk.AcscError) as e:
         pk.sc_build_prior(None, M, 8, 0.9, 1e-3, 4, 2, ws=small)
     assert e.value.code == pk.ACSC_ENOSPC
+
+
+def test_batched_calls_equal_single_calls(pk):
+    """One batched call over mixed shapes gives bit-identical results to one
+    call per matrix (matrix i of the batch uses seed + i)."""
+    shapes = [(256, 384), (384, 256), (200, 328)]
+    r, p, q = 16, 8, 2
+    mats = []
+    for i, (m, n) in enumerate(shapes):
+        gp = workloads.grad_pair(workloads.GradSpec(((m, n),), 16, (1.0, 100.0), (r,), torch.bfloat16,
+                                                    None, None), 9, 0, 0, "cpu")
+        mats.append(gp)
+    single = []
+    for i, gp in enumerate(mats):
+        m, n = gp.G_anc.shape
+        M = torch.zeros(m, n, device="cuda")
+        U, s, V, d = pk.sc_build_prior(gp.G_anc.cuda(), M, r, 0.9, 1e-3, p, q, seed=40 + i)
+        out = pk.sc_correct(gp.G_mask.cuda(), U, d, V, 0.3)
+        single.append((M, U, s, V, d, out))
+    items, corr = [], []
+    for i, gp in enumerate(mats):
+        m, n = gp.G_anc.shape
+        M = torch.zeros(m, n, device="cuda")
+        outs = (torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
+                torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda"))
+        items.append(dict(G_anc=gp.G_anc.cuda(), M=M, out=outs,
+                          ws=pk.workspace(m, n, r, p, torch.bfloat16)))
+    pk.sc_build_prior_batched(items, r, 0.9, 1e-3, p, q, seed=40)
+    for it, gp in zip(items, mats):
+        m, n = gp.G_anc.shape
+        U, s, V, d = it["out"]
+        corr.append(dict(G=gp.G_mask.cuda(), prior=(U, d, V), out=torch.empty(m, n, dtype=torch.bfloat16,
+                                                                               device="cuda"),
+                         ws=pk.workspace(m, n, r, 0, torch.bfloat16)))
+    pk.sc_correct_batched(corr, r, 0.3)
+    torch.cuda.synchronize()
+    for it, c, ref in zip(items, corr, single):
+        got = (it["M"],) + tuple(it["out"]) + (c["out"],)
+        for x, y in zip(got, ref):
+            assert torch.equal(x, y)
