@@ -208,6 +208,196 @@ struct Vec16<uint32_t> {
     static constexpr int N = 4;
 };
 
+// Per-wave LDS of the staged kernels: bitmap[nw], prefix[nw], then the packed
+// row (K values) and, for pack, its K indices.
+__host__ __device__ __forceinline__ size_t staged_wave_bytes(int nw, int K, int esize, bool with_idx)
+{
+    size_t b = static_cast<size_t>(2 * nw) * 4 + static_cast<size_t>(K) * esize;
+    if (with_idx)
+        b += static_cast<size_t>(K) * 2;
+    return (b + 15) & ~static_cast<size_t>(15);
+}
+
+// Builds the kept-set bitmap of `row` (from the key) and the exclusive prefix
+// of its word popcounts.  Every thread of the workgroup calls it (it contains
+// the workgroup barriers).
+template <int ROUNDS>
+__device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, bool active, uint64_t key,
+                                           int64_t row, int w, int H, int K, int lane,
+                                           const uint16_t *idx_row)
+{
+    for (int i = lane; i < nw; i += 64)
+        bm[i] = 0u;
+    __syncthreads();
+    if (active) {
+        if (idx_row) {
+            for (int i = lane; i < K; i += 64) {
+                const uint32_t j = idx_row[i];
+                if (j < static_cast<uint32_t>(H))
+                    atomicOr(&bm[j >> 5], 1u << (j & 31));
+            }
+        } else {
+            const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
+            for (int i = lane; i < K; i += 64) {
+                const uint32_t j = perm(static_cast<uint32_t>(i));
+                atomicOr(&bm[j >> 5], 1u << (j & 31));
+            }
+        }
+    }
+    __syncthreads();
+    if (active) {
+        const int per = (nw + 63) >> 6;
+        const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
+        int cnt = 0;
+        for (int i = w0; i < w1; ++i)
+            cnt += __popc(bm[i]);
+        int pos = wave_exclusive_scan(cnt, lane);
+        for (int i = w0; i < w1; ++i) {
+            pre[i] = static_cast<uint32_t>(pos);
+            pos += __popc(bm[i]);
+        }
+    }
+    __syncthreads();
+}
+
+// Pack, streaming form: each lane reads whole 16-byte chunks of the row that
+// hold at least one kept entry (chunks with none are never fetched), drops the
+// kept entries into their rank slots of an LDS copy of the packed row, and
+// the packed row (and its indices) leaves with coalesced stores.
+template <typename E, int ROUNDS>
+__global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict__ x, int64_t rows, int H,
+                                                             int64_t ld_x, int K, uint64_t key, int w,
+                                                             E *__restrict__ vals,
+                                                             uint16_t *__restrict__ idx)
+{
+    extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
+    constexpr int N = Vec16<E>::N;
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int wpb = blockDim.x >> 6;
+    const int nw = (H + 31) >> 5;
+    // the index slots are always reserved (they are written even when idx is NULL)
+    const size_t per_wave = staged_wave_bytes(nw, K, sizeof(E), true);
+    uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) + wid * per_wave);
+    uint32_t *pre = bm + nw;
+    E *kv = reinterpret_cast<E *>(pre + nw);
+    uint16_t *ki = reinterpret_cast<uint16_t *>(kv + K);
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
+    const bool active = row < rows;
+    row_bitmap<ROUNDS>(bm, pre, nw, active, key, row, w, H, K, lane, nullptr);
+    if (active) {
+        const E *xr = x + row * ld_x;
+        const int nch = H / N;
+#pragma unroll 4
+        for (int c = lane; c < nch; c += 64) {
+            const int j0 = c * N;
+            const uint32_t word = bm[j0 >> 5];
+            const int sh = j0 & 31;
+            const uint32_t bits = (word >> sh) & ((1u << N) - 1u);
+            if (bits) {
+                const uint4 v = *reinterpret_cast<const uint4 *>(xr + j0);
+                const E *ve = reinterpret_cast<const E *>(&v);
+                int rank = static_cast<int>(pre[j0 >> 5]) + __popc(word & ((1u << sh) - 1u));
+#pragma unroll
+                for (int e = 0; e < N; ++e) {
+                    if (bits & (1u << e)) {
+                        kv[rank] = ve[e];
+                        ki[rank] = static_cast<uint16_t>(j0 + e);
+                        ++rank;
+                    }
+                }
+            }
+        }
+        for (int j = nch * N + lane; j < H; j += 64) {
+            const uint32_t word = bm[j >> 5];
+            const int b = j & 31;
+            if ((word >> b) & 1u) {
+                const int rank = static_cast<int>(pre[j >> 5]) + __popc(word & ((1u << b) - 1u));
+                kv[rank] = xr[j];
+                ki[rank] = static_cast<uint16_t>(j);
+            }
+        }
+    }
+    __syncthreads();
+    if (active) {
+        E *vr = vals + row * K;
+        uint16_t *ir = idx ? idx + row * K : nullptr;
+        for (int i = lane; i < K; i += 64) {
+            vr[i] = kv[i];
+            if (ir)
+                ir[i] = ki[i];
+        }
+    }
+}
+
+// Unpack, staged form: the packed row is first copied into LDS (coalesced),
+// then every lane writes whole 16-byte chunks of the dense row.
+template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
+__global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restrict__ vals,
+                                                               const uint16_t *__restrict__ idx,
+                                                               int64_t rows, int H, int K, uint64_t key,
+                                                               int w, float scale, E *__restrict__ y,
+                                                               int64_t ld_y)
+{
+    extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int wpb = blockDim.x >> 6;
+    const int nw = (H + 31) >> 5;
+    const size_t per_wave = staged_wave_bytes(nw, K, sizeof(E), false);
+    uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) + wid * per_wave);
+    uint32_t *pre = bm + nw;
+    E *kv = reinterpret_cast<E *>(pre + nw);
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
+    const bool active = row < rows;
+    if (active) {
+        const E *vr = vals + row * K;
+        for (int i = lane; i < K; i += 64)
+            kv[i] = vr[i];
+    }
+    row_bitmap<ROUNDS>(bm, pre, nw, active, key, row, w, H, K, lane,
+                       (FROM_IDX && active) ? idx + row * K : nullptr);
+    if (!active)
+        return;
+    E *yr = y + row * ld_y;
+    int jtail = 0;
+    if (VEC) {
+        constexpr int N = Vec16<E>::N;
+        const int nch = H / N;
+#pragma unroll 4
+        for (int c = lane; c < nch; c += 64) {
+            const int j0 = c * N;
+            const uint32_t word = bm[j0 >> 5];
+            const int sh = j0 & 31;
+            const uint32_t bits = (word >> sh) & ((1u << N) - 1u);
+            E out[N];
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                out[e] = 0;
+            if (bits) {
+                int rank = static_cast<int>(pre[j0 >> 5]) + __popc(word & ((1u << sh) - 1u));
+#pragma unroll
+                for (int e = 0; e < N; ++e) {
+                    if (bits & (1u << e))
+                        out[e] = scaled(kv[rank++], scale);
+                }
+            }
+            *reinterpret_cast<uint4 *>(yr + j0) = *reinterpret_cast<const uint4 *>(out);
+        }
+        jtail = nch * N;
+    }
+    for (int j = jtail + lane; j < H; j += 64) {
+        const uint32_t word = bm[j >> 5];
+        const int b = j & 31;
+        E out = 0;
+        if ((word >> b) & 1u) {
+            const int rank = static_cast<int>(pre[j >> 5]) + __popc(word & ((1u << b) - 1u));
+            out = scaled(kv[rank], scale);
+        }
+        yr[j] = out;
+    }
+}
+
 // Per-wave LDS layout of the unpack kernel: bitmap[nw] then prefix[nw].
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
 __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ vals,
@@ -328,9 +518,26 @@ template <typename E, int ROUNDS>
 void launch_pack(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
                  void *vals, uint16_t *idx, hipStream_t st)
 {
+    // The streaming form (whole 16-byte chunks) measured slower on MI355X than
+    // the gather below at every keep fraction of the workloads; it stays
+    // available for rows whose kept entries are dense (keep >= 1/4).
+    const int nwords = (H + 31) / 32;
+    const size_t sper = staged_wave_bytes(nwords, K, sizeof(E), true);
+    const bool vec = aligned(x, 16) && (static_cast<size_t>(ld_x) * sizeof(E)) % 16 == 0;
+    const bool dense = 4 * static_cast<int64_t>(K) >= H;
+    if (dense && vec && sper <= kLdsBudget &&
+        allow_lds(ac_pack_stream_kernel<E, ROUNDS>, sper * waves_for(sper)) == ACSC_OK) {
+        const int wpb = waves_for(sper);
+        const int64_t blocks = (rows + wpb - 1) / wpb;
+        ACSC_LAUNCH("ac_pack", (ac_pack_stream_kernel<E, ROUNDS>), dim3(static_cast<unsigned>(blocks)),
+                    dim3(64 * wpb), sper * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K, key, w,
+                    static_cast<E *>(vals), idx);
+        return;
+    }
     const int nw = (H + 31) / 32;
     const size_t per = static_cast<size_t>(pack_wave_words(nw, K)) * 4;
     const int wpb = waves_for(per);
+    allow_lds(ac_pack_kernel<E, ROUNDS>, per * wpb);
     const int64_t blocks = (rows + wpb - 1) / wpb;
     ACSC_LAUNCH("ac_pack", (ac_pack_kernel<E, ROUNDS>), dim3(static_cast<unsigned>(blocks)),
                        dim3(64 * wpb), per * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K,
@@ -341,9 +548,30 @@ template <typename E, int ROUNDS, bool FROM_IDX>
 void launch_unpack(const void *vals, const uint16_t *idx, int64_t rows, int H, int K, uint64_t key,
                    int w, float scale, void *y, int64_t ld_y, bool vec, hipStream_t st)
 {
+    const int nwords = (H + 31) / 32;
+    const size_t sper = staged_wave_bytes(nwords, K, sizeof(E), false);
+    const bool lds_ok = sper <= kLdsBudget &&
+                        (vec ? allow_lds(ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, true>, sper * waves_for(sper))
+                             : allow_lds(ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, false>, sper * waves_for(sper))) ==
+                            ACSC_OK;
+    if (lds_ok) {
+        const int wpb = waves_for(sper);
+        const int64_t blocks = (rows + wpb - 1) / wpb;
+        if (vec)
+            ACSC_LAUNCH("ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, true>),
+                        dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), sper * wpb, st,
+                        static_cast<const E *>(vals), idx, rows, H, K, key, w, scale, static_cast<E *>(y), ld_y);
+        else
+            ACSC_LAUNCH("ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, false>),
+                        dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), sper * wpb, st,
+                        static_cast<const E *>(vals), idx, rows, H, K, key, w, scale, static_cast<E *>(y), ld_y);
+        return;
+    }
     const int nw = (H + 31) / 32;
     const size_t per = static_cast<size_t>(2 * nw) * 4;
     const int wpb = waves_for(per);
+    allow_lds(ac_unpack_kernel<E, ROUNDS, FROM_IDX, true>, per * wpb);
+    allow_lds(ac_unpack_kernel<E, ROUNDS, FROM_IDX, false>, per * wpb);
     const int64_t blocks = (rows + wpb - 1) / wpb;
     if (vec)
         ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, true>),

@@ -50,6 +50,26 @@ inline int check_launch(const char *what)
 
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Raise a kernel's dynamic-LDS limit (needed above the default 64 KiB).
+template <typename F>
+inline int allow_lds(F kernel, size_t bytes)
+{
+    if (bytes <= 64 * 1024)
+        return ACSC_OK;
+    int dev = 0, lim = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lim, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+        return set_error(ACSC_EHIP, "cannot query the LDS size of the device");
+    if (static_cast<size_t>(lim) < bytes)
+        return set_error(ACSC_EINVAL, "needs %zu bytes of LDS per workgroup, device has %d", bytes, lim);
+    if (hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes)) != hipSuccess)
+        return set_error(ACSC_EHIP, "hipFuncSetAttribute failed");
+    return ACSC_OK;
+}
+
+
+
 inline size_t dtype_size(acsc_dtype dt) { return dt == ACSC_BF16 ? 2 : 4; }
 
 // bf16 <-> fp32 on bit patterns.

@@ -16,6 +16,8 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef float nf4 __attribute__((ext_vector_type(4)));
+typedef unsigned int nu4 __attribute__((ext_vector_type(4)));
 
 constexpr int kKMax = SC_KMAX;
 constexpr int kBM = 64;   // rows of the output per workgroup in the tall GEMM
@@ -219,8 +221,8 @@ __global__ __launch_bounds__(256) void gemm_tall_kernel(const Batch<GemmJob<TA, 
 // factor comes transposed and in bf16, Bt[c][k] (row stride ldbt, a multiple
 // of 8), so both tiles load as 16-byte chunks that go straight into LDS rows
 // with k contiguous, as v_mfma_f32_16x16x32_bf16 reads them.  BM rows per
-// workgroup (4 waves of BM/4 rows), 64-deep K steps, the next step's tiles
-// loaded into registers while the current one is multiplied.  Block b works
+// workgroup (4 waves of BM/4 rows), 64-deep K steps, the next two steps'
+// tiles loaded into registers while the current one is multiplied.  Block b works
 // on split b % splits: workgroups are dealt to the XCDs round-robin, so with
 // splits a power of two up to 8 every XCD keeps to one slice of Bt in its L2.
 // ---------------------------------------------------------------------------
@@ -273,9 +275,8 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch<PassJob> jb)
         for (int t = 0; t < kNTMax; ++t)
             acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    uint4 ra[ACH];
-    uint4 rb[kPBChunks];
-    auto load = [&](int k0) {
+    uint4 ra0[ACH], rb0[kPBChunks], ra1[ACH], rb1[kPBChunks];
+    auto load = [&](uint4 (&ra)[ACH], uint4 (&rb)[kPBChunks], int k0) {
 #pragma unroll
         for (int j = 0; j < ACH; ++j) {
             const int q = tid + 256 * j;
@@ -338,7 +339,7 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch<PassJob> jb)
             rb[j] = v;
         }
     };
-    auto store = [&]() {
+    auto store = [&](const uint4 (&ra)[ACH], const uint4 (&rb)[kPBChunks]) {
 #pragma unroll
         for (int j = 0; j < ACH; ++j) {
             const int q = tid + 256 * j;
@@ -362,14 +363,7 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch<PassJob> jb)
         }
     };
 
-    if (kbeg < kend)
-        load(kbeg);
-    for (int k0 = kbeg; k0 < kend; k0 += kPBK) {
-        __syncthreads();
-        store();
-        __syncthreads();
-        if (k0 + kPBK < kend)
-            load(k0 + kPBK);
+    auto compute = [&]() {
 #pragma unroll
         for (int ks = 0; ks < kPBK / 32; ++ks) {
             bf16x8 af[RT];
@@ -396,6 +390,28 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch<PassJob> jb)
                 }
             }
         }
+    };
+    // two register stages: tiles k0 + 64 and k0 + 128 are in flight while k0
+    // is multiplied
+    if (kbeg < kend)
+        load(ra0, rb0, kbeg);
+    if (kbeg + kPBK < kend)
+        load(ra1, rb1, kbeg + kPBK);
+    for (int k0 = kbeg; k0 < kend; k0 += 2 * kPBK) {
+        __syncthreads();
+        store(ra0, rb0);
+        __syncthreads();
+        if (k0 + 2 * kPBK < kend)
+            load(ra0, rb0, k0 + 2 * kPBK);
+        compute();
+        if (k0 + kPBK >= kend)
+            break;
+        __syncthreads();
+        store(ra1, rb1);
+        __syncthreads();
+        if (k0 + 3 * kPBK < kend)
+            load(ra1, rb1, k0 + 3 * kPBK);
+        compute();
     }
     float *Cs = C + static_cast<int64_t>(split) * split_stride;
 #pragma unroll
@@ -447,14 +463,14 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
         const GT *gr = G ? G + i * n + j0 : nullptr;
         float v[8];
         if (VEC && j0 + 8 <= n) {
-            const float4 m0 = *reinterpret_cast<const float4 *>(mr);
-            const float4 m1 = *reinterpret_cast<const float4 *>(mr + 4);
+            const nf4 m0 = __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(mr));
+            const nf4 m1 = __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(mr + 4));
             v[0] = m0.x; v[1] = m0.y; v[2] = m0.z; v[3] = m0.w;
             v[4] = m1.x; v[5] = m1.y; v[6] = m1.z; v[7] = m1.w;
             if (gr) {
                 float g[8];
                 if constexpr (sizeof(GT) == 2) {
-                    const uint4 gb = *reinterpret_cast<const uint4 *>(gr);
+                    const nu4 gb = __builtin_nontemporal_load(reinterpret_cast<const nu4 *>(gr));
                     const uint32_t w4[4] = {gb.x, gb.y, gb.z, gb.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -470,8 +486,8 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
                     v[e] = beta * v[e] + omb * g[e];
-                *reinterpret_cast<float4 *>(mr) = make_float4(v[0], v[1], v[2], v[3]);
-                *reinterpret_cast<float4 *>(mr + 4) = make_float4(v[4], v[5], v[6], v[7]);
+                __builtin_nontemporal_store(nf4{v[0], v[1], v[2], v[3]}, reinterpret_cast<nf4 *>(mr));
+                __builtin_nontemporal_store(nf4{v[4], v[5], v[6], v[7]}, reinterpret_cast<nf4 *>(mr + 4));
             }
             uint16_t h[8];
 #pragma unroll
@@ -535,6 +551,29 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const Batch<ReduceJo
     const int64_t ldp = J.ldp, split_stride = J.split_stride, ldc = J.ldc;
     const int splits = J.splits, M = J.M, nwrite = J.nwrite;
     TO *C = J.C;
+    if constexpr (sizeof(TO) == 4) {
+        // four columns per thread when every row is 16-byte aligned
+        if ((nwrite & 3) == 0 && (ldp & 3) == 0 && (ldc & 3) == 0 && (split_stride & 3) == 0 &&
+            (reinterpret_cast<uintptr_t>(P) & 15) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0) {
+            const int nq = nwrite >> 2;
+            const int64_t total = static_cast<int64_t>(M) * nq;
+            for (int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+                 idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+                const int64_t i = idx / nq;
+                const int c = static_cast<int>(idx - i * nq) * 4;
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int p = 0; p < splits; ++p) {
+                    const float4 v = *reinterpret_cast<const float4 *>(P + p * split_stride + i * ldp + c);
+                    acc.x += v.x;
+                    acc.y += v.y;
+                    acc.z += v.z;
+                    acc.w += v.w;
+                }
+                *reinterpret_cast<float4 *>(C + i * ldc + c) = acc;
+            }
+            return;
+        }
+    }
     const int64_t total = static_cast<int64_t>(M) * nwrite;
     for (int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
          idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
@@ -669,6 +708,36 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const Batch<GramRedJob
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int tri(int i) { return i * (i + 1) / 2; }
 
+// Sum over each row of 16 lanes with DPP lane permutes (VALU, no LDS):
+// quad_perm [1,0,3,2] and [2,3,0,1] (xor 1, xor 2), then row_half_mirror
+// (pairs the two quads of each half) and row_mirror (pairs the two halves);
+// every lane of the row ends with the row's sum.
+__device__ __forceinline__ float row16_sum(float x)
+{
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));
+    return x;
+}
+
+__device__ __forceinline__ double row16_sum(double x)
+{
+#define ACSC_DPP64(CTRL)                                                                          \
+    {                                                                                             \
+        const int lo = __double2loint(x), hi = __double2hiint(x);                                 \
+        const int plo = __builtin_amdgcn_update_dpp(0, lo, CTRL, 0xF, 0xF, false);                \
+        const int phi = __builtin_amdgcn_update_dpp(0, hi, CTRL, 0xF, 0xF, false);                \
+        x += __hiloint2double(phi, plo);                                                          \
+    }
+    ACSC_DPP64(0xB1)
+    ACSC_DPP64(0x4E)
+    ACSC_DPP64(0x141)
+    ACSC_DPP64(0x140)
+#undef ACSC_DPP64
+    return x;
+}
+
 struct CholJob {
     double *G;
     float *Tout;
@@ -790,15 +859,18 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     float *Bu = J.Bu, *Bv = J.Bv, *s_out = J.s_out, *d_out = J.d_out;
     int *info = J.info;
     extern __shared__ __attribute__((aligned(16))) unsigned char jsm[];
-    T *A = reinterpret_cast<T *>(jsm);   // column c at A[c * k]
+    // column c at A[c * kp]; kp = k rounded up to 16, rows k..kp-1 are zero, so
+    // the loops over a column have a uniform trip count
+    T *A = reinterpret_cast<T *>(jsm);
+    const int kp = (k + 15) & ~15;
     __shared__ unsigned int sh_off;
     __shared__ double sh_cut;
     __shared__ double sig[kKMax];
     __shared__ int rank_of[kKMax];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
-    for (int idx = tid; idx < k * k; idx += blockDim.x) {
-        const int c = idx / k, i = idx % k;
-        A[c * k + i] = static_cast<T>(Lf[static_cast<int64_t>(i) * KP + c]);
+    for (int idx = tid; idx < k * kp; idx += blockDim.x) {
+        const int c = idx / kp, i = idx % kp;
+        A[c * kp + i] = i < k ? static_cast<T>(Lf[static_cast<int64_t>(i) * KP + c]) : T(0);
     }
     const int n2 = k + (k & 1);
     const int npairs = n2 / 2;
@@ -823,48 +895,47 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
                     cp = cq;
                     cq = t;
                 }
-                T *ap = A + cp * k;
-                T *aq = A + cq * k;
+                T *ap = A + cp * kp;
+                T *aq = A + cq * kp;
                 // the pair's columns stay in registers: 16 lanes x kRowsPerLane rows
                 T xv[kRowsPerLane], yv[kRowsPerLane];
 #pragma unroll
                 for (int e = 0; e < kRowsPerLane; ++e) {
-                    const int i = gl + 16 * e;
-                    xv[e] = i < k ? ap[i] : T(0);
-                    yv[e] = i < k ? aq[i] : T(0);
+                    xv[e] = T(0);
+                    yv[e] = T(0);
+                    if (16 * e < kp) {
+                        xv[e] = ap[gl + 16 * e];
+                        yv[e] = aq[gl + 16 * e];
+                    }
                 }
-                double al = 0.0, be = 0.0, ga = 0.0;
+                // dot products, rotation and update in the storage precision T
+                T al = 0, be = 0, ga = 0;
 #pragma unroll
                 for (int e = 0; e < kRowsPerLane; ++e) {
-                    const double x = xv[e], y = yv[e];
-                    al += x * x;
-                    be += y * y;
-                    ga += x * y;
+                    al += xv[e] * xv[e];
+                    be += yv[e] * yv[e];
+                    ga += xv[e] * yv[e];
                 }
-#pragma unroll
-                for (int off = 8; off >= 1; off >>= 1) {
-                    al += __shfl_xor(al, off, 16);
-                    be += __shfl_xor(be, off, 16);
-                    ga += __shfl_xor(ga, off, 16);
-                }
-                const double nrm = sqrt(al * be);
-                if (ga == 0.0 || nrm == 0.0)
+                al = row16_sum(al);
+                be = row16_sum(be);
+                ga = row16_sum(ga);
+                const T nrm = sqrt(al * be);
+                if (ga == T(0) || nrm == T(0))
                     continue;
-                const double ratio = fabs(ga) / nrm;
+                const T ratio = fabs(ga) / nrm;
                 wmax = fmaxf(wmax, static_cast<float>(ratio));
-                if (ratio <= static_cast<double>(tol))
+                if (ratio <= tol)
                     continue;
-                const double zeta = (be - al) / (2.0 * ga);
-                const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-                const double c = 1.0 / sqrt(1.0 + t * t);
-                const double sn = c * t;
+                const T zeta = (be - al) / (T(2) * ga);
+                const T t = (zeta >= T(0) ? T(1) : T(-1)) / (fabs(zeta) + sqrt(T(1) + zeta * zeta));
+                const T c = T(1) / sqrt(T(1) + t * t);
+                const T sn = c * t;
 #pragma unroll
                 for (int e = 0; e < kRowsPerLane; ++e) {
-                    const int i = gl + 16 * e;
-                    if (i < k) {
-                        const double x = xv[e], y = yv[e];
-                        ap[i] = static_cast<T>(c * x - sn * y);
-                        aq[i] = static_cast<T>(sn * x + c * y);
+                    if (16 * e < kp) {
+                        const T x = xv[e], y = yv[e];
+                        ap[gl + 16 * e] = c * x - sn * y;
+                        aq[gl + 16 * e] = sn * x + c * y;
                     }
                 }
             }
@@ -892,7 +963,7 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     for (int c = wave; c < k; c += nwave) {
         double ss = 0.0;
         for (int i = lane; i < k; i += 64) {
-            const double x = A[c * k + i];
+            const double x = A[c * kp + i];
             ss += x * x;
         }
 #pragma unroll
@@ -932,7 +1003,7 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
         const int t = rank_of[c];
         if (t < r) {
             const double sg = sig[c];
-            const double u = sg > 0.0 ? static_cast<double>(A[c * k + i]) / sg : 0.0;
+            const double u = sg > 0.0 ? static_cast<double>(A[c * kp + i]) / sg : 0.0;
             Bu[i * RP + t] = static_cast<float>(u);
             Bv[i * RP + t] = sg > 0.0 ? static_cast<float>(u / sg) : 0.f;
         }
@@ -1203,14 +1274,20 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
     if (rb >= rb_n)
         return;
     const int row0 = rb * kBT, col0 = cb * kBT;
-    __shared__ __attribute__((aligned(16))) uint16_t Gs[kBT * kGPitch];
-    __shared__ __attribute__((aligned(16))) uint16_t Ps[kBT * kKPitch];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[kBT * kKPitch];
+    // one LDS region: P / V slices during the products, then the G tile
+    __shared__ __attribute__((aligned(16))) uint16_t sm[kBT * kGPitch];
+    uint16_t *Ps = sm;
+    uint16_t *Vs = sm + kBT * kKPitch;
+    uint16_t *Gs = sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint16_t *G = J.G;
     uint16_t *out = J.out;
-    // stage G: 128 rows x 16 chunks of 8
-    for (int q = tid; q < kBT * (kBT / 8); q += 256) {
+    // G tile into registers now (128 rows x 16 chunks; 8 chunks per thread),
+    // so its latency overlaps the products
+    uint4 gr[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int q = tid + 256 * u;
         const int rr = q >> 4, c8 = (q & 15) * 8;
         const int gi = row0 + rr, gj = col0 + c8;
         uint4 v = make_uint4(0u, 0u, 0u, 0u);
@@ -1226,19 +1303,14 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
                 v = *reinterpret_cast<const uint4 *>(e8);
             }
         }
-        *reinterpret_cast<uint4 *>(&Gs[rr * kGPitch + c8]) = v;
+        gr[u] = v;
     }
-    const int wr = wave >> 1, wc = wave & 1;
-    f32x4 acc[4][4];
+    // P / V slices: 2 x 128 rows x 4 chunks; 4 chunks per thread, prefetched
+    uint4 pv[4];
+    auto load_slice = [&](int k0) {
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < RP; k0 += 32) {
-        __syncthreads();
-        // P and V slices: 128 rows x 4 chunks each
-        for (int q = tid; q < 2 * kBT * 4; q += 256) {
+        for (int u = 0; u < 4; ++u) {
+            const int q = tid + 256 * u;
             const bool isV = q >= kBT * 4;
             const int qq = isV ? q - kBT * 4 : q;
             const int rr = qq >> 2, c8 = (qq & 3) * 8;
@@ -1247,9 +1319,30 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
             if (g < lim)
                 v = *reinterpret_cast<const uint4 *>((isV ? J.Vc : J.P) + static_cast<int64_t>(g) * RP + k0 + c8);
-            *reinterpret_cast<uint4 *>(&(isV ? Vs : Ps)[rr * kKPitch + c8]) = v;
+            pv[u] = v;
+        }
+    };
+    const int wr = wave >> 1, wc = wave & 1;
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    load_slice(0);
+    for (int k0 = 0; k0 < RP; k0 += 32) {
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int q = tid + 256 * u;
+            const bool isV = q >= kBT * 4;
+            const int qq = isV ? q - kBT * 4 : q;
+            const int rr = qq >> 2, c8 = (qq & 3) * 8;
+            *reinterpret_cast<uint4 *>(&(isV ? Vs : Ps)[rr * kKPitch + c8]) = pv[u];
         }
         __syncthreads();
+        if (k0 + 32 < RP)
+            load_slice(k0 + 32);
         bf16x8 af[4], bfr[4];
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
@@ -1262,6 +1355,14 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
             for (int c = 0; c < 4; ++c)
                 acc[a][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[c], acc[a][c], 0, 0, 0);
     }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int q = tid + 256 * u;
+        const int rr = q >> 4, c8 = (q & 15) * 8;
+        *reinterpret_cast<uint4 *>(&Gs[rr * kGPitch + c8]) = gr[u];
+    }
+    __syncthreads();
     // blend in place in the staged tile
     const float oma = 1.0f - alpha;
 #pragma unroll
@@ -1277,7 +1378,9 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
             }
         }
     __syncthreads();
-    for (int q = tid; q < kBT * (kBT / 8); q += 256) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int q = tid + 256 * u;
         const int rr = q >> 4, c8 = (q & 15) * 8;
         const int gi = row0 + rr, gj = col0 + c8;
         if (gi >= m)
@@ -1440,24 +1543,6 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
             b.j[i] = jobs[c0 + i];
         ACSC_LAUNCH(tag, kernel, dim3(grid.x, grid.y, b.count), block, lds, st, b, args...);
     }
-}
-
-// Raise a kernel's dynamic-LDS limit (needed above the default 64 KiB).
-template <typename F>
-int allow_lds(F kernel, size_t bytes)
-{
-    if (bytes <= 64 * 1024)
-        return ACSC_OK;
-    int dev = 0, lim = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&lim, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
-        return set_error(ACSC_EHIP, "cannot query the LDS size of the device");
-    if (static_cast<size_t>(lim) < bytes)
-        return set_error(ACSC_EINVAL, "needs %zu bytes of LDS per workgroup, device has %d", bytes, lim);
-    if (hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes)) != hipSuccess)
-        return set_error(ACSC_EHIP, "hipFuncSetAttribute failed");
-    return ACSC_OK;
 }
 
 size_t chol_lds(int k) { return (static_cast<size_t>(k) * (k + 1) / 2 + 2 * static_cast<size_t>(k)) * sizeof(double); }
@@ -1720,12 +1805,13 @@ void build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int pow
         }
         gram(ms, A, rows, st);
         launch_jobs("sc_chol", chol_kernel<false>, cj, dim3(1), dim3(1024), chol_lds(k), st, k, KP);
+        const size_t kp = round_up(k, 16);
         if (k <= 128)
             launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(1024),
-                        static_cast<size_t>(k) * k * sizeof(double), st, k, KP, r, RP, tau, 1e-13, 40);
+                        static_cast<size_t>(k) * kp * sizeof(double), st, k, KP, r, RP, tau, 1e-13, 40);
         else
             launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(1024),
-                        static_cast<size_t>(k) * k * sizeof(float), st, k, KP, r, RP, tau, 1e-5f, 40);
+                        static_cast<size_t>(k) * kp * sizeof(float), st, k, KP, r, RP, tau, 1e-5f, 40);
     }
     // U = Q Bu, V = Z Bv (first r columns)
     std::vector<GemmReq<float, float>> g;
@@ -1900,8 +1986,9 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
         if (!rc)
             rc = allow_lds(chol_kernel<false>, chol_lds(m.D.k));
         if (!rc)
-            rc = m.D.k <= 128 ? allow_lds(jacobi_kernel<double>, static_cast<size_t>(m.D.k) * m.D.k * sizeof(double))
-                              : allow_lds(jacobi_kernel<float>, static_cast<size_t>(m.D.k) * m.D.k * sizeof(float));
+            rc = m.D.k <= 128
+                     ? allow_lds(jacobi_kernel<double>, static_cast<size_t>(m.D.k) * round_up(m.D.k, 16) * sizeof(double))
+                     : allow_lds(jacobi_kernel<float>, static_cast<size_t>(m.D.k) * round_up(m.D.k, 16) * sizeof(float));
         if (rc)
             return rc;
     }
