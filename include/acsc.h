@@ -116,7 +116,7 @@ int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int6
                       hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * Spectral corrector (paper Sec. 3.2; Alg. 1; App. D).
+ * Spectral corrector (paper Sec. 3.2; Alg. 1; App. E).
  * ---------------------------------------------------------------------- */
 
 /* Largest supported k = r + oversample (columns of the subspace iteration). */
@@ -127,7 +127,7 @@ int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int6
  * Requires 1 <= r <= min(m, n, SC_KMAX), p >= 0. */
 int sc_workspace_size(int m, int n, int r, int oversample, acsc_dtype dt, size_t *bytes);
 
-/* Anchor prior (Sec. 3.2; Alg. 1 on anchor arrival; App. D):
+/* Anchor prior (Sec. 3.2; Alg. 1 on anchor arrival; App. E):
  *   1. if G_anc != NULL:  M <- beta * M + (1 - beta) * G_anc       (EMA)
  *   2. (U, s, V) = the top-r singular triplets of M                 (SVD)
  *   3. d_i = s_i / (s_i + tau), with 0/0 taken as 0                 (filter)

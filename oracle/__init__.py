@@ -1,7 +1,7 @@
 """CPU oracle of the paper's hot path: masking compressor and spectral corrector.
 
 TEST INFRASTRUCTURE ONLY.  Plain, slow, obviously correct definitions written
-from the paper (Sec. 3.1, Sec. 3.2, Alg. 1, App. D, App. F), used to check the
+from the paper (Sec. 3.1, Sec. 3.2, Alg. 1, App. E, App. F), used to check the
 HIP library.  Only the test suite, the smoke check and the benchmark's
 CPU-baseline leg may import it; the library never does, and the two share no
 code.

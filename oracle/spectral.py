@@ -1,17 +1,17 @@
-"""Spectral-correction oracle (paper Sec. 3.2; Alg. 1; App. D), float64 numpy.
+"""Spectral-correction oracle (paper Sec. 3.2; Alg. 1; App. E), float64 numpy.
 
 TEST INFRASTRUCTURE ONLY.  Plain definitions, one step per function, in the
 order and notation of the paper:
 
   anchor EMA          M <- beta * M + (1 - beta) * G_anc          (Sec. 3.2 eq.)
-  SVD of the EMA      M = U S V^T, truncated to the top r triplets  (Sec. 3.2; App. D)
+  SVD of the EMA      M = U S V^T, truncated to the top r triplets  (Sec. 3.2; App. E)
   soft filter         d_i = s_i / (s_i + tau)                      (Sec. 3.2 eq.)
   two-sided filter    X = U^T G V;  X_f = diag(d) X diag(d);
                       G_filt = U X_f V^T                           (Sec. 3.2)
   blend               G_proj = alpha * G + (1 - alpha) * G_filt    (Sec. 3.2 eq.)
 
 Readings of the paper taken here (the paper does not fix them):
-  * the top-r truncation of App. D, applied before the soft filter;
+  * the top-r truncation of App. E, applied before the soft filter;
   * tau acts on the raw singular values of the EMA;
   * 0 / 0 in the filter (s_i = 0 with tau = 0) is taken as d_i = 0, so an
     empty prior (M = 0) gives G_proj = alpha * G.
@@ -28,7 +28,7 @@ def ema(M_prev: np.ndarray, G_anc: np.ndarray, beta: float) -> np.ndarray:
 
 
 def top_r_svd(M: np.ndarray, r: int):
-    """Top-r singular triplets of M (Sec. 3.2; App. D truncation).
+    """Top-r singular triplets of M (Sec. 3.2; App. E truncation).
 
     Returns U [m, r], s [r] (descending), V [n, r]."""
     M = np.asarray(M, dtype=np.float64)
@@ -47,7 +47,7 @@ def filter_weights(s: np.ndarray, tau: float) -> np.ndarray:
 
 
 def two_sided_filter(G: np.ndarray, U: np.ndarray, d: np.ndarray, V: np.ndarray) -> np.ndarray:
-    """G_filt = U diag(d) (U^T G V) diag(d) V^T (Sec. 3.2; App. D P_t)."""
+    """G_filt = U diag(d) (U^T G V) diag(d) V^T (Sec. 3.2; App. E P_t)."""
     G = np.asarray(G, dtype=np.float64)
     X = U.T @ G @ V
     Xf = d[:, None] * X * d[None, :]

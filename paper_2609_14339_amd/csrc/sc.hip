@@ -1,4 +1,4 @@
-// Spectral corrector for gfx950 (paper Sec. 3.2; Alg. 1; App. D).
+// Spectral corrector for gfx950 (paper Sec. 3.2; Alg. 1; App. E).
 //
 // sc_build_prior: anchor EMA, then the top-r SVD of the EMA by randomised
 // block subspace iteration (MFMA tall-skinny passes over M, CholeskyQR2 with an

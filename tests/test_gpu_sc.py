@@ -1,5 +1,5 @@
 """GPU parity of the spectral corrector against the CPU oracle (Sec. 3.2; Alg. 1;
-App. D).
+App. E).
 
 Tolerances (relative Frobenius error of G_proj against the float64 oracle):
 1e-4 for fp32 inputs, 2e-2 for bf16 inputs with fp32 accumulation.  The

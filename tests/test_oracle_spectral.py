@@ -1,4 +1,4 @@
-"""Pins of the spectral-correction oracle (paper Sec. 3.2; Alg. 1; App. D).
+"""Pins of the spectral-correction oracle (paper Sec. 3.2; Alg. 1; App. E).
 
 The oracle is checked against things other than itself: closed forms for
 inputs whose SVD is known by construction, the special cases the paper names
