@@ -1,0 +1,234 @@
+// Fused blend for gfx950 (see sc_blend.h), bf16 gradients.
+//
+// One workgroup per 128 x 128 tile of G.  The tile's 128 rows of P and 128
+// rows of V (RP bf16 each) go straight from L2 into LDS (global_load_lds:
+// lane L's 16 bytes land at the wave-uniform LDS address in M0 plus 16 L),
+// XOR-swizzled in 128-byte groups; the G tile is loaded into registers right
+// after and stays in flight while the four waves form P V^T on
+// v_mfma_f32_32x32x16_bf16 (64 x 64 per wave).  The fp32 product is staged in
+// LDS in G's row order, and each thread blends its own 16-byte chunks of G
+// and writes them out.  Tiles are dealt so that XCD x owns the row blocks
+// congruent to x mod 8, which keeps each P slice in one L2.
+#include "common.h"
+#include "sc_blend.h"
+
+#include <algorithm>
+
+namespace acsc {
+namespace blend {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((address_space(3))) unsigned char lds_byte;
+
+constexpr int kT = 128;          // tile edge
+constexpr int kStPitch = 132;    // floats per staged product row (conflict-free column writes)
+constexpr int kMaxJobs = 16;
+
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct Job {
+    const uint16_t *G;
+    uint16_t *out;
+    int m, n;
+    const uint16_t *P, *V;
+    int vec;
+};
+struct Batch {
+    int count;
+    Job j[kMaxJobs];
+};
+
+__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row & 8) >> 1); }
+
+__device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
+{
+    // M0 is not otherwise used by this kernel
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr) : "memory");
+}
+
+__device__ __forceinline__ void sync_lds()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int RP>
+__global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
+{
+    constexpr int RB = RP * 2;                  // bytes per P / V row
+    constexpr int SLICE = kT * RB;              // bytes of one 128-row slice
+    constexpr int NI = 2 * SLICE / 1024;        // DMA instructions for P and V
+    static_assert(NI % 4 == 0 && RB % 128 == 0, "slice layout");
+    constexpr int LDS = (2 * SLICE > kT * kStPitch * 4) ? 2 * SLICE : kT * kStPitch * 4;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[LDS];
+
+    const Job &J = jb.j[blockIdx.z];
+    const int m = J.m, n = J.n;
+    const int rb_n = static_cast<int>(cdiv(m, kT)), cb_n = static_cast<int>(cdiv(n, kT));
+    const int b = blockIdx.x;
+    const int xcd = b & 7, t = b >> 3;
+    const int rb = xcd + 8 * (t / cb_n);
+    const int cb = t % cb_n;
+    if (rb >= rb_n)
+        return;
+    const int row0 = rb * kT, col0 = cb * kT;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_byte *)smem));
+
+    // P rows row0.. and V rows col0.. (clamped: rows past the end only feed
+    // outputs that are never stored), 16 bytes per lane, swizzled per row
+#pragma unroll
+    for (int u = 0; u < NI / 4; ++u) {
+        const int ins = u * 4 + wave;
+        const int off = (ins * 1024 + lane * 16) % SLICE;   // byte offset within the slice
+        const bool isV = ins * 1024 >= SLICE;
+        const int r = off / RB;
+        const int cl = (off % RB) / 16;
+        const int c = (cl & ~7) | ((cl & 7) ^ swz(r));
+        const uint16_t *src = isV ? J.V + static_cast<int64_t>(min(col0 + r, n - 1)) * RP
+                                  : J.P + static_cast<int64_t>(min(row0 + r, m - 1)) * RP;
+        dma16(src + c * 8, lds0 + ins * 1024);
+    }
+    // the G tile into registers: thread q holds row q / 16, columns 8 (q % 16) ..
+    uint4 g[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int q = tid + 256 * u;
+        const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (gi < m) {
+            const uint16_t *src = J.G + static_cast<int64_t>(gi) * n + gj;
+            if (J.vec && gj + 8 <= n) {
+                v = *reinterpret_cast<const uint4 *>(src);
+            } else {
+                uint16_t e8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    e8[e] = gj + e < n ? src[e] : uint16_t(0);
+                __builtin_memcpy(&v, e8, sizeof(v));
+            }
+        }
+        g[u] = v;
+    }
+    // the slices have landed once at most the G loads are outstanding
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    sync_lds();
+
+    // P V^T: wave w computes rows 64 (w / 2) .., columns 64 (w % 2) .. as 2 x 2
+    // tiles of 32 x 32; A[i][k] / B[k][j] in lane i (j) + 32 (k / 8), element k % 8
+    const unsigned char *Ps = smem, *Vs = smem + SLICE;
+    const int wr = (wave >> 1) * 64, wc = (wave & 1) * 64;
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[a][c][e] = 0.f;
+#pragma unroll
+    for (int kq = 0; kq < RP / 16; ++kq) {
+        const int cs = kq * 2 + (lane >> 5);   // logical 16-byte chunk of the row
+        bf16x8 af[2], bfr[2];
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+            const int r = wr + a * 32 + (lane & 31);
+            af[a] = *reinterpret_cast<const bf16x8 *>(Ps + r * RB + 16 * ((cs & ~7) | ((cs & 7) ^ swz(r))));
+        }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int r = wc + c * 32 + (lane & 31);
+            bfr[c] = *reinterpret_cast<const bf16x8 *>(Vs + r * RB + 16 * ((cs & ~7) | ((cs & 7) ^ swz(r))));
+        }
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+                acc[a][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[c], acc[a][c], 0, 0, 0);
+    }
+    sync_lds();
+    // stage the product (D[i][j]: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4)
+    float *St = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int i = wr + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+                const int j = wc + c * 32 + (lane & 31);
+                St[i * kStPitch + j] = acc[a][c][e];
+            }
+    sync_lds();
+    const float oma = 1.0f - alpha;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int q = tid + 256 * u;
+        const int rr = q >> 4, c8 = (q & 15) * 8;
+        const int gi = row0 + rr, gj = col0 + c8;
+        if (gi >= m)
+            continue;
+        const float4 p0 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8]);
+        const float4 p1 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8 + 4]);
+        const float pf[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+        const uint32_t w[4] = {g[u].x, g[u].y, g[u].z, g[u].w};
+        uint32_t o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = alpha * __uint_as_float(w[e] << 16) + oma * pf[2 * e];
+            const float hi = alpha * __uint_as_float(w[e] & 0xFFFF0000u) + oma * pf[2 * e + 1];
+            o[e] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+        }
+        uint16_t *dst = J.out + static_cast<int64_t>(gi) * n + gj;
+        if (J.vec && gj + 8 <= n) {
+            *reinterpret_cast<uint4 *>(dst) = make_uint4(o[0], o[1], o[2], o[3]);
+        } else {
+            const uint16_t *e8 = reinterpret_cast<const uint16_t *>(o);
+            for (int e = 0; e < 8 && gj + e < n; ++e)
+                dst[e] = e8[e];
+        }
+    }
+}
+
+template <int RP>
+void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float alpha, hipStream_t st)
+{
+    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
+        Batch b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
+        for (int i = 0; i < b.count; ++i)
+            b.j[i] = jobs[c0 + i];
+        auto kern = blend_kernel<RP>;
+        ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha);
+    }
+}
+
+}  // namespace
+
+bool supported(int RP) { return RP == 64 || RP == 128 || RP == 192; }
+
+int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st)
+{
+    if (!supported(RP))
+        return set_error(ACSC_EINVAL, "blend: padded rank %d not handled by the streamed-tile kernel", RP);
+    std::vector<Job> jobs;
+    int tiles = 1;
+    for (const Req &q : reqs) {
+        const bool vec = q.n % 8 == 0 && reinterpret_cast<uintptr_t>(q.G) % 16 == 0 &&
+                         reinterpret_cast<uintptr_t>(q.out) % 16 == 0;
+        jobs.push_back(Job{q.G, q.out, q.m, q.n, q.P, q.V, vec ? 1 : 0});
+        const int64_t rbn = cdiv(q.m, kT), cbn = cdiv(q.n, kT);
+        tiles = std::max<int>(tiles, static_cast<int>(cdiv(rbn, 8) * 8 * cbn));
+    }
+    switch (RP) {
+    case 64: launch_rp<64>(tag, jobs, tiles, alpha, st); break;
+    case 128: launch_rp<128>(tag, jobs, tiles, alpha, st); break;
+    default: launch_rp<192>(tag, jobs, tiles, alpha, st); break;
+    }
+    return ACSC_OK;
+}
+
+}  // namespace blend
+}  // namespace acsc

@@ -1,0 +1,700 @@
+// Streaming passes for gfx950: a large bf16 matrix times a thin bf16 factor,
+// fp32 accumulation on v_mfma_f32_16x16x32_bf16 (see sc_pass.h).
+//
+// The large operand is the HBM stream; the thin factor is small and is read
+// from L2.  A workgroup owns 256 output rows (four waves of 64) and walks its
+// K range in 64-deep steps.  Each step's slice of the thin factor is staged
+// once in LDS and shared by the four waves; each wave stages its own 64 lines
+// of A (128 contiguous bytes each) in LDS in the order they were loaded and
+// reads its MFMA fragments back from there: 16-byte reads for opA = A,
+// 16-bit gathers for opA = A^T.  Loads run two steps ahead in registers and
+// the LDS tiles are double-buffered: one barrier per step.  Output rows are independent, so the K range is only
+// split (into power-of-two slices, partials summed by a second kernel) when
+// the batch has too few row blocks to give every CU one; block b works on
+// split b % splits, which keeps each split on the same XCDs.
+#include "common.h"
+#include "sc_pass.h"
+
+#include <algorithm>
+
+namespace acsc {
+namespace pass {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) unsigned char lds_byte;
+
+constexpr int kBM = 256;            // output rows per workgroup
+constexpr int kBK = 64;             // depth of one step
+constexpr int kBPitch = kBK + 8;    // bf16 per LDS row of the thin factor (144 B, 16-B aligned)
+constexpr int kTPitch = 66;         // bf16 per k-row of a wave's A^T tile (33 dwords: conflict-free reads)
+constexpr int kMaxNT = SC_KMAX / 16;
+constexpr int kMaxJobs = 16;
+
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+
+struct Job {
+    const uint16_t *A;
+    int64_t lda;
+    const uint16_t *Bt;
+    int64_t ldbt;
+    float *C;
+    int64_t ldc, split_stride;
+    int M, K, kchunk, splits, nblocks, avec;
+};
+
+struct Batch {
+    int count;
+    Job j[kMaxJobs];
+};
+
+// Keep the first `avail` bf16 elements of an 8-element chunk, zero the rest.
+__device__ __forceinline__ uint4 keep_first(uint4 v, int avail)
+{
+    auto m = [&](int e) -> uint32_t { return (e < avail ? 0xFFFFu : 0u) | (e + 1 < avail ? 0xFFFF0000u : 0u); };
+    v.x &= m(0);
+    v.y &= m(2);
+    v.z &= m(4);
+    v.w &= m(6);
+    return v;
+}
+
+// 8 bf16 from a possibly unaligned address, elements >= avail read as zero.
+__device__ __forceinline__ uint4 load8_scalar(const uint16_t *src, int avail)
+{
+    uint16_t e8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        e8[e] = e < avail ? src[e] : uint16_t(0);
+    uint4 v;
+    __builtin_memcpy(&v, e8, sizeof(v));
+    return v;
+}
+
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// fences global memory, which makes every wave wait for its outstanding
+// global loads at the barrier and would drain the prefetch pipeline.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ bf16x8 as_frag(const uint4 &v)
+{
+    bf16x8 f;
+    __builtin_memcpy(&f, &v, sizeof(f));
+    return f;
+}
+
+// VEC: A rows start 16-byte aligned and the row stride is a multiple of 8,
+// so every 16-byte chunk that starts inside a row lies inside its padded
+// extent.  Loads then need no guards: rows past the end are clamped to the
+// last row (they only feed outputs that are never stored, or meet zero rows
+// of the thin factor) and k is masked when a tail step is staged in LDS.
+// !VEC: element loads with full guards (unaligned operands).
+// NTK column tiles are computed; tiles at or past np / 16 read zeros and are
+// not stored.
+template <bool TRANS, int NTK, bool VEC>
+__global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
+{
+    const Job &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.x) >= J.nblocks)
+        return;
+    constexpr int NT = NTK;
+    constexpr int NP = NT * 16;
+    constexpr int BCH = NP * (kBK / 8);        // 16-byte chunks of one thin-factor step
+    constexpr int BPT = (BCH + 255) / 256;
+    // A step per wave: opA = A: [64 rows][kBPitch] (k contiguous);
+    //                  opA = A^T: [64 k][kTPitch] (rows contiguous)
+    constexpr int AW = TRANS ? kBK * kTPitch : 64 * kBPitch;
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][NP * kBPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][4 * AW];
+
+    const uint16_t *__restrict__ A = J.A;
+    const uint16_t *__restrict__ Bt = J.Bt;
+    const int64_t lda = J.lda, ldbt = J.ldbt;
+    const int M = J.M, splits = J.splits;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int split = static_cast<int>(blockIdx.x % splits);
+    const int row0 = static_cast<int>(blockIdx.x / splits) * kBM;
+    const int wrow0 = row0 + wave * 64;
+    const int kbeg = split * J.kchunk;
+    const int kend = min(J.K, kbeg + J.kchunk);
+    const int nsteps = kend > kbeg ? static_cast<int>(cdiv(kend - kbeg, kBK)) : 0;
+    const int bch_live = np * (kBK / 8);
+    // Row blocks walk their K range from different starting steps, so that
+    // at any moment the workgroups read different columns of the stream
+    // (rows of one block are a large power-of-two stride apart and would
+    // otherwise all address the same HBM channels in lockstep).
+    const int rot = nsteps > 0 ? static_cast<int>((static_cast<int64_t>(blockIdx.x / splits) * 37) % nsteps) : 0;
+    auto phys = [&](int s) { const int p = s + rot; return p >= nsteps ? p - nsteps : p; };
+
+    f32x4 acc[4][NT];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Loads never post-process what they fetch (that would wait for the data
+    // right after issue): addresses are clamped into the operand, and the
+    // masking of a tail step happens when the registers are stored to LDS.
+    uint4 rb[BPT];
+    auto load_b = [&](int s) {
+        const int k0 = kbeg + phys(s) * kBK;
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            const int q = min(tid + 256 * j, BCH - 1);
+            const int c = min(q >> 3, np - 1);
+            const int gk = k0 + (q & 7) * 8;
+            rb[j] = *reinterpret_cast<const uint4 *>(Bt + static_cast<int64_t>(c) * ldbt + (gk < kend ? gk : kbeg));
+        }
+    };
+    auto store_b = [&](int buf, int s) {
+        const int k0 = kbeg + phys(s) * kBK;
+        const bool full = k0 + kBK <= kend;
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            const int q = tid + 256 * j;
+            if (q < BCH) {
+                uint4 v = rb[j];
+                if (!full)
+                    v = keep_first(v, kend - (k0 + (q & 7) * 8));
+                if (q >= bch_live)
+                    v = make_uint4(0u, 0u, 0u, 0u);
+                *reinterpret_cast<uint4 *>(&Bs[buf][(q >> 3) * kBPitch + (q & 7) * 8]) = v;
+            }
+        }
+    };
+    // One step of this wave's A: eight 16-byte chunks per lane, chunk j at
+    // line j * 8 + lane / 8 (a row of A, or a k-row of A^T), 16-byte column
+    // (lane % 8): each 128-byte line is read by eight consecutive lanes.
+    auto load_a = [&](uint4 (&ra)[8], int s) {
+        const int k0 = kbeg + phys(s) * kBK;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int line = j * 8 + (lane >> 3);
+            const int c8 = (lane & 7) * 8;
+            if (!TRANS) {
+                const int gi = wrow0 + line;
+                const int gk = k0 + c8;
+                if (VEC) {
+                    // rows past M only feed outputs that are never stored
+                    ra[j] = *reinterpret_cast<const uint4 *>(A + static_cast<int64_t>(min(gi, M - 1)) * lda +
+                                                             (gk < kend ? gk : kbeg));
+                } else {
+                    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+                    if (gi < M)
+                        v = load8_scalar(A + static_cast<int64_t>(gi) * lda + gk, kend - gk);
+                    ra[j] = v;
+                }
+            } else {
+                const int gk = k0 + line;
+                const int gi = wrow0 + c8;
+                if (VEC) {
+                    // k-rows past kend meet zero rows of the thin factor;
+                    // columns past M only feed outputs that are never stored
+                    ra[j] = *reinterpret_cast<const uint4 *>(A + static_cast<int64_t>(min(gk, kend - 1)) * lda +
+                                                             min(gi, (M - 1) & ~7));
+                } else {
+                    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+                    if (gk < kend)
+                        v = load8_scalar(A + static_cast<int64_t>(gk) * lda + gi, M - gi);
+                    ra[j] = v;
+                }
+            }
+        }
+    };
+    auto store_a = [&](const uint4 (&ra)[8], int buf, int s) {
+        const int k0 = kbeg + phys(s) * kBK;
+        const bool full = k0 + kBK <= kend;
+        uint16_t *w = &As[buf][wave * AW];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int line = j * 8 + (lane >> 3);
+            const int c8 = (lane & 7) * 8;
+            if (!TRANS) {
+                uint4 v = ra[j];
+                if (VEC && !full)   // the padding past K may hold anything
+                    v = keep_first(v, kend - (k0 + c8));
+                *reinterpret_cast<uint4 *>(&w[line * kBPitch + c8]) = v;
+            } else {
+                // 33-dword rows: 4-byte stores
+                uint32_t *dst = reinterpret_cast<uint32_t *>(&w[line * kTPitch + c8]);
+                dst[0] = ra[j].x;
+                dst[1] = ra[j].y;
+                dst[2] = ra[j].z;
+                dst[3] = ra[j].w;
+            }
+        }
+    };
+    auto compute = [&](int buf) {
+        const uint16_t *w = &As[buf][wave * AW];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            bf16x8 af[4];
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+                if (!TRANS) {
+                    af[a] = *reinterpret_cast<const bf16x8 *>(
+                        &w[(a * 16 + (lane & 15)) * kBPitch + ks * 32 + (lane >> 4) * 8]);
+                } else {
+                    const uint16_t *col = &w[(ks * 32 + (lane >> 4) * 8) * kTPitch + a * 16 + (lane & 15)];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        af[a][e] = static_cast<short>(col[e * kTPitch]);
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const bf16x8 b = *reinterpret_cast<const bf16x8 *>(
+                    &Bs[buf][(t * 16 + (lane & 15)) * kBPitch + ks * 32 + (lane >> 4) * 8]);
+#pragma unroll
+                for (int a = 0; a < 4; ++a)
+                    acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b, acc[a][t], 0, 0, 0);
+            }
+        }
+    };
+
+    // Pipeline, step s: stage A(s + 1) and B(s + 1) from registers into the
+    // other LDS buffers; issue B(s + 2), then A(s + 3) (two steps of A stay in
+    // flight); multiply step s; barrier.  Every step issues the same loads
+    // (step indices past the end are clamped to the last step, which is
+    // still in L2), so the wait counts stay the same around the loop.
+    if (nsteps > 0) {
+        const int last = nsteps - 1;
+        uint4 r0[8], r1[8];
+        load_b(0);
+        load_a(r0, 0);
+        load_a(r1, min(1, last));
+        store_b(0, 0);
+        store_a(r0, 0, 0);
+        load_b(min(1, last));
+        load_a(r0, min(2, last));
+        lds_barrier();
+        auto step = [&](int s, uint4 (&nxt)[8]) {
+            store_a(nxt, (s + 1) & 1, s + 1);
+            store_b((s + 1) & 1, s + 1);
+            load_b(min(s + 2, last));
+            load_a(nxt, min(s + 3, last));
+            compute(s & 1);
+            lds_barrier();
+        };
+        int s = 0;
+        for (; s + 2 <= nsteps; s += 2) {
+            step(s, r1);
+            step(s + 1, r0);
+        }
+        if (s < nsteps)
+            step(s, r1);
+    }
+
+    float *Cs = J.C + static_cast<int64_t>(split) * J.split_stride;
+    const int64_t ldc = J.ldc;
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int col = t * 16 + (lane & 15);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = wrow0 + a * 16 + (lane >> 4) * 4 + e;
+                if (row < M && col < np)
+                    Cs[static_cast<int64_t>(row) * ldc + col] = acc[a][t][e];
+            }
+        }
+}
+
+// ---------------------------------------------------------------------------
+// Streaming pass with the loads going straight from HBM into LDS
+// (global_load_lds_dwordx4: lane L's 16 bytes land at the wave-uniform LDS
+// address in M0 plus 16 L).  An LDS ring of S stages holds, per step, the
+// workgroup's 256 lines of A (a row of A, or a k-row of A^T: 128 bytes each)
+// and the NP lines of the thin factor (128 bytes of k each).  Each line's
+// eight 16-byte chunks are stored XOR-swizzled (slot = chunk ^ swz(line)) so
+// that fragment reads from consecutive lines hit distinct banks.  No
+// register staging: registers hold only the accumulators, and S - 1 steps of
+// the stream are in flight while one is multiplied.  Used for 16-byte
+// aligned operands (VEC); waits on the DMA counters are explicit.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int swz(int line) { return (line & 7) ^ ((line & 8) >> 1); }
+
+__device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
+{
+    // M0 is not otherwise used by these kernels (no GWS, no indirect register moves)
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_dma()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void sync_lds()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// One workgroup per CU (the LDS ring takes most of the 160 KiB), so the
+// register budget is that of one wave per SIMD.
+template <bool TRANS, int NT, int S>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void pass_dma_kernel(const Batch jb, int np)
+{
+    const Job &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.x) >= J.nblocks)
+        return;
+    constexpr int NP = NT * 16;
+    constexpr int A_BYTES = 256 * 128;
+    constexpr int STAGE = A_BYTES + NP * 128;
+    constexpr int BI = NT / 2;            // thin-factor DMA instructions per wave and step
+    constexpr int PER_STEP = 8 + BI;      // DMA instructions per wave and step
+    static_assert(S >= 2 && PER_STEP * (S - 2) < 64, "vmcnt range");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[S * STAGE];
+
+    const uint16_t *__restrict__ A = J.A;
+    const uint16_t *__restrict__ Bt = J.Bt;
+    const int64_t lda = J.lda, ldbt = J.ldbt;
+    const int M = J.M, splits = J.splits;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int split = static_cast<int>(blockIdx.x % splits);
+    const int row0 = static_cast<int>(blockIdx.x / splits) * kBM;
+    const int wrow0 = row0 + wave * 64;
+    const int kbeg = split * J.kchunk;
+    const int kend = min(J.K, kbeg + J.kchunk);
+    const int nsteps = kend > kbeg ? static_cast<int>(cdiv(kend - kbeg, kBK)) : 0;
+    const int rot = nsteps > 0 ? static_cast<int>((static_cast<int64_t>(blockIdx.x / splits) * 37) % nsteps) : 0;
+    auto phys = [&](int s) { const int p = s + rot; return p >= nsteps ? p - nsteps : p; };
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_byte *)smem));
+
+    f32x16 acc[2][NT / 2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int t = 0; t < NT / 2; ++t)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[a][t][e] = 0.f;
+
+    // Issue one step's DMA into stage `st`: this wave's 64 lines of A (8
+    // instructions), then BI of the 2 NT instructions of the thin factor.
+    // Addresses are clamped into the operands: rows past M feed outputs that
+    // are never stored, thin-factor rows past np feed columns that are never
+    // stored, k past kend is zeroed in LDS before the tail step is used.
+    auto issue = [&](int s, int st) {
+        const int k0 = kbeg + phys(s) * kBK;
+        const uint32_t sbase = lds0 + st * STAGE;
+        const int sub = lane >> 3;            // line within the instruction
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int line = j * 8 + sub;     // line within this wave's 64
+            const int c = (lane & 7) ^ swz(line);
+            const uint16_t *src;
+            if (!TRANS) {
+                const int gk = k0 + c * 8;
+                src = A + static_cast<int64_t>(min(wrow0 + line, M - 1)) * lda + (gk < kend ? gk : kbeg);
+            } else {
+                src = A + static_cast<int64_t>(min(k0 + line, kend - 1)) * lda + min(wrow0 + c * 8, (M - 1) & ~7);
+            }
+            dma16(src, sbase + wave * 8192 + j * 1024);
+        }
+#pragma unroll
+        for (int b = 0; b < BI; ++b) {
+            const int m = b * 4 + wave;       // instruction index within the thin-factor tile
+            const int line = m * 8 + sub;
+            const int c = (lane & 7) ^ swz(line);
+            const int gk = k0 + c * 8;
+            const uint16_t *src = Bt + static_cast<int64_t>(min(line, np - 1)) * ldbt + (gk < kend ? gk : kbeg);
+            dma16(src, sbase + A_BYTES + m * 1024);
+        }
+    };
+    // Tail step: zero k >= kend in the thin factor (and in A when k runs
+    // along A's rows, whose padding may hold anything).
+    auto fix_tail = [&](int st, int k0) {
+        unsigned char *base = smem + st * STAGE;
+        const int kk = kend - k0;
+        const int nlines = (TRANS ? 0 : 256) + NP;
+        for (int q = tid; q < nlines * 8; q += 256) {
+            const int l = q >> 3, c = q & 7;
+            if (c * 8 + 8 <= kk)
+                continue;
+            unsigned char *line = !TRANS && l < 256 ? base + l * 128 : base + A_BYTES + (l - (TRANS ? 0 : 256)) * 128;
+            const int lidx = !TRANS && l < 256 ? (l & 63) : (l - (TRANS ? 0 : 256));
+            uint4 *slot = reinterpret_cast<uint4 *>(line + 16 * (c ^ swz(lidx)));
+            *slot = keep_first(*slot, kk - c * 8);
+        }
+    };
+    // v_mfma_f32_32x32x16_bf16 (one wave per SIMD reaches its full rate with
+    // it, unlike 16x16x32): A[i][k] / B[k][j] in lane i (j) + 32 (k / 8),
+    // element k % 8.  The wave's 64 rows are two row tiles, the NP columns NC
+    // column tiles; a 64-deep step is four 16-deep substeps.
+    constexpr int NC = NT / 2;
+    auto frags = [&](const unsigned char *aw, const unsigned char *bw, int kq, bf16x8 (&af)[2], bf16x8 (&bf)[NC]) {
+        const int c = kq * 2 + (lane >> 5);
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+            if (!TRANS) {
+                const int line = a * 32 + (lane & 31);
+                af[a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
+            } else {
+                // ds_read_b64_tr_b16: in each group of 16 lanes, result lane
+                // L, element e = element L % 4 of what lane 4 e + L / 4 read.
+                // Source lane 4 e + q of the group reads columns 4 q .. 4 q + 3
+                // (of the group's 16) from k-line e, so lane L receives column
+                // L of four consecutive k-lines; two reads give the eight k of
+                // a fragment.
+                const int l16 = lane & 15;
+                const int col = a * 32 + ((lane >> 4) & 1) * 16 + (l16 & 3) * 4;
+                const int line0 = kq * 16 + (lane >> 5) * 8 + (l16 >> 2);
+                v4i16 h0, h1;
+                {
+                    const int line = line0;
+                    h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
+                        (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
+                }
+                {
+                    const int line = line0 + 4;
+                    h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
+                        (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
+                }
+                af[a] = bf16x8{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NC; ++t) {
+            const int line = t * 32 + (lane & 31);
+            bf[t] = *reinterpret_cast<const bf16x8 *>(bw + line * 128 + 16 * (c ^ swz(line)));
+        }
+    };
+    auto compute = [&](int st) {
+        const unsigned char *base = smem + st * STAGE;
+        const unsigned char *aw = base + wave * 8192;
+        const unsigned char *bw = base + A_BYTES;
+        bf16x8 af[2][2], bf[2][NC];
+        frags(aw, bw, 0, af[0], bf[0]);
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) {
+            if (kq + 1 < 4)
+                frags(aw, bw, kq + 1, af[(kq + 1) & 1], bf[(kq + 1) & 1]);
+#pragma unroll
+            for (int t = 0; t < NC; ++t)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    acc[a][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kq & 1][a], bf[kq & 1][t], acc[a][t], 0, 0, 0);
+        }
+        // keep each substep's fragment reads ahead of the previous substep's MFMAs
+        constexpr int DS = (TRANS ? 4 : 2) + NC;
+        __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
+#pragma unroll
+        for (int kq = 0; kq < 3; ++kq) {
+            __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * NC, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NC, 0);
+    };
+
+    if (nsteps > 0) {
+        const int last = nsteps - 1;
+#pragma unroll
+        for (int p = 0; p < S - 1; ++p)
+            issue(min(p, last), p);
+        int st = 0;   // stage of step s
+        for (int s = 0; s < nsteps; ++s) {
+            wait_dma<PER_STEP * (S - 2)>();   // this wave's DMA for step s has landed
+            sync_lds();                        // everyone's has; stage (s - 1) % S is free
+            const int k0 = kbeg + phys(s) * kBK;
+            if (k0 + kBK > kend) {
+                fix_tail(st, k0);
+                sync_lds();
+            }
+            int nst = st + S - 1;
+            if (nst >= S)
+                nst -= S;
+            issue(min(s + S - 1, last), nst);
+            compute(st);
+            if (++st == S)
+                st = 0;
+        }
+        wait_dma<0>();
+    }
+
+    // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
+    float *Cs = J.C + static_cast<int64_t>(split) * J.split_stride;
+    const int64_t ldc = J.ldc;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int t = 0; t < NT / 2; ++t) {
+            const int col = t * 32 + (lane & 31);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = wrow0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+                if (row < M && col < np)
+                    Cs[static_cast<int64_t>(row) * ldc + col] = acc[a][t][e];
+            }
+        }
+}
+
+// C[i, c] = sum over splits of part[s][i, c] (NP columns, float4 when aligned).
+struct RedJob {
+    const float *part;
+    int64_t split_stride;
+    float *C;
+    int64_t ldc;
+    int M, NP, splits;
+};
+struct RedBatch {
+    int count;
+    RedJob j[kMaxJobs];
+};
+
+__global__ __launch_bounds__(256) void pass_reduce_kernel(const RedBatch jb)
+{
+    const RedJob &J = jb.j[blockIdx.z];
+    const int64_t n4 = static_cast<int64_t>(J.M) * (J.NP / 4);
+    const int q4 = J.NP / 4;
+    for (int64_t idx = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; idx < n4;
+         idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t i = idx / q4;
+        const int c = static_cast<int>(idx % q4) * 4;
+        float4 s = *reinterpret_cast<const float4 *>(J.part + i * J.NP + c);
+        for (int p = 1; p < J.splits; ++p) {
+            const float4 v = *reinterpret_cast<const float4 *>(J.part + p * J.split_stride + i * J.NP + c);
+            s.x += v.x;
+            s.y += v.y;
+            s.z += v.z;
+            s.w += v.w;
+        }
+        *reinterpret_cast<float4 *>(J.C + i * J.ldc + c) = s;
+    }
+}
+
+template <bool TRANS, int NTK, bool VEC>
+void launch_nt(const char *tag, const std::vector<Job> &jobs, int gx, int np, hipStream_t st)
+{
+    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
+        Batch b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
+        for (int i = 0; i < b.count; ++i)
+            b.j[i] = jobs[c0 + i];
+        if (VEC) {
+            // three LDS stages while they fit in 160 KiB, else two
+            constexpr int S = (3 * (256 * 128 + NTK * 16 * 128) <= 160 * 1024) ? 3 : 2;
+            auto kern = pass_dma_kernel<TRANS, NTK, S>;
+            ACSC_LAUNCH(tag, kern, dim3(gx, 1, b.count), dim3(256), 0, st, b, np);
+        } else {
+            auto kern = pass_kernel<TRANS, NTK, false>;
+            ACSC_LAUNCH(tag, kern, dim3(gx, 1, b.count), dim3(256), 0, st, b, np);
+        }
+    }
+}
+
+// Column tiles are computed in pairs (even NTK); unaligned operands take the
+// element-load variant, which is built for the largest width only.
+template <bool TRANS>
+int launch(const char *tag, int np, bool vec, const std::vector<Job> &jobs, int gx, hipStream_t st)
+{
+    if (jobs.empty())
+        return ACSC_OK;
+    if (np < 16 || np % 16 != 0 || np > SC_KMAX)
+        return set_error(ACSC_EINVAL, "pass with %d thin-factor columns (a multiple of 16 up to %d)", np, SC_KMAX);
+    if (!vec) {
+        launch_nt<TRANS, kMaxNT, false>(tag, jobs, gx, np, st);
+        return ACSC_OK;
+    }
+    switch ((np / 16 + 1) / 2) {
+    case 1: launch_nt<TRANS, 2, true>(tag, jobs, gx, np, st); break;
+    case 2: launch_nt<TRANS, 4, true>(tag, jobs, gx, np, st); break;
+    case 3: launch_nt<TRANS, 6, true>(tag, jobs, gx, np, st); break;
+    case 4: launch_nt<TRANS, 8, true>(tag, jobs, gx, np, st); break;
+    case 5: launch_nt<TRANS, 10, true>(tag, jobs, gx, np, st); break;
+    default: launch_nt<TRANS, 12, true>(tag, jobs, gx, np, st); break;
+    }
+    return ACSC_OK;
+}
+
+}  // namespace
+
+int max_splits(int64_t M, int64_t K)
+{
+    const int64_t mb = cdiv(M, kBM);
+    int s = 1;
+    while (s < 16 && mb * s < 256 && K / (2 * s) >= 512)
+        s *= 2;
+    return s;
+}
+
+int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t st)
+{
+    if (reqs.empty())
+        return ACSC_OK;
+    const int NP = reqs[0].NP;
+    for (const auto &q : reqs)
+        if (q.NP != NP)
+            return set_error(ACSC_EINVAL, "pass: thin factors of one launch must have the same width");
+    // Split K only as far as needed for one workgroup per CU over the batch.
+    int64_t blocks = 0;
+    for (const auto &q : reqs)
+        blocks += cdiv(q.M, kBM);
+    int want = 1;
+    while (want < 16 && blocks * want < 256)
+        want *= 2;
+    // Longest K first: workgroups are dispatched in job order, so the long
+    // row blocks start early and the short ones fill in behind them.
+    std::vector<size_t> order(reqs.size());
+    for (size_t i = 0; i < order.size(); ++i)
+        order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return reqs[a].K > reqs[b].K; });
+    std::vector<Job> jobs;
+    std::vector<RedJob> red;
+    int gx = 1;
+    int64_t rtot = 1;
+    for (size_t oi : order) {
+        const Req &q = reqs[oi];
+        int splits = std::min(want, max_splits(q.M, q.K));
+        const int64_t chunk = round_up(cdiv(q.K, splits), kBK);
+        splits = static_cast<int>(std::max<int64_t>(1, cdiv(q.K, chunk)));
+        const int nb = static_cast<int>(cdiv(q.M, kBM) * splits);
+        gx = std::max(gx, nb);
+        if (splits == 1) {
+            jobs.push_back(Job{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, 0, q.M, q.K, static_cast<int>(chunk), 1,
+                               nb, q.avec ? 1 : 0});
+        } else {
+            const int64_t ss = static_cast<int64_t>(q.M) * NP;
+            jobs.push_back(Job{q.A, q.lda, q.Bt, q.ldbt, q.part, NP, ss, q.M, q.K, static_cast<int>(chunk),
+                               splits, nb, q.avec ? 1 : 0});
+            red.push_back(RedJob{q.part, ss, q.C, q.ldc, q.M, NP, splits});
+            rtot = std::max<int64_t>(rtot, static_cast<int64_t>(q.M) * (NP / 4));
+        }
+    }
+    gx = static_cast<int>(round_up(gx, 8));   // block -> XCD placement is the same for every job
+    std::vector<Job> vj, sj;
+    for (const Job &j : jobs)
+        (j.avec ? vj : sj).push_back(j);
+    for (int v = 0; v < 2; ++v) {
+        const std::vector<Job> &js = v == 0 ? vj : sj;
+        const int rc = trans ? launch<true>(tag, NP, v == 0, js, gx, st) : launch<false>(tag, NP, v == 0, js, gx, st);
+        if (rc != ACSC_OK)
+            return rc;
+    }
+    for (size_t c0 = 0; c0 < red.size(); c0 += kMaxJobs) {
+        RedBatch b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxJobs, red.size() - c0));
+        for (int i = 0; i < b.count; ++i)
+            b.j[i] = red[c0 + i];
+        const unsigned g = static_cast<unsigned>(std::min<int64_t>(cdiv(rtot, 256), 8192));
+        ACSC_LAUNCH("sc_split_reduce", pass_reduce_kernel, dim3(g, 1, b.count), dim3(256), 0, st, b);
+    }
+    return ACSC_OK;
+}
+
+}  // namespace pass
+}  // namespace acsc

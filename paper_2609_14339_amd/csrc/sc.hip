@@ -7,6 +7,8 @@
 // sc_correct: T = G V (MFMA, split-K), X = U^T T, X_f = d X d, P = U X_f, then
 // one fused pass G_proj = alpha G + (1 - alpha) P V^T.
 #include "common.h"
+#include "sc_pass.h"
+#include "sc_blend.h"
 
 #include <algorithm>
 #include <vector>
@@ -212,222 +214,6 @@ __global__ __launch_bounds__(256) void gemm_tall_kernel(const Batch<GemmJob<TA, 
             }
         }
     }
-}
-
-// ---------------------------------------------------------------------------
-// Streaming pass over a large bf16 matrix with a thin right factor:
-//   C[s][i, c] = sum_{k in split s} opA[i, k] * B[k, c],   c < NP (<= SC_KMAX)
-// opA = A ([M, K] row-major, lda) or A^T (A stored [K, M], lda).  The thin
-// factor comes transposed and in bf16, Bt[c][k] (row stride ldbt, a multiple
-// of 8), so both tiles load as 16-byte chunks that go straight into LDS rows
-// with k contiguous, as v_mfma_f32_16x16x32_bf16 reads them.  BM rows per
-// workgroup (4 waves of BM/4 rows), 64-deep K steps, the next two steps'
-// tiles loaded into registers while the current one is multiplied.  Block b works
-// on split b % splits: workgroups are dealt to the XCDs round-robin, so with
-// splits a power of two up to 8 every XCD keeps to one slice of Bt in its L2.
-// ---------------------------------------------------------------------------
-constexpr int kPBK = 64;
-constexpr int kPPitch = kPBK + 8;   // 144-byte LDS rows: 16-byte aligned, staggered banks
-constexpr int kPBChunks = (kKMax * (kPBK / 8) + 255) / 256;
-
-struct PassJob {
-    const uint16_t *A;
-    int64_t lda;
-    const uint16_t *Bt;
-    int64_t ldbt;
-    float *C;
-    int64_t ldc, split_stride;
-    int M, K, NP, kchunk, splits, avec, nblocks;
-};
-
-template <bool TRANS, int BM>
-__global__ __launch_bounds__(256) void pass_kernel(const Batch<PassJob> jb)
-{
-    const PassJob &J = jb.j[blockIdx.z];
-    if (static_cast<int>(blockIdx.x) >= J.nblocks)
-        return;
-    const uint16_t *__restrict__ A = J.A;
-    const int64_t lda = J.lda;
-    const uint16_t *__restrict__ Bt = J.Bt;
-    const int64_t ldbt = J.ldbt;
-    float *__restrict__ C = J.C;
-    const int64_t ldc = J.ldc, split_stride = J.split_stride;
-    const int M = J.M, K = J.K, NP = J.NP, kchunk = J.kchunk, splits = J.splits, avec = J.avec;
-    constexpr int RT = BM / 64;                    // 16-row MFMA tiles per wave
-    constexpr int ACH = BM * (kPBK / 8) / 256;     // 16-byte A chunks per thread
-    // A^T tiles stay in their loaded [k][i] order (row pitch BM + 4: 8-byte
-    // aligned rows, conflict-free column reads); A tiles are [i][k].
-    constexpr int TPITCH = BM + 4;
-    __shared__ __attribute__((aligned(16))) uint16_t As[TRANS ? kPBK * TPITCH : BM * kPPitch];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[kKMax * kPPitch];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int split = static_cast<int>(blockIdx.x % splits);
-    const int row0 = static_cast<int>(blockIdx.x / splits) * BM;
-    const int kbeg = split * kchunk;
-    const int kend = min(K, kbeg + kchunk);
-    const int NT = NP / 16;
-    const int nbch = NP * (kPBK / 8);
-
-    f32x4 acc[RT][kNTMax];
-#pragma unroll
-    for (int a = 0; a < RT; ++a)
-#pragma unroll
-        for (int t = 0; t < kNTMax; ++t)
-            acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    uint4 ra0[ACH], rb0[kPBChunks], ra1[ACH], rb1[kPBChunks];
-    auto load = [&](uint4 (&ra)[ACH], uint4 (&rb)[kPBChunks], int k0) {
-#pragma unroll
-        for (int j = 0; j < ACH; ++j) {
-            const int q = tid + 256 * j;
-            int gi, gk;
-            if (!TRANS) {
-                gi = row0 + q / (kPBK / 8);
-                gk = k0 + (q % (kPBK / 8)) * 8;
-            } else {
-                gk = k0 + q / (BM / 8);
-                gi = row0 + (q % (BM / 8)) * 8;
-            }
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (!TRANS) {
-                if (gi < M) {
-                    const uint16_t *src = A + static_cast<int64_t>(gi) * lda + gk;
-                    if (avec && gk + 8 <= kend) {
-                        v = *reinterpret_cast<const uint4 *>(src);
-                    } else {
-                        uint16_t e8[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            e8[e] = (gk + e < kend) ? src[e] : uint16_t(0);
-                        v = *reinterpret_cast<const uint4 *>(e8);
-                    }
-                }
-            } else {
-                if (gk < kend) {
-                    const uint16_t *src = A + static_cast<int64_t>(gk) * lda + gi;
-                    if (avec && gi + 8 <= M) {
-                        v = *reinterpret_cast<const uint4 *>(src);
-                    } else {
-                        uint16_t e8[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            e8[e] = (gi + e < M) ? src[e] : uint16_t(0);
-                        v = *reinterpret_cast<const uint4 *>(e8);
-                    }
-                }
-            }
-            ra[j] = v;
-        }
-#pragma unroll
-        for (int j = 0; j < kPBChunks; ++j) {
-            const int q = tid + 256 * j;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (q < nbch) {
-                const int c = q / (kPBK / 8);
-                const int gk = k0 + (q % (kPBK / 8)) * 8;
-                const uint16_t *src = Bt + static_cast<int64_t>(c) * ldbt + gk;
-                if (gk + 8 <= kend) {
-                    v = *reinterpret_cast<const uint4 *>(src);
-                } else {
-                    uint16_t e8[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        e8[e] = (gk + e < kend) ? src[e] : uint16_t(0);
-                    v = *reinterpret_cast<const uint4 *>(e8);
-                }
-            }
-            rb[j] = v;
-        }
-    };
-    auto store = [&](const uint4 (&ra)[ACH], const uint4 (&rb)[kPBChunks]) {
-#pragma unroll
-        for (int j = 0; j < ACH; ++j) {
-            const int q = tid + 256 * j;
-            if (!TRANS) {
-                const int r = q / (kPBK / 8), c8 = (q % (kPBK / 8)) * 8;
-                *reinterpret_cast<uint4 *>(&As[r * kPPitch + c8]) = ra[j];
-            } else {
-                const int kk = q / (BM / 8), i8 = (q % (BM / 8)) * 8;
-                uint2 *dst = reinterpret_cast<uint2 *>(&As[kk * TPITCH + i8]);
-                dst[0] = make_uint2(ra[j].x, ra[j].y);
-                dst[1] = make_uint2(ra[j].z, ra[j].w);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < kPBChunks; ++j) {
-            const int q = tid + 256 * j;
-            if (q < nbch) {
-                const int c = q / (kPBK / 8), k8 = (q % (kPBK / 8)) * 8;
-                *reinterpret_cast<uint4 *>(&Bs[c * kPPitch + k8]) = rb[j];
-            }
-        }
-    };
-
-    auto compute = [&]() {
-#pragma unroll
-        for (int ks = 0; ks < kPBK / 32; ++ks) {
-            bf16x8 af[RT];
-#pragma unroll
-            for (int a = 0; a < RT; ++a) {
-                const int ii = wave * RT * 16 + a * 16 + (lane & 15);
-                if (!TRANS) {
-                    af[a] = *reinterpret_cast<const bf16x8 *>(&As[ii * kPPitch + ks * 32 + (lane >> 4) * 8]);
-                } else {
-                    const uint16_t *col = &As[(ks * 32 + (lane >> 4) * 8) * TPITCH + ii];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        af[a][e] = static_cast<short>(col[e * TPITCH]);
-                }
-            }
-#pragma unroll
-            for (int t = 0; t < kNTMax; ++t) {
-                if (t < NT) {
-                    const bf16x8 b = *reinterpret_cast<const bf16x8 *>(
-                        &Bs[(t * 16 + (lane & 15)) * kPPitch + ks * 32 + (lane >> 4) * 8]);
-#pragma unroll
-                    for (int a = 0; a < RT; ++a)
-                        acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b, acc[a][t], 0, 0, 0);
-                }
-            }
-        }
-    };
-    // two register stages: tiles k0 + 64 and k0 + 128 are in flight while k0
-    // is multiplied
-    if (kbeg < kend)
-        load(ra0, rb0, kbeg);
-    if (kbeg + kPBK < kend)
-        load(ra1, rb1, kbeg + kPBK);
-    for (int k0 = kbeg; k0 < kend; k0 += 2 * kPBK) {
-        __syncthreads();
-        store(ra0, rb0);
-        __syncthreads();
-        if (k0 + 2 * kPBK < kend)
-            load(ra0, rb0, k0 + 2 * kPBK);
-        compute();
-        if (k0 + kPBK >= kend)
-            break;
-        __syncthreads();
-        store(ra1, rb1);
-        __syncthreads();
-        if (k0 + 3 * kPBK < kend)
-            load(ra1, rb1, k0 + 3 * kPBK);
-        compute();
-    }
-    float *Cs = C + static_cast<int64_t>(split) * split_stride;
-#pragma unroll
-    for (int a = 0; a < RT; ++a)
-#pragma unroll
-        for (int t = 0; t < kNTMax; ++t) {
-            if (t < NT) {
-                const int col = t * 16 + (lane & 15);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int row = row0 + wave * RT * 16 + a * 16 + (lane >> 4) * 4 + e;
-                    if (row < M)
-                        Cs[static_cast<int64_t>(row) * ldc + col] = acc[a][t][e];
-                }
-            }
-        }
 }
 
 // Anchor EMA with a bf16 shadow for the streaming passes (one thread per 8
@@ -1424,22 +1210,6 @@ int split_count(int64_t Mdim, int64_t Kdim)
 
 int64_t split_chunk(int64_t Kdim, int splits) { return round_up(cdiv(Kdim, splits), kBK); }
 
-constexpr int kPassBM = 128;
-
-// Splits of the K range for a streaming pass: a power of two up to 8 (so the
-// round-robin XCD placement keeps each split on its own XCDs), enough to give
-// the chip about two workgroups per CU, and at least 512 of K per split.
-int pass_splits(int64_t Mdim, int64_t Kdim)
-{
-    const int64_t mb = cdiv(Mdim, kPassBM);
-    int s = 1;
-    while (s < 8 && mb * s < 512 && Kdim / (2 * s) >= 512)
-        s *= 2;
-    return s;
-}
-
-int64_t pass_chunk(int64_t Kdim, int splits) { return round_up(cdiv(Kdim, splits), kPBK); }
-
 int gram_blocks(int64_t rows) { return static_cast<int>(std::min<int64_t>(64, cdiv(rows, 512))); }
 
 struct Dims {
@@ -1473,8 +1243,8 @@ size_t carve_prior(const Dims &d, bool use16, void *base, PriorWs *w)
     const int64_t mx = std::max(d.m, d.n);
     int64_t s1 = split_count(d.m, d.n), s2 = split_count(d.n, d.m);
     if (use16) {
-        s1 = std::max<int64_t>(s1, pass_splits(d.m, d.n));
-        s2 = std::max<int64_t>(s2, pass_splits(d.n, d.m));
+        s1 = std::max<int64_t>(s1, pass::max_splits(d.m, d.n));
+        s2 = std::max<int64_t>(s2, pass::max_splits(d.n, d.m));
     }
     const int64_t part = std::max<int64_t>(s1 * d.m, s2 * d.n) * d.KP;
     PriorWs t;
@@ -1509,7 +1279,7 @@ struct CorrWs {
 size_t carve_correct(const Dims &d, size_t esize, void *base, CorrWs *w)
 {
     Carve c(base);
-    const int s1 = std::max(split_count(d.m, d.n), esize == 2 ? pass_splits(d.m, d.n) : 1);
+    const int s1 = std::max(split_count(d.m, d.n), esize == 2 ? pass::max_splits(d.m, d.n) : 1);
     const int s2 = split_count(d.r, d.m);
     CorrWs t;
     t.ldv16 = round_up(d.n, 8);
@@ -1599,50 +1369,6 @@ void tall_gemm(const char *tag, const std::vector<GemmReq<TA, TO>> &reqs, hipStr
     }
 }
 
-// One streaming pass per job: C[M, NP] (fp32) = opA * B for a bf16 matrix
-// A and the thin factor given transposed in bf16 (Bt[NP][ldbt]).
-struct PassReq {
-    const uint16_t *A;
-    int64_t lda;
-    bool avec;
-    const uint16_t *Bt;
-    int64_t ldbt;
-    float *C;
-    int64_t ldc;
-    int M, K, NP;
-    float *part;
-};
-
-template <bool TRANS>
-void stream_pass(const char *tag, const std::vector<PassReq> &reqs, hipStream_t st)
-{
-    std::vector<PassJob> jobs;
-    std::vector<ReduceJob<float>> red;
-    int gx = 1;
-    int64_t rtot = 1;
-    for (const auto &q : reqs) {
-        int splits = pass_splits(q.M, q.K);
-        const int64_t chunk = pass_chunk(q.K, splits);
-        splits = static_cast<int>(cdiv(q.K, chunk));
-        const int nb = static_cast<int>(cdiv(q.M, kPassBM) * splits);
-        gx = std::max(gx, nb);
-        if (splits == 1) {
-            jobs.push_back(PassJob{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, 0, q.M, q.K, q.NP, static_cast<int>(chunk),
-                                   1, q.avec ? 1 : 0, nb});
-        } else {
-            const int64_t ss = static_cast<int64_t>(q.M) * q.NP;
-            jobs.push_back(PassJob{q.A, q.lda, q.Bt, q.ldbt, q.part, q.NP, ss, q.M, q.K, q.NP,
-                                   static_cast<int>(chunk), splits, q.avec ? 1 : 0, nb});
-            red.push_back(ReduceJob<float>{q.part, q.NP, ss, splits, q.M, q.NP, q.C, q.ldc});
-            rtot = std::max<int64_t>(rtot, ss);
-        }
-    }
-    gx = static_cast<int>(round_up(gx, 8));   // keeps block -> XCD placement per job
-    launch_jobs(tag, pass_kernel<TRANS, kPassBM>, jobs, dim3(gx), dim3(256), 0, st);
-    if (!red.empty())
-        launch_jobs("sc_split_reduce", reduce_splits_kernel<float>, red, dim3(grid1d(rtot)), dim3(256), 0, st);
-}
-
 // Per-matrix state of a batched call.
 struct Mat {
     const sc_matrix *in;
@@ -1707,7 +1433,7 @@ void orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipS
 }
 
 // EMA + top-r SVD + filter for a group of matrices with the same k.
-void build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int power_iters, float tau,
+int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int power_iters, float tau,
                  hipStream_t st)
 {
     const Dims &d0 = ms[0].D;
@@ -1753,19 +1479,16 @@ void build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int pow
     // one pass Y = M Z  /  Z = M^T Y over every EMA (bf16 shadow on matrix cores, or fp32)
     auto pass = [&](bool mz) {
         if (use16) {
-            std::vector<PassReq> q;
+            std::vector<pass::Req> q;
             for (auto &m : ms) {
                 if (mz)
-                    q.push_back(PassReq{m.pw.M16, m.pw.ld16, true, m.pw.Zt16, m.pw.ldz16, m.pw.Y, KP, m.D.m, m.D.n,
+                    q.push_back(pass::Req{m.pw.M16, m.pw.ld16, true, m.pw.Zt16, m.pw.ldz16, m.pw.Y, KP, m.D.m, m.D.n,
                                         KP, m.pw.part});
                 else
-                    q.push_back(PassReq{m.pw.M16, m.pw.ld16, true, m.pw.Yt16, m.pw.ldy16, m.pw.Z, KP, m.D.n, m.D.m,
+                    q.push_back(pass::Req{m.pw.M16, m.pw.ld16, true, m.pw.Yt16, m.pw.ldy16, m.pw.Z, KP, m.D.n, m.D.m,
                                         KP, m.pw.part});
             }
-            if (mz)
-                stream_pass<false>("sc_pass_mz", q, st);
-            else
-                stream_pass<true>("sc_pass_mtq", q, st);
+            return mz ? pass::run("sc_pass_mz", false, q, st) : pass::run("sc_pass_mtq", true, q, st);
         } else {
             std::vector<GemmReq<float, float>> q;
             for (auto &m : ms) {
@@ -1780,18 +1503,24 @@ void build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int pow
                 tall_gemm<float, false, float>("sc_pass_mz", q, st);
             else
                 tall_gemm<float, true, float>("sc_pass_mtq", q, st);
+            return ACSC_OK;
         }
     };
-    pass(true);
+    int rc = pass(true);
+    if (rc)
+        return rc;
     orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st);
     for (int it = 0; it < power_iters; ++it) {
-        pass(false);
+        if ((rc = pass(false)))
+            return rc;
         orthonormalise(ms, false, 1, use16, st);
-        pass(true);
+        if ((rc = pass(true)))
+            return rc;
         orthonormalise(ms, true, it + 1 == power_iters ? 2 : 1, use16, st);
     }
     // Rayleigh-Ritz: Z = M^T Q (= B^T), B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
-    pass(false);
+    if ((rc = pass(false)))
+        return rc;
     {
         std::vector<const float *> A;
         std::vector<int> rows;
@@ -1820,28 +1549,31 @@ void build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int pow
         g.push_back(GemmReq<float, float>{m.pw.Z, KP, m.pw.Bv, RP, m.in->V, r, m.D.n, KP, r, r, nullptr, nullptr, 0});
     }
     tall_gemm<float, false, float>("sc_basis", g, st);
+    return ACSC_OK;
 }
 
 // X = U^T G V, X_f = d X d, P = U X_f, then G_proj = alpha G + (1 - alpha) P V^T.
 template <typename GT>
-void correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
+int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
 {
     const int RP = ms[0].D.RP;
     const bool b16 = sizeof(GT) == 2;
     // T = G V   [m, RP]
     if (b16) {
         std::vector<TrJob> t;
-        std::vector<PassReq> q;
+        std::vector<pass::Req> q;
         int64_t tot = 1;
         for (auto &m : ms) {
             t.push_back(TrJob{m.in->V, r, m.D.n, r, RP, m.cw.Vt16, m.cw.ldv16});
             tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * RP);
             const bool avec = aligned(m.in->G, 16) && (m.D.n % 8) == 0;
-            q.push_back(PassReq{static_cast<const uint16_t *>(m.in->G), m.D.n, avec, m.cw.Vt16, m.cw.ldv16, m.cw.Tm,
+            q.push_back(pass::Req{static_cast<const uint16_t *>(m.in->G), m.D.n, avec, m.cw.Vt16, m.cw.ldv16, m.cw.Tm,
                                 RP, m.D.m, m.D.n, RP, m.cw.part});
         }
         launch_jobs("sc_transpose", transpose_bf16_kernel, t, dim3(grid1d(tot)), dim3(256), 0, st);
-        stream_pass<false>("sc_gv", q, st);
+        const int rc = pass::run("sc_gv", false, q, st);
+        if (rc)
+            return rc;
     } else {
         std::vector<GemmReq<float, float>> q;
         for (auto &m : ms)
@@ -1887,6 +1619,14 @@ void correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
             gy = std::max<int>(gy, static_cast<int>(cdiv(m.D.m, 64)));
         }
         if constexpr (sizeof(GT) == 2) {
+            if (blend::supported(RP)) {
+                std::vector<blend::Req> q;
+                for (auto &m : ms)
+                    q.push_back(blend::Req{static_cast<const uint16_t *>(m.in->G), static_cast<uint16_t *>(m.in->G_proj),
+                                           m.D.m, m.D.n, static_cast<const uint16_t *>(m.cw.Pc),
+                                           static_cast<const uint16_t *>(m.cw.Vc)});
+                return blend::run("sc_blend", q, RP, alpha, st);
+            }
             // 128 x 128 tiles, XCD-aware order (see blend16_kernel)
             int tiles = 1, cbm = 1;
             bool vec = true;
@@ -1906,6 +1646,7 @@ void correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
             launch_jobs("sc_blend", blend_kernel<GT>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha);
         }
     }
+    return ACSC_OK;
 }
 
 int check_matrix(const sc_matrix &a, int r, int oversample, acsc_dtype dt, bool build, size_t *need)
@@ -2003,7 +1744,9 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
                 group.push_back(all[j]);
                 done[j] = true;
             }
-        build_group(group, dt, beta, r, power_iters, tau, stream);
+        const int rc = build_group(group, dt, beta, r, power_iters, tau, stream);
+        if (rc)
+            return rc;
     }
     return check_launch("sc_build_prior");
 }
@@ -2037,9 +1780,11 @@ extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype d
     if (rc)
         return rc;
     if (dt == ACSC_BF16)
-        correct_group<uint16_t>(all, r, alpha, stream);
+        rc = correct_group<uint16_t>(all, r, alpha, stream);
     else
-        correct_group<float>(all, r, alpha, stream);
+        rc = correct_group<float>(all, r, alpha, stream);
+    if (rc)
+        return rc;
     return check_launch("sc_correct");
 }
 
