@@ -25,8 +25,6 @@ constexpr int kKMax = SC_KMAX;
 constexpr int kBM = 64;   // rows of the output per workgroup in the tall GEMM
 constexpr int kBK = 32;   // depth of one K step
 constexpr int kNTMax = kKMax / 16;
-// Rows of a Jacobi column pair held by each of its 16 lanes.
-constexpr int kRowsPerLane = (kKMax + 15) / 16;
 // Singular values of the prior at or below this fraction of the largest are
 // returned as zero (numerical rank of an fp32 subspace iteration).
 constexpr double kRankCutoff = 1e-5;
@@ -645,10 +643,12 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     float *Bu = J.Bu, *Bv = J.Bv, *s_out = J.s_out, *d_out = J.d_out;
     int *info = J.info;
     extern __shared__ __attribute__((aligned(16))) unsigned char jsm[];
-    // column c at A[c * kp]; kp = k rounded up to 16, rows k..kp-1 are zero, so
-    // the loops over a column have a uniform trip count
+    // column c at A[c * kp]; kp = k rounded up to 32, rows k..kp-1 are zero.
+    // Lane gl of a pair's 16 lanes holds the R = kp / 16 consecutive rows
+    // gl R .. gl R + R - 1 of both columns (R even: 8-byte LDS accesses).
     T *A = reinterpret_cast<T *>(jsm);
-    const int kp = (k + 15) & ~15;
+    const int kp = (k + 31) & ~31;
+    T *nrm = A + static_cast<size_t>(k) * kp;   // squared column norms
     __shared__ unsigned int sh_off;
     __shared__ double sh_cut;
     __shared__ double sig[kKMax];
@@ -663,16 +663,39 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     // four column pairs per wave, 16 lanes each
     const int grp = lane >> 4, gl = lane & 15;
     const int slots = nwave * 4;
+    const int R = kp / 16;
+    constexpr int RMAX = (kKMax + 31) / 32 * 2;
     int sweeps_used = 0;
     float last_off = 0.f;
+    __syncthreads();
     for (int sweep = 0; sweep < max_sweeps; ++sweep) {
+        // exact squared norms at the start of every sweep (the rotations
+        // update them incrementally within it)
+        for (int c = wave * 4 + grp; c < k; c += slots) {
+            const T *ac = A + c * kp + gl * R;
+            T ss = 0;
+#pragma unroll
+            for (int e = 0; e < RMAX; ++e)
+                if (e < R)
+                    ss += ac[e] * ac[e];
+            ss = row16_sum(ss);
+            if (gl == 0)
+                nrm[c] = ss;
+        }
         if (tid == 0)
             sh_off = 0u;
         __syncthreads();
         float wmax = 0.f;
         for (int round = 0; round < n2 - 1; ++round) {
             for (int p = wave * 4 + grp; p < npairs; p += slots) {
-                auto pos = [&](int x) { return x == 0 ? 0 : ((x - 1 + round) % (n2 - 1)) + 1; };
+                auto pos = [&](int x) {
+                    if (x == 0)
+                        return 0;
+                    int t = x - 1 + round;
+                    if (t >= n2 - 1)
+                        t -= n2 - 1;
+                    return t + 1;
+                };
                 int cp = pos(p), cq = pos(n2 - 1 - p);
                 if (cp >= k || cq >= k)
                     continue;
@@ -681,34 +704,39 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
                     cp = cq;
                     cq = t;
                 }
-                T *ap = A + cp * kp;
-                T *aq = A + cq * kp;
-                // the pair's columns stay in registers: 16 lanes x kRowsPerLane rows
-                T xv[kRowsPerLane], yv[kRowsPerLane];
+                T *ap = A + cp * kp + gl * R;
+                T *aq = A + cq * kp + gl * R;
+                T xv[RMAX], yv[RMAX];
 #pragma unroll
-                for (int e = 0; e < kRowsPerLane; ++e) {
-                    xv[e] = T(0);
-                    yv[e] = T(0);
-                    if (16 * e < kp) {
-                        xv[e] = ap[gl + 16 * e];
-                        yv[e] = aq[gl + 16 * e];
+                for (int e = 0; e < RMAX; e += 2) {
+                    if (e < R) {
+                        if constexpr (sizeof(T) == 4) {
+                            const float2 x2 = *reinterpret_cast<const float2 *>(ap + e);
+                            const float2 y2 = *reinterpret_cast<const float2 *>(aq + e);
+                            xv[e] = x2.x;
+                            xv[e + 1] = x2.y;
+                            yv[e] = y2.x;
+                            yv[e + 1] = y2.y;
+                        } else {
+                            xv[e] = ap[e];
+                            xv[e + 1] = ap[e + 1];
+                            yv[e] = aq[e];
+                            yv[e + 1] = aq[e + 1];
+                        }
+                    } else {
+                        xv[e] = xv[e + 1] = yv[e] = yv[e + 1] = T(0);
                     }
                 }
-                // dot products, rotation and update in the storage precision T
-                T al = 0, be = 0, ga = 0;
+                const T al = nrm[cp], be = nrm[cq];
+                T ga = 0;
 #pragma unroll
-                for (int e = 0; e < kRowsPerLane; ++e) {
-                    al += xv[e] * xv[e];
-                    be += yv[e] * yv[e];
+                for (int e = 0; e < RMAX; ++e)
                     ga += xv[e] * yv[e];
-                }
-                al = row16_sum(al);
-                be = row16_sum(be);
                 ga = row16_sum(ga);
-                const T nrm = sqrt(al * be);
-                if (ga == T(0) || nrm == T(0))
+                const T nab = sqrt(al * be);
+                if (ga == T(0) || nab == T(0))
                     continue;
-                const T ratio = fabs(ga) / nrm;
+                const T ratio = fabs(ga) / nab;
                 wmax = fmaxf(wmax, static_cast<float>(ratio));
                 if (ratio <= tol)
                     continue;
@@ -717,12 +745,25 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
                 const T c = T(1) / sqrt(T(1) + t * t);
                 const T sn = c * t;
 #pragma unroll
-                for (int e = 0; e < kRowsPerLane; ++e) {
-                    if (16 * e < kp) {
-                        const T x = xv[e], y = yv[e];
-                        ap[gl + 16 * e] = c * x - sn * y;
-                        aq[gl + 16 * e] = sn * x + c * y;
+                for (int e = 0; e < RMAX; e += 2) {
+                    if (e < R) {
+                        const T x0 = c * xv[e] - sn * yv[e], x1 = c * xv[e + 1] - sn * yv[e + 1];
+                        const T y0 = sn * xv[e] + c * yv[e], y1 = sn * xv[e + 1] + c * yv[e + 1];
+                        if constexpr (sizeof(T) == 4) {
+                            *reinterpret_cast<float2 *>(ap + e) = make_float2(x0, x1);
+                            *reinterpret_cast<float2 *>(aq + e) = make_float2(y0, y1);
+                        } else {
+                            ap[e] = x0;
+                            ap[e + 1] = x1;
+                            aq[e] = y0;
+                            aq[e + 1] = y1;
+                        }
                     }
+                }
+                // the rotation zeroes the pair's inner product: the norms move by t gamma
+                if (gl == 0) {
+                    nrm[cp] = al - t * ga;
+                    nrm[cq] = be + t * ga;
                 }
             }
             __syncthreads();
@@ -1315,6 +1356,9 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
     }
 }
 
+// columns padded to a multiple of 32 rows, plus the squared norms
+size_t jacobi_lds(int k, size_t es) { return (static_cast<size_t>(k) * round_up(k, 32) + k) * es; }
+
 size_t chol_lds(int k) { return (static_cast<size_t>(k) * (k + 1) / 2 + 2 * static_cast<size_t>(k)) * sizeof(double); }
 
 // One tall-skinny product per job (opA * B), split-K through the job's
@@ -1534,13 +1578,12 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         }
         gram(ms, A, rows, st);
         launch_jobs("sc_chol", chol_kernel<false>, cj, dim3(1), dim3(1024), chol_lds(k), st, k, KP);
-        const size_t kp = round_up(k, 16);
         if (k <= 128)
-            launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(1024),
-                        static_cast<size_t>(k) * kp * sizeof(double), st, k, KP, r, RP, tau, 1e-13, 40);
+            launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(1024), jacobi_lds(k, sizeof(double)), st,
+                        k, KP, r, RP, tau, 1e-13, 40);
         else
-            launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(1024),
-                        static_cast<size_t>(k) * kp * sizeof(float), st, k, KP, r, RP, tau, 1e-5f, 40);
+            launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(1024), jacobi_lds(k, sizeof(float)), st,
+                        k, KP, r, RP, tau, 1e-5f, 40);
     }
     // U = Q Bu, V = Z Bv (first r columns)
     std::vector<GemmReq<float, float>> g;
@@ -1727,9 +1770,8 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
         if (!rc)
             rc = allow_lds(chol_kernel<false>, chol_lds(m.D.k));
         if (!rc)
-            rc = m.D.k <= 128
-                     ? allow_lds(jacobi_kernel<double>, static_cast<size_t>(m.D.k) * round_up(m.D.k, 16) * sizeof(double))
-                     : allow_lds(jacobi_kernel<float>, static_cast<size_t>(m.D.k) * round_up(m.D.k, 16) * sizeof(float));
+            rc = m.D.k <= 128 ? allow_lds(jacobi_kernel<double>, jacobi_lds(m.D.k, sizeof(double)))
+                              : allow_lds(jacobi_kernel<float>, jacobi_lds(m.D.k, sizeof(float)));
         if (rc)
             return rc;
     }
