@@ -110,6 +110,47 @@ __device__ __forceinline__ int wave_exclusive_scan(int v, int lane)
     return incl - v;
 }
 
+// Each wave owns one row and its own slice of LDS, so the kernels only need
+// their LDS accesses ordered within the wave (an LDS queue serves a wave in
+// order); no workgroup barrier.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Set the bits of pi(0) .. pi(K - 1) in the row bitmap.  Cycle walking takes a
+// varying number of Feistel evaluations per index, so instead of one index
+// per lane at a time (the wave waiting for its longest walk), every lane
+// performs one evaluation per step and a lane whose walk ended takes the next
+// unassigned index; the wave runs about 2 K / 64 steps for H about half the
+// Feistel domain.
+template <int ROUNDS>
+__device__ __forceinline__ void mark_kept(const RowPerm<ROUNDS> &perm, int K, uint32_t H, uint32_t *bm, int lane)
+{
+    int i = lane;
+    bool live = i < K;
+    uint32_t y = live ? perm.feistel(static_cast<uint32_t>(i)) : 0u;
+    int next = 64;
+    while (__ballot(live)) {
+        const bool done = live && y < H;
+        if (done)
+            atomicOr(&bm[y >> 5], 1u << (y & 31));
+        const unsigned long long fin = __ballot(done);
+        const int before = __popcll(fin & ((1ull << lane) - 1ull));
+        uint32_t src = y;
+        if (done) {
+            i = next + before;
+            live = i < K;
+            src = static_cast<uint32_t>(i);
+        }
+        if (live)
+            y = perm.feistel(src);
+        next += __popcll(fin);
+    }
+}
+
 // Per-wave LDS layout of the pack kernel: bitmap[nw] then uint16 kidx[K].
 __host__ __device__ __forceinline__ int pack_wave_words(int nw, int K) { return nw + (K + 1) / 2; }
 
@@ -129,18 +170,17 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
 
+    if (!active)
+        return;
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
-    __syncthreads();
-    if (active) {
+    wave_sync();
+    {
         const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
-        for (int i = lane; i < K; i += 64) {
-            const uint32_t j = perm(static_cast<uint32_t>(i));
-            atomicOr(&bm[j >> 5], 1u << (j & 31));
-        }
+        mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
     }
-    __syncthreads();
-    if (active) {
+    wave_sync();
+    {
         const int per = (nw + 63) >> 6;
         const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
         int cnt = 0;
@@ -156,16 +196,31 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
             }
         }
     }
-    __syncthreads();
-    if (active) {
+    wave_sync();
+    {
+        // gather four kept values per lane before storing any, so that their
+        // HBM latencies overlap
         const E *xr = x + row * ld_x;
         E *vr = vals + row * K;
         uint16_t *ir = idx ? idx + row * K : nullptr;
-        for (int i = lane; i < K; i += 64) {
-            const uint16_t j = kidx[i];
-            vr[i] = xr[j];
-            if (ir)
-                ir[i] = j;
+        for (int base = 0; base < K; base += 256) {
+            E v[4];
+            uint16_t jj[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = base + lane + 64 * u;
+                jj[u] = i < K ? kidx[i] : uint16_t(0);
+                v[u] = i < K ? xr[jj[u]] : E(0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = base + lane + 64 * u;
+                if (i < K) {
+                    vr[i] = v[u];
+                    if (ir)
+                        ir[i] = jj[u];
+                }
+            }
         }
     }
 }
@@ -210,17 +265,29 @@ struct Vec16<uint32_t> {
 
 // Per-wave LDS of the staged kernels: bitmap[nw], prefix[nw], then the packed
 // row (K values) and, for pack, its K indices.
+// Unpack: bitmap[nw], prefix[nw], the packed row (K values, padded to 8) and
+// a segment of kSegWords bitmap words of the dense row.
+constexpr int kSegWords = 64;
+
+// byte offset of the unpack segment in a wave's LDS (16-byte aligned)
+__host__ __device__ __forceinline__ size_t unpack_seg_offset(int nw, int K, int esize)
+{
+    return (static_cast<size_t>(2 * nw) * 4 + static_cast<size_t>(K) * esize + 15) & ~static_cast<size_t>(15);
+}
+
 __host__ __device__ __forceinline__ size_t staged_wave_bytes(int nw, int K, int esize, bool with_idx)
 {
     size_t b = static_cast<size_t>(2 * nw) * 4 + static_cast<size_t>(K) * esize;
     if (with_idx)
         b += static_cast<size_t>(K) * 2;
+    else
+        b = unpack_seg_offset(nw, K, esize) + static_cast<size_t>(kSegWords) * 32 * esize;
     return (b + 15) & ~static_cast<size_t>(15);
 }
 
-// Builds the kept-set bitmap of `row` (from the key) and the exclusive prefix
-// of its word popcounts.  Every thread of the workgroup calls it (it contains
-// the workgroup barriers).
+// Builds the kept-set bitmap of `row` (from the key, or from the transmitted
+// indices) and the exclusive prefix of its word popcounts.  Every lane of the
+// row's wave calls it.
 template <int ROUNDS>
 __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, bool active, uint64_t key,
                                            int64_t row, int w, int H, int K, int lane,
@@ -228,7 +295,7 @@ __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, 
 {
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
-    __syncthreads();
+    wave_sync();
     if (active) {
         if (idx_row) {
             for (int i = lane; i < K; i += 64) {
@@ -238,13 +305,10 @@ __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, 
             }
         } else {
             const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
-            for (int i = lane; i < K; i += 64) {
-                const uint32_t j = perm(static_cast<uint32_t>(i));
-                atomicOr(&bm[j >> 5], 1u << (j & 31));
-            }
+            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
         }
     }
-    __syncthreads();
+    wave_sync();
     if (active) {
         const int per = (nw + 63) >> 6;
         const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
@@ -257,7 +321,7 @@ __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, 
             pos += __popc(bm[i]);
         }
     }
-    __syncthreads();
+    wave_sync();
 }
 
 // Pack, streaming form: each lane reads whole 16-byte chunks of the row that
@@ -318,7 +382,7 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
             }
         }
     }
-    __syncthreads();
+    wave_sync();
     if (active) {
         E *vr = vals + row * K;
         uint16_t *ir = idx ? idx + row * K : nullptr;
@@ -331,7 +395,10 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
 }
 
 // Unpack, staged form: the packed row is first copied into LDS (coalesced),
-// then every lane writes whole 16-byte chunks of the dense row.
+// then the dense row is built in LDS segment by segment and streamed out.
+// Every lane's work is uniform (zeroing and copying) except the drop of the
+// few kept entries, where writing each 16-byte chunk with its kept entries in
+// place made every lane of the wave pay for the chunks that hold one.
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
 __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restrict__ vals,
                                                                const uint16_t *__restrict__ idx,
@@ -359,46 +426,44 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
                        (FROM_IDX && active) ? idx + row * K : nullptr);
     if (!active)
         return;
+    // The dense row is assembled in LDS one segment (64 bitmap words) at a
+    // time: zero the segment, drop the kept entries into it, then write it out
+    // with whole 16-byte stores.  Global memory only sees full lines.
     E *yr = y + row * ld_y;
-    int jtail = 0;
-    if (VEC) {
-        constexpr int N = Vec16<E>::N;
-        const int nch = H / N;
-#pragma unroll 4
-        for (int c = lane; c < nch; c += 64) {
-            const int j0 = c * N;
-            const uint32_t word = bm[j0 >> 5];
-            const int sh = j0 & 31;
-            const uint32_t bits = (word >> sh) & ((1u << N) - 1u);
-            E out[N];
+    E *seg = reinterpret_cast<E *>(reinterpret_cast<unsigned char *>(bm) + unpack_seg_offset(nw, K, sizeof(E)));
+    constexpr int N = Vec16<E>::N;
+    for (int s0 = 0; s0 < nw; s0 += kSegWords) {
+        const int e0 = s0 * 32;                            // first element of the segment
+        const int len = min(kSegWords * 32, H - e0);       // elements in it
 #pragma unroll
-            for (int e = 0; e < N; ++e)
-                out[e] = 0;
-            if (bits) {
-                int rank = static_cast<int>(pre[j0 >> 5]) + __popc(word & ((1u << sh) - 1u));
-#pragma unroll
-                for (int e = 0; e < N; ++e) {
-                    if (bits & (1u << e))
-                        out[e] = scaled(kv[rank++], scale);
-                }
+        for (int c = lane; c < kSegWords * 32 / N; c += 64)
+            reinterpret_cast<uint4 *>(seg)[c] = make_uint4(0u, 0u, 0u, 0u);
+        wave_sync();
+        const int wd = s0 + lane;
+        if (wd < nw) {
+            uint32_t bits = bm[wd];
+            int rank = static_cast<int>(pre[wd]);
+            while (bits) {
+                const int t = __ffs(bits) - 1;
+                bits &= bits - 1u;
+                seg[lane * 32 + t] = scaled(kv[rank++], scale);
             }
-            *reinterpret_cast<uint4 *>(yr + j0) = *reinterpret_cast<const uint4 *>(out);
         }
-        jtail = nch * N;
-    }
-    for (int j = jtail + lane; j < H; j += 64) {
-        const uint32_t word = bm[j >> 5];
-        const int b = j & 31;
-        E out = 0;
-        if ((word >> b) & 1u) {
-            const int rank = static_cast<int>(pre[j >> 5]) + __popc(word & ((1u << b) - 1u));
-            out = scaled(kv[rank], scale);
+        wave_sync();
+        if (VEC) {
+            const int nch = len / N;
+            for (int c = lane; c < nch; c += 64)
+                *reinterpret_cast<uint4 *>(yr + e0 + c * N) = reinterpret_cast<const uint4 *>(seg)[c];
+            for (int j = nch * N + lane; j < len; j += 64)
+                yr[e0 + j] = seg[j];
+        } else {
+            for (int j = lane; j < len; j += 64)
+                yr[e0 + j] = seg[j];
         }
-        yr[j] = out;
+        wave_sync();
     }
 }
 
-// Per-wave LDS layout of the unpack kernel: bitmap[nw] then prefix[nw].
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
 __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ vals,
                                                         const uint16_t *__restrict__ idx,
@@ -418,7 +483,7 @@ __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ va
 
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
-    __syncthreads();
+    wave_sync();
     if (active) {
         if (FROM_IDX) {
             const uint16_t *ir = idx + row * K;
@@ -436,7 +501,7 @@ __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ va
             }
         }
     }
-    __syncthreads();
+    wave_sync();
     if (active) {
         const int per = (nw + 63) >> 6;
         const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
@@ -449,7 +514,7 @@ __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ va
             pos += __popc(bm[i]);
         }
     }
-    __syncthreads();
+    wave_sync();
     if (!active)
         return;
     const E *vr = vals + row * K;
