@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run one plain copy kernel of known size (512 MiB in, 512 MiB out) before the "
+                         "warmup, as the reference for scaling HBM byte counters")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="approximate budget of the CPU-oracle sample")
     return ap.parse_args()
@@ -112,6 +115,15 @@ def main():
     setup_s = time.time() - t0
     print(f"[bench] inputs ready in {setup_s:.1f} s; HBM in use "
           f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB", file=sys.stderr, flush=True)
+
+    if args.copy_probe:
+        # torch.neg over 128 Mi floats: a plain elementwise kernel that reads
+        # and writes exactly 512 MiB each
+        src = torch.ones(1 << 27, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
     phase_ms = {"ac": 0.0, "build": 0.0, "correct": 0.0}
@@ -236,7 +248,8 @@ def main():
         roof = {"bound": "latency", "achieved": None, "peak": None, "unit": None, "frac": None}
     roof.update({"kernel": dom, "avg_launch_us": round(avg_s * 1e6, 2),
                  "launches_per_step": dom_n, "work_per_launch": per_launch,
-                 "work_unit": "bytes" if bound == "hbm" else "flops", "traffic": None})
+                 "work_unit": "bytes" if bound == "hbm" else "flops",
+                 "traffic": measured_traffic(dom, cfg.cid)})
 
     comp = {}
     for name in ("ac_pack", "ac_unpack", "sc_ema", "sc_gv", "sc_blend"):
@@ -280,6 +293,41 @@ def main():
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hotpath_70b_4layer_hbm_traffic.txt")
+
+
+def kernel_sources_digest() -> str:
+    """SHA-256 over the library's kernel sources (csrc/*.hip, csrc/*.h), in name order."""
+    import hashlib
+    d = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_14339_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                d.update(name.encode() + b"\0" + f.read())
+    return d.hexdigest()
+
+
+def measured_traffic(tag: str, cid: int):
+    """HBM bytes per launch of kernel `tag` from the stored counter summary
+    (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy kernel's reading),
+    or None when there is none for this workload or the kernel sources have
+    changed since the counters were taken."""
+    if cid != 5 or not os.path.exists(TRAFFIC_FILE):
+        return None
+    digest, table = None, {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if line.startswith("# sources_sha256:"):
+                digest = line.split(":", 1)[1].strip()
+            elif line.startswith("traffic "):
+                _, name, per_launch = line.split()[:3]
+                table[name] = float(per_launch)
+    if digest != kernel_sources_digest() or tag not in table:
+        return None
+    return table[tag]
 
 
 def cpu_baseline(cfg, budget_s: float):

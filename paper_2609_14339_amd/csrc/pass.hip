@@ -129,12 +129,6 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
     const int kend = min(J.K, kbeg + J.kchunk);
     const int nsteps = kend > kbeg ? static_cast<int>(cdiv(kend - kbeg, kBK)) : 0;
     const int bch_live = np * (kBK / 8);
-    // Row blocks walk their K range from different starting steps, so that
-    // at any moment the workgroups read different columns of the stream
-    // (rows of one block are a large power-of-two stride apart and would
-    // otherwise all address the same HBM channels in lockstep).
-    const int rot = nsteps > 0 ? static_cast<int>((static_cast<int64_t>(blockIdx.x / splits) * 37) % nsteps) : 0;
-    auto phys = [&](int s) { const int p = s + rot; return p >= nsteps ? p - nsteps : p; };
 
     f32x4 acc[4][NT];
 #pragma unroll
@@ -148,7 +142,7 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
     // masking of a tail step happens when the registers are stored to LDS.
     uint4 rb[BPT];
     auto load_b = [&](int s) {
-        const int k0 = kbeg + phys(s) * kBK;
+        const int k0 = kbeg + s * kBK;
 #pragma unroll
         for (int j = 0; j < BPT; ++j) {
             const int q = min(tid + 256 * j, BCH - 1);
@@ -158,7 +152,7 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
         }
     };
     auto store_b = [&](int buf, int s) {
-        const int k0 = kbeg + phys(s) * kBK;
+        const int k0 = kbeg + s * kBK;
         const bool full = k0 + kBK <= kend;
 #pragma unroll
         for (int j = 0; j < BPT; ++j) {
@@ -177,7 +171,7 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
     // line j * 8 + lane / 8 (a row of A, or a k-row of A^T), 16-byte column
     // (lane % 8): each 128-byte line is read by eight consecutive lanes.
     auto load_a = [&](uint4 (&ra)[8], int s) {
-        const int k0 = kbeg + phys(s) * kBK;
+        const int k0 = kbeg + s * kBK;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int line = j * 8 + (lane >> 3);
@@ -213,7 +207,7 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
         }
     };
     auto store_a = [&](const uint4 (&ra)[8], int buf, int s) {
-        const int k0 = kbeg + phys(s) * kBK;
+        const int k0 = kbeg + s * kBK;
         const bool full = k0 + kBK <= kend;
         uint16_t *w = &As[buf][wave * AW];
 #pragma unroll
@@ -371,8 +365,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int kbeg = split * J.kchunk;
     const int kend = min(J.K, kbeg + J.kchunk);
     const int nsteps = kend > kbeg ? static_cast<int>(cdiv(kend - kbeg, kBK)) : 0;
-    const int rot = nsteps > 0 ? static_cast<int>((static_cast<int64_t>(blockIdx.x / splits) * 37) % nsteps) : 0;
-    auto phys = [&](int s) { const int p = s + rot; return p >= nsteps ? p - nsteps : p; };
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_byte *)smem));
 
     f32x16 acc[2][NT / 2];
@@ -390,7 +382,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // are never stored, thin-factor rows past np feed columns that are never
     // stored, k past kend is zeroed in LDS before the tail step is used.
     auto issue = [&](int s, int st) {
-        const int k0 = kbeg + phys(s) * kBK;
+        const int k0 = kbeg + s * kBK;
         const uint32_t sbase = lds0 + st * STAGE;
         const int sub = lane >> 3;            // line within the instruction
 #pragma unroll
@@ -510,7 +502,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int s = 0; s < nsteps; ++s) {
             wait_dma<PER_STEP * (S - 2)>();   // this wave's DMA for step s has landed
             sync_lds();                        // everyone's has; stage (s - 1) % S is free
-            const int k0 = kbeg + phys(s) * kBK;
+            const int k0 = kbeg + s * kBK;
             if (k0 + kBK > kend) {
                 fix_tail(st, k0);
                 sync_lds();
