@@ -371,12 +371,16 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const Batch<ReduceJo
 }
 
 // ---------------------------------------------------------------------------
-// fp64 Gram matrix of the first KP columns of A (rows x lda, fp32):
-// upper 64x64 tiles per workgroup, rows split across grid.y, partials summed
-// by gram_reduce_kernel, which also mirrors the lower triangle.
+// fp64 Gram matrix of the first KP columns of A (rows x lda, fp32), on
+// v_mfma_f64_16x16x4_f64: one workgroup per block of rows computes every
+// upper 32 x 32 tile (ti <= tj) of that block's partial Gram; the partials
+// are summed by gram_reduce_kernel, which also mirrors the lower triangle.
+// Operands (one fp64 per lane): A[i][k] in lane i + 16 k, B[k][j] in lane
+// j + 16 k; the result D[i][j] sits in lane j + 16 (i % 4), element i / 4.
 // ---------------------------------------------------------------------------
-constexpr int kGT = 64;
-constexpr int kGRows = 32;
+constexpr int kGT = 32;
+constexpr int kGRows = 64;
+typedef double v4d __attribute__((ext_vector_type(4)));
 
 struct GramJob {
     const float *A;
@@ -385,69 +389,85 @@ struct GramJob {
     double *part;
 };
 
+template <int NT>
 __global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> jb, int KP)
 {
     const GramJob &J = jb.j[blockIdx.z];
-    if (static_cast<int>(blockIdx.y) >= J.blocks)
+    if (static_cast<int>(blockIdx.x) >= J.blocks)
         return;
+    constexpr int NTILES = NT * (NT + 1) / 2;
+    constexpr int TPW = (NTILES + 3) / 4;          // tiles per wave
+    constexpr int PITCH = NT * kGT + 4;            // floats per staged row
+    __shared__ __attribute__((aligned(16))) float Ys[kGRows * PITCH];
     const float *A = J.A;
     const int64_t lda = J.lda;
-    const int rows = J.rows, rows_per_block = J.rows_per_block;
-    double *part = J.part;
-    __shared__ float Ai[kGRows][kGT + 1];
-    __shared__ float Aj[kGRows][kGT + 1];
-    const int nt = static_cast<int>(cdiv(KP, kGT));
-    // map blockIdx.x to an upper tile (ti <= tj)
-    int t = blockIdx.x, ti = 0;
-    while (t >= nt - ti) {
-        t -= nt - ti;
-        ++ti;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r0 = blockIdx.x * J.rows_per_block;
+    const int r1 = min(J.rows, r0 + J.rows_per_block);
+    // this wave's tiles: t = wave + 4 u, upper tiles in row-major order
+    int tri_[TPW], trj_[TPW];
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+        int t = wave + 4 * u, ti = 0;
+        if (t >= NTILES)
+            t = 0;   // idle slot: recomputes tile 0, never stored
+        while (t >= NT - ti) {
+            t -= NT - ti;
+            ++ti;
+        }
+        tri_[u] = ti;
+        trj_[u] = ti + t;
     }
-    const int tj = ti + t;
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    const int r0 = blockIdx.y * rows_per_block;
-    const int r1 = min(rows, r0 + rows_per_block);
-    double acc[4][4];
+    v4d acc[TPW][2][2];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int u = 0; u < TPW; ++u)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
-            acc[a][b] = 0.0;
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+                acc[u][a][c] = v4d{0.0, 0.0, 0.0, 0.0};
+    const int q4 = NT * kGT / 4;                   // float4 per staged row
     for (int rb = r0; rb < r1; rb += kGRows) {
         __syncthreads();
-        for (int idx = threadIdx.x; idx < kGRows * kGT; idx += 256) {
-            const int rr = idx / kGT, c = idx % kGT;
+        for (int idx = tid; idx < kGRows * q4; idx += 256) {
+            const int rr = idx / q4, c4 = (idx % q4) * 4;
             const int gr = rb + rr;
-            const int ci = ti * kGT + c, cj = tj * kGT + c;
-            Ai[rr][c] = (gr < r1 && ci < KP) ? A[static_cast<int64_t>(gr) * lda + ci] : 0.f;
-            Aj[rr][c] = (gr < r1 && cj < KP) ? A[static_cast<int64_t>(gr) * lda + cj] : 0.f;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (gr < r1 && c4 < KP)
+                v = *reinterpret_cast<const float4 *>(A + static_cast<int64_t>(gr) * lda + c4);
+            *reinterpret_cast<float4 *>(&Ys[rr * PITCH + c4]) = v;
         }
         __syncthreads();
-#pragma unroll 4
-        for (int rr = 0; rr < kGRows; ++rr) {
-            double ai[4], aj[4];
+#pragma unroll 2
+        for (int k0 = 0; k0 < kGRows; k0 += 4) {
+            const float *yr = &Ys[(k0 + (lane >> 4)) * PITCH + (lane & 15)];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                ai[e] = static_cast<double>(Ai[rr][ty * 4 + e]);
-                aj[e] = static_cast<double>(Aj[rr][tx * 4 + e]);
+            for (int u = 0; u < TPW; ++u) {
+                const double a0 = yr[tri_[u] * kGT], a1 = yr[tri_[u] * kGT + 16];
+                const double b0 = yr[trj_[u] * kGT], b1 = yr[trj_[u] * kGT + 16];
+                acc[u][0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[u][0][0], 0, 0, 0);
+                acc[u][0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[u][0][1], 0, 0, 0);
+                acc[u][1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[u][1][0], 0, 0, 0);
+                acc[u][1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[u][1][1], 0, 0, 0);
             }
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int b = 0; b < 4; ++b)
-                    acc[a][b] = __builtin_fma(ai[a], aj[b], acc[a][b]);
         }
     }
-    double *pb = part + static_cast<int64_t>(blockIdx.y) * KP * KP;
+    double *pb = J.part + static_cast<int64_t>(blockIdx.x) * KP * KP;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-        const int i = ti * kGT + ty * 4 + a;
+    for (int u = 0; u < TPW; ++u) {
+        if (wave + 4 * u >= NTILES)
+            continue;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int j = tj * kGT + tx * 4 + b;
-            if (i < KP && j < KP)
-                pb[static_cast<int64_t>(i) * KP + j] = acc[a][b];
-        }
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = tri_[u] * kGT + a * 16 + (lane >> 4) + 4 * e;
+                    const int j = trj_[u] * kGT + c * 16 + (lane & 15);
+                    if (i < KP && j < KP)
+                        pb[static_cast<int64_t>(i) * KP + j] = acc[u][a][c][e];
+                }
     }
 }
 
@@ -1438,7 +1458,14 @@ void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const
         rj.push_back(GramRedJob{ms[i].pw.gpart, gb, ms[i].pw.gram});
         gy = std::max(gy, gb);
     }
-    launch_jobs("sc_gram", gram_partial_kernel, gj, dim3(nt * (nt + 1) / 2, gy), dim3(256), 0, st, KP);
+    switch (nt) {
+    case 1: launch_jobs("sc_gram", gram_partial_kernel<1>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 2: launch_jobs("sc_gram", gram_partial_kernel<2>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 3: launch_jobs("sc_gram", gram_partial_kernel<3>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 4: launch_jobs("sc_gram", gram_partial_kernel<4>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 5: launch_jobs("sc_gram", gram_partial_kernel<5>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    default: launch_jobs("sc_gram", gram_partial_kernel<6>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    }
     launch_jobs("sc_gram_reduce", gram_reduce_kernel, rj, dim3(grid1d(int64_t(KP) * KP)), dim3(256), 0, st, KP);
 }
 
