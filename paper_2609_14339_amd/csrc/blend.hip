@@ -53,7 +53,7 @@ __device__ __forceinline__ void sync_lds()
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int RP>
+template <int RP, bool VEC>
 __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
 {
     constexpr int RB = RP * 2;                  // bytes per P / V row
@@ -92,28 +92,34 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
         dma16(src + c * 8, lds0 + ins * 1024);
     }
     // the G tile into registers: thread q holds row q / 16, columns 8 (q % 16) ..
+    // VEC: exactly eight 16-byte loads per thread (row and column clamped into
+    // G; what lies outside is never stored), so that "at most eight loads
+    // outstanding" below means every slice DMA has landed.  Otherwise element
+    // loads, and the wait is for everything.
     uint4 g[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
         const int q = tid + 256 * u;
         const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (gi < m) {
-            const uint16_t *src = J.G + static_cast<int64_t>(gi) * n + gj;
-            if (J.vec && gj + 8 <= n) {
-                v = *reinterpret_cast<const uint4 *>(src);
-            } else {
+        if (VEC) {
+            g[u] = *reinterpret_cast<const uint4 *>(J.G + static_cast<int64_t>(min(gi, m - 1)) * n + min(gj, n - 8));
+        } else {
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (gi < m) {
+                const uint16_t *src = J.G + static_cast<int64_t>(gi) * n + gj;
                 uint16_t e8[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
                     e8[e] = gj + e < n ? src[e] : uint16_t(0);
                 __builtin_memcpy(&v, e8, sizeof(v));
             }
+            g[u] = v;
         }
-        g[u] = v;
     }
-    // the slices have landed once at most the G loads are outstanding
-    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    if (VEC)
+        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     sync_lds();
 
     // P V^T: wave w computes rows 64 (w / 2) .., columns 64 (w % 2) .. as 2 x 2
@@ -182,7 +188,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
             o[e] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
         }
         uint16_t *dst = J.out + static_cast<int64_t>(gi) * n + gj;
-        if (J.vec && gj + 8 <= n) {
+        if (VEC && gj + 8 <= n) {
             *reinterpret_cast<uint4 *>(dst) = make_uint4(o[0], o[1], o[2], o[3]);
         } else {
             const uint16_t *e8 = reinterpret_cast<const uint16_t *>(o);
@@ -195,14 +201,23 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
 template <int RP>
 void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float alpha, hipStream_t st)
 {
-    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
-        Batch b{};
-        b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
-        for (int i = 0; i < b.count; ++i)
-            b.j[i] = jobs[c0 + i];
-        auto kern = blend_kernel<RP>;
-        ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha);
-    }
+    std::vector<Job> part[2];
+    for (const Job &j : jobs)
+        part[j.vec ? 1 : 0].push_back(j);
+    for (int v = 0; v < 2; ++v)
+        for (size_t c0 = 0; c0 < part[v].size(); c0 += kMaxJobs) {
+            Batch b{};
+            b.count = static_cast<int>(std::min<size_t>(kMaxJobs, part[v].size() - c0));
+            for (int i = 0; i < b.count; ++i)
+                b.j[i] = part[v][c0 + i];
+            if (v) {
+                auto kern = blend_kernel<RP, true>;
+                ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha);
+            } else {
+                auto kern = blend_kernel<RP, false>;
+                ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha);
+            }
+        }
 }
 
 }  // namespace
@@ -216,7 +231,7 @@ int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipS
     std::vector<Job> jobs;
     int tiles = 1;
     for (const Req &q : reqs) {
-        const bool vec = q.n % 8 == 0 && reinterpret_cast<uintptr_t>(q.G) % 16 == 0 &&
+        const bool vec = q.n % 8 == 0 && q.n >= 8 && reinterpret_cast<uintptr_t>(q.G) % 16 == 0 &&
                          reinterpret_cast<uintptr_t>(q.out) % 16 == 0;
         jobs.push_back(Job{q.G, q.out, q.m, q.n, q.P, q.V, vec ? 1 : 0});
         const int64_t rbn = cdiv(q.m, kT), cbn = cdiv(q.n, kT);
