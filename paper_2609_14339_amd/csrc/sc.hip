@@ -9,6 +9,7 @@
 #include "common.h"
 #include "sc_pass.h"
 #include "sc_blend.h"
+#include "sc_chol.h"
 
 #include <algorithm>
 #include <vector>
@@ -498,20 +499,6 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const Batch<GramRedJob
     G[idx] = s;
 }
 
-// ---------------------------------------------------------------------------
-// Cholesky G = L L^T of a k x k Gram matrix in LDS (fp64, packed lower
-// triangle), one workgroup of 32 x 32 threads, one barrier per column:
-// right-looking elimination on the unscaled columns (a_ic -= a_ij a_cj / d_j),
-// scaled at the end (l_ij = a_ij / sqrt(d_j)).  Pivots d_j at or below
-// 1e-15 * k * max(diag) are taken as zero: that column of L is zero (a
-// rank-deficient block).
-//   INVERT: then X = L^{-1} in place (right-looking forward elimination, one
-//           barrier per row) and T = X^T (fp32, zero-padded to KP x KP), so
-//           that Q = Y T has orthonormal columns (CholeskyQR).
-//   else:   write L itself (fp64, KP x KP, zero upper part) over G.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ int tri(int i) { return i * (i + 1) / 2; }
-
 // Sum over each row of 16 lanes with DPP lane permutes (VALU, no LDS):
 // quad_perm [1,0,3,2] and [2,3,0,1] (xor 1, xor 2), then row_half_mirror
 // (pairs the two quads of each half) and row_mirror (pairs the two halves);
@@ -540,104 +527,6 @@ __device__ __forceinline__ double row16_sum(double x)
     ACSC_DPP64(0x140)
 #undef ACSC_DPP64
     return x;
-}
-
-struct CholJob {
-    double *G;
-    float *Tout;
-};
-
-template <bool INVERT>
-__global__ __launch_bounds__(1024) void chol_kernel(const Batch<CholJob> jb, int k, int KP)
-{
-    double *G = jb.j[blockIdx.z].G;
-    float *Tout = jb.j[blockIdx.z].Tout;
-    extern __shared__ double Lp[];
-    double *buf0 = Lp + tri(k);
-    double *buf1 = buf0 + k;
-    __shared__ double sh_thresh;
-    const int tid = threadIdx.x;
-    const int tx = tid & 31, ty = tid >> 5;
-    for (int i = ty; i < k; i += 32)
-        for (int c = tx; c <= i; c += 32)
-            Lp[tri(i) + c] = G[static_cast<int64_t>(i) * KP + c];
-    __syncthreads();
-    if (tid == 0) {
-        double mx = 0.0;
-        for (int i = 0; i < k; ++i)
-            mx = fmax(mx, Lp[tri(i) + i]);
-        sh_thresh = 1e-15 * k * mx;
-    }
-    __syncthreads();
-    const double thresh = sh_thresh;
-    for (int j = 0; j < k; ++j) {
-        const double dj = Lp[tri(j) + j];
-        if (dj > thresh) {
-            const double inv = 1.0 / dj;
-            for (int i = j + 1 + ty; i < k; i += 32) {
-                const double aij = Lp[tri(i) + j] * inv;
-                for (int c = j + 1 + tx; c <= i; c += 32)
-                    Lp[tri(i) + c] -= aij * Lp[tri(c) + j];
-            }
-        }
-        __syncthreads();
-    }
-    for (int j = tid; j < k; j += 1024) {
-        const double dj = Lp[tri(j) + j];
-        buf0[j] = dj > thresh ? 1.0 / sqrt(dj) : 0.0;
-    }
-    __syncthreads();
-    for (int i = ty; i < k; i += 32)
-        for (int c = tx; c <= i; c += 32)
-            Lp[tri(i) + c] = (i == c) ? (buf0[c] > 0.0 ? 1.0 / buf0[c] : 0.0) : Lp[tri(i) + c] * buf0[c];
-    __syncthreads();
-    if (!INVERT) {
-        for (int idx = tid; idx < KP * KP; idx += 1024) {
-            const int i = idx / KP, c = idx % KP;
-            G[idx] = (i < k && c < k && c <= i) ? Lp[tri(i) + c] : 0.0;
-        }
-        return;
-    }
-    // X = L^{-1}:  row j of X is (e_j - sum_{c<j} L[j][c] X[c][:]) / L[j][j].
-    // Entries (i, c), c < i, hold L[i][c] until column c is consumed, then the
-    // running residual of row i; row j is final once scaled.
-    {
-        const double l00 = Lp[0];
-        for (int i = 1 + tid; i < k; i += 1024)
-            buf0[i] = Lp[tri(i)];
-        __syncthreads();
-        if (tid == 0)
-            Lp[0] = l00 > 0.0 ? 1.0 / l00 : 0.0;
-        __syncthreads();
-    }
-    for (int j = 0; j + 1 < k; ++j) {
-        double *cur = (j & 1) ? buf1 : buf0;
-        double *nxt = (j & 1) ? buf0 : buf1;
-        const double l1 = Lp[tri(j + 1) + j + 1];
-        const double inv1 = l1 > 0.0 ? 1.0 / l1 : 0.0;
-        for (int i = j + 1 + ty; i < k; i += 32) {
-            const double li = cur[i];
-            for (int c = tx; c <= j; c += 32) {
-                double v = (c == j ? 0.0 : Lp[tri(i) + c]) - li * Lp[tri(j) + c];
-                if (i == j + 1)
-                    v *= inv1;
-                Lp[tri(i) + c] = v;
-            }
-        }
-        for (int i = j + 2 + tid; i < k; i += 1024)
-            nxt[i] = Lp[tri(i) + j + 1];
-        if (tid == 0)
-            Lp[tri(j + 1) + j + 1] = inv1;
-        __syncthreads();
-    }
-    // T[c][i] = X[i][c]
-    for (int idx = tid; idx < KP * KP; idx += 1024) {
-        const int c = idx / KP, i = idx % KP;
-        float v = 0.f;
-        if (i < k && c < k && c <= i)
-            v = static_cast<float>(Lp[tri(i) + c]);
-        Tout[idx] = v;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1379,8 +1268,6 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
 // columns padded to a multiple of 32 rows, plus the squared norms
 size_t jacobi_lds(int k, size_t es) { return (static_cast<size_t>(k) * round_up(k, 32) + k) * es; }
 
-size_t chol_lds(int k) { return (static_cast<size_t>(k) * (k + 1) / 2 + 2 * static_cast<size_t>(k)) * sizeof(double); }
-
 // One tall-skinny product per job (opA * B), split-K through the job's
 // partial buffer `part` (nullptr: one split, straight into C).
 template <typename TA, typename TO>
@@ -1476,7 +1363,7 @@ void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const
 // 1e-7 * cond(Y); the iteration only needs a well-conditioned basis, and the
 // final basis gets the second pass.  The last pass also writes the bf16
 // transposed copy that the next streaming pass reads.
-void orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipStream_t st)
+int orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipStream_t st)
 {
     const Dims &d0 = ms[0].D;
     std::vector<const float *> A;
@@ -1487,10 +1374,11 @@ void orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipS
     }
     for (int pass = 0; pass < passes; ++pass) {
         gram(ms, A, rows, st);
-        std::vector<CholJob> cj;
+        std::vector<chol::Req> cj;
         for (auto &m : ms)
-            cj.push_back(CholJob{m.pw.gram, m.pw.T});
-        launch_jobs("sc_chol_inv", chol_kernel<true>, cj, dim3(1), dim3(1024), chol_lds(d0.k), st, d0.k, d0.KP);
+            cj.push_back(chol::Req{m.pw.gram, m.pw.T});
+        if (int rc = chol::run("sc_chol_inv", cj, d0.k, d0.KP, true, st))
+            return rc;
         std::vector<GemmReq<float, float>> g;
         for (size_t i = 0; i < ms.size(); ++i) {
             float *Y = const_cast<float *>(A[i]);
@@ -1501,6 +1389,7 @@ void orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipS
         }
         tall_gemm<float, false, float>("sc_orth_apply", g, st);
     }
+    return ACSC_OK;
 }
 
 // EMA + top-r SVD + filter for a group of matrices with the same k.
@@ -1580,14 +1469,17 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     int rc = pass(true);
     if (rc)
         return rc;
-    orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st);
+    if ((rc = orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st)))
+        return rc;
     for (int it = 0; it < power_iters; ++it) {
         if ((rc = pass(false)))
             return rc;
-        orthonormalise(ms, false, 1, use16, st);
+        if ((rc = orthonormalise(ms, false, 1, use16, st)))
+            return rc;
         if ((rc = pass(true)))
             return rc;
-        orthonormalise(ms, true, it + 1 == power_iters ? 2 : 1, use16, st);
+        if ((rc = orthonormalise(ms, true, it + 1 == power_iters ? 2 : 1, use16, st)))
+            return rc;
     }
     // Rayleigh-Ritz: Z = M^T Q (= B^T), B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
     if ((rc = pass(false)))
@@ -1595,16 +1487,17 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     {
         std::vector<const float *> A;
         std::vector<int> rows;
-        std::vector<CholJob> cj;
+        std::vector<chol::Req> cj;
         std::vector<JacJob> jj;
         for (auto &m : ms) {
             A.push_back(m.pw.Z);
             rows.push_back(m.D.n);
-            cj.push_back(CholJob{m.pw.gram, nullptr});
+            cj.push_back(chol::Req{m.pw.gram, nullptr});
             jj.push_back(JacJob{m.pw.gram, m.pw.Bu, m.pw.Bv, m.in->s, m.in->d, m.pw.info});
         }
         gram(ms, A, rows, st);
-        launch_jobs("sc_chol", chol_kernel<false>, cj, dim3(1), dim3(1024), chol_lds(k), st, k, KP);
+        if ((rc = chol::run("sc_chol", cj, k, KP, false, st)))
+            return rc;
         if (k <= 128)
             launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(1024), jacobi_lds(k, sizeof(double)), st,
                         k, KP, r, RP, tau, 1e-13, 40);
@@ -1793,9 +1686,7 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
         return ACSC_OK;
     // LDS of the one-workgroup kernels, for every k in the batch
     for (const Mat &m : all) {
-        int rc = allow_lds(chol_kernel<true>, chol_lds(m.D.k));
-        if (!rc)
-            rc = allow_lds(chol_kernel<false>, chol_lds(m.D.k));
+        int rc = chol::prepare(m.D.KP);
         if (!rc)
             rc = m.D.k <= 128 ? allow_lds(jacobi_kernel<double>, jacobi_lds(m.D.k, sizeof(double)))
                               : allow_lds(jacobi_kernel<float>, jacobi_lds(m.D.k, sizeof(float)));
