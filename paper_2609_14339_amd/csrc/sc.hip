@@ -10,6 +10,7 @@
 #include "sc_pass.h"
 #include "sc_blend.h"
 #include "sc_chol.h"
+#include "sc_orth.h"
 
 #include <algorithm>
 #include <vector>
@@ -29,6 +30,9 @@ constexpr int kNTMax = kKMax / 16;
 // Singular values of the prior at or below this fraction of the largest are
 // returned as zero (numerical rank of an fp32 subspace iteration).
 constexpr double kRankCutoff = 1e-5;
+// Largest k whose Rayleigh-Ritz Jacobi runs in fp64 (beyond it: fp32, whose
+// columns take half the LDS)
+constexpr int kJacobiF64MaxK = 128;
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
@@ -499,20 +503,19 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const Batch<GramRedJob
     G[idx] = s;
 }
 
-// Sum over each row of 16 lanes with DPP lane permutes (VALU, no LDS):
+// Sum over each group of 8 lanes with DPP lane permutes (VALU, no LDS):
 // quad_perm [1,0,3,2] and [2,3,0,1] (xor 1, xor 2), then row_half_mirror
-// (pairs the two quads of each half) and row_mirror (pairs the two halves);
-// every lane of the row ends with the row's sum.
-__device__ __forceinline__ float row16_sum(float x)
+// (pairs the two quads of each 8-lane half row); every lane of the group ends
+// with the group's sum.
+__device__ __forceinline__ float group8_sum(float x)
 {
     x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
     x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
     x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));
     return x;
 }
 
-__device__ __forceinline__ double row16_sum(double x)
+__device__ __forceinline__ double group8_sum(double x)
 {
 #define ACSC_DPP64(CTRL)                                                                          \
     {                                                                                             \
@@ -524,15 +527,22 @@ __device__ __forceinline__ double row16_sum(double x)
     ACSC_DPP64(0xB1)
     ACSC_DPP64(0x4E)
     ACSC_DPP64(0x141)
-    ACSC_DPP64(0x140)
 #undef ACSC_DPP64
     return x;
 }
 
+// Reciprocal and reciprocal square root of the rotation formulas: the fp32
+// path takes the hardware approximations (about 1 ulp; a rotation only has to
+// be orthogonal, and the next sweep corrects its angle), fp64 the rounded ops.
+__device__ __forceinline__ float jac_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
+__device__ __forceinline__ double jac_rsqrt(double x) { return 1.0 / sqrt(x); }
+__device__ __forceinline__ float jac_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ double jac_rcp(double x) { return 1.0 / x; }
+
 // ---------------------------------------------------------------------------
 // One-sided (Hestenes) Jacobi SVD of the k x k factor L in LDS, one
-// workgroup: rotate column pairs (round-robin tournament, one pair per wave at
-// a time) until every pair is orthogonal to `tol`.  Then sigma_c = ||a_c||,
+// workgroup: rotate column pairs (round-robin tournament, every pair of a round
+// at once on 8 lanes) until every pair is orthogonal to `tol`.  Then sigma_c = ||a_c||,
 // u_c = a_c / sigma_c, sorted descending, and the right factors of the final
 // products are written:  Bu[:, t] = u_(t), Bv[:, t] = u_(t) / sigma_(t),
 // s[t] = sigma_(t), d[t] = s / (s + tau) for t < r.
@@ -553,8 +563,9 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     int *info = J.info;
     extern __shared__ __attribute__((aligned(16))) unsigned char jsm[];
     // column c at A[c * kp]; kp = k rounded up to 32, rows k..kp-1 are zero.
-    // Lane gl of a pair's 16 lanes holds the R = kp / 16 consecutive rows
-    // gl R .. gl R + R - 1 of both columns (R even: 8-byte LDS accesses).
+    // Lane gl of a pair's 8 lanes holds the R = kp / 8 consecutive rows
+    // gl R .. gl R + R - 1 of both columns (R a multiple of 4: 16-byte LDS
+    // accesses).
     T *A = reinterpret_cast<T *>(jsm);
     const int kp = (k + 31) & ~31;
     T *nrm = A + static_cast<size_t>(k) * kp;   // squared column norms
@@ -569,25 +580,27 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     }
     const int n2 = k + (k & 1);
     const int npairs = n2 / 2;
-    // four column pairs per wave, 16 lanes each
-    const int grp = lane >> 4, gl = lane & 15;
-    const int slots = nwave * 4;
-    const int R = kp / 16;
-    constexpr int RMAX = (kKMax + 31) / 32 * 2;
+    // eight column pairs per wave, 8 lanes each
+    const int grp = lane >> 3, gl = lane & 7;
+    const int slots = nwave * 8;
+    const int R = kp / 8;
+    // fp64 runs for k <= kJacobiF64MaxK only
+    constexpr int RMAX = ((sizeof(T) == 8 ? kJacobiF64MaxK : kKMax) + 31) / 32 * 4;
+    constexpr int V = 16 / sizeof(T);   // elements per 16-byte access
     int sweeps_used = 0;
     float last_off = 0.f;
     __syncthreads();
     for (int sweep = 0; sweep < max_sweeps; ++sweep) {
         // exact squared norms at the start of every sweep (the rotations
         // update them incrementally within it)
-        for (int c = wave * 4 + grp; c < k; c += slots) {
+        for (int c = wave * 8 + grp; c < k; c += slots) {
             const T *ac = A + c * kp + gl * R;
             T ss = 0;
 #pragma unroll
             for (int e = 0; e < RMAX; ++e)
                 if (e < R)
                     ss += ac[e] * ac[e];
-            ss = row16_sum(ss);
+            ss = group8_sum(ss);
             if (gl == 0)
                 nrm[c] = ss;
         }
@@ -596,7 +609,7 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
         __syncthreads();
         float wmax = 0.f;
         for (int round = 0; round < n2 - 1; ++round) {
-            for (int p = wave * 4 + grp; p < npairs; p += slots) {
+            for (int p = wave * 8 + grp; p < npairs; p += slots) {
                 auto pos = [&](int x) {
                     if (x == 0)
                         return 0;
@@ -617,56 +630,47 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
                 T *aq = A + cq * kp + gl * R;
                 T xv[RMAX], yv[RMAX];
 #pragma unroll
-                for (int e = 0; e < RMAX; e += 2) {
+                for (int e = 0; e < RMAX; e += V) {
+                    uint4 ux = make_uint4(0u, 0u, 0u, 0u), uy = ux;
                     if (e < R) {
-                        if constexpr (sizeof(T) == 4) {
-                            const float2 x2 = *reinterpret_cast<const float2 *>(ap + e);
-                            const float2 y2 = *reinterpret_cast<const float2 *>(aq + e);
-                            xv[e] = x2.x;
-                            xv[e + 1] = x2.y;
-                            yv[e] = y2.x;
-                            yv[e + 1] = y2.y;
-                        } else {
-                            xv[e] = ap[e];
-                            xv[e + 1] = ap[e + 1];
-                            yv[e] = aq[e];
-                            yv[e + 1] = aq[e + 1];
-                        }
-                    } else {
-                        xv[e] = xv[e + 1] = yv[e] = yv[e + 1] = T(0);
+                        ux = *reinterpret_cast<const uint4 *>(ap + e);
+                        uy = *reinterpret_cast<const uint4 *>(aq + e);
                     }
+                    __builtin_memcpy(&xv[e], &ux, 16);
+                    __builtin_memcpy(&yv[e], &uy, 16);
                 }
                 const T al = nrm[cp], be = nrm[cq];
-                T ga = 0;
+                T gp[4] = {0, 0, 0, 0};
 #pragma unroll
                 for (int e = 0; e < RMAX; ++e)
-                    ga += xv[e] * yv[e];
-                ga = row16_sum(ga);
-                const T nab = sqrt(al * be);
-                if (ga == T(0) || nab == T(0))
+                    gp[e & 3] += xv[e] * yv[e];
+                const T ga = group8_sum((gp[0] + gp[1]) + (gp[2] + gp[3]));
+                const T prod = al * be;
+                if (ga == T(0) || prod == T(0))
                     continue;
-                const T ratio = fabs(ga) / nab;
+                const T ratio = fabs(ga) * jac_rsqrt(prod);
                 wmax = fmaxf(wmax, static_cast<float>(ratio));
                 if (ratio <= tol)
                     continue;
-                const T zeta = (be - al) / (T(2) * ga);
-                const T t = (zeta >= T(0) ? T(1) : T(-1)) / (fabs(zeta) + sqrt(T(1) + zeta * zeta));
-                const T c = T(1) / sqrt(T(1) + t * t);
+                const T zeta = (be - al) * jac_rcp(T(2) * ga);
+                const T z2 = T(1) + zeta * zeta;
+                const T t = (zeta >= T(0) ? T(1) : T(-1)) * jac_rcp(fabs(zeta) + z2 * jac_rsqrt(z2));
+                const T c = jac_rsqrt(T(1) + t * t);
                 const T sn = c * t;
 #pragma unroll
-                for (int e = 0; e < RMAX; e += 2) {
+                for (int e = 0; e < RMAX; e += V) {
                     if (e < R) {
-                        const T x0 = c * xv[e] - sn * yv[e], x1 = c * xv[e + 1] - sn * yv[e + 1];
-                        const T y0 = sn * xv[e] + c * yv[e], y1 = sn * xv[e + 1] + c * yv[e + 1];
-                        if constexpr (sizeof(T) == 4) {
-                            *reinterpret_cast<float2 *>(ap + e) = make_float2(x0, x1);
-                            *reinterpret_cast<float2 *>(aq + e) = make_float2(y0, y1);
-                        } else {
-                            ap[e] = x0;
-                            ap[e + 1] = x1;
-                            aq[e] = y0;
-                            aq[e + 1] = y1;
+                        T xo[V], yo[V];
+#pragma unroll
+                        for (int v = 0; v < V; ++v) {
+                            xo[v] = c * xv[e + v] - sn * yv[e + v];
+                            yo[v] = sn * xv[e + v] + c * yv[e + v];
                         }
+                        uint4 ux, uy;
+                        __builtin_memcpy(&ux, xo, 16);
+                        __builtin_memcpy(&uy, yo, 16);
+                        *reinterpret_cast<uint4 *>(ap + e) = ux;
+                        *reinterpret_cast<uint4 *>(aq + e) = uy;
                     }
                 }
                 // the rotation zeroes the pair's inner product: the norms move by t gamma
@@ -1265,6 +1269,13 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
     }
 }
 
+// one 8-lane group per column pair of a round, at least 4 and at most 16 waves
+unsigned jacobi_threads(int k)
+{
+    const int npairs = (k + (k & 1)) / 2;
+    return 64u * static_cast<unsigned>(std::min<int64_t>(16, std::max<int64_t>(4, cdiv(npairs, 8))));
+}
+
 // columns padded to a multiple of 32 rows, plus the squared norms
 size_t jacobi_lds(int k, size_t es) { return (static_cast<size_t>(k) * round_up(k, 32) + k) * es; }
 
@@ -1379,15 +1390,17 @@ int orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipSt
             cj.push_back(chol::Req{m.pw.gram, m.pw.T});
         if (int rc = chol::run("sc_chol_inv", cj, d0.k, d0.KP, true, st))
             return rc;
-        std::vector<GemmReq<float, float>> g;
+        // fp32 Q is read by the second Gram of CholeskyQR2 and by the final
+        // basis; otherwise (bf16 passes) only its bf16 transposed copy is
+        std::vector<orth::Req> g;
         for (size_t i = 0; i < ms.size(); ++i) {
             float *Y = const_cast<float *>(A[i]);
             uint16_t *t16 = (use16 && pass + 1 == passes) ? (onY ? ms[i].pw.Yt16 : ms[i].pw.Zt16) : nullptr;
             const int64_t ldt = onY ? ms[i].pw.ldy16 : ms[i].pw.ldz16;
-            g.push_back(GemmReq<float, float>{Y, d0.KP, ms[i].pw.T, d0.KP, Y, d0.KP, rows[i], d0.KP, d0.KP, d0.KP,
-                                              nullptr, t16, ldt});
+            g.push_back(orth::Req{Y, rows[i], ms[i].pw.T, t16, ldt, !use16 || passes == 2});
         }
-        tall_gemm<float, false, float>("sc_orth_apply", g, st);
+        if (int rc = orth::run("sc_orth_apply", g, d0.KP, st))
+            return rc;
     }
     return ACSC_OK;
 }
@@ -1498,11 +1511,13 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         gram(ms, A, rows, st);
         if ((rc = chol::run("sc_chol", cj, k, KP, false, st)))
             return rc;
-        if (k <= 128)
-            launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(1024), jacobi_lds(k, sizeof(double)), st,
+        if (k <= kJacobiF64MaxK)
+            launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(jacobi_threads(k)),
+                        jacobi_lds(k, sizeof(double)), st,
                         k, KP, r, RP, tau, 1e-13, 40);
         else
-            launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(1024), jacobi_lds(k, sizeof(float)), st,
+            launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(jacobi_threads(k)),
+                        jacobi_lds(k, sizeof(float)), st,
                         k, KP, r, RP, tau, 1e-5f, 40);
     }
     // U = Q Bu, V = Z Bv (first r columns)
@@ -1688,7 +1703,7 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
     for (const Mat &m : all) {
         int rc = chol::prepare(m.D.KP);
         if (!rc)
-            rc = m.D.k <= 128 ? allow_lds(jacobi_kernel<double>, jacobi_lds(m.D.k, sizeof(double)))
+            rc = m.D.k <= kJacobiF64MaxK ? allow_lds(jacobi_kernel<double>, jacobi_lds(m.D.k, sizeof(double)))
                               : allow_lds(jacobi_kernel<float>, jacobi_lds(m.D.k, sizeof(float)));
         if (rc)
             return rc;
