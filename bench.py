@@ -224,7 +224,16 @@ def main():
     candidates["sc_pass"] = pass_ms
     dom = max(candidates, key=candidates.get)
     if dom == "sc_pass":
-        bound, amount, calls = "mfma", work["sc_pass"]["flops"], work["sc_pass"]["calls"]
+        # a pass is bound by whichever roof is lower at its arithmetic
+        # intensity (k FLOP per byte of the streamed shadow): below the ridge
+        # point (peak FLOP/s over peak B/s) that is HBM
+        peak_mm = PEAK_BF16 if gs.dtype == torch.bfloat16 else PEAK_F32
+        ai = work["sc_pass"]["flops"] / work["sc_pass"]["bytes"]
+        ridge = peak_mm * 1e12 / (PEAK_HBM * 1e9)
+        if ai < ridge:
+            bound, amount, calls = "hbm", work["sc_pass"]["bytes"], work["sc_pass"]["calls"]
+        else:
+            bound, amount, calls = "mfma", work["sc_pass"]["flops"], work["sc_pass"]["calls"]
         dom_ms, dom_n = pass_ms, pass_n
     else:
         mm = model(dom)
@@ -263,6 +272,7 @@ def main():
         pk_ = PEAK_BF16 if gs.dtype == torch.bfloat16 else PEAK_F32
         comp["sc_pass"] = {"TFLOP/s": round(tf, 2), "frac_mfma": round(tf / pk_, 4),
                            "GB/s": round(work["sc_pass"]["bytes"] / (pass_ms * 1e-3) / 1e9, 1),
+                           "frac_hbm": round(work["sc_pass"]["bytes"] / (pass_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
                            "ms_per_step": round(pass_ms, 4), "launches_per_step": pass_n}
     comp["phase_ms"] = {k: round(v, 4) for k, v in phase_ms.items()}
     comp["sc_correct_step"] = {"GB/s": round(work["sc_correct"]["bytes"] / (phase_ms["correct"] * 1e-3) / 1e9, 1),

@@ -8,7 +8,8 @@
 // v_mfma_f32_32x32x16_bf16 (64 x 64 per wave).  The fp32 product is staged in
 // LDS in G's row order, and each thread blends its own 16-byte chunks of G
 // and writes them out.  Tiles are dealt so that XCD x owns the row blocks
-// congruent to x mod 8, which keeps each P slice in one L2.
+// congruent to x mod 8 (each P slice stays in one L2) and walks them in bands
+// of columns (the band's V slices stay there too).
 #include "common.h"
 #include "sc_blend.h"
 
@@ -21,10 +22,12 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((address_space(3))) unsigned char lds_byte;
+typedef unsigned int nu4 __attribute__((ext_vector_type(4)));
 
 constexpr int kT = 128;          // tile edge
 constexpr int kStPitch = 132;    // floats per staged product row (conflict-free column writes)
 constexpr int kMaxJobs = 16;
+constexpr int kBand = 16;        // column blocks per band of the tile walk
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -66,12 +69,19 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
     const Job &J = jb.j[blockIdx.z];
     const int m = J.m, n = J.n;
     const int rb_n = static_cast<int>(cdiv(m, kT)), cb_n = static_cast<int>(cdiv(n, kT));
+    // XCD x (= block % 8) owns the row blocks x, x + 8, ...; it walks them in
+    // column bands of kBand column blocks, row blocks outer, so that a band's
+    // V slices and the current P slice stay in its L2
     const int b = blockIdx.x;
     const int xcd = b & 7, t = b >> 3;
-    const int rb = xcd + 8 * (t / cb_n);
-    const int cb = t % cb_n;
-    if (rb >= rb_n)
+    const int nr = (rb_n - xcd + 7) / 8;
+    if (t >= nr * cb_n)
         return;
+    const int band = t / (nr * kBand);
+    const int rem = t - band * nr * kBand;
+    const int bw = min(kBand, cb_n - band * kBand);
+    const int rb = xcd + 8 * (rem / bw);
+    const int cb = band * kBand + rem % bw;
     const int row0 = rb * kT, col0 = cb * kT;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -102,7 +112,10 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
         const int q = tid + 256 * u;
         const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
         if (VEC) {
-            g[u] = *reinterpret_cast<const uint4 *>(J.G + static_cast<int64_t>(min(gi, m - 1)) * n + min(gj, n - 8));
+            // G streams through once: non-temporal, so that it does not push P and V out of L2
+            const nu4 v = __builtin_nontemporal_load(
+                reinterpret_cast<const nu4 *>(J.G + static_cast<int64_t>(min(gi, m - 1)) * n + min(gj, n - 8)));
+            g[u] = make_uint4(v.x, v.y, v.z, v.w);
         } else {
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
             if (gi < m) {
@@ -189,7 +202,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
         }
         uint16_t *dst = J.out + static_cast<int64_t>(gi) * n + gj;
         if (VEC && gj + 8 <= n) {
-            *reinterpret_cast<uint4 *>(dst) = make_uint4(o[0], o[1], o[2], o[3]);
+            __builtin_nontemporal_store(nu4{o[0], o[1], o[2], o[3]}, reinterpret_cast<nu4 *>(dst));
         } else {
             const uint16_t *e8 = reinterpret_cast<const uint16_t *>(o);
             for (int e = 0; e < 8 && gj + e < n; ++e)
