@@ -431,18 +431,34 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> 
 #pragma unroll
             for (int c = 0; c < 2; ++c)
                 acc[u][a][c] = v4d{0.0, 0.0, 0.0, 0.0};
-    const int q4 = NT * kGT / 4;                   // float4 per staged row
-    for (int rb = r0; rb < r1; rb += kGRows) {
-        __syncthreads();
-        for (int idx = tid; idx < kGRows * q4; idx += 256) {
+    constexpr int q4 = NT * kGT / 4;               // float4 per staged row
+    constexpr int PF = (kGRows * q4 + 255) / 256;  // float4 per thread and chunk
+    // the next chunk is loaded into registers while this one is multiplied
+    float4 pf[PF];
+    auto load = [&](int rb) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int idx = tid + 256 * u;
             const int rr = idx / q4, c4 = (idx % q4) * 4;
             const int gr = rb + rr;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (gr < r1 && c4 < KP)
+            if (idx < kGRows * q4 && gr < r1 && c4 < KP)
                 v = *reinterpret_cast<const float4 *>(A + static_cast<int64_t>(gr) * lda + c4);
-            *reinterpret_cast<float4 *>(&Ys[rr * PITCH + c4]) = v;
+            pf[u] = v;
+        }
+    };
+    load(r0);
+    for (int rb = r0; rb < r1; rb += kGRows) {
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int idx = tid + 256 * u;
+            if (idx < kGRows * q4)
+                *reinterpret_cast<float4 *>(&Ys[(idx / q4) * PITCH + (idx % q4) * 4]) = pf[u];
         }
         __syncthreads();
+        if (rb + kGRows < r1)
+            load(rb + kGRows);
 #pragma unroll 2
         for (int k0 = 0; k0 < kGRows; k0 += 4) {
             const float *yr = &Ys[(k0 + (lane >> 4)) * PITCH + (lane & 15)];
@@ -484,23 +500,39 @@ struct GramRedJob {
 
 __global__ __launch_bounds__(256) void gram_reduce_kernel(const Batch<GramRedJob> jb, int KP)
 {
+    // 32 consecutive elements x 8 groups of blocks per workgroup; only the
+    // upper tiles are read (coalesced) and each is also written mirrored
     const GramRedJob &J = jb.j[blockIdx.z];
-    const double *part = J.part;
-    const int blocks = J.blocks;
-    double *G = J.G;
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= KP * KP)
-        return;
-    int i = idx / KP, j = idx % KP;
-    if (i / kGT > j / kGT) {   // lower tiles were not computed: use the mirror
-        const int t = i;
-        i = j;
-        j = t;
-    }
+    __shared__ double red[8][32];
+    const int e = threadIdx.x & 31, g = threadIdx.x >> 5;
+    const int idx = blockIdx.x * 32 + e;
+    const int i = idx / KP, j = idx - (idx / KP) * KP;
+    const bool live = idx < KP * KP && i / kGT <= j / kGT;
     double s = 0.0;
-    for (int b = 0; b < blocks; ++b)
-        s += part[static_cast<int64_t>(b) * KP * KP + static_cast<int64_t>(i) * KP + j];
-    G[idx] = s;
+    if (live) {
+        const int64_t stride = static_cast<int64_t>(KP) * KP;
+        const double *p = J.part + idx;
+        double s0 = 0.0, s1 = 0.0;
+        int b = g;
+        for (; b + 8 < J.blocks; b += 16) {
+            s0 += p[b * stride];
+            s1 += p[(b + 8) * stride];
+        }
+        if (b < J.blocks)
+            s0 += p[b * stride];
+        s = s0 + s1;
+    }
+    red[g][e] = s;
+    __syncthreads();
+    if (g == 0 && live) {
+        double t = 0.0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            t += red[q][e];
+        J.G[idx] = t;
+        if (i / kGT < j / kGT)
+            J.G[static_cast<int64_t>(j) * KP + i] = t;
+    }
 }
 
 // Sum over each group of 8 lanes with DPP lane permutes (VALU, no LDS):
@@ -1164,7 +1196,8 @@ int split_count(int64_t Mdim, int64_t Kdim)
 
 int64_t split_chunk(int64_t Kdim, int splits) { return round_up(cdiv(Kdim, splits), kBK); }
 
-int gram_blocks(int64_t rows) { return static_cast<int>(std::min<int64_t>(64, cdiv(rows, 512))); }
+// Most Gram partial blocks a matrix of this many rows may be split into.
+int gram_blocks_max(int64_t rows) { return static_cast<int>(std::min<int64_t>(128, cdiv(rows, kGRows))); }
 
 struct Dims {
     int m, n, r, k, KP, RP;
@@ -1215,7 +1248,7 @@ size_t carve_prior(const Dims &d, bool use16, void *base, PriorWs *w)
     t.T = c.take<float>(static_cast<size_t>(d.KP) * d.KP);
     t.Bu = c.take<float>(static_cast<size_t>(d.KP) * d.RP);
     t.Bv = c.take<float>(static_cast<size_t>(d.KP) * d.RP);
-    t.gpart = c.take<double>(static_cast<size_t>(gram_blocks(mx)) * d.KP * d.KP);
+    t.gpart = c.take<double>(static_cast<size_t>(gram_blocks_max(mx)) * d.KP * d.KP);
     t.gram = c.take<double>(static_cast<size_t>(d.KP) * d.KP);
     if (w)
         *w = t;
@@ -1349,9 +1382,26 @@ void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const
     std::vector<GramJob> gj;
     std::vector<GramRedJob> rj;
     int gy = 1;
+    // one row count per block across the batch, so that the blocks of all
+    // matrices (one workgroup each) come to at most two per CU
+    int64_t total = 0;
+    for (int r : rows)
+        total += r;
+    auto rpb_of = [&](size_t i, int64_t rpb_batch) {
+        return std::max<int64_t>(rpb_batch, round_up(cdiv(rows[i], gram_blocks_max(rows[i])), kGRows));
+    };
+    int64_t rpb_batch = round_up(std::max<int64_t>(1, cdiv(total, 512)), kGRows);
+    for (;;) {
+        int64_t nb = 0;
+        for (size_t i = 0; i < ms.size(); ++i)
+            nb += cdiv(rows[i], rpb_of(i, rpb_batch));
+        if (nb <= 512 || rpb_batch >= total)
+            break;
+        rpb_batch += kGRows;
+    }
     for (size_t i = 0; i < ms.size(); ++i) {
-        const int gb = gram_blocks(rows[i]);
-        const int rpb = static_cast<int>(round_up(cdiv(rows[i], gb), kGRows));
+        const int rpb = static_cast<int>(rpb_of(i, rpb_batch));
+        const int gb = static_cast<int>(cdiv(rows[i], rpb));
         gj.push_back(GramJob{A[i], KP, rows[i], rpb, gb, ms[i].pw.gpart});
         rj.push_back(GramRedJob{ms[i].pw.gpart, gb, ms[i].pw.gram});
         gy = std::max(gy, gb);
@@ -1364,7 +1414,8 @@ void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const
     case 5: launch_jobs("sc_gram", gram_partial_kernel<5>, gj, dim3(gy), dim3(256), 0, st, KP); break;
     default: launch_jobs("sc_gram", gram_partial_kernel<6>, gj, dim3(gy), dim3(256), 0, st, KP); break;
     }
-    launch_jobs("sc_gram_reduce", gram_reduce_kernel, rj, dim3(grid1d(int64_t(KP) * KP)), dim3(256), 0, st, KP);
+    launch_jobs("sc_gram_reduce", gram_reduce_kernel, rj, dim3(static_cast<unsigned>(cdiv(int64_t(KP) * KP, 32))),
+                dim3(256), 0, st, KP);
 }
 
 // Q <- Y L^{-T}, `passes` times (CholeskyQR; two passes = CholeskyQR2), for
