@@ -1572,6 +1572,16 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
                         k, KP, r, RP, tau, 1e-5f, 40);
     }
     // U = Q Bu, V = Z Bv (first r columns)
+    std::vector<orth::GemmReq> og;
+    for (auto &m : ms) {
+        og.push_back(orth::GemmReq{m.pw.Y, KP, m.D.m, KP, m.pw.Bu, RP, RP, m.in->U, nullptr, r, r});
+        og.push_back(orth::GemmReq{m.pw.Z, KP, m.D.n, KP, m.pw.Bv, RP, RP, m.in->V, nullptr, r, r});
+    }
+    bool fast = true;
+    for (const auto &q : og)
+        fast = fast && orth::gemm_supported(q);
+    if (fast)
+        return orth::gemm("sc_basis", og, st);
     std::vector<GemmReq<float, float>> g;
     for (auto &m : ms) {
         g.push_back(GemmReq<float, float>{m.pw.Y, KP, m.pw.Bu, RP, m.in->U, r, m.D.m, KP, r, r, nullptr, nullptr, 0});
@@ -1612,11 +1622,23 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
     }
     // X = U^T T   [r, RP]
     {
-        std::vector<GemmReq<float, float>> q;
-        for (auto &m : ms)
-            q.push_back(GemmReq<float, float>{m.in->U, r, m.cw.Tm, RP, m.cw.X, RP, r, m.D.m, RP, RP, m.cw.xpart,
-                                              nullptr, 0});
-        tall_gemm<float, true, float>("sc_utt", q, st);
+        std::vector<orth::InnerReq> iq;
+        bool fast = true;
+        for (auto &m : ms) {
+            iq.push_back(orth::InnerReq{m.in->U, r, m.cw.Tm, RP, m.D.m, r, RP, m.cw.X, RP, m.cw.xpart,
+                                        split_count(m.D.r, m.D.m)});
+            fast = fast && orth::inner_supported(iq.back());
+        }
+        if (fast) {
+            if (int rc = orth::inner("sc_utt", iq, st))
+                return rc;
+        } else {
+            std::vector<GemmReq<float, float>> q;
+            for (auto &m : ms)
+                q.push_back(GemmReq<float, float>{m.in->U, r, m.cw.Tm, RP, m.cw.X, RP, r, m.D.m, RP, RP, m.cw.xpart,
+                                                  nullptr, 0});
+            tall_gemm<float, true, float>("sc_utt", q, st);
+        }
     }
     {
         std::vector<FilterJob> f;
@@ -1635,7 +1657,20 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
             pj.push_back(PadJob<GT>{m.in->V, m.D.n, static_cast<GT *>(m.cw.Vc)});
             tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * RP);
         }
-        tall_gemm<float, false, GT>("sc_ux", q, st);
+        std::vector<orth::GemmReq> og;
+        bool fast = true;
+        for (auto &m : ms) {
+            og.push_back(orth::GemmReq{m.in->U, r, m.D.m, r, m.cw.Xf, RP, RP,
+                                       b16 ? nullptr : static_cast<float *>(m.cw.Pc),
+                                       b16 ? static_cast<uint16_t *>(m.cw.Pc) : nullptr, RP, RP});
+            fast = fast && orth::gemm_supported(og.back());
+        }
+        if (fast) {
+            if (int rc = orth::gemm("sc_ux", og, st))
+                return rc;
+        } else {
+            tall_gemm<float, false, GT>("sc_ux", q, st);
+        }
         launch_jobs("sc_vconvert", pad_convert_kernel<GT>, pj, dim3(grid1d(tot)), dim3(256), 0, st, r, RP);
     }
     {
