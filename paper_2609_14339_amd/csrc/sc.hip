@@ -296,32 +296,6 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
     }
 }
 
-// Xt[c][i] = bf16(X[i][c]) for c < cols (zero for cols <= c < CP), i < rows;
-// Xt has row stride ldt.
-struct TrJob {
-    const float *X;
-    int64_t ldx;
-    int rows, cols, CP;
-    uint16_t *Xt;
-    int64_t ldt;
-};
-
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const Batch<TrJob> jb)
-{
-    const TrJob &J = jb.j[blockIdx.z];
-    const float *X = J.X;
-    const int64_t ldx = J.ldx, ldt = J.ldt;
-    const int rows = J.rows, cols = J.cols, CP = J.CP;
-    uint16_t *Xt = J.Xt;
-    const int64_t total = static_cast<int64_t>(CP) * rows;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; q < total;
-         q += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int c = static_cast<int>(q / rows);
-        const int64_t i = q - static_cast<int64_t>(c) * rows;
-        Xt[static_cast<int64_t>(c) * ldt + i] = c < cols ? f32_to_bf16(X[i * ldx + c]) : uint16_t(0);
-    }
-}
-
 // C[i, c] = sum_s P[s][i, c] for c < nwrite (P has row stride ldp).
 template <typename TO>
 struct ReduceJob {
@@ -844,6 +818,17 @@ __global__ __launch_bounds__(256) void ema_kernel(const Batch<Ema32Job<GT>> jb, 
 // Starting block Z0 [n, KP]: V_warm columns first (if given), then uniform
 // random values in [-1, 1) from a counter-based hash of (seed, i, c); zero
 // beyond k.
+// Entry (i, c) of the seeded starting block: one SplitMix64 finalisation of
+// seed ^ (i * 0x100000001B3 + c), top 24 bits mapped to [-1, 1).
+__device__ __forceinline__ float start_uniform(uint64_t seed, int64_t i, int c)
+{
+    uint64_t z = seed ^ (static_cast<uint64_t>(i) * 0x100000001B3ull + c);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    return static_cast<float>(z >> 40) * (2.0f / 16777216.0f) - 1.0f;
+}
+
 struct InitJob {
     float *Z;
     int n;
@@ -865,17 +850,83 @@ __global__ __launch_bounds__(256) void init_block_kernel(const Batch<InitJob> jb
         const int c = static_cast<int>(idx - i * KP);
         float v = 0.f;
         if (c < k) {
-            if (Vw && c < rw) {
+            if (Vw && c < rw)
                 v = Vw[i * rw + c];
-            } else {
-                uint64_t z = seed ^ (static_cast<uint64_t>(i) * 0x100000001B3ull + c);
-                z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-                z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-                z ^= z >> 31;
-                v = static_cast<float>(z >> 40) * (2.0f / 16777216.0f) - 1.0f;
-            }
+            else
+                v = start_uniform(seed, i, c);
         }
         Z[idx] = v;
+    }
+}
+
+// 64-row tiles of a thin fp32 block [rows, cols] to bf16, zero-padded to CP
+// columns, through LDS: the transposed copy Xt[c][i] (row stride ldt, 16-byte
+// stores along i) and/or the row-major copy Xc[i][c] (row stride CP).  With
+// X == nullptr the block is the starting block of the subspace iteration
+// (V_warm columns, then seeded uniform draws, for c < cols).
+struct TileJob {
+    const float *X;
+    int64_t ldx;
+    int rows, cols, CP;
+    uint16_t *Xt;
+    int64_t ldt;
+    uint16_t *Xc;
+    const float *Vw;
+    int rw;
+    uint64_t seed;
+};
+
+constexpr int kTileRows = 64;
+
+__global__ __launch_bounds__(256) void tile_bf16_kernel(const Batch<TileJob> jb)
+{
+    const TileJob &J = jb.j[blockIdx.z];
+    const int row0 = blockIdx.x * kTileRows;
+    if (row0 >= J.rows)
+        return;
+    __shared__ float Ts[kTileRows * (kKMax + 1)];
+    const int CP = J.CP, P = CP + 1;
+    for (int idx = threadIdx.x; idx < kTileRows * CP; idx += 256) {
+        const int r = idx / CP, c = idx - (idx / CP) * CP;
+        const int64_t i = row0 + r;
+        float v = 0.f;
+        if (i < J.rows && c < J.cols) {
+            if (J.X)
+                v = J.X[i * J.ldx + c];
+            else if (J.Vw && c < J.rw)
+                v = J.Vw[i * J.rw + c];
+            else
+                v = start_uniform(J.seed, i, c);
+        }
+        Ts[r * P + c] = v;
+    }
+    __syncthreads();
+    if (J.Xc) {
+        const int c8n = CP / 8;
+        for (int idx = threadIdx.x; idx < kTileRows * c8n; idx += 256) {
+            const int r = idx / c8n, c8 = (idx - (idx / c8n) * c8n) * 8;
+            if (row0 + r >= J.rows)
+                continue;
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                w[e] = static_cast<uint32_t>(f32_to_bf16(Ts[r * P + c8 + 2 * e])) |
+                       (static_cast<uint32_t>(f32_to_bf16(Ts[r * P + c8 + 2 * e + 1])) << 16);
+            *reinterpret_cast<uint4 *>(J.Xc + static_cast<int64_t>(row0 + r) * CP + c8) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+    if (J.Xt) {
+        for (int idx = threadIdx.x; idx < CP * (kTileRows / 8); idx += 256) {
+            const int c = idx / (kTileRows / 8), r8 = (idx % (kTileRows / 8)) * 8;
+            if (row0 + r8 >= J.rows)
+                continue;
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                w[e] = static_cast<uint32_t>(f32_to_bf16(Ts[(r8 + 2 * e) * P + c])) |
+                       (static_cast<uint32_t>(f32_to_bf16(Ts[(r8 + 2 * e + 1) * P + c])) << 16);
+            *reinterpret_cast<uint4 *>(J.Xt + static_cast<int64_t>(c) * J.ldt + row0 + r8) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
     }
 }
 
@@ -1489,16 +1540,24 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     }
     {
         std::vector<InitJob> j;
-        std::vector<TrJob> t;
         int64_t tot = 1;
         for (auto &m : ms) {
             j.push_back(InitJob{m.pw.Z, m.D.n, m.in->V_warm, m.seed});
-            t.push_back(TrJob{m.pw.Z, KP, m.D.n, KP, KP, m.pw.Zt16, m.pw.ldz16});
             tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * KP);
         }
-        launch_jobs("sc_init", init_block_kernel, j, dim3(grid1d(tot)), dim3(256), 0, st, k, KP, r);
-        if (use16)
-            launch_jobs("sc_transpose", transpose_bf16_kernel, t, dim3(grid1d(tot)), dim3(256), 0, st);
+        if (use16) {
+            // the bf16 passes read only the transposed copy of the starting block
+            std::vector<TileJob> tj;
+            int gx = 1;
+            for (auto &m : ms) {
+                tj.push_back(TileJob{nullptr, 0, m.D.n, k, KP, m.pw.Zt16, m.pw.ldz16, nullptr, m.in->V_warm,
+                                     m.in->V_warm ? r : 0, m.seed});
+                gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, kTileRows)));
+            }
+            launch_jobs("sc_init", tile_bf16_kernel, tj, dim3(gx), dim3(256), 0, st);
+        } else {
+            launch_jobs("sc_init", init_block_kernel, j, dim3(grid1d(tot)), dim3(256), 0, st, k, KP, r);
+        }
     }
     // one pass Y = M Z  /  Z = M^T Y over every EMA (bf16 shadow on matrix cores, or fp32)
     auto pass = [&](bool mz) {
@@ -1599,17 +1658,19 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
     const bool b16 = sizeof(GT) == 2;
     // T = G V   [m, RP]
     if (b16) {
-        std::vector<TrJob> t;
+        // V to bf16 once: transposed for T = G V, row-major for the blend
+        std::vector<TileJob> t;
         std::vector<pass::Req> q;
-        int64_t tot = 1;
+        int gx = 1;
         for (auto &m : ms) {
-            t.push_back(TrJob{m.in->V, r, m.D.n, r, RP, m.cw.Vt16, m.cw.ldv16});
-            tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.n) * RP);
+            t.push_back(TileJob{m.in->V, r, m.D.n, r, RP, m.cw.Vt16, m.cw.ldv16, static_cast<uint16_t *>(m.cw.Vc),
+                                nullptr, 0, 0});
+            gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, kTileRows)));
             const bool avec = aligned(m.in->G, 16) && (m.D.n % 8) == 0;
             q.push_back(pass::Req{static_cast<const uint16_t *>(m.in->G), m.D.n, avec, m.cw.Vt16, m.cw.ldv16, m.cw.Tm,
                                 RP, m.D.m, m.D.n, RP, m.cw.part});
         }
-        launch_jobs("sc_transpose", transpose_bf16_kernel, t, dim3(grid1d(tot)), dim3(256), 0, st);
+        launch_jobs("sc_vconvert", tile_bf16_kernel, t, dim3(gx), dim3(256), 0, st);
         const int rc = pass::run("sc_gv", false, q, st);
         if (rc)
             return rc;
@@ -1671,7 +1732,8 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
         } else {
             tall_gemm<float, false, GT>("sc_ux", q, st);
         }
-        launch_jobs("sc_vconvert", pad_convert_kernel<GT>, pj, dim3(grid1d(tot)), dim3(256), 0, st, r, RP);
+        if (!b16)   // the bf16 copy was made with the transposed one
+            launch_jobs("sc_vconvert", pad_convert_kernel<GT>, pj, dim3(grid1d(tot)), dim3(256), 0, st, r, RP);
     }
     {
         std::vector<BlendJob<GT>> bj;
