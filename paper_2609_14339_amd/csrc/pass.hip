@@ -613,6 +613,209 @@ int launch(const char *tag, int np, bool vec, const std::vector<Job> &jobs, int 
     return ACSC_OK;
 }
 
+
+// ---------------------------------------------------------------------------
+// Anchor EMA fused with the first pass (see sc_pass.h).  A workgroup owns 256
+// rows; per 64-deep step each thread takes eight 8-element chunks of M (two
+// 16-byte loads each) and of G, forms the EMA, stores M (non-temporal) and
+// the bf16 shadow, and drops the bf16 chunk into the swizzled LDS layout of
+// the streaming pass, where the step is multiplied on 32x32x16 MFMA.  All
+// loads go through registers (the next step's are issued before this step's
+// product), so the compiler's own wait counts are exact.
+// ---------------------------------------------------------------------------
+struct EmaJob {
+    float *M;
+    const uint16_t *G;
+    uint16_t *M16;
+    const uint16_t *Bt;
+    int64_t ldbt;
+    float *C;
+    int64_t ldc;
+    int m, n, nblocks;
+};
+struct EmaBatch {
+    int count;
+    EmaJob j[kMaxJobs];
+};
+
+template <int NT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void ema_pass_kernel(const EmaBatch jb, int np,
+                                                                                                 float beta, float omb)
+{
+    const EmaJob &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.x) >= J.nblocks)
+        return;
+    constexpr int NP = NT * 16;
+    constexpr int NC = NT / 2;
+    constexpr int A_BYTES = 256 * 128;
+    constexpr int STAGE = A_BYTES + NP * 128;
+    constexpr int BCH = NP * 8;                 // 16-byte chunks of one thin-factor step
+    constexpr int BPT = (BCH + 255) / 256;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE];
+
+    float *__restrict__ M = J.M;
+    const uint16_t *__restrict__ G = J.G;
+    uint16_t *__restrict__ M16 = J.M16;
+    const uint16_t *__restrict__ Bt = J.Bt;
+    const int64_t ldbt = J.ldbt;
+    const int m = J.m, n = J.n;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int row0 = blockIdx.x * kBM;
+    const int nsteps = static_cast<int>(cdiv(n, kBK));
+
+    f32x16 acc[2][NC];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int t = 0; t < NC; ++t)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[a][t][e] = 0.f;
+
+    // chunk u of this thread: row (tid + 256 u) / 8 of the block, 8 elements
+    // at column 8 ((tid + 256 u) % 8) of the step
+    float4 rm[16];
+    uint4 rg[8], rb[BPT];
+    auto load = [&](int s) {
+        const int k0 = s * kBK;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int q = tid + 256 * u;
+            const int gi = row0 + (q >> 3), gk = k0 + (q & 7) * 8;
+            float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+            uint4 g = make_uint4(0u, 0u, 0u, 0u);
+            if (gi < m && gk < n) {
+                const int64_t o = static_cast<int64_t>(gi) * n + gk;
+                a = *reinterpret_cast<const float4 *>(M + o);
+                b = *reinterpret_cast<const float4 *>(M + o + 4);
+                if (G)
+                    g = *reinterpret_cast<const uint4 *>(G + o);
+            }
+            rm[2 * u] = a;
+            rm[2 * u + 1] = b;
+            rg[u] = g;
+        }
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            const int q = min(tid + 256 * j, BCH - 1);
+            const int c = min(q >> 3, np - 1);
+            const int gk = k0 + (q & 7) * 8;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (gk < n)
+                v = *reinterpret_cast<const uint4 *>(Bt + static_cast<int64_t>(c) * ldbt + gk);
+            rb[j] = v;
+        }
+    };
+    auto store = [&](int buf, int s) {
+        const int k0 = s * kBK;
+        unsigned char *base = smem + buf * STAGE;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int q = tid + 256 * u;
+            const int row = q >> 3, c = q & 7;
+            const int gi = row0 + row, gk = k0 + c * 8;
+            float v[8] = {rm[2 * u].x, rm[2 * u].y, rm[2 * u].z, rm[2 * u].w,
+                          rm[2 * u + 1].x, rm[2 * u + 1].y, rm[2 * u + 1].z, rm[2 * u + 1].w};
+            uint4 h = make_uint4(0u, 0u, 0u, 0u);
+            if (gi < m && gk < n) {
+                const int64_t o = static_cast<int64_t>(gi) * n + gk;
+                if (G) {
+                    const uint32_t w4[4] = {rg[u].x, rg[u].y, rg[u].z, rg[u].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[2 * e] = beta * v[2 * e] + omb * __uint_as_float(w4[e] << 16);
+                        v[2 * e + 1] = beta * v[2 * e + 1] + omb * __uint_as_float(w4[e] & 0xFFFF0000u);
+                    }
+                    __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4 *>(M + o));
+                    __builtin_nontemporal_store(f32x4{v[4], v[5], v[6], v[7]}, reinterpret_cast<f32x4 *>(M + o + 4));
+                }
+                h.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+                h.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+                h.z = static_cast<uint32_t>(f32_to_bf16(v[4])) | (static_cast<uint32_t>(f32_to_bf16(v[5])) << 16);
+                h.w = static_cast<uint32_t>(f32_to_bf16(v[6])) | (static_cast<uint32_t>(f32_to_bf16(v[7])) << 16);
+                *reinterpret_cast<uint4 *>(M16 + o) = h;
+            }
+            *reinterpret_cast<uint4 *>(base + row * 128 + 16 * (c ^ swz(row & 63))) = h;
+        }
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            const int q = tid + 256 * j;
+            if (q < BCH) {
+                const int line = q >> 3, c = q & 7;
+                uint4 v = rb[j];
+                if (line >= np)
+                    v = make_uint4(0u, 0u, 0u, 0u);
+                *reinterpret_cast<uint4 *>(base + A_BYTES + line * 128 + 16 * (c ^ swz(line))) = v;
+            }
+        }
+    };
+    // v_mfma_f32_32x32x16_bf16 on the step in LDS (the layout of pass_dma_kernel<false>)
+    auto compute = [&](int buf) {
+        const unsigned char *aw = smem + buf * STAGE + wave * 8192;
+        const unsigned char *bw = smem + buf * STAGE + A_BYTES;
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) {
+            const int c = kq * 2 + (lane >> 5);
+            bf16x8 af[2], bf[NC];
+#pragma unroll
+            for (int a = 0; a < 2; ++a) {
+                const int line = a * 32 + (lane & 31);
+                af[a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
+            }
+#pragma unroll
+            for (int t = 0; t < NC; ++t) {
+                const int line = t * 32 + (lane & 31);
+                bf[t] = *reinterpret_cast<const bf16x8 *>(bw + line * 128 + 16 * (c ^ swz(line)));
+            }
+#pragma unroll
+            for (int t = 0; t < NC; ++t)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    acc[a][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[t], acc[a][t], 0, 0, 0);
+        }
+    };
+
+    load(0);
+    store(0, 0);
+    lds_barrier();
+    for (int s = 0; s < nsteps; ++s) {
+        if (s + 1 < nsteps)
+            load(s + 1);
+        compute(s & 1);
+        if (s + 1 < nsteps)
+            store((s + 1) & 1, s + 1);
+        lds_barrier();
+    }
+
+    // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
+    const int wrow0 = row0 + wave * 64;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int t = 0; t < NC; ++t) {
+            const int col = t * 32 + (lane & 31);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = wrow0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+                if (row < m && col < np)
+                    J.C[static_cast<int64_t>(row) * J.ldc + col] = acc[a][t][e];
+            }
+        }
+}
+
+template <int NT>
+void ema_launch(const char *tag, const std::vector<EmaJob> &jobs, int gx, int np, float beta, hipStream_t st)
+{
+    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
+        EmaBatch b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
+        for (int i = 0; i < b.count; ++i)
+            b.j[i] = jobs[c0 + i];
+        ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(gx, 1, b.count), dim3(256), 0, st, b, np, beta, 1.0f - beta);
+    }
+}
+
 }  // namespace
 
 int max_splits(int64_t M, int64_t K)
@@ -684,6 +887,49 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
             b.j[i] = red[c0 + i];
         const unsigned g = static_cast<unsigned>(std::min<int64_t>(cdiv(rtot, 256), 8192));
         ACSC_LAUNCH("sc_split_reduce", pass_reduce_kernel, dim3(g, 1, b.count), dim3(256), 0, st, b);
+    }
+    return ACSC_OK;
+}
+
+bool ema_fusable(const std::vector<EmaReq> &reqs)
+{
+    if (reqs.empty())
+        return false;
+    int64_t blocks = 0;
+    for (const EmaReq &q : reqs) {
+        if (q.NP != reqs[0].NP || q.NP < 16 || q.NP % 16 != 0 || q.NP > SC_KMAX || q.n % 8 != 0 || q.ldbt % 8 != 0 ||
+            !aligned(q.M, 16) || (q.G && !aligned(q.G, 16)) || !aligned(q.M16, 16) || !aligned(q.Bt, 16))
+            return false;
+        blocks += cdiv(q.m, kBM);
+    }
+    return blocks >= 256;
+}
+
+int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float beta, hipStream_t st)
+{
+    if (!ema_fusable(reqs))
+        return set_error(ACSC_EINVAL, "fused EMA pass: operands not aligned or batch too small");
+    const int NP = reqs[0].NP;
+    // longest rows first, as for the streaming passes
+    std::vector<size_t> order(reqs.size());
+    for (size_t i = 0; i < order.size(); ++i)
+        order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return reqs[a].n > reqs[b].n; });
+    std::vector<EmaJob> jobs;
+    int gx = 1;
+    for (size_t oi : order) {
+        const EmaReq &q = reqs[oi];
+        const int nb = static_cast<int>(cdiv(q.m, kBM));
+        jobs.push_back(EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, nb});
+        gx = std::max(gx, nb);
+    }
+    switch ((NP / 16 + 1) / 2) {   // column tiles in pairs; tiles past NP read zeros
+    case 1: ema_launch<2>(tag, jobs, gx, NP, beta, st); break;
+    case 2: ema_launch<4>(tag, jobs, gx, NP, beta, st); break;
+    case 3: ema_launch<6>(tag, jobs, gx, NP, beta, st); break;
+    case 4: ema_launch<8>(tag, jobs, gx, NP, beta, st); break;
+    case 5: ema_launch<10>(tag, jobs, gx, NP, beta, st); break;
+    default: ema_launch<12>(tag, jobs, gx, NP, beta, st); break;
     }
     return ACSC_OK;
 }

@@ -1515,28 +1515,37 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     const int k = d0.k, KP = d0.KP, RP = d0.RP;
     const bool use16 = dt == ACSC_BF16;
     const float omb = 1.0f - beta;
-    if (use16) {
-        std::vector<EmaJob<uint16_t>> j;
-        int64_t tot = 1;
-        for (auto &m : ms) {
-            j.push_back(EmaJob<uint16_t>{m.in->M, static_cast<const uint16_t *>(m.in->G), m.D.m, m.D.n,
-                                         (m.D.n % 8) == 0 ? 1 : 0, m.pw.M16, m.pw.ld16});
-            tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.m) * cdiv(m.D.n, 8));
+    // with a bf16 shadow and a large enough batch, the EMA runs fused with the
+    // first pass Y = M16 Z (after the starting block exists)
+    std::vector<pass::EmaReq> er;
+    for (auto &m : ms)
+        er.push_back(pass::EmaReq{m.in->M, static_cast<const uint16_t *>(m.in->G), m.pw.M16, m.pw.Zt16, m.pw.ldz16,
+                                  m.pw.Y, KP, m.D.m, m.D.n, KP});
+    const bool fused = use16 && pass::ema_fusable(er);
+    if (!fused) {
+        if (use16) {
+            std::vector<EmaJob<uint16_t>> j;
+            int64_t tot = 1;
+            for (auto &m : ms) {
+                j.push_back(EmaJob<uint16_t>{m.in->M, static_cast<const uint16_t *>(m.in->G), m.D.m, m.D.n,
+                                             (m.D.n % 8) == 0 ? 1 : 0, m.pw.M16, m.pw.ld16});
+                tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.m) * cdiv(m.D.n, 8));
+            }
+            launch_jobs("sc_ema", ema_shadow_kernel<uint16_t>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
+        } else {
+            std::vector<Ema32Job<float>> j;
+            int64_t tot = 1;
+            for (auto &m : ms) {
+                const int64_t c = static_cast<int64_t>(m.D.m) * m.D.n;
+                j.push_back(Ema32Job<float>{m.in->M, static_cast<const float *>(m.in->G), c});
+                tot = std::max(tot, cdiv(c, 4));
+            }
+            bool any = false;
+            for (auto &m : ms)
+                any = any || m.in->G;
+            if (any)
+                launch_jobs("sc_ema", ema_kernel<float>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
         }
-        launch_jobs("sc_ema", ema_shadow_kernel<uint16_t>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
-    } else {
-        std::vector<Ema32Job<float>> j;
-        int64_t tot = 1;
-        for (auto &m : ms) {
-            const int64_t c = static_cast<int64_t>(m.D.m) * m.D.n;
-            j.push_back(Ema32Job<float>{m.in->M, static_cast<const float *>(m.in->G), c});
-            tot = std::max(tot, cdiv(c, 4));
-        }
-        bool any = false;
-        for (auto &m : ms)
-            any = any || m.in->G;
-        if (any)
-            launch_jobs("sc_ema", ema_kernel<float>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
     }
     {
         std::vector<InitJob> j;
@@ -1589,7 +1598,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
             return ACSC_OK;
         }
     };
-    int rc = pass(true);
+    int rc = fused ? pass::ema_run("sc_ema", er, beta, st) : pass(true);
     if (rc)
         return rc;
     if ((rc = orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st)))

@@ -36,5 +36,27 @@ int max_splits(int64_t M, int64_t K);
 // Enqueue one pass per request (all requests share NP) on `st`.
 int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t st);
 
+// The anchor EMA fused with the first pass of the subspace iteration
+// (Sec. 3.2): M <- beta M + (1 - beta) G (G may be null: M is kept), the bf16
+// shadow M16 = bf16(M) written for the later passes, and C = M16 * B in the
+// same sweep over M, so that the first pass does not read the shadow back.
+struct EmaReq {
+    float *M;             // [m, n] fp32, row stride n
+    const uint16_t *G;    // [m, n] bf16, or nullptr
+    uint16_t *M16;        // [m, n] bf16, row stride n
+    const uint16_t *Bt;   // thin factor transposed [NP, ldbt] bf16
+    int64_t ldbt;
+    float *C;             // [m, NP] fp32, row stride ldc
+    int64_t ldc;
+    int m, n, NP;
+};
+
+// Whether the fused kernel takes this batch: 16-byte aligned operands, n a
+// multiple of 8, one NP, and enough row blocks over the batch to fill the
+// GPU without splitting K.
+bool ema_fusable(const std::vector<EmaReq> &reqs);
+
+int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float beta, hipStream_t st);
+
 }  // namespace pass
 }  // namespace acsc
