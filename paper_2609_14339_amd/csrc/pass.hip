@@ -616,12 +616,13 @@ int launch(const char *tag, int np, bool vec, const std::vector<Job> &jobs, int 
 
 // ---------------------------------------------------------------------------
 // Anchor EMA fused with the first pass (see sc_pass.h).  A workgroup owns 256
-// rows; per 64-deep step each thread takes eight 8-element chunks of M (two
-// 16-byte loads each) and of G, forms the EMA, stores M (non-temporal) and
-// the bf16 shadow, and drops the bf16 chunk into the swizzled LDS layout of
-// the streaming pass, where the step is multiplied on 32x32x16 MFMA.  All
-// loads go through registers (the next step's are issued before this step's
-// product), so the compiler's own wait counts are exact.
+// rows; per 64-deep step each thread takes sixteen 4-element pieces of M
+// (16-byte loads, 16 lanes per row) and of G, forms the EMA, stores M
+// (non-temporal) and the bf16 shadow, and drops the bf16 piece into the
+// swizzled LDS layout of the streaming pass, where the step is multiplied on
+// 32x32x16 MFMA.  All loads go through registers (the next step's are
+// issued before this step's product), so the compiler's own wait counts are
+// exact.
 // ---------------------------------------------------------------------------
 struct EmaJob {
     float *M;
@@ -673,27 +674,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             for (int e = 0; e < 16; ++e)
                 acc[a][t][e] = 0.f;
 
-    // chunk u of this thread: row (tid + 256 u) / 8 of the block, 8 elements
-    // at column 8 ((tid + 256 u) % 8) of the step
+    // piece u of this thread: row (tid + 256 u) / 16 of the block, 4 elements
+    // at column 4 ((tid + 256 u) % 16) of the step, so that 16 lanes cover a
+    // row's 256 bytes of M (128 of G) with one instruction
     float4 rm[16];
-    uint4 rg[8], rb[BPT];
+    uint2 rg[16];
+    uint4 rb[BPT];
     auto load = [&](int s) {
         const int k0 = s * kBK;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 16; ++u) {
             const int q = tid + 256 * u;
-            const int gi = row0 + (q >> 3), gk = k0 + (q & 7) * 8;
-            float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
-            uint4 g = make_uint4(0u, 0u, 0u, 0u);
+            const int gi = row0 + (q >> 4), gk = k0 + (q & 15) * 4;
+            float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+            uint2 g = make_uint2(0u, 0u);
             if (gi < m && gk < n) {
                 const int64_t o = static_cast<int64_t>(gi) * n + gk;
                 a = *reinterpret_cast<const float4 *>(M + o);
-                b = *reinterpret_cast<const float4 *>(M + o + 4);
                 if (G)
-                    g = *reinterpret_cast<const uint4 *>(G + o);
+                    g = *reinterpret_cast<const uint2 *>(G + o);
             }
-            rm[2 * u] = a;
-            rm[2 * u + 1] = b;
+            rm[u] = a;
             rg[u] = g;
         }
 #pragma unroll
@@ -711,32 +712,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const int k0 = s * kBK;
         unsigned char *base = smem + buf * STAGE;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 16; ++u) {
             const int q = tid + 256 * u;
-            const int row = q >> 3, c = q & 7;
-            const int gi = row0 + row, gk = k0 + c * 8;
-            float v[8] = {rm[2 * u].x, rm[2 * u].y, rm[2 * u].z, rm[2 * u].w,
-                          rm[2 * u + 1].x, rm[2 * u + 1].y, rm[2 * u + 1].z, rm[2 * u + 1].w};
-            uint4 h = make_uint4(0u, 0u, 0u, 0u);
+            const int row = q >> 4, f = q & 15;
+            const int gi = row0 + row, gk = k0 + f * 4;
+            float v[4] = {rm[u].x, rm[u].y, rm[u].z, rm[u].w};
+            uint2 h = make_uint2(0u, 0u);
             if (gi < m && gk < n) {
                 const int64_t o = static_cast<int64_t>(gi) * n + gk;
                 if (G) {
-                    const uint32_t w4[4] = {rg[u].x, rg[u].y, rg[u].z, rg[u].w};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        v[2 * e] = beta * v[2 * e] + omb * __uint_as_float(w4[e] << 16);
-                        v[2 * e + 1] = beta * v[2 * e + 1] + omb * __uint_as_float(w4[e] & 0xFFFF0000u);
-                    }
+                    v[0] = beta * v[0] + omb * __uint_as_float(rg[u].x << 16);
+                    v[1] = beta * v[1] + omb * __uint_as_float(rg[u].x & 0xFFFF0000u);
+                    v[2] = beta * v[2] + omb * __uint_as_float(rg[u].y << 16);
+                    v[3] = beta * v[3] + omb * __uint_as_float(rg[u].y & 0xFFFF0000u);
                     __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4 *>(M + o));
-                    __builtin_nontemporal_store(f32x4{v[4], v[5], v[6], v[7]}, reinterpret_cast<f32x4 *>(M + o + 4));
                 }
                 h.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
                 h.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-                h.z = static_cast<uint32_t>(f32_to_bf16(v[4])) | (static_cast<uint32_t>(f32_to_bf16(v[5])) << 16);
-                h.w = static_cast<uint32_t>(f32_to_bf16(v[6])) | (static_cast<uint32_t>(f32_to_bf16(v[7])) << 16);
-                *reinterpret_cast<uint4 *>(M16 + o) = h;
+                *reinterpret_cast<uint2 *>(M16 + o) = h;
             }
-            *reinterpret_cast<uint4 *>(base + row * 128 + 16 * (c ^ swz(row & 63))) = h;
+            *reinterpret_cast<uint2 *>(base + row * 128 + 16 * ((f >> 1) ^ swz(row & 63)) + 8 * (f & 1)) = h;
         }
 #pragma unroll
         for (int j = 0; j < BPT; ++j) {
