@@ -559,7 +559,7 @@ struct JacJob {
     int *info;
 };
 
-template <typename T>
+template <typename T, int RC>
 __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, int k, int KP, int r,
                                                       int RP, float tau, T tol, int max_sweeps)
 {
@@ -568,10 +568,10 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     float *Bu = J.Bu, *Bv = J.Bv, *s_out = J.s_out, *d_out = J.d_out;
     int *info = J.info;
     extern __shared__ __attribute__((aligned(16))) unsigned char jsm[];
-    // column c at A[c * kp]; kp = k rounded up to 32, rows k..kp-1 are zero.
-    // Lane gl of a pair's 8 lanes holds the R = kp / 8 consecutive rows
-    // gl R .. gl R + R - 1 of both columns (R a multiple of 4: 16-byte LDS
-    // accesses).
+    // column c at A[c * kp]; kp = k rounded up to 32 (= 8 RC), rows k..kp-1
+    // are zero.  Lane gl of a pair's 8 lanes holds the R = kp / 8 consecutive
+    // rows gl R .. gl R + R - 1 of both columns (R a multiple of 4: 16-byte
+    // LDS accesses).
     T *A = reinterpret_cast<T *>(jsm);
     const int kp = (k + 31) & ~31;
     T *nrm = A + static_cast<size_t>(k) * kp;   // squared column norms
@@ -589,10 +589,10 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     // eight column pairs per wave, 8 lanes each
     const int grp = lane >> 3, gl = lane & 7;
     const int slots = nwave * 8;
-    const int R = kp / 8;
-    // fp64 runs for k <= kJacobiF64MaxK only
-    constexpr int RMAX = ((sizeof(T) == 8 ? kJacobiF64MaxK : kKMax) + 31) / 32 * 4;
+    constexpr int R = RC;
+    constexpr int RMAX = RC;
     constexpr int V = 16 / sizeof(T);   // elements per 16-byte access
+    static_assert(R % 4 == 0, "rows per lane");
     int sweeps_used = 0;
     float last_off = 0.f;
     __syncthreads();
@@ -1353,6 +1353,33 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
     }
 }
 
+// The Jacobi kernel for order k, by rows per lane (k rounded up to 32, over 8).
+template <typename T>
+using JacobiFn = void (*)(const Batch<JacJob>, int, int, int, int, float, T, int);
+
+template <typename T>
+JacobiFn<T> jacobi_fn(int k)
+{
+    switch (((k + 31) & ~31) / 8) {
+    case 4: return jacobi_kernel<T, 4>;
+    case 8: return jacobi_kernel<T, 8>;
+    case 12: return jacobi_kernel<T, 12>;
+    default: return jacobi_kernel<T, 16>;
+    }
+}
+template <>
+JacobiFn<float> jacobi_fn<float>(int k)
+{
+    switch (((k + 31) & ~31) / 8) {
+    case 4: return jacobi_kernel<float, 4>;
+    case 8: return jacobi_kernel<float, 8>;
+    case 12: return jacobi_kernel<float, 12>;
+    case 16: return jacobi_kernel<float, 16>;
+    case 20: return jacobi_kernel<float, 20>;
+    default: return jacobi_kernel<float, 24>;
+    }
+}
+
 // one 8-lane group per column pair of a round, at least 4 and at most 16 waves
 unsigned jacobi_threads(int k)
 {
@@ -1631,11 +1658,11 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         if ((rc = chol::run("sc_chol", cj, k, KP, false, st)))
             return rc;
         if (k <= kJacobiF64MaxK)
-            launch_jobs("sc_jacobi", jacobi_kernel<double>, jj, dim3(1), dim3(jacobi_threads(k)),
+            launch_jobs("sc_jacobi", jacobi_fn<double>(k), jj, dim3(1), dim3(jacobi_threads(k)),
                         jacobi_lds(k, sizeof(double)), st,
                         k, KP, r, RP, tau, 1e-13, 40);
         else
-            launch_jobs("sc_jacobi", jacobi_kernel<float>, jj, dim3(1), dim3(jacobi_threads(k)),
+            launch_jobs("sc_jacobi", jacobi_fn<float>(k), jj, dim3(1), dim3(jacobi_threads(k)),
                         jacobi_lds(k, sizeof(float)), st,
                         k, KP, r, RP, tau, 1e-5f, 40);
     }
@@ -1860,8 +1887,8 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
     for (const Mat &m : all) {
         int rc = chol::prepare(m.D.KP);
         if (!rc)
-            rc = m.D.k <= kJacobiF64MaxK ? allow_lds(jacobi_kernel<double>, jacobi_lds(m.D.k, sizeof(double)))
-                              : allow_lds(jacobi_kernel<float>, jacobi_lds(m.D.k, sizeof(float)));
+            rc = m.D.k <= kJacobiF64MaxK ? allow_lds(jacobi_fn<double>(m.D.k), jacobi_lds(m.D.k, sizeof(double)))
+                                         : allow_lds(jacobi_fn<float>(m.D.k), jacobi_lds(m.D.k, sizeof(float)));
         if (rc)
             return rc;
     }
