@@ -60,6 +60,24 @@ def correct(G: np.ndarray, U: np.ndarray, d: np.ndarray, V: np.ndarray, alpha: f
     return alpha * G + (1.0 - alpha) * two_sided_filter(G, U, d, V)
 
 
+def correct_rows(G, U: np.ndarray, d: np.ndarray, V: np.ndarray, alpha: float, rows) -> np.ndarray:
+    """Rows `rows` of G_proj = alpha G + (1 - alpha) U diag(d) (U^T G V) diag(d)
+    V^T (Sec. 3.2 eq.; Alg. 1), for matrices too large to form G_proj whole.
+
+    X = U^T (G V) needs all of G; it is accumulated in float64 over blocks of
+    rows of G (an array or a callable giving rows [a, b) as an array)."""
+    m = U.shape[0]
+    get = G if callable(G) else (lambda a, b: np.asarray(G[a:b], dtype=np.float64))
+    X = np.zeros((U.shape[1], V.shape[1]))
+    for a in range(0, m, 1024):
+        b = min(m, a + 1024)
+        X += U[a:b].T @ (get(a, b) @ V)
+    Xf = d[:, None] * X * d[None, :]
+    rows = np.asarray(rows)
+    Gr = np.concatenate([get(int(i), int(i) + 1) for i in rows], axis=0)
+    return alpha * Gr + (1.0 - alpha) * (U[rows] @ Xf @ V.T)
+
+
 def build_prior(M_prev, G_anc, beta: float, r: int, tau: float):
     """EMA (if an anchor gradient arrived), then top-r SVD and filter weights.
 

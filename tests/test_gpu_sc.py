@@ -207,8 +207,10 @@ def test_errors_raise_before_any_work(pk):
 
 def test_batched_calls_equal_single_calls(pk):
     """One batched call over mixed shapes gives bit-identical results to one
-    call per matrix (matrix i of the batch uses seed + i)."""
-    shapes = [(256, 384), (384, 256), (200, 328)]
+    call per matrix (matrix i of the batch uses seed + i).  The (20, 300)
+    matrix has k = min(r + p, m, n) = 20 rather than 24, so the batch runs as
+    two groups."""
+    shapes = [(256, 384), (384, 256), (20, 300), (200, 328)]
     r, p, q = 16, 8, 2
     mats = []
     for i, (m, n) in enumerate(shapes):

@@ -235,3 +235,21 @@ def test_planted_mistakes_are_caught_by_the_pins(monkeypatch):
     # amplifying filter weights break Lemma 1
     monkeypatch.setattr(osp, "filter_weights", lambda s_, t: 1.0 + s_ / (s_ + t))
     assert not lemma1_ok()
+
+
+def test_correct_rows_equals_the_rows_of_the_whole_correction():
+    """The row-sampled correction (for matrices too large to form whole)
+    gives exactly the rows of the whole correction, whether G is an array or
+    a row-block callable, including a block boundary at 1024 rows."""
+    rng = np.random.default_rng(5)
+    m, n, r = 2100, 70, 6
+    G = rng.standard_normal((m, n))
+    U = np.linalg.qr(rng.standard_normal((m, r)))[0]
+    V = np.linalg.qr(rng.standard_normal((n, r)))[0]
+    d = rng.uniform(0.2, 0.9, r)
+    rows = np.array([0, 1023, 1024, 2099, 17])
+    whole = osp.correct(G, U, d, V, 0.3)
+    got = osp.correct_rows(G, U, d, V, 0.3, rows)
+    assert np.allclose(got, whole[rows], rtol=1e-12, atol=1e-12)
+    got2 = osp.correct_rows(lambda a, b: G[a:b], U, d, V, 0.3, rows)
+    assert np.allclose(got2, whole[rows], rtol=1e-12, atol=1e-12)
