@@ -14,6 +14,8 @@
 namespace acsc {
 namespace {
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
 constexpr int kMaxWavesPerBlock = 4;
 constexpr size_t kLdsBudget = 160 * 1024;
@@ -98,6 +100,56 @@ struct RowPerm {
     }
 };
 
+// The round function's output is masked to hb <= 8 bits and its input R has
+// hb bits, so a row's whole round function is a table of ROUNDS x 2^hb bytes.
+// Filling it costs ROUNDS * 2^hb mixer evaluations per row instead of ROUNDS
+// per Feistel evaluation (about K * 2^w / H of those), which is what bounds
+// the kernels when K is large next to 2^hb.  Rounds sit at a 256-byte stride
+// so that the round offset is an immediate of the LDS read.
+constexpr int kTabStride = 256;
+
+template <int ROUNDS>
+__host__ __device__ __forceinline__ constexpr int table_bytes() { return ROUNDS * kTabStride; }
+
+// Whether a row's round table is cheaper than evaluating the round function
+// per Feistel step: 2^hb entries per round against about K * 2^w / H
+// evaluations (cycle walking rejects 1 - H / 2^w of them).
+inline bool use_table(int H, int K, int w)
+{
+    const int hb = w >> 1;
+    return hb <= 8 && static_cast<int64_t>(K) << w >= static_cast<int64_t>(H) << hb;
+}
+
+template <int ROUNDS>
+struct TabPerm {
+    const uint8_t *tab;
+    uint32_t mask;
+    int hb;
+
+    // Every lane of the wave calls this; the caller orders the table writes
+    // before the first read (wave_sync).
+    __device__ __forceinline__ TabPerm(const RowPerm<ROUNDS> &p, uint8_t *t, int lane) : tab(t), mask(p.mask), hb(p.hb)
+    {
+        const int n = 1 << hb;
+#pragma unroll
+        for (int j = 0; j < ROUNDS; ++j)
+            for (int r = lane; r < n; r += 64)
+                t[j * kTabStride + r] = static_cast<uint8_t>(fmix32(static_cast<uint32_t>(r) ^ p.sk[j]) & p.mask);
+    }
+
+    __device__ __forceinline__ uint32_t feistel(uint32_t x) const
+    {
+        uint32_t L = x >> hb, R = x & mask;
+#pragma unroll
+        for (int j = 0; j < ROUNDS; ++j) {
+            const uint32_t t = L ^ tab[j * kTabStride + R];
+            L = R;
+            R = t;
+        }
+        return (L << hb) | R;
+    }
+};
+
 __device__ __forceinline__ int wave_exclusive_scan(int v, int lane)
 {
     int incl = v;
@@ -126,8 +178,8 @@ __device__ __forceinline__ void wave_sync()
 // performs one evaluation per step and a lane whose walk ended takes the next
 // unassigned index; the wave runs about 2 K / 64 steps for H about half the
 // Feistel domain.
-template <int ROUNDS>
-__device__ __forceinline__ void mark_kept(const RowPerm<ROUNDS> &perm, int K, uint32_t H, uint32_t *bm, int lane)
+template <typename Perm>
+__device__ __forceinline__ void mark_kept(const Perm &perm, int K, uint32_t H, uint32_t *bm, int lane)
 {
     int i = lane;
     bool live = i < K;
@@ -154,7 +206,15 @@ __device__ __forceinline__ void mark_kept(const RowPerm<ROUNDS> &perm, int K, ui
 // Per-wave LDS layout of the pack kernel: bitmap[nw] then uint16 kidx[K].
 __host__ __device__ __forceinline__ int pack_wave_words(int nw, int K) { return nw + (K + 1) / 2; }
 
-template <typename E, int ROUNDS>
+// Per-wave LDS of the pack kernel in bytes: the words above, then (TABLE) the
+// row's round table.
+template <int ROUNDS, bool TABLE>
+__host__ __device__ __forceinline__ int pack_wave_bytes(int nw, int K)
+{
+    return 4 * pack_wave_words(nw, K) + (TABLE ? table_bytes<ROUNDS>() : 0);
+}
+
+template <typename E, int ROUNDS, bool TABLE>
 __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, int64_t rows, int H,
                                                       int64_t ld_x, int K, uint64_t key, int w,
                                                       E *__restrict__ vals,
@@ -162,10 +222,11 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
 {
     extern __shared__ uint32_t smem[];
     const int lane = threadIdx.x & 63;
-    const int wid = threadIdx.x >> 6;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wpb = blockDim.x >> 6;
     const int nw = (H + 31) >> 5;
-    uint32_t *bm = smem + wid * pack_wave_words(nw, K);
+    uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) +
+                                                wid * pack_wave_bytes<ROUNDS, TABLE>(nw, K));
     uint16_t *kidx = reinterpret_cast<uint16_t *>(bm + nw);
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
@@ -174,10 +235,16 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
         return;
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
-    wave_sync();
     {
         const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
-        mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
+        if (TABLE) {
+            const TabPerm<ROUNDS> tp(perm, reinterpret_cast<uint8_t *>(bm + pack_wave_words(nw, K)), lane);
+            wave_sync();
+            mark_kept(tp, K, static_cast<uint32_t>(H), bm, lane);
+        } else {
+            wave_sync();
+            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
+        }
     }
     wave_sync();
     {
@@ -288,24 +355,32 @@ __host__ __device__ __forceinline__ size_t staged_wave_bytes(int nw, int K, int 
 // Builds the kept-set bitmap of `row` (from the key, or from the transmitted
 // indices) and the exclusive prefix of its word popcounts.  Every lane of the
 // row's wave calls it.
-template <int ROUNDS>
+// With TABLE, `tab` is the wave's round-table space (table_bytes<ROUNDS>()).
+template <int ROUNDS, bool TABLE>
 __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, bool active, uint64_t key,
                                            int64_t row, int w, int H, int K, int lane,
-                                           const uint16_t *idx_row)
+                                           const uint16_t *idx_row, uint8_t *tab)
 {
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
-    wave_sync();
-    if (active) {
-        if (idx_row) {
+    if (active && !idx_row) {
+        const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
+        if (TABLE) {
+            const TabPerm<ROUNDS> tp(perm, tab, lane);
+            wave_sync();
+            mark_kept(tp, K, static_cast<uint32_t>(H), bm, lane);
+        } else {
+            wave_sync();
+            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
+        }
+    } else {
+        wave_sync();
+        if (active) {
             for (int i = lane; i < K; i += 64) {
                 const uint32_t j = idx_row[i];
                 if (j < static_cast<uint32_t>(H))
                     atomicOr(&bm[j >> 5], 1u << (j & 31));
             }
-        } else {
-            const RowPerm<ROUNDS> perm(key, static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
-            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
         }
     }
     wave_sync();
@@ -328,7 +403,7 @@ __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, 
 // hold at least one kept entry (chunks with none are never fetched), drops the
 // kept entries into their rank slots of an LDS copy of the packed row, and
 // the packed row (and its indices) leaves with coalesced stores.
-template <typename E, int ROUNDS>
+template <typename E, int ROUNDS, bool TABLE>
 __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict__ x, int64_t rows, int H,
                                                              int64_t ld_x, int K, uint64_t key, int w,
                                                              E *__restrict__ vals,
@@ -337,18 +412,20 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
     extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
     constexpr int N = Vec16<E>::N;
     const int lane = threadIdx.x & 63;
-    const int wid = threadIdx.x >> 6;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wpb = blockDim.x >> 6;
     const int nw = (H + 31) >> 5;
     // the index slots are always reserved (they are written even when idx is NULL)
-    const size_t per_wave = staged_wave_bytes(nw, K, sizeof(E), true);
+    const size_t staged = staged_wave_bytes(nw, K, sizeof(E), true);
+    const size_t per_wave = staged + (TABLE ? table_bytes<ROUNDS>() : 0);
     uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) + wid * per_wave);
     uint32_t *pre = bm + nw;
     E *kv = reinterpret_cast<E *>(pre + nw);
     uint16_t *ki = reinterpret_cast<uint16_t *>(kv + K);
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
-    row_bitmap<ROUNDS>(bm, pre, nw, active, key, row, w, H, K, lane, nullptr);
+    row_bitmap<ROUNDS, TABLE>(bm, pre, nw, active, key, row, w, H, K, lane, nullptr,
+                              reinterpret_cast<uint8_t *>(bm) + staged);
     if (active) {
         const E *xr = x + row * ld_x;
         const int nch = H / N;
@@ -399,7 +476,7 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
 // Every lane's work is uniform (zeroing and copying) except the drop of the
 // few kept entries, where writing each 16-byte chunk with its kept entries in
 // place made every lane of the wave pay for the chunks that hold one.
-template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
+template <typename E, int ROUNDS, bool FROM_IDX, bool VEC, bool TABLE>
 __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restrict__ vals,
                                                                const uint16_t *__restrict__ idx,
                                                                int64_t rows, int H, int K, uint64_t key,
@@ -408,10 +485,11 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
 {
     extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
     const int lane = threadIdx.x & 63;
-    const int wid = threadIdx.x >> 6;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wpb = blockDim.x >> 6;
     const int nw = (H + 31) >> 5;
-    const size_t per_wave = staged_wave_bytes(nw, K, sizeof(E), false);
+    const size_t staged = staged_wave_bytes(nw, K, sizeof(E), false);
+    const size_t per_wave = staged + (TABLE ? table_bytes<ROUNDS>() : 0);
     uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) + wid * per_wave);
     uint32_t *pre = bm + nw;
     E *kv = reinterpret_cast<E *>(pre + nw);
@@ -422,8 +500,9 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
         for (int i = lane; i < K; i += 64)
             kv[i] = vr[i];
     }
-    row_bitmap<ROUNDS>(bm, pre, nw, active, key, row, w, H, K, lane,
-                       (FROM_IDX && active) ? idx + row * K : nullptr);
+    row_bitmap<ROUNDS, TABLE>(bm, pre, nw, active, key, row, w, H, K, lane,
+                              (FROM_IDX && active) ? idx + row * K : nullptr,
+                              reinterpret_cast<uint8_t *>(bm) + staged);
     if (!active)
         return;
     // The dense row is assembled in LDS one segment (64 bitmap words) at a
@@ -452,8 +531,12 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
         wave_sync();
         if (VEC) {
             const int nch = len / N;
+            // non-temporal: the dense rows are not read again by this stage,
+            // and stores that stay dirty in the memory-side cache are only
+            // paid for by whichever kernel runs next
             for (int c = lane; c < nch; c += 64)
-                *reinterpret_cast<uint4 *>(yr + e0 + c * N) = reinterpret_cast<const uint4 *>(seg)[c];
+                __builtin_nontemporal_store(reinterpret_cast<const u32x4 *>(seg)[c],
+                                            reinterpret_cast<u32x4 *>(yr + e0 + c * N));
             for (int j = nch * N + lane; j < len; j += 64)
                 yr[e0 + j] = seg[j];
         } else {
@@ -579,59 +662,78 @@ int waves_for(size_t per_wave_bytes)
     return wpb;
 }
 
-template <typename E, int ROUNDS>
-void launch_pack(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
-                 void *vals, uint16_t *idx, hipStream_t st)
+template <typename E, int ROUNDS, bool TABLE>
+void launch_pack_t(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
+                   void *vals, uint16_t *idx, hipStream_t st)
 {
     // The streaming form (whole 16-byte chunks) measured slower on MI355X than
     // the gather below at every keep fraction of the workloads; it stays
     // available for rows whose kept entries are dense (keep >= 1/4).
-    const int nwords = (H + 31) / 32;
-    const size_t sper = staged_wave_bytes(nwords, K, sizeof(E), true);
+    const int nw = (H + 31) / 32;
+    const size_t tab = TABLE ? table_bytes<ROUNDS>() : 0;
+    const size_t sper = staged_wave_bytes(nw, K, sizeof(E), true) + tab;
     const bool vec = aligned(x, 16) && (static_cast<size_t>(ld_x) * sizeof(E)) % 16 == 0;
     const bool dense = 4 * static_cast<int64_t>(K) >= H;
     if (dense && vec && sper <= kLdsBudget &&
-        allow_lds(ac_pack_stream_kernel<E, ROUNDS>, sper * waves_for(sper)) == ACSC_OK) {
+        allow_lds(ac_pack_stream_kernel<E, ROUNDS, TABLE>, sper * waves_for(sper)) == ACSC_OK) {
         const int wpb = waves_for(sper);
         const int64_t blocks = (rows + wpb - 1) / wpb;
-        ACSC_LAUNCH("ac_pack", (ac_pack_stream_kernel<E, ROUNDS>), dim3(static_cast<unsigned>(blocks)),
+        ACSC_LAUNCH("ac_pack", (ac_pack_stream_kernel<E, ROUNDS, TABLE>), dim3(static_cast<unsigned>(blocks)),
                     dim3(64 * wpb), sper * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K, key, w,
                     static_cast<E *>(vals), idx);
         return;
     }
-    const int nw = (H + 31) / 32;
-    const size_t per = static_cast<size_t>(pack_wave_words(nw, K)) * 4;
+    const size_t per = static_cast<size_t>(pack_wave_bytes<ROUNDS, TABLE>(nw, K));
     const int wpb = waves_for(per);
-    allow_lds(ac_pack_kernel<E, ROUNDS>, per * wpb);
+    allow_lds(ac_pack_kernel<E, ROUNDS, TABLE>, per * wpb);
     const int64_t blocks = (rows + wpb - 1) / wpb;
-    ACSC_LAUNCH("ac_pack", (ac_pack_kernel<E, ROUNDS>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(64 * wpb), per * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K,
-                       key, w, static_cast<E *>(vals), idx);
+    ACSC_LAUNCH("ac_pack", (ac_pack_kernel<E, ROUNDS, TABLE>), dim3(static_cast<unsigned>(blocks)),
+                dim3(64 * wpb), per * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K,
+                key, w, static_cast<E *>(vals), idx);
+}
+
+template <typename E, int ROUNDS>
+void launch_pack(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
+                 void *vals, uint16_t *idx, hipStream_t st)
+{
+    if (use_table(H, K, w))
+        launch_pack_t<E, ROUNDS, true>(x, rows, H, ld_x, K, key, w, vals, idx, st);
+    else
+        launch_pack_t<E, ROUNDS, false>(x, rows, H, ld_x, K, key, w, vals, idx, st);
+}
+
+template <typename E, int ROUNDS, bool FROM_IDX, bool VEC, bool TABLE>
+bool launch_unpack_stream(const void *vals, const uint16_t *idx, int64_t rows, int H, int K, uint64_t key,
+                          int w, float scale, void *y, int64_t ld_y, hipStream_t st)
+{
+    const int nw = (H + 31) / 32;
+    const size_t sper = staged_wave_bytes(nw, K, sizeof(E), false) + (TABLE ? table_bytes<ROUNDS>() : 0);
+    if (sper > kLdsBudget ||
+        allow_lds(ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, VEC, TABLE>, sper * waves_for(sper)) != ACSC_OK)
+        return false;
+    const int wpb = waves_for(sper);
+    const int64_t blocks = (rows + wpb - 1) / wpb;
+    ACSC_LAUNCH("ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, VEC, TABLE>),
+                dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), sper * wpb, st,
+                static_cast<const E *>(vals), idx, rows, H, K, key, w, scale, static_cast<E *>(y), ld_y);
+    return true;
 }
 
 template <typename E, int ROUNDS, bool FROM_IDX>
 void launch_unpack(const void *vals, const uint16_t *idx, int64_t rows, int H, int K, uint64_t key,
                    int w, float scale, void *y, int64_t ld_y, bool vec, hipStream_t st)
 {
-    const int nwords = (H + 31) / 32;
-    const size_t sper = staged_wave_bytes(nwords, K, sizeof(E), false);
-    const bool lds_ok = sper <= kLdsBudget &&
-                        (vec ? allow_lds(ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, true>, sper * waves_for(sper))
-                             : allow_lds(ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, false>, sper * waves_for(sper))) ==
-                            ACSC_OK;
-    if (lds_ok) {
-        const int wpb = waves_for(sper);
-        const int64_t blocks = (rows + wpb - 1) / wpb;
-        if (vec)
-            ACSC_LAUNCH("ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, true>),
-                        dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), sper * wpb, st,
-                        static_cast<const E *>(vals), idx, rows, H, K, key, w, scale, static_cast<E *>(y), ld_y);
-        else
-            ACSC_LAUNCH("ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, false>),
-                        dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), sper * wpb, st,
-                        static_cast<const E *>(vals), idx, rows, H, K, key, w, scale, static_cast<E *>(y), ld_y);
+    // transmitted indices need no permutation, so no round table either
+    const bool table = !FROM_IDX && use_table(H, K, w);
+    bool done;
+    if (vec)
+        done = table ? launch_unpack_stream<E, ROUNDS, FROM_IDX, true, true>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st)
+                     : launch_unpack_stream<E, ROUNDS, FROM_IDX, true, false>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st);
+    else
+        done = table ? launch_unpack_stream<E, ROUNDS, FROM_IDX, false, true>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st)
+                     : launch_unpack_stream<E, ROUNDS, FROM_IDX, false, false>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st);
+    if (done)
         return;
-    }
     const int nw = (H + 31) / 32;
     const size_t per = static_cast<size_t>(2 * nw) * 4;
     const int wpb = waves_for(per);
@@ -640,14 +742,14 @@ void launch_unpack(const void *vals, const uint16_t *idx, int64_t rows, int H, i
     const int64_t blocks = (rows + wpb - 1) / wpb;
     if (vec)
         ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, true>),
-                           dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
-                           static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
-                           static_cast<E *>(y), ld_y);
+                    dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
+                    static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
+                    static_cast<E *>(y), ld_y);
     else
         ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, false>),
-                           dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
-                           static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
-                           static_cast<E *>(y), ld_y);
+                    dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
+                    static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
+                    static_cast<E *>(y), ld_y);
 }
 
 }  // namespace

@@ -615,8 +615,8 @@ int launch(const char *tag, int np, bool vec, const std::vector<Job> &jobs, int 
 
 
 // ---------------------------------------------------------------------------
-// Anchor EMA fused with the first pass (see sc_pass.h).  A workgroup owns 256
-// rows; per 64-deep step each thread takes sixteen 4-element pieces of M
+// Anchor EMA fused with the first pass (see sc_pass.h).  A workgroup of 512
+// threads owns 256 rows; per 64-deep step each thread takes eight 4-element pieces of M
 // (16-byte loads, 16 lanes per row) and of G, forms the EMA, stores M
 // (non-temporal) and the bf16 shadow, and drops the bf16 piece into the
 // swizzled LDS layout of the streaming pass, where the step is multiplied on
@@ -639,8 +639,10 @@ struct EmaBatch {
     EmaJob j[kMaxJobs];
 };
 
+// Eight waves per workgroup, two per SIMD (four waves left the stream with
+// too few loads in flight); each wave multiplies 32 rows.
 template <int NT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void ema_pass_kernel(const EmaBatch jb, int np,
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void ema_pass_kernel(const EmaBatch jb, int np,
                                                                                                  float beta, float omb)
 {
     const EmaJob &J = jb.j[blockIdx.z];
@@ -651,7 +653,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     constexpr int A_BYTES = 256 * 128;
     constexpr int STAGE = A_BYTES + NP * 128;
     constexpr int BCH = NP * 8;                 // 16-byte chunks of one thin-factor step
-    constexpr int BPT = (BCH + 255) / 256;
+    constexpr int W = 8;                        // waves
+    constexpr int NTH = 64 * W;                 // threads
+    constexpr int PU = 4096 / NTH;              // 4-element pieces of M per thread and step
+    constexpr int RT = 8 / W;                   // 32-row tiles per wave
+    constexpr int BPT = (BCH + NTH - 1) / NTH;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE];
 
     float *__restrict__ M = J.M;
@@ -665,26 +671,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int row0 = blockIdx.x * kBM;
     const int nsteps = static_cast<int>(cdiv(n, kBK));
 
-    f32x16 acc[2][NC];
+    f32x16 acc[RT][NC];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < RT; ++a)
 #pragma unroll
         for (int t = 0; t < NC; ++t)
 #pragma unroll
             for (int e = 0; e < 16; ++e)
                 acc[a][t][e] = 0.f;
 
-    // piece u of this thread: row (tid + 256 u) / 16 of the block, 4 elements
-    // at column 4 ((tid + 256 u) % 16) of the step, so that 16 lanes cover a
+    // piece u of this thread: row (tid + 512 u) / 16 of the block, 4 elements
+    // at column 4 ((tid + 512 u) % 16) of the step, so that 16 lanes cover a
     // row's 256 bytes of M (128 of G) with one instruction
-    float4 rm[16];
-    uint2 rg[16];
+    float4 rm[PU];
+    uint2 rg[PU];
     uint4 rb[BPT];
     auto load = [&](int s) {
         const int k0 = s * kBK;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int q = tid + 256 * u;
+        for (int u = 0; u < PU; ++u) {
+            const int q = tid + NTH * u;
             const int gi = row0 + (q >> 4), gk = k0 + (q & 15) * 4;
             float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
             uint2 g = make_uint2(0u, 0u);
@@ -699,7 +705,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
 #pragma unroll
         for (int j = 0; j < BPT; ++j) {
-            const int q = min(tid + 256 * j, BCH - 1);
+            const int q = min(tid + NTH * j, BCH - 1);
             const int c = min(q >> 3, np - 1);
             const int gk = k0 + (q & 7) * 8;
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
@@ -712,8 +718,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const int k0 = s * kBK;
         unsigned char *base = smem + buf * STAGE;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int q = tid + 256 * u;
+        for (int u = 0; u < PU; ++u) {
+            const int q = tid + NTH * u;
             const int row = q >> 4, f = q & 15;
             const int gi = row0 + row, gk = k0 + f * 4;
             float v[4] = {rm[u].x, rm[u].y, rm[u].z, rm[u].w};
@@ -735,7 +741,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
 #pragma unroll
         for (int j = 0; j < BPT; ++j) {
-            const int q = tid + 256 * j;
+            const int q = tid + NTH * j;
             if (q < BCH) {
                 const int line = q >> 3, c = q & 7;
                 uint4 v = rb[j];
@@ -747,14 +753,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     };
     // v_mfma_f32_32x32x16_bf16 on the step in LDS (the layout of pass_dma_kernel<false>)
     auto compute = [&](int buf) {
-        const unsigned char *aw = smem + buf * STAGE + wave * 8192;
+        const unsigned char *aw = smem + buf * STAGE + wave * (RT * 4096);
         const unsigned char *bw = smem + buf * STAGE + A_BYTES;
 #pragma unroll
         for (int kq = 0; kq < 4; ++kq) {
             const int c = kq * 2 + (lane >> 5);
-            bf16x8 af[2], bf[NC];
+            bf16x8 af[RT], bf[NC];
 #pragma unroll
-            for (int a = 0; a < 2; ++a) {
+            for (int a = 0; a < RT; ++a) {
                 const int line = a * 32 + (lane & 31);
                 af[a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
             }
@@ -766,7 +772,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
             for (int t = 0; t < NC; ++t)
 #pragma unroll
-                for (int a = 0; a < 2; ++a)
+                for (int a = 0; a < RT; ++a)
                     acc[a][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[t], acc[a][t], 0, 0, 0);
         }
     };
@@ -784,9 +790,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 
     // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
-    const int wrow0 = row0 + wave * 64;
+    const int wrow0 = row0 + wave * (RT * 32);
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < RT; ++a)
 #pragma unroll
         for (int t = 0; t < NC; ++t) {
             const int col = t * 32 + (lane & 31);
@@ -807,7 +813,7 @@ void ema_launch(const char *tag, const std::vector<EmaJob> &jobs, int gx, int np
         b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
         for (int i = 0; i < b.count; ++i)
             b.j[i] = jobs[c0 + i];
-        ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(gx, 1, b.count), dim3(256), 0, st, b, np, beta, 1.0f - beta);
+        ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(gx, 1, b.count), dim3(512), 0, st, b, np, beta, 1.0f - beta);
     }
 }
 
