@@ -15,4 +15,8 @@ Pins (tests run without a GPU) and their status:
                projector idempotence and self-adjointness at tau = 0,
                Lemma 1 (non-expansive) and Lemma 2 (noise contraction, Monte
                Carlo), EMA closed forms, SVD against eigh brute force.
+  adamw.*      pinned: torch.optim.AdamW and torch.nn.utils.clip_grad_norm_ in
+               float64 (independent library routines), the closed form of the
+               first step from zero moments, clipping invariants, the norm
+               identity the library clips with, planted-mistake checks.
 """
