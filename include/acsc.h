@@ -198,6 +198,58 @@ int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dtype dt, floa
 int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,
                        hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Corrected AdamW step (Alg. 1: the fast weights are updated by AdamW on
+ * G_proj; App. I: AdamW, betas (0.9, 0.999), gradient norm clipped at 0.2).
+ * The correction and the update run as one step: G_proj is never written to
+ * device memory.
+ * ---------------------------------------------------------------------- */
+
+/* Optimiser state of one weight matrix: device fp32 arrays of the matrix's
+ * [m, n] shape (row-major), read and written in place; the first and second
+ * moments start at zero.  16-byte aligned arrays (with n % 8 == 0) take the
+ * vectorised path; 4-byte alignment is required. */
+typedef struct sc_adamw_state {
+    float *W;     /* weights                    */
+    float *m1;    /* first moment (Adam's m_t)  */
+    float *m2;    /* second moment (Adam's v_t) */
+} sc_adamw_state;
+
+/* Hyperparameters of one step (shared by every matrix of a call). */
+typedef struct sc_adamw_hparams {
+    float lr;             /* this step's learning rate (any schedule is the caller's) */
+    float beta1, beta2;   /* moment decay rates, each in [0, 1)                        */
+    float eps;            /* > 0, added to the bias-corrected sqrt(m2)                 */
+    float weight_decay;   /* >= 0, decoupled: W <- W (1 - lr * weight_decay)           */
+    int64_t step;         /* t >= 1: bias corrections 1 - beta^t                       */
+    float max_norm;       /* > 0: global-norm clipping at max_norm; <= 0: none          */
+} sc_adamw_hparams;
+
+/* Bytes of workspace sc_correct_adamw_batched needs per matrix (it is also
+ * covered by sc_workspace_size for the same shape, so one workspace serves the
+ * build, the correction and this step). */
+int sc_adamw_workspace_size(int m, int n, int r, acsc_dtype dt, size_t *bytes);
+
+/* For every matrix i of the call (mats[i] as for sc_correct_batched, except
+ * that G_proj is unused and may be NULL; states[i] its optimiser state):
+ *   G_proj_i = alpha G_i + (1 - alpha) U_i diag(d) (U_i^T G_i V_i) diag(d) V_i^T
+ *   N        = sqrt(sum_i ||G_proj_i||_F^2)            (the call's global norm)
+ *   c        = min(1, max_norm / (N + 1e-6))  if max_norm > 0, else 1
+ *   g        = c G_proj_i
+ *   W  <- W (1 - lr wd);  m1 <- beta1 m1 + (1 - beta1) g;  m2 <- beta2 m2 + (1 - beta2) g^2
+ *   W  <- W - lr (m1 / (1 - beta1^t)) / (sqrt(m2 / (1 - beta2^t)) + eps)
+ * The decoupled weight decay is that of AdamW (Loshchilov & Hutter 2019);
+ * the clipping that of the common global-norm form.  N is formed as
+ * alpha^2 ||G||^2 + 2 alpha (1 - alpha) <X, X_f> + (1 - alpha)^2 ||X_f||^2,
+ * which holds for the orthonormal U, V of sc_build_prior.
+ * norm_out  device fp32 scalar or NULL: receives N (before clipping).
+ * The state arrays of different matrices must not overlap; G is only read.
+ * Arithmetic is fp32 (as sc_correct for the blend).  All arguments of all
+ * matrices are checked before anything is enqueued; errors as elsewhere. */
+int sc_correct_adamw_batched(int count, const sc_matrix *mats, const sc_adamw_state *states,
+                             acsc_dtype dt, int r, float alpha, const sc_adamw_hparams *hp,
+                             float *norm_out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -45,6 +45,17 @@ class ScMatrix(C.Structure):
                 ("ws_bytes", C.c_size_t)]
 
 
+class AdamwState(C.Structure):
+    """sc_adamw_state: one matrix's fp32 weights and Adam moments (in place)."""
+    _fields_ = [("W", C.c_void_p), ("m1", C.c_void_p), ("m2", C.c_void_p)]
+
+
+class AdamwHparams(C.Structure):
+    """sc_adamw_hparams: one step's AdamW hyperparameters."""
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float), ("step", C.c_int64), ("max_norm", C.c_float)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -72,6 +83,11 @@ def _load():
     lib.sc_build_prior_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, f32, i32, i32, i32, f32, u64, vp]
     lib.sc_correct_batched.restype = i32
     lib.sc_correct_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, i32, f32, vp]
+    lib.sc_adamw_workspace_size.restype = i32
+    lib.sc_adamw_workspace_size.argtypes = [i32, i32, i32, i32, C.POINTER(sz)]
+    lib.sc_correct_adamw_batched.restype = i32
+    lib.sc_correct_adamw_batched.argtypes = [i32, C.POINTER(ScMatrix), C.POINTER(AdamwState), i32, i32, f32,
+                                             C.POINTER(AdamwHparams), vp, vp]
     lib.acsc_stats_enable.restype = i32
     lib.acsc_stats_enable.argtypes = [i32]
     lib.acsc_stats_read.restype = i32
@@ -83,7 +99,8 @@ lib = _load()
 
 EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
-            "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched")
+            "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched",
+            "sc_adamw_workspace_size", "sc_correct_adamw_batched")
 
 
 def _check(rc: int):
@@ -282,3 +299,39 @@ def sc_correct_batched(items, r: int, alpha: float, dtype: torch.dtype = torch.b
                           ws.numel())
     code = BF16 if dtype == torch.bfloat16 else F32
     _check(lib.sc_correct_batched(len(items), arr, code, r, float(alpha), _stream(stream)))
+
+
+def sc_adamw_workspace_size(m: int, n: int, r: int, dtype: torch.dtype) -> int:
+    b = C.c_size_t(0)
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(lib.sc_adamw_workspace_size(m, n, r, code, C.byref(b)))
+    return b.value
+
+
+def sc_correct_adamw_batched(items, r: int, alpha: float, lr: float, beta1: float = 0.9,
+                             beta2: float = 0.999, eps: float = 1e-8, weight_decay: float = 0.0,
+                             step: int = 1, max_norm: float = 0.0, dtype: torch.dtype = torch.bfloat16,
+                             norm_out: Optional[torch.Tensor] = None, stream=None):
+    """items: list of dicts with G, prior=(U, d, V), ws and state=(W, m1, m2)
+    (fp32, updated in place).  norm_out: optional fp32 device scalar that
+    receives the global norm of the G_proj before clipping."""
+    arr = (ScMatrix * max(len(items), 1))()
+    st = (AdamwState * max(len(items), 1))()
+    keep = []
+    for i, it in enumerate(items):
+        G, (U, d, V), ws, (W, m1, m2) = _in(it["G"]), it["prior"], it["ws"], it["state"]
+        U, d, V = _in(U), _in(d), _in(V)
+        _need_cuda(G, U, d, V, ws, W, m1, m2, norm_out)
+        _out(W, m1, m2)
+        for t in (W, m1, m2):
+            if t.dtype != torch.float32 or tuple(t.shape) != tuple(G.shape):
+                raise AcscError(ACSC_EINVAL, "W, m1, m2 must be fp32 tensors of G's shape")
+        keep += [G, U, d, V]
+        m, n = G.shape
+        arr[i] = ScMatrix(_p(G), None, m, n, _p(U), _p(d), _p(V), _p(d), None, None, _p(ws), ws.numel())
+        st[i] = AdamwState(_p(W), _p(m1), _p(m2))
+    hp = AdamwHparams(float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
+                      float(max_norm))
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(lib.sc_correct_adamw_batched(len(items), arr, st, code, r, float(alpha), C.byref(hp),
+                                        _ptr(norm_out), _stream(stream)))

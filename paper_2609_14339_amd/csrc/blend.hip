@@ -23,6 +23,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((address_space(3))) unsigned char lds_byte;
 typedef unsigned int nu4 __attribute__((ext_vector_type(4)));
+typedef float nf4 __attribute__((ext_vector_type(4)));
 
 constexpr int kT = 128;          // tile edge
 constexpr int kStPitch = 132;    // floats per staged product row (conflict-free column writes)
@@ -36,6 +37,7 @@ struct Job {
     uint16_t *out;
     int m, n;
     const uint16_t *P, *V;
+    float *W, *m1, *m2;
     int vec;
 };
 struct Batch {
@@ -56,8 +58,10 @@ __device__ __forceinline__ void sync_lds()
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int RP, bool VEC>
-__global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
+// ADAM: the blended values are not stored; they are the gradient of the
+// AdamW step applied to the tile's weights and moments (fp32, in place).
+template <int RP, bool VEC, bool ADAM>
+__global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha, const AdamArgs ad)
 {
     constexpr int RB = RP * 2;                  // bytes per P / V row
     constexpr int SLICE = kT * RB;              // bytes of one 128-row slice
@@ -182,6 +186,63 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
             }
     sync_lds();
     const float oma = 1.0f - alpha;
+    if constexpr (ADAM) {
+        const float cf = *ad.coef;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int q = tid + 256 * u;
+            const int rr = q >> 4, c8 = (q & 15) * 8;
+            const int gi = row0 + rr, gj = col0 + c8;
+            if (gi >= m)
+                continue;
+            const float4 p0 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8]);
+            const float4 p1 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8 + 4]);
+            const float pf[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+            const uint32_t w[4] = {g[u].x, g[u].y, g[u].z, g[u].w};
+            float gp[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                gp[2 * e] = cf * (alpha * __uint_as_float(w[e] << 16) + oma * pf[2 * e]);
+                gp[2 * e + 1] = cf * (alpha * __uint_as_float(w[e] & 0xFFFF0000u) + oma * pf[2 * e + 1]);
+            }
+            const int64_t o = static_cast<int64_t>(gi) * n + gj;
+            if (VEC && gj + 8 <= n) {
+                // the state streams through once: non-temporal both ways
+                nf4 wv[2], mv[2], vv[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    wv[h] = __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(J.W + o) + h);
+                    mv[h] = __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(J.m1 + o) + h);
+                    vv[h] = __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(J.m2 + o) + h);
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        float we = wv[h][e], me = mv[h][e], ve = vv[h][e];
+                        adamw_elem(gp[4 * h + e], we, me, ve, ad);
+                        wv[h][e] = we;
+                        mv[h][e] = me;
+                        vv[h][e] = ve;
+                    }
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    __builtin_nontemporal_store(wv[h], reinterpret_cast<nf4 *>(J.W + o) + h);
+                    __builtin_nontemporal_store(mv[h], reinterpret_cast<nf4 *>(J.m1 + o) + h);
+                    __builtin_nontemporal_store(vv[h], reinterpret_cast<nf4 *>(J.m2 + o) + h);
+                }
+            } else {
+                for (int e = 0; e < 8 && gj + e < n; ++e) {
+                    float wv = J.W[o + e], mv = J.m1[o + e], vv = J.m2[o + e];
+                    adamw_elem(gp[e], wv, mv, vv, ad);
+                    J.W[o + e] = wv;
+                    J.m1[o + e] = mv;
+                    J.m2[o + e] = vv;
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
         const int q = tid + 256 * u;
@@ -211,8 +272,9 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha)
     }
 }
 
-template <int RP>
-void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float alpha, hipStream_t st)
+template <int RP, bool ADAM>
+void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float alpha, const AdamArgs &ad,
+               hipStream_t st)
 {
     std::vector<Job> part[2];
     for (const Job &j : jobs)
@@ -224,11 +286,11 @@ void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float a
             for (int i = 0; i < b.count; ++i)
                 b.j[i] = part[v][c0 + i];
             if (v) {
-                auto kern = blend_kernel<RP, true>;
-                ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha);
+                auto kern = blend_kernel<RP, true, ADAM>;
+                ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha, ad);
             } else {
-                auto kern = blend_kernel<RP, false>;
-                ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha);
+                auto kern = blend_kernel<RP, false, ADAM>;
+                ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha, ad);
             }
         }
 }
@@ -237,23 +299,26 @@ void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float a
 
 bool supported(int RP) { return RP == 64 || RP == 128 || RP == 192; }
 
-int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st)
+int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st, const AdamArgs *adam)
 {
     if (!supported(RP))
         return set_error(ACSC_EINVAL, "blend: padded rank %d not handled by the streamed-tile kernel", RP);
     std::vector<Job> jobs;
     int tiles = 1;
+    auto a16 = [](const void *p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
     for (const Req &q : reqs) {
-        const bool vec = q.n % 8 == 0 && q.n >= 8 && reinterpret_cast<uintptr_t>(q.G) % 16 == 0 &&
-                         reinterpret_cast<uintptr_t>(q.out) % 16 == 0;
-        jobs.push_back(Job{q.G, q.out, q.m, q.n, q.P, q.V, vec ? 1 : 0});
+        bool vec = q.n % 8 == 0 && q.n >= 8 && a16(q.G);
+        vec = vec && (adam ? a16(q.W) && a16(q.m1) && a16(q.m2) : a16(q.out));
+        jobs.push_back(Job{q.G, q.out, q.m, q.n, q.P, q.V, q.W, q.m1, q.m2, vec ? 1 : 0});
         const int64_t rbn = cdiv(q.m, kT), cbn = cdiv(q.n, kT);
         tiles = std::max<int>(tiles, static_cast<int>(cdiv(rbn, 8) * 8 * cbn));
     }
+    const AdamArgs none{};
+    const AdamArgs &ad = adam ? *adam : none;
     switch (RP) {
-    case 64: launch_rp<64>(tag, jobs, tiles, alpha, st); break;
-    case 128: launch_rp<128>(tag, jobs, tiles, alpha, st); break;
-    default: launch_rp<192>(tag, jobs, tiles, alpha, st); break;
+    case 64: adam ? launch_rp<64, true>(tag, jobs, tiles, alpha, ad, st) : launch_rp<64, false>(tag, jobs, tiles, alpha, ad, st); break;
+    case 128: adam ? launch_rp<128, true>(tag, jobs, tiles, alpha, ad, st) : launch_rp<128, false>(tag, jobs, tiles, alpha, ad, st); break;
+    default: adam ? launch_rp<192, true>(tag, jobs, tiles, alpha, ad, st) : launch_rp<192, false>(tag, jobs, tiles, alpha, ad, st); break;
     }
     return ACSC_OK;
 }

@@ -950,6 +950,118 @@ __global__ __launch_bounds__(256) void filter_x_kernel(const Batch<FilterJob> jb
     Xf[idx] = (i < r && j < r) ? d[i] * X[static_cast<int64_t>(i) * ldx + j] * d[j] : 0.f;
 }
 
+// ---------------------------------------------------------------------------
+// Global-norm clipping of the corrected AdamW step without a pass over
+// G_proj: with U and V orthonormal, X = U^T G V and X_f = d X d,
+//   ||alpha G + (1 - alpha) U X_f V^T||^2
+//     = alpha^2 ||G||^2 + 2 alpha (1 - alpha) <X, X_f> + (1 - alpha)^2 ||X_f||^2.
+// ||G||^2 is summed by sumsq_kernel (kSumBlocks fp64 partials per matrix, a
+// grid and order that never depend on the device), the rest by
+// clip_norm_kernel in one workgroup, matrix by matrix in call order.
+// ---------------------------------------------------------------------------
+constexpr int kSumBlocks = 512;
+
+struct SumJob {
+    const void *G;
+    int64_t count;    // elements of G (contiguous)
+    int vec;          // 16-byte aligned G and count % 8 == 0: 16-byte loads
+    double *part;     // [kSumBlocks]
+};
+
+__device__ __forceinline__ double block_sum(double v, double *red)
+{
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (static_cast<int>(threadIdx.x) < w)
+            red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const double t = red[0];
+    __syncthreads();
+    return t;
+}
+
+template <typename GT>
+__global__ __launch_bounds__(256) void sumsq_kernel(const Batch<SumJob> jb)
+{
+    __shared__ double red[256];
+    const SumJob &J = jb.j[blockIdx.z];
+    const GT *G = static_cast<const GT *>(J.G);
+    double acc = 0.0;
+    constexpr int V = 16 / sizeof(GT);
+    const int64_t stride = static_cast<int64_t>(kSumBlocks) * 256;
+    const int64_t start = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (J.vec) {
+        // squares of bf16 are exact in fp32; the V of one chunk are added in fp32
+        for (int64_t c = start; c < J.count / V; c += stride) {
+            const uint4 raw = reinterpret_cast<const uint4 *>(G)[c];
+            const GT *e = reinterpret_cast<const GT *>(&raw);
+            float s = 0.f;
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const float g = to_f32<GT>(e[i]);
+                s += g * g;
+            }
+            acc += s;
+        }
+    } else {
+        for (int64_t i = start; i < J.count; i += stride) {
+            const double g = to_f32<GT>(G[i]);
+            acc += g * g;
+        }
+    }
+    const double t = block_sum(acc, red);
+    if (threadIdx.x == 0)
+        J.part[blockIdx.x] = t;
+}
+
+struct NormJob {
+    const double *part;   // ||G||^2 partials [kSumBlocks]
+    const float *X;       // [r, RP]
+    const float *Xf;      // [RP, RP] (rows >= r are zero)
+    int r, RP;
+};
+
+// One workgroup.  acc (fp64) carries the squared norm over the launches of
+// one call (first: start at zero; last: write the clip coefficient and the
+// norm).
+__global__ __launch_bounds__(256) void clip_norm_kernel(const Batch<NormJob> jb, float alpha, float max_norm,
+                                                        double *acc, float *coef, float *norm_out, int first,
+                                                        int last)
+{
+    __shared__ double red[256];
+    double total = first ? 0.0 : *acc;
+    const double a = alpha, b = 1.0 - static_cast<double>(alpha);
+    for (int i = 0; i < jb.count; ++i) {
+        const NormJob &J = jb.j[i];
+        double gg = 0.0, xx = 0.0, ff = 0.0;
+        for (int p = threadIdx.x; p < kSumBlocks; p += 256)
+            gg += J.part[p];
+        for (int q = threadIdx.x; q < J.r * J.RP; q += 256) {
+            const double x = J.X[q], f = J.Xf[q];
+            xx += x * f;
+            ff += f * f;
+        }
+        total += block_sum(a * a * gg + 2.0 * a * b * xx + b * b * ff, red);
+    }
+    if (threadIdx.x == 0) {
+        *acc = total;
+        if (last) {
+            const double N = sqrt(total > 0.0 ? total : 0.0);
+            float c = 1.0f;
+            if (max_norm > 0.f) {
+                const double q = static_cast<double>(max_norm) / (N + 1e-6);
+                if (q < 1.0)
+                    c = static_cast<float>(q);
+            }
+            *coef = c;
+            if (norm_out)
+                *norm_out = static_cast<float>(N);
+        }
+    }
+}
+
 // Vc[i][c] = V[i][c] for c < r, zero up to RP, converted to the compute type.
 template <typename CT>
 struct PadJob {
@@ -984,14 +1096,32 @@ struct BlendJob {
     GT *out;
     int m, n;
     const GT *P, *Vc;
+    float *W, *m1, *m2;   // corrected AdamW: fp32 weights and moments, in place
 };
 
-template <typename GT>
-__global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb, int RP, float alpha)
+// Element (row, col) of G_proj = gp: stored, or (ADAM) the gradient of the
+// AdamW step of the same element of W (scaled by the call's clip coefficient).
+template <bool ADAM, typename GT>
+__device__ __forceinline__ void blend_out(const BlendJob<GT> &J, int64_t o, float gp, float cf,
+                                          const blend::AdamArgs &ad)
+{
+    if constexpr (ADAM) {
+        float w = J.W[o], m1 = J.m1[o], m2 = J.m2[o];
+        blend::adamw_elem(cf * gp, w, m1, m2, ad);
+        J.W[o] = w;
+        J.m1[o] = m1;
+        J.m2[o] = m2;
+    } else {
+        J.out[o] = from_f32<GT>(gp);
+    }
+}
+
+template <typename GT, bool ADAM>
+__global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb, int RP, float alpha,
+                                                    const blend::AdamArgs ad)
 {
     const BlendJob<GT> &J = jb.j[blockIdx.z];
     const GT *G = J.G;
-    GT *out = J.out;
     const int m = J.m, n = J.n;
     const GT *P = J.P, *Vc = J.Vc;
     if (static_cast<int>(blockIdx.x) * 64 >= n || static_cast<int>(blockIdx.y) * 64 >= m)
@@ -1049,6 +1179,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb
         }
     }
     const float oma = 1.0f - alpha;
+    const float cf = ADAM ? *ad.coef : 1.0f;
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -1060,7 +1191,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb
                 if (row < m && col < n) {
                     const int64_t o = static_cast<int64_t>(row) * n + col;
                     const float g = to_f32<GT>(G[o]);
-                    out[o] = from_f32<GT>(alpha * g + oma * acc[a][b][e]);
+                    blend_out<ADAM>(J, o, alpha * g + oma * acc[a][b][e], cf, ad);
                 }
             }
         }
@@ -1081,9 +1212,9 @@ constexpr int kBT = 128;              // tile edge
 constexpr int kGPitch = kBT + 8;      // bf16 elements per staged G row (272 bytes)
 constexpr int kKPitch = 32 + 8;       // P / V slice rows (80 bytes)
 
-template <bool VEC>
+template <bool VEC, bool ADAM>
 __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint16_t>> jb, int RP, float alpha,
-                                                      int col_blocks_max)
+                                                      int col_blocks_max, const blend::AdamArgs ad)
 {
     const BlendJob<uint16_t> &J = jb.j[blockIdx.z];
     const int m = J.m, n = J.n;
@@ -1188,6 +1319,25 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
     __syncthreads();
     // blend in place in the staged tile
     const float oma = 1.0f - alpha;
+    if constexpr (ADAM) {
+        // the blended values are the AdamW gradient, never stored
+        const float cf = *ad.coef;
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int cc = wc * 64 + c * 16 + (lane & 15);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int rr = wr * 64 + a * 16 + (lane >> 4) * 4 + e;
+                    const int gi = row0 + rr, gj = col0 + cc;
+                    if (gi < m && gj < n)
+                        blend_out<true>(J, static_cast<int64_t>(gi) * n + gj,
+                                        alpha * bf16_to_f32(Gs[rr * kGPitch + cc]) + oma * acc[a][c][e], cf, ad);
+                }
+            }
+        return;
+    }
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -1312,6 +1462,8 @@ struct CorrWs {
     void *Pc, *Vc;
     uint16_t *Vt16;
     int64_t ldv16;
+    double *sq, *acc;
+    float *coef;
 };
 
 size_t carve_correct(const Dims &d, size_t esize, void *base, CorrWs *w)
@@ -1329,6 +1481,10 @@ size_t carve_correct(const Dims &d, size_t esize, void *base, CorrWs *w)
     t.Xf = c.take<float>(static_cast<size_t>(d.RP) * d.RP);
     t.Pc = c.take<unsigned char>(static_cast<size_t>(d.m) * d.RP * esize);
     t.Vc = c.take<unsigned char>(static_cast<size_t>(d.n) * d.RP * esize);
+    // corrected AdamW: ||G||^2 partials, the norm accumulator, the clip coefficient
+    t.sq = c.take<double>(kSumBlocks);
+    t.acc = c.take<double>(1);
+    t.coef = c.take<float>(1);
     if (w)
         *w = t;
     return c.off;
@@ -1449,6 +1605,15 @@ struct Mat {
     PriorWs pw;
     CorrWs cw;
     uint64_t seed;
+    const sc_adamw_state *ad = nullptr;   // corrected AdamW: this matrix's optimiser state
+};
+
+// Corrected AdamW: the epilogue constants and the call's norm accumulator.
+struct AdamCtx {
+    blend::AdamArgs args;   // args.coef: the clip coefficient (workspace of the call's first matrix)
+    double *acc;            // squared-norm accumulator (same workspace)
+    float max_norm;
+    float *norm_out;        // device or NULL
 };
 
 // Gram matrices (fp64) of the first KP columns of one block per matrix.
@@ -1686,9 +1851,35 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     return ACSC_OK;
 }
 
-// X = U^T G V, X_f = d X d, P = U X_f, then G_proj = alpha G + (1 - alpha) P V^T.
+// Squared global norm of the call's G_proj and the clip coefficient (see
+// clip_norm_kernel), from ||G||^2 and the filtered projections X, X_f.
 template <typename GT>
-int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
+void clip_norm(const std::vector<Mat> &ms, int r, float alpha, const AdamCtx &ad, hipStream_t st)
+{
+    std::vector<SumJob> sj;
+    for (const Mat &m : ms) {
+        const int64_t cnt = static_cast<int64_t>(m.D.m) * m.D.n;
+        const bool vec = aligned(m.in->G, 16) && cnt % (16 / sizeof(GT)) == 0;
+        sj.push_back(SumJob{m.in->G, cnt, vec ? 1 : 0, m.cw.sq});
+    }
+    launch_jobs("sc_sumsq", sumsq_kernel<GT>, sj, dim3(kSumBlocks), dim3(256), 0, st);
+    for (size_t c0 = 0; c0 < ms.size(); c0 += kMaxBatch) {
+        Batch<NormJob> b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxBatch, ms.size() - c0));
+        for (int i = 0; i < b.count; ++i) {
+            const Mat &m = ms[c0 + i];
+            b.j[i] = NormJob{m.cw.sq, m.cw.X, m.cw.Xf, r, m.D.RP};
+        }
+        const int first = c0 == 0, last = c0 + b.count == ms.size();
+        ACSC_LAUNCH("sc_clip_norm", clip_norm_kernel, dim3(1), dim3(256), 0, st, b, alpha, ad.max_norm, ad.acc,
+                    const_cast<float *>(ad.args.coef), ad.norm_out, first, last);
+    }
+}
+
+// X = U^T G V, X_f = d X d, P = U X_f, then G_proj = alpha G + (1 - alpha) P V^T,
+// stored, or (adam) taken as the gradient of the AdamW step of each matrix.
+template <typename GT>
+int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st, const AdamCtx *adam = nullptr)
 {
     const int RP = ms[0].D.RP;
     const bool b16 = sizeof(GT) == 2;
@@ -1771,12 +1962,18 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
         if (!b16)   // the bf16 copy was made with the transposed one
             launch_jobs("sc_vconvert", pad_convert_kernel<GT>, pj, dim3(grid1d(tot)), dim3(256), 0, st, r, RP);
     }
+    if (adam)
+        clip_norm<GT>(ms, r, alpha, *adam, st);
+    const blend::AdamArgs ad = adam ? adam->args : blend::AdamArgs{};
+    const char *btag = adam ? "sc_blend_adamw" : "sc_blend";
     {
         std::vector<BlendJob<GT>> bj;
         int gx = 1, gy = 1;
         for (auto &m : ms) {
             bj.push_back(BlendJob<GT>{static_cast<const GT *>(m.in->G), static_cast<GT *>(m.in->G_proj), m.D.m, m.D.n,
-                                      static_cast<const GT *>(m.cw.Pc), static_cast<const GT *>(m.cw.Vc)});
+                                      static_cast<const GT *>(m.cw.Pc), static_cast<const GT *>(m.cw.Vc),
+                                      m.ad ? m.ad->W : nullptr, m.ad ? m.ad->m1 : nullptr,
+                                      m.ad ? m.ad->m2 : nullptr});
             gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, 64)));
             gy = std::max<int>(gy, static_cast<int>(cdiv(m.D.m, 64)));
         }
@@ -1786,8 +1983,9 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
                 for (auto &m : ms)
                     q.push_back(blend::Req{static_cast<const uint16_t *>(m.in->G), static_cast<uint16_t *>(m.in->G_proj),
                                            m.D.m, m.D.n, static_cast<const uint16_t *>(m.cw.Pc),
-                                           static_cast<const uint16_t *>(m.cw.Vc)});
-                return blend::run("sc_blend", q, RP, alpha, st);
+                                           static_cast<const uint16_t *>(m.cw.Vc), m.ad ? m.ad->W : nullptr,
+                                           m.ad ? m.ad->m1 : nullptr, m.ad ? m.ad->m2 : nullptr});
+                return blend::run(btag, q, RP, alpha, st, adam ? &ad : nullptr);
             }
             // 128 x 128 tiles, XCD-aware order (see blend16_kernel)
             int tiles = 1, cbm = 1;
@@ -1796,22 +1994,33 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st)
                 const int rbn = static_cast<int>(cdiv(m.D.m, kBT)), cbn = static_cast<int>(cdiv(m.D.n, kBT));
                 tiles = std::max(tiles, static_cast<int>(round_up(rbn, 8)) * cbn);
                 cbm = std::max(cbm, cbn);
-                vec = vec && (m.D.n % 8) == 0 && aligned(m.in->G, 16) && aligned(m.in->G_proj, 16);
+                vec = vec && (m.D.n % 8) == 0 && aligned(m.in->G, 16) && (adam || aligned(m.in->G_proj, 16));
             }
-            if (vec)
-                launch_jobs("sc_blend", blend16_kernel<true>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm);
-            else
-                launch_jobs("sc_blend", blend16_kernel<false>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm);
+            if (adam) {
+                if (vec)
+                    launch_jobs(btag, blend16_kernel<true, true>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm, ad);
+                else
+                    launch_jobs(btag, blend16_kernel<false, true>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm, ad);
+            } else {
+                if (vec)
+                    launch_jobs(btag, blend16_kernel<true, false>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm, ad);
+                else
+                    launch_jobs(btag, blend16_kernel<false, false>, bj, dim3(tiles), dim3(256), 0, st, RP, alpha, cbm, ad);
+            }
         } else {
             const size_t pitch = RP + 1;
             const size_t blds = 2 * 64 * pitch * sizeof(GT);
-            launch_jobs("sc_blend", blend_kernel<GT>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha);
+            if (adam)
+                launch_jobs(btag, blend_kernel<GT, true>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha, ad);
+            else
+                launch_jobs(btag, blend_kernel<GT, false>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha, ad);
         }
     }
     return ACSC_OK;
 }
 
-int check_matrix(const sc_matrix &a, int r, int oversample, acsc_dtype dt, bool build, size_t *need)
+int check_matrix(const sc_matrix &a, int r, int oversample, acsc_dtype dt, bool build, size_t *need,
+                 bool need_gproj = true)
 {
     ACSC_CHECK_ARG(a.m >= 1 && a.n >= 1, ACSC_EINVAL, "m=%d, n=%d must be >= 1", a.m, a.n);
     ACSC_CHECK_ARG(r >= 1 && r <= std::min(std::min(a.m, a.n), kKMax), ACSC_EINVAL,
@@ -1829,8 +2038,9 @@ int check_matrix(const sc_matrix &a, int r, int oversample, acsc_dtype dt, bool 
         ACSC_CHECK_ARG(aligned(a.M, 16), ACSC_EALIGN, "M must be 16-byte aligned");
         ACSC_CHECK_ARG(!a.G || aligned(a.G, 16), ACSC_EALIGN, "G_anc must be 16-byte aligned");
     } else {
-        ACSC_CHECK_ARG(a.G && a.G_proj, ACSC_EINVAL, "G or G_proj is NULL");
-        ACSC_CHECK_ARG(aligned(a.G, es) && aligned(a.G_proj, es), ACSC_EALIGN, "G, G_proj must be element-aligned");
+        ACSC_CHECK_ARG(a.G && (a.G_proj || !need_gproj), ACSC_EINVAL, "G or G_proj is NULL");
+        ACSC_CHECK_ARG(aligned(a.G, es) && (!need_gproj || aligned(a.G_proj, es)), ACSC_EALIGN,
+                       "G, G_proj must be element-aligned");
     }
     return ACSC_OK;
 }
@@ -1935,7 +2145,7 @@ extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype d
         return ACSC_OK;
     const size_t es = dtype_size(dt);
     const size_t blds = 2 * 64 * (all[0].D.RP + (dt == ACSC_BF16 ? 8 : 1)) * es;
-    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t>, blds) : allow_lds(blend_kernel<float>, blds);
+    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t, false>, blds) : allow_lds(blend_kernel<float, false>, blds);
     if (rc)
         return rc;
     if (dt == ACSC_BF16)
@@ -1945,6 +2155,88 @@ extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype d
     if (rc)
         return rc;
     return check_launch("sc_correct");
+}
+
+extern "C" int sc_adamw_workspace_size(int m, int n, int r, acsc_dtype dt, size_t *bytes)
+{
+    clear_error();
+    ACSC_CHECK_ARG(bytes != nullptr, ACSC_EINVAL, "bytes is NULL");
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(m >= 1 && n >= 1, ACSC_EINVAL, "m=%d, n=%d must be >= 1", m, n);
+    ACSC_CHECK_ARG(r >= 1 && r <= std::min(std::min(m, n), kKMax), ACSC_EINVAL,
+                   "r=%d outside [1, min(m, n, %d)]", r, kKMax);
+    *bytes = carve_correct(dims_of(m, n, r, 0), dtype_size(dt), nullptr, nullptr);
+    return ACSC_OK;
+}
+
+extern "C" int sc_correct_adamw_batched(int count, const sc_matrix *mats, const sc_adamw_state *states,
+                                        acsc_dtype dt, int r, float alpha, const sc_adamw_hparams *hp,
+                                        float *norm_out, hipStream_t stream)
+{
+    clear_error();
+    ACSC_CHECK_ARG(count >= 0, ACSC_EINVAL, "count=%d < 0", count);
+    ACSC_CHECK_ARG(count == 0 || (mats != nullptr && states != nullptr), ACSC_EINVAL, "mats or states is NULL");
+    ACSC_CHECK_ARG(hp != nullptr, ACSC_EINVAL, "hp is NULL");
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(std::isfinite(alpha), ACSC_EINVAL, "alpha must be finite");
+    ACSC_CHECK_ARG(std::isfinite(hp->lr) && hp->lr >= 0.f, ACSC_EINVAL, "lr=%g must be finite, >= 0", hp->lr);
+    ACSC_CHECK_ARG(hp->beta1 >= 0.f && hp->beta1 < 1.f && hp->beta2 >= 0.f && hp->beta2 < 1.f, ACSC_EINVAL,
+                   "betas (%g, %g) must lie in [0, 1)", hp->beta1, hp->beta2);
+    ACSC_CHECK_ARG(std::isfinite(hp->eps) && hp->eps > 0.f, ACSC_EINVAL, "eps=%g must be finite, > 0", hp->eps);
+    ACSC_CHECK_ARG(std::isfinite(hp->weight_decay) && hp->weight_decay >= 0.f, ACSC_EINVAL,
+                   "weight_decay=%g must be finite, >= 0", hp->weight_decay);
+    ACSC_CHECK_ARG(hp->step >= 1, ACSC_EINVAL, "step=%lld must be >= 1", (long long)hp->step);
+    ACSC_CHECK_ARG(std::isfinite(hp->max_norm), ACSC_EINVAL, "max_norm must be finite");
+    ACSC_CHECK_ARG(!norm_out || aligned(norm_out, 4), ACSC_EALIGN, "norm_out must be 4-byte aligned");
+    std::vector<Mat> all;
+    for (int i = 0; i < count; ++i) {
+        size_t need = 0;
+        int rc = check_matrix(mats[i], r, 0, dt, false, &need, false);
+        if (rc)
+            return rc;
+        const sc_adamw_state &a = states[i];
+        ACSC_CHECK_ARG(a.W && a.m1 && a.m2, ACSC_EINVAL, "state %d: W, m1 or m2 is NULL", i);
+        ACSC_CHECK_ARG(aligned(a.W, 4) && aligned(a.m1, 4) && aligned(a.m2, 4), ACSC_EALIGN,
+                       "state %d: W, m1, m2 must be 4-byte aligned", i);
+        Mat m;
+        m.in = &mats[i];
+        m.D = dims_of(mats[i].m, mats[i].n, r, 0);
+        carve_correct(m.D, dtype_size(dt), mats[i].ws, &m.cw);
+        m.seed = 0;
+        m.ad = &a;
+        all.push_back(m);
+    }
+    if (all.empty())
+        return ACSC_OK;
+    const size_t es = dtype_size(dt);
+    const size_t blds = 2 * 64 * (all[0].D.RP + (dt == ACSC_BF16 ? 8 : 1)) * es;
+    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t, true>, blds) : allow_lds(blend_kernel<float, true>, blds);
+    if (rc)
+        return rc;
+    // bias corrections and the step size in double on the host, then fp32
+    const double t = static_cast<double>(hp->step);
+    const double bc1 = 1.0 - std::pow(static_cast<double>(hp->beta1), t);
+    const double bc2 = 1.0 - std::pow(static_cast<double>(hp->beta2), t);
+    AdamCtx ctx{};
+    ctx.args.beta1 = hp->beta1;
+    ctx.args.beta2 = hp->beta2;
+    ctx.args.omb1 = static_cast<float>(1.0 - hp->beta1);
+    ctx.args.omb2 = static_cast<float>(1.0 - hp->beta2);
+    ctx.args.wdf = static_cast<float>(1.0 - static_cast<double>(hp->lr) * hp->weight_decay);
+    ctx.args.step = static_cast<float>(hp->lr / bc1);
+    ctx.args.isbc2 = static_cast<float>(1.0 / std::sqrt(bc2));
+    ctx.args.eps = hp->eps;
+    ctx.args.coef = all[0].cw.coef;
+    ctx.acc = all[0].cw.acc;
+    ctx.max_norm = hp->max_norm;
+    ctx.norm_out = norm_out;
+    if (dt == ACSC_BF16)
+        rc = correct_group<uint16_t>(all, r, alpha, stream, &ctx);
+    else
+        rc = correct_group<float>(all, r, alpha, stream, &ctx);
+    if (rc)
+        return rc;
+    return check_launch("sc_correct_adamw");
 }
 
 extern "C" int sc_build_prior(const void *G_anc, acsc_dtype dt, float *M, int m, int n, float beta, int r,

@@ -14,17 +14,42 @@ namespace blend {
 
 struct Req {
     const uint16_t *G;   // [m, n] bf16, row stride n
-    uint16_t *out;       // [m, n] bf16 (may equal G)
+    uint16_t *out;       // [m, n] bf16 (may equal G); unused with an AdamW epilogue
     int m, n;
     const uint16_t *P;   // [m, RP] bf16
     const uint16_t *V;   // [n, RP] bf16
+    float *W, *m1, *m2;  // AdamW epilogue: fp32 [m, n] weights and moments, in place
 };
+
+// Constants of the AdamW epilogue (Alg. 1 update; the optimiser of App. I):
+// with g = coef * G_proj,
+//   m1 <- beta1 m1 + (1 - beta1) g;  m2 <- beta2 m2 + (1 - beta2) g^2;
+//   W  <- W (1 - lr wd) - (lr / bc1) m1 / (sqrt(m2) / sqrt(bc2) + eps),
+// bc = 1 - beta^t; coef (device) is the clipping scale of the whole call.
+struct AdamArgs {
+    float beta1, beta2, omb1, omb2;
+    float wdf;     // 1 - lr wd
+    float step;    // lr / bc1
+    float isbc2;   // 1 / sqrt(bc2)
+    float eps;
+    const float *coef;
+};
+
+// One element of the update; every corrected-AdamW kernel uses this.
+__device__ __forceinline__ void adamw_elem(float g, float &w, float &m1, float &m2, const AdamArgs &a)
+{
+    m1 = a.beta1 * m1 + a.omb1 * g;
+    m2 = a.beta2 * m2 + a.omb2 * (g * g);
+    w = w * a.wdf - a.step * m1 / (__builtin_sqrtf(m2) * a.isbc2 + a.eps);
+}
 
 // Whether the streamed-tile kernel handles this padded rank.
 bool supported(int RP);
 
-// Enqueue the blend of every request (all share RP) on `st`.
-int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st);
+// Enqueue the blend of every request (all share RP) on `st`; with `adam`,
+// G_proj is not stored and the requests' W, m1, m2 take the AdamW step.
+int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st,
+        const AdamArgs *adam = nullptr);
 
 }  // namespace blend
 }  // namespace acsc
