@@ -47,6 +47,8 @@ def parse():
                          "warmup, as the reference for scaling HBM byte counters")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="approximate budget of the CPU-oracle sample")
+    ap.add_argument("--no-adamw", action="store_true",
+                    help="skip the separate measurement of the corrected AdamW step")
     return ap.parse_args()
 
 
@@ -289,6 +291,9 @@ def main():
     comp["kernels"] = {k: {kk_: round(v, 4) if isinstance(v, float) else v for kk_, v in d.items()}
                        for k, d in sorted(kern.items())}
 
+    if not args.no_adamw:
+        comp["sc_correct_adamw"] = adamw_component(pk, mats, r, gs, max(1, min(args.steps, 5)), stream)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, args.cpu_seconds)
@@ -310,6 +315,53 @@ def main():
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+def adamw_component(pk, mats, r, gs, calls, stream):
+    """The next row after the correction: the corrected AdamW step (the
+    correction with the optimiser update fused into its blend), on the same
+    matrices, timed on its own after the step loop.  Algorithmic bytes per
+    element: G read twice (X = U^T G V needs all of G before any element of
+    G_proj exists) and the fp32 weights and both moments read and written."""
+    import torch
+    import workloads
+    dev = mats[0]["G_mask"].device
+    items = []
+    for j, mt in enumerate(mats):
+        g = torch.Generator(device=dev).manual_seed(500 + j)
+        W = torch.randn(mt["m"], mt["n"], device=dev, generator=g)
+        items.append(dict(G=mt["G_mask"], prior=(mt["out"][0], mt["out"][3], mt["out"][2]), ws=mt["ws"],
+                          state=(W, torch.zeros_like(W), torch.zeros_like(W))))
+    hp = dict(lr=2e-5, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, max_norm=0.2)
+    pk.sc_correct_adamw_batched(items, r, workloads.ALPHA, step=1, dtype=gs.dtype, **hp)
+    torch.cuda.synchronize()
+    pk.acsc_stats_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for t in range(calls):
+        pk.sc_correct_adamw_batched(items, r, workloads.ALPHA, step=t + 2, dtype=gs.dtype, **hp)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    st = pk.acsc_stats_read()
+    pk.acsc_stats_enable(False)
+    ms = e0.elapsed_time(e1) / calls
+    elems = float(sum(mt["m"] * mt["n"] for mt in mats))
+    gsz = 2 if gs.dtype == torch.bfloat16 else 4
+    algo = elems * (2 * gsz + 24)
+    out = {"ms_per_call": round(ms, 4), "GB/s": round(algo / (ms * 1e-3) / 1e9, 1),
+           "frac_hbm": round(algo / (ms * 1e-3) / 1e9 / PEAK_HBM, 4), "bytes_per_call": algo,
+           "hparams": hp}
+    if "sc_blend_adamw" in st:
+        n, kms = st["sc_blend_adamw"]
+        bb = elems * (gsz + 24)
+        rate = bb * calls / (kms * 1e-3) / 1e9     # every call's launches cover all elements once
+        out["sc_blend_adamw"] = {"ms_per_call": round(kms / calls, 4), "GB/s": round(rate, 1),
+                                 "frac_hbm": round(rate / PEAK_HBM, 4)}
+    out["kernels"] = {k: {"launches_per_call": n / calls, "ms_per_call": round(v / calls, 4)}
+                      for k, (n, v) in sorted(st.items())}
+    del items
+    torch.cuda.empty_cache()
+    return out
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hotpath_70b_4layer_hbm_traffic.txt")
