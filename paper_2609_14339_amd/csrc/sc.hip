@@ -1016,49 +1016,66 @@ __global__ __launch_bounds__(256) void sumsq_kernel(const Batch<SumJob> jb)
         J.part[blockIdx.x] = t;
 }
 
+constexpr int kTermBlocks = 16;   // partial terms per matrix
+static_assert(kSumBlocks % kTermBlocks == 0, "term slices");
+
 struct NormJob {
     const double *part;   // ||G||^2 partials [kSumBlocks]
     const float *X;       // [r, RP]
     const float *Xf;      // [RP, RP] (rows >= r are zero)
     int r, RP;
+    double *terms;        // [kTermBlocks]
 };
+
+// Block b of matrix z: its share of alpha^2 ||G||^2 + 2 alpha (1 - alpha)
+// <X, X_f> + (1 - alpha)^2 ||X_f||^2, from fixed slices (grid kTermBlocks).
+__global__ __launch_bounds__(256) void norm_terms_kernel(const Batch<NormJob> jb, float alpha)
+{
+    __shared__ double red[256];
+    const NormJob &J = jb.j[blockIdx.z];
+    const int b = blockIdx.x;
+    const double a = alpha, c = 1.0 - static_cast<double>(alpha);
+    double gg = 0.0, xx = 0.0, ff = 0.0;
+    constexpr int PB = kSumBlocks / kTermBlocks;
+    for (int p = threadIdx.x; p < PB; p += 256)
+        gg += J.part[b * PB + p];
+    const int n = J.r * J.RP;
+    const int per = (n + kTermBlocks - 1) / kTermBlocks;
+    const int q0 = b * per, q1 = min(n, q0 + per);
+    for (int q = q0 + static_cast<int>(threadIdx.x); q < q1; q += 256) {
+        const double x = J.X[q], f = J.Xf[q];
+        xx += x * f;
+        ff += f * f;
+    }
+    const double t = block_sum(a * a * gg + 2.0 * a * c * xx + c * c * ff, red);
+    if (threadIdx.x == 0)
+        J.terms[b] = t;
+}
 
 // One workgroup.  acc (fp64) carries the squared norm over the launches of
 // one call (first: start at zero; last: write the clip coefficient and the
-// norm).
-__global__ __launch_bounds__(256) void clip_norm_kernel(const Batch<NormJob> jb, float alpha, float max_norm,
-                                                        double *acc, float *coef, float *norm_out, int first,
-                                                        int last)
+// norm).  Terms are added matrix by matrix in call order.
+__global__ __launch_bounds__(64) void clip_norm_kernel(const Batch<NormJob> jb, float max_norm, double *acc,
+                                                       float *coef, float *norm_out, int first, int last)
 {
-    __shared__ double red[256];
+    if (threadIdx.x != 0)
+        return;
     double total = first ? 0.0 : *acc;
-    const double a = alpha, b = 1.0 - static_cast<double>(alpha);
-    for (int i = 0; i < jb.count; ++i) {
-        const NormJob &J = jb.j[i];
-        double gg = 0.0, xx = 0.0, ff = 0.0;
-        for (int p = threadIdx.x; p < kSumBlocks; p += 256)
-            gg += J.part[p];
-        for (int q = threadIdx.x; q < J.r * J.RP; q += 256) {
-            const double x = J.X[q], f = J.Xf[q];
-            xx += x * f;
-            ff += f * f;
+    for (int i = 0; i < jb.count; ++i)
+        for (int b = 0; b < kTermBlocks; ++b)
+            total += jb.j[i].terms[b];
+    *acc = total;
+    if (last) {
+        const double N = sqrt(total > 0.0 ? total : 0.0);
+        float c = 1.0f;
+        if (max_norm > 0.f) {
+            const double q = static_cast<double>(max_norm) / (N + 1e-6);
+            if (q < 1.0)
+                c = static_cast<float>(q);
         }
-        total += block_sum(a * a * gg + 2.0 * a * b * xx + b * b * ff, red);
-    }
-    if (threadIdx.x == 0) {
-        *acc = total;
-        if (last) {
-            const double N = sqrt(total > 0.0 ? total : 0.0);
-            float c = 1.0f;
-            if (max_norm > 0.f) {
-                const double q = static_cast<double>(max_norm) / (N + 1e-6);
-                if (q < 1.0)
-                    c = static_cast<float>(q);
-            }
-            *coef = c;
-            if (norm_out)
-                *norm_out = static_cast<float>(N);
-        }
+        *coef = c;
+        if (norm_out)
+            *norm_out = static_cast<float>(N);
     }
 }
 
@@ -1462,7 +1479,7 @@ struct CorrWs {
     void *Pc, *Vc;
     uint16_t *Vt16;
     int64_t ldv16;
-    double *sq, *acc;
+    double *sq, *terms, *acc;
     float *coef;
 };
 
@@ -1483,6 +1500,7 @@ size_t carve_correct(const Dims &d, size_t esize, void *base, CorrWs *w)
     t.Vc = c.take<unsigned char>(static_cast<size_t>(d.n) * d.RP * esize);
     // corrected AdamW: ||G||^2 partials, the norm accumulator, the clip coefficient
     t.sq = c.take<double>(kSumBlocks);
+    t.terms = c.take<double>(kTermBlocks);
     t.acc = c.take<double>(1);
     t.coef = c.take<float>(1);
     if (w)
@@ -1868,10 +1886,11 @@ void clip_norm(const std::vector<Mat> &ms, int r, float alpha, const AdamCtx &ad
         b.count = static_cast<int>(std::min<size_t>(kMaxBatch, ms.size() - c0));
         for (int i = 0; i < b.count; ++i) {
             const Mat &m = ms[c0 + i];
-            b.j[i] = NormJob{m.cw.sq, m.cw.X, m.cw.Xf, r, m.D.RP};
+            b.j[i] = NormJob{m.cw.sq, m.cw.X, m.cw.Xf, r, m.D.RP, m.cw.terms};
         }
         const int first = c0 == 0, last = c0 + b.count == ms.size();
-        ACSC_LAUNCH("sc_clip_norm", clip_norm_kernel, dim3(1), dim3(256), 0, st, b, alpha, ad.max_norm, ad.acc,
+        ACSC_LAUNCH("sc_norm_terms", norm_terms_kernel, dim3(kTermBlocks, 1, b.count), dim3(256), 0, st, b, alpha);
+        ACSC_LAUNCH("sc_clip_norm", clip_norm_kernel, dim3(1), dim3(64), 0, st, b, ad.max_norm, ad.acc,
                     const_cast<float *>(ad.args.coef), ad.norm_out, first, last);
     }
 }
