@@ -1,0 +1,170 @@
+"""GPU tests of the in-graph masked boundary and of the anchor-prior
+scheduler (paper Sec. 3.1, Sec. 3.2; Alg. 1), against the CPU oracle.
+
+Boundary: the forward output, the input gradient and the packed gradient
+that crosses the link backwards are compared with the oracle bit for bit;
+masked positions get exactly zero gradient; inside a two-layer model the
+weight gradients match a plain PyTorch fp32 CPU reference of the same masked
+network.  Scheduler: a run of training steps with anchor arrivals every
+few steps (EMA, rebuild with a warm start) is followed step by step by the
+oracle (float64 EMA, LAPACK SVD, the correction), within the correction's
+tolerances (1e-4 fp32, 2e-2 bf16).
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import mask as om
+from oracle import spectral as osp
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pk():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_14339_amd as pk
+    return pk
+
+
+def _bits(t: torch.Tensor) -> np.ndarray:
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.view(torch.int32).numpy().view(np.uint32)
+
+
+def _host(t: torch.Tensor) -> np.ndarray:
+    return _bits(t) if t.dtype == torch.bfloat16 else t.detach().cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,S,H,keep", [(2, 64, 2048, 0.05), (1, 33, 300, 0.1)])
+def test_boundary_forward_and_backward_bit_exact(pk, dtype, B, S, H, keep):
+    from paper_2609_14339_amd.autograd import BoundaryRecv, BoundarySend, boundary_key, masked_boundary
+    dev = torch.device("cuda")
+    h = workloads.gaussian((B, S, H), seed=H + B, dtype=dtype).to(dev).requires_grad_(True)
+    gy = workloads.gaussian((B, S, H), seed=H + B + 1, dtype=dtype).to(dev)
+    key = boundary_key(seed=5, layer=3, step=11, microbatch=2, h=h)
+    okey = om.mask_key(5, 3, 11, 2, B, S, H)
+    K = om.keep_count(H, keep)
+    scale = H / K
+    y = masked_boundary(h, keep, key)
+    y.backward(gy)
+    torch.cuda.synchronize()
+    xh = _host(h.reshape(B * S, H))
+    ov, oi = om.pack(xh, K, okey)
+    oy = om.unpack(ov, H, okey, scale)
+    assert np.array_equal(_bits(y.reshape(B * S, H)).view(np.uint8), oy.view(np.uint8))
+    gv, _ = om.pack(_host(gy.reshape(B * S, H)), K, okey)
+    ogx = om.unpack(gv, H, okey, scale)
+    assert np.array_equal(_bits(h.grad.reshape(B * S, H)).view(np.uint8), ogx.view(np.uint8))
+    # masked entries get exactly zero gradient (Alg. 1, backward inherits the mask)
+    m = np.zeros((B * S, H), bool)
+    np.put_along_axis(m, oi.astype(np.int64), True, axis=1)
+    assert not np.any(_bits(h.grad.reshape(B * S, H))[~m])
+    # the two halves: the payload that crosses the link backwards is pack(gy)
+    h2 = h.detach().clone().requires_grad_(True)
+    vals, idx = BoundarySend.apply(h2, K, key, scale)
+    vals.retain_grad()
+    y2 = BoundaryRecv.apply(vals, idx, (B, S, H), key, scale)
+    y2.backward(gy)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(vals.grad).view(np.uint8), gv.view(np.uint8))
+    assert torch.equal(y2, y) and torch.equal(h2.grad, h.grad)
+
+
+def test_boundary_inside_a_two_layer_model(pk):
+    """x -> Linear -> masked boundary -> Linear -> loss: the weight gradients
+    match a PyTorch fp32 CPU reference that applies the oracle's mask."""
+    from paper_2609_14339_amd.autograd import boundary_key, masked_boundary
+    B, S, D, H, keep = 2, 32, 64, 512, 0.1
+    dev = torch.device("cuda")
+    torch.manual_seed(0)
+    l1, l2 = torch.nn.Linear(D, H), torch.nn.Linear(H, D)
+    x = torch.randn(B, S, D)
+    # CPU reference with the oracle's mask
+    K = om.keep_count(H, keep)
+    okey = om.mask_key(1, 0, 1, 0, B, S, H)
+    _, oi = om.pack(np.zeros((B * S, H), np.float32), K, okey)
+    mask = torch.zeros(B * S, H)
+    mask.scatter_(1, torch.from_numpy(oi.astype(np.int64)), 1.0)
+    r1, r2 = torch.nn.Linear(D, H), torch.nn.Linear(H, D)
+    r1.load_state_dict(l1.state_dict())
+    r2.load_state_dict(l2.state_dict())
+    hr = r1(x)
+    loss_r = (r2(hr * mask.view(B, S, H) * (H / K)) ** 2).mean()
+    loss_r.backward()
+    # GPU with the library boundary
+    l1, l2 = l1.to(dev), l2.to(dev)
+    hg = l1(x.to(dev))
+    key = boundary_key(1, 0, 1, 0, hg)
+    loss_g = (l2(masked_boundary(hg, keep, key)) ** 2).mean()
+    loss_g.backward()
+    torch.cuda.synchronize()
+    for a, b in ((l1.weight.grad, r1.weight.grad), (l2.weight.grad, r2.weight.grad), (l1.bias.grad, r1.bias.grad)):
+        assert osp.rel_fro(a.double().cpu().numpy(), b.double().numpy()) <= 1e-5
+    assert abs(loss_g.item() - loss_r.item()) <= 1e-5 * abs(loss_r.item())
+
+
+def _prior_run(pk, cid, steps, every, warm, dtype, tol, drift):
+    """drift: per-entry std of the change between successive anchor
+    gradients, kept below the configuration's noise so that the top-r
+    subspace stays separated from the rest (a vanishing gap makes it
+    ill-posed for any SVD)."""
+    cfg = workloads.CONFIGS[cid]
+    gs = cfg.grad
+    r = gs.r[0]
+    shapes = gs.shapes[:2] if len(gs.shapes) > 1 else gs.shapes
+    dev = torch.device("cuda")
+    from paper_2609_14339_amd.prior import AnchorPrior
+    ap = AnchorPrior(shapes, r, workloads.BETA, workloads.TAU, cfg.oversample, cfg.power_iters,
+                     dtype=dtype, device=dev, warm_start=warm, seed=3)
+    pairs = [workloads.grad_pair(gs, cid, 0, j, "cpu") for j in range(len(shapes))]
+    Mo = [np.zeros(s) for s in shapes]
+    prior_o = [None] * len(shapes)
+    for t in range(steps):
+        if t % every == 0:
+            a = t // every
+            G_anc = [(p.G_anc.float() + drift * a * workloads.gaussian(p.G_anc.shape, seed=100 * a + j)).to(dtype)
+                     for j, p in enumerate(pairs)]
+            ap.arrive([g.to(dev) for g in G_anc])
+            for j, g in enumerate(G_anc):
+                Mo[j], U, s, V, d = osp.build_prior(Mo[j], g.double().numpy(), workloads.BETA, r, workloads.TAU)
+                prior_o[j] = (U, d, V)
+        G = [(p.G_mask.float() + drift * workloads.gaussian(p.G_mask.shape, seed=1000 + t)).to(dtype)
+             for p in pairs]
+        out = ap.correct([g.to(dev) for g in G], workloads.ALPHA)
+        torch.cuda.synchronize()
+        for j, (g, o) in enumerate(zip(G, out)):
+            U, d, V = prior_o[j]
+            ref = osp.correct(g.double().numpy(), U, d, V, workloads.ALPHA)
+            err = osp.rel_fro(o.double().cpu().numpy(), ref)
+            assert err <= tol, f"step {t}, matrix {j}: rel. error {err:.2e}"
+    # the EMA state itself follows the oracle's
+    for j in range(len(shapes)):
+        assert osp.rel_fro(ap.M[j].double().cpu().numpy(), Mo[j]) <= 1e-6
+    assert ap.arrivals == (steps + every - 1) // every
+
+
+@pytest.mark.parametrize("warm", [True, False])
+def test_anchor_prior_over_steps_fp32(pk, warm):
+    # tiny configuration: anchor noise 0.01 per entry
+    _prior_run(pk, 1, steps=7, every=3, warm=warm, dtype=torch.float32, tol=1e-4, drift=0.003)
+
+
+def test_anchor_prior_over_steps_bf16(pk):
+    # 1B-class shapes: noise 0.05 ||S||_F / sqrt(mn), about 4.5e-3 per entry
+    _prior_run(pk, 2, steps=5, every=2, warm=True, dtype=torch.bfloat16, tol=2e-2, drift=0.001)
+
+
+def test_empty_prior_gives_alpha_g(pk):
+    from paper_2609_14339_amd.prior import AnchorPrior
+    dev = torch.device("cuda")
+    ap = AnchorPrior([(96, 64)], 4, 0.9, 1e-3, 4, 2, dtype=torch.float32, device=dev)
+    G = workloads.gaussian((96, 64), seed=4).to(dev)
+    out = ap.correct([G], 0.3)[0]
+    torch.cuda.synchronize()
+    assert torch.allclose(out, 0.3 * G, rtol=1e-6, atol=0)
