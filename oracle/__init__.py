@@ -15,6 +15,10 @@ Pins (tests run without a GPU) and their status:
                projector idempotence and self-adjointness at tau = 0,
                Lemma 1 (non-expansive) and Lemma 2 (noise contraction, Monte
                Carlo), EMA closed forms, SVD against eigh brute force.
+  mask.bern_*  pinned (the per-entry draw is our specification): inclusion
+               frequency per position, binomial row counts, independence of
+               neighbouring entries, uniform patterns on a tiny row, keep = 1,
+               App. F unbiasedness and variance (p / (1 - p)) h^2, layout.
   adamw.*      pinned: torch.optim.AdamW and torch.nn.utils.clip_grad_norm_ in
                float64 (independent library routines), the closed form of the
                first step from zero moments, clipping invariants, the norm

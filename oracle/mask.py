@@ -51,6 +51,18 @@ def _lib():
                                    C.c_void_p, i64]
         lib.orc_mask_dense.restype = i32
         lib.orc_mask_dense.argtypes = [i64, i32, i32, u64, i64, C.c_void_p]
+        lib.orc_bern_threshold.restype = i32
+        lib.orc_bern_threshold.argtypes = [C.c_double, C.POINTER(i32)]
+        lib.orc_bern_kept.restype = i32
+        lib.orc_bern_kept.argtypes = [u64, u32, i32]
+        lib.orc_bern_row_ptr.restype = i32
+        lib.orc_bern_row_ptr.argtypes = [u64, i64, i32, i32, i64, C.c_void_p]
+        lib.orc_bern_pack.restype = i32
+        lib.orc_bern_pack.argtypes = [C.c_void_p, i32, i64, i32, i64, i32, u64, i64, C.c_void_p, C.c_void_p,
+                                      C.c_void_p]
+        lib.orc_bern_unpack.restype = i32
+        lib.orc_bern_unpack.argtypes = [C.c_void_p, C.c_void_p, i32, i64, i32, i32, u64, i64, C.c_void_p,
+                                        C.c_float, C.c_void_p, i64]
         lib.orc_bf16_from_double.restype = C.c_uint16
         lib.orc_bf16_from_double.argtypes = [C.c_double]
         lib.orc_bf16_to_double.restype = C.c_double
@@ -165,3 +177,70 @@ def bf16_from_double(v: float) -> int:
 
 def bf16_to_double(h: int) -> float:
     return float(_lib().orc_bf16_to_double(h))
+
+
+# --------------------------------------------------------------------------
+# Bernoulli variant (App. F): each entry kept independently, rows of variable
+# length laid out by row_ptr.
+# --------------------------------------------------------------------------
+def bern_threshold(keep: float) -> int:
+    """T = round(keep * 65536) in [1, 65536]; inclusion probability T / 65536."""
+    t = C.c_int(0)
+    if _lib().orc_bern_threshold(keep, C.byref(t)) != 0:
+        raise ValueError(f"invalid keep={keep}")
+    return t.value
+
+
+def bern_kept(key: int, row: int, j: int, keep: float) -> bool:
+    return bool(_lib().orc_bern_kept(row_key(key, row), j, bern_threshold(keep)))
+
+
+def bern_row_ptr(key: int, rows: int, H: int, keep: float, row0: int = 0) -> np.ndarray:
+    """row_ptr [rows + 1] of rows row0 .. row0 + rows - 1, starting at 0."""
+    rp = np.zeros(rows + 1, dtype=np.int64)
+    _lib().orc_bern_row_ptr(key, rows, H, bern_threshold(keep), row0, rp.ctypes.data)
+    return rp
+
+
+def bern_mask_dense(key: int, rows: int, H: int, keep: float, row0: int = 0) -> np.ndarray:
+    T = bern_threshold(keep)
+    m = np.zeros((rows, H), dtype=np.uint8)
+    lib = _lib()
+    for r in range(rows):
+        rk = row_key(key, row0 + r)
+        for j in range(H):
+            m[r, j] = lib.orc_bern_kept(rk, j, T)
+    return m
+
+
+def bern_pack(x: np.ndarray, keep: float, key: int, row0: int = 0, with_idx: bool = True):
+    """(row_ptr, vals, idx): the kept entries of every row, ascending, in one
+    flat array (App. F Bernoulli mask; only kept values cross the link)."""
+    x = np.ascontiguousarray(x)
+    rows, H = x.shape
+    rp = bern_row_ptr(key, rows, H, keep, row0)
+    nnz = int(rp[-1])
+    vals = np.zeros(max(nnz, 1), dtype=x.dtype)[:nnz]
+    idx = np.zeros(max(nnz, 1), dtype=np.uint16)[:nnz] if with_idx else None
+    rc = _lib().orc_bern_pack(x.ctypes.data, x.dtype.itemsize, rows, H, H, bern_threshold(keep), key, row0,
+                              rp.ctypes.data, vals.ctypes.data, idx.ctypes.data if idx is not None else None)
+    if rc != 0:
+        raise ValueError("bern_pack failed")
+    return rp, vals, idx
+
+
+def bern_unpack(vals: np.ndarray, row_ptr: np.ndarray, H: int, key: int, keep: float, scale: float = 1.0,
+                idx=None, row0: int = 0):
+    """Dense y: round(scale * value) at the kept entries, +0 elsewhere."""
+    vals = np.ascontiguousarray(vals)
+    rp = np.ascontiguousarray(row_ptr, dtype=np.int64)
+    rows = rp.size - 1
+    code = _dtype_code(vals)
+    y = np.zeros((rows, H), dtype=vals.dtype)
+    ip = None
+    if idx is not None:
+        idx = np.ascontiguousarray(idx, dtype=np.uint16)
+        ip = idx.ctypes.data
+    _lib().orc_bern_unpack(vals.ctypes.data, ip, code, rows, H, bern_threshold(keep), key, row0, rp.ctypes.data,
+                           np.float32(scale), y.ctypes.data, H)
+    return y

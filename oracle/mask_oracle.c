@@ -282,3 +282,109 @@ int orc_mask_dense(int64_t rows, int H, int K, uint64_t key, int64_t row0, uint8
     free(I);
     return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Bernoulli variant (App. F: each entry kept independently with probability
+ * 1 - p; the receiver rescales by 1 / (1 - p)).  Rows keep a variable number
+ * of entries, so the payload is laid out by rows: row_ptr[r] .. row_ptr[r+1]
+ * index the kept values (and indices) of row r, ascending.
+ *
+ * The per-entry draw is our specification (the paper gives no PRF): with k_r
+ * the row key above, a its low and b its high 32 bits, entries 2q and 2q + 1
+ * of the row take the low and the high 16 bits of
+ *     h_q = fmix32(fmix32(a ^ q) ^ b),
+ * and entry j is kept iff its 16 bits are below T = floor(keep * 65536 + 0.5),
+ * 1 <= T <= 65536: inclusion probability T / 65536.
+ * ---------------------------------------------------------------------- */
+int orc_bern_threshold(double keep, int *T)
+{
+    if (!(keep > 0.0 && keep <= 1.0))
+        return -1;
+    double t = floor(keep * 65536.0 + 0.5);
+    if (t < 1.0)
+        return -1;
+    if (t > 65536.0)
+        t = 65536.0;
+    *T = (int)t;
+    return 0;
+}
+
+int orc_bern_kept(uint64_t row_key, uint32_t j, int T)
+{
+    uint32_t a = (uint32_t)row_key, b = (uint32_t)(row_key >> 32);
+    uint32_t h = orc_fmix32(orc_fmix32(a ^ (j >> 1)) ^ b);
+    uint32_t u = (j & 1u) ? (h >> 16) : (h & 0xFFFFu);
+    return u < (uint32_t)T;
+}
+
+/* row_ptr[0] = 0, row_ptr[r + 1] = row_ptr[r] + (entries kept in row row0 + r). */
+int orc_bern_row_ptr(uint64_t key, int64_t rows, int H, int T, int64_t row0, int64_t *row_ptr)
+{
+    row_ptr[0] = 0;
+    for (int64_t r = 0; r < rows; ++r) {
+        uint64_t rk = orc_row_key(key, (uint64_t)(row0 + r));
+        int64_t c = 0;
+        for (int j = 0; j < H; ++j)
+            c += orc_bern_kept(rk, (uint32_t)j, T);
+        row_ptr[r + 1] = row_ptr[r] + c;
+    }
+    return 0;
+}
+
+/* pack: the kept entries of row r, ascending, at vals[row_ptr[r] ..] (bit
+ * copies) and their positions at idx[row_ptr[r] ..] (if idx is given). */
+int orc_bern_pack(const void *x, int esize, int64_t rows, int H, int64_t ld_x, int T, uint64_t key,
+                  int64_t row0, const int64_t *row_ptr, void *vals, uint16_t *idx)
+{
+    const unsigned char *xb = (const unsigned char *)x;
+    unsigned char *vb = (unsigned char *)vals;
+    for (int64_t r = 0; r < rows; ++r) {
+        uint64_t rk = orc_row_key(key, (uint64_t)(row0 + r));
+        int64_t pos = row_ptr[r];
+        for (int j = 0; j < H; ++j) {
+            if (!orc_bern_kept(rk, (uint32_t)j, T))
+                continue;
+            memcpy(vb + (size_t)pos * esize, xb + ((size_t)r * ld_x + j) * esize, (size_t)esize);
+            if (idx)
+                idx[pos] = (uint16_t)j;
+            ++pos;
+        }
+        if (pos != row_ptr[r + 1])
+            return -1;
+    }
+    return 0;
+}
+
+/* unpack: y[r, :] = +0, then y[r, j] = round(scale * vals[...]) for the kept
+ * j of the row in ascending order (positions from idx when given). */
+int orc_bern_unpack(const void *vals, const uint16_t *idx, int dtype, int64_t rows, int H, int T,
+                    uint64_t key, int64_t row0, const int64_t *row_ptr, float scale, void *y, int64_t ld_y)
+{
+    for (int64_t r = 0; r < rows; ++r) {
+        uint64_t rk = orc_row_key(key, (uint64_t)(row0 + r));
+        int64_t pos = row_ptr[r], end = row_ptr[r + 1];
+        if (dtype == 0) {
+            float *yr = (float *)y + (size_t)r * ld_y;
+            for (int j = 0; j < H; ++j)
+                yr[j] = 0.0f;
+        } else {
+            uint16_t *yr = (uint16_t *)y + (size_t)r * ld_y;
+            for (int j = 0; j < H; ++j)
+                yr[j] = 0;
+        }
+        for (int j = 0; j < H && pos < end; ++j) {
+            int kept = idx ? (idx[pos] == (uint16_t)j) : orc_bern_kept(rk, (uint32_t)j, T);
+            if (!kept)
+                continue;
+            if (dtype == 0) {
+                double p = (double)((const float *)vals)[pos] * (double)scale;
+                ((float *)y)[(size_t)r * ld_y + j] = (float)p;
+            } else {
+                double p = orc_bf16_to_double(((const uint16_t *)vals)[pos]) * (double)scale;
+                ((uint16_t *)y)[(size_t)r * ld_y + j] = orc_bf16_from_double(p);
+            }
+            ++pos;
+        }
+    }
+    return 0;
+}
