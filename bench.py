@@ -49,6 +49,8 @@ def parse():
                     help="approximate budget of the CPU-oracle sample")
     ap.add_argument("--no-adamw", action="store_true",
                     help="skip the separate measurement of the corrected AdamW step")
+    ap.add_argument("--no-bernoulli", action="store_true",
+                    help="skip the separate measurement of the Bernoulli mask variant")
     return ap.parse_args()
 
 
@@ -293,6 +295,9 @@ def main():
 
     if not args.no_adamw:
         comp["sc_correct_adamw"] = adamw_component(pk, mats, r, gs, max(1, min(args.steps, 5)), stream)
+    if not args.no_bernoulli:
+        comp["ac_bernoulli"] = bernoulli_component(pk, xs, gxs, keys, act, keep, esz, max(1, min(args.steps, 5)),
+                                                   stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -361,6 +366,60 @@ def adamw_component(pk, mats, r, gs, calls, stream):
                       for k, (n, v) in sorted(st.items())}
     del items
     torch.cuda.empty_cache()
+    return out
+
+
+def bernoulli_component(pk, xs, gxs, keys, act, keep, esz, calls, stream):
+    """The Bernoulli mask variant on the same boundaries: per layer the mask
+    (row offsets and bitmaps, from the key) once, then pack and unpack of the
+    activation and of its gradient; timed on its own after the step loop.
+    Algorithmic bytes: pack, the 128-byte lines of x holding a kept entry
+    (1 - (1 - q)^E of them, E entries per line) plus the payload and its
+    indices; unpack, the dense write plus the payload read; mask, the
+    bitmaps and offsets written."""
+    import torch
+    H, rows = act.H, act.B * act.S
+    L = len(xs)
+    ys = torch.empty(rows, H, dtype=act.dtype, device=xs[0].device)
+    masks = [pk.ac_bern_mask(rows, H, keep, keys[l]) for l in range(L)]
+    torch.cuda.synchronize()
+    nnz = [int(rp[-1].item()) for rp, _ in masks]
+    bufs = [torch.empty(n, dtype=act.dtype, device=xs[0].device) for n in nnz]
+    idxs = [torch.empty(n, dtype=torch.int16, device=xs[0].device) for n in nnz]
+
+    def run():
+        for l in range(L):
+            rp, bits = pk.ac_bern_mask(rows, H, keep, keys[l])
+            for src in (xs[l], gxs[l]):
+                pk.lib.ac_bern_pack(pk._ptr(src), pk._dt(src), rows, H, H, pk._ptr(rp), pk._ptr(bits),
+                                    pk._ptr(bufs[l]), pk._ptr(idxs[l]), nnz[l], pk._stream())
+                pk.ac_bern_unpack(bufs[l], H, rp, bits, 1.0 / keep, y=ys)
+    run()
+    torch.cuda.synchronize()
+    pk.acsc_stats_enable(True)
+    for _ in range(calls):
+        run()
+    torch.cuda.synchronize()
+    st = pk.acsc_stats_read()
+    pk.acsc_stats_enable(False)
+    q = round(keep * 65536) / 65536
+    E = 128 // esz
+    line = 1.0 - (1.0 - q) ** E
+    nz = sum(nnz) / L
+    work = {"ac_bern_pack": line * rows * H * esz + nz * (esz + 2),
+            "ac_bern_unpack": rows * H * esz + nz * esz + rows * H / 8,
+            "ac_bern_mask": rows * H / 8 + 8 * (rows + 1)}
+    out = {"keep": keep, "kept_per_row": round(nz / rows, 2)}
+    for k, b in work.items():
+        if k in st:
+            n, ms = st[k]
+            per = ms / n
+            out[k] = {"launches_per_step": n / calls, "avg_us": round(1e3 * per, 2),
+                      "GB/s": round(b / (per * 1e-3) / 1e9, 1), "frac_hbm": round(b / (per * 1e-3) / 1e9 / PEAK_HBM, 4)}
+    if "ac_bern_scan" in st:
+        n, ms = st["ac_bern_scan"]
+        out["ac_bern_scan"] = {"avg_us": round(1e3 * ms / n, 2)}
+    del bufs, idxs, ys
     return out
 
 

@@ -116,6 +116,50 @@ int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int6
                       hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Bernoulli mask variant (App. F: every entry of the mask an independent
+ * Bernoulli draw, kept with probability 1 - p; the receiver rescales by
+ * 1 / (1 - p)).  Rows keep a variable number of entries, so the payload is
+ * laid out by row offsets: row r owns vals[row_ptr[r] .. row_ptr[r + 1]),
+ * its kept entries in ascending position order.
+ * The per-entry draw (our specification; the paper gives no PRF): with k_r
+ * the row key of the fixed-K mask (the same key chain), a and b its low and
+ * high 32 bits, entries 2q and 2q + 1 of the row take the low and the high 16
+ * bits of fmix32(fmix32(a ^ q) ^ b), and are kept when those are below
+ * T = floor(keep * 65536 + 0.5) (inclusion probability T / 65536).
+ * ---------------------------------------------------------------------- */
+
+/* The mask of a [rows, H] tensor for `key`, computed once and reused by
+ * every pack and unpack with that key (both directions of a boundary):
+ *   row_ptr  device int64 [rows + 1] out: row_ptr[0] = 0, row_ptr[r + 1] -
+ *            row_ptr[r] = entries kept in row r; row_ptr[rows] = nnz.
+ *   bits     device uint32 [rows, ceil(H / 32)] out: bit j % 32 of word
+ *            j / 32 of row r is set iff entry (r, j) is kept.
+ * Requires 0 < keep <= 1 with T >= 1, 1 <= H <= 65536, key->H == H,
+ * key->B * key->S == rows, 8-byte aligned row_ptr, 4-byte aligned bits.
+ * The sender and the receiver compute the same row_ptr and bits from the
+ * key alone; nothing but the values needs to cross the link. */
+int ac_bern_mask(int64_t rows, int H, double keep, const ac_mask_key *key, int64_t *row_ptr,
+                 uint32_t *bits, hipStream_t stream);
+
+/* Pack: vals[row_ptr[r] + i] = x[r, j_i] (bit copies) for the kept entries
+ * j_0 < j_1 < ... of row r; idx (device uint16 or NULL) gets the j_i.
+ * x     device [rows, ld_x] of dt (ld_x >= H).
+ * vals  device, capacity `cap` elements (size it by row_ptr[rows]); slots
+ *       at or past cap are not written.
+ * row_ptr, bits  from ac_bern_mask for the same rows, H and key. */
+int ac_bern_pack(const void *x, acsc_dtype dt, int64_t rows, int H, int64_t ld_x,
+                 const int64_t *row_ptr, const uint32_t *bits, void *vals, uint16_t *idx,
+                 int64_t cap, hipStream_t stream);
+
+/* Unpack: y[r, j] = round(scale * vals[row_ptr[r] + i]) at the i-th kept
+ * entry j of row r, +0 elsewhere (columns >= H untouched).  The product is
+ * rounded once (as ac_unpack_scatter).  Slots at or past cap read as zero.
+ * y device [rows, ld_y], ld_y >= H, must not overlap vals. */
+int ac_bern_unpack(const void *vals, acsc_dtype dt, int64_t rows, int H, const int64_t *row_ptr,
+                   const uint32_t *bits, int64_t cap, float scale, void *y, int64_t ld_y,
+                   hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Spectral corrector (paper Sec. 3.2; Alg. 1; App. E).
  * ---------------------------------------------------------------------- */
 

@@ -72,6 +72,12 @@ def _load():
     lib.ac_unpack_scatter.restype = i32
     lib.ac_unpack_scatter.argtypes = [vp, vp, i32, i64, i32, i32, C.POINTER(MaskKey), f32, vp,
                                       i64, vp]
+    lib.ac_bern_mask.restype = i32
+    lib.ac_bern_mask.argtypes = [i64, i32, C.c_double, C.POINTER(MaskKey), vp, vp, vp]
+    lib.ac_bern_pack.restype = i32
+    lib.ac_bern_pack.argtypes = [vp, i32, i64, i32, i64, vp, vp, vp, vp, i64, vp]
+    lib.ac_bern_unpack.restype = i32
+    lib.ac_bern_unpack.argtypes = [vp, i32, i64, i32, vp, vp, i64, f32, vp, i64, vp]
     lib.sc_workspace_size.restype = i32
     lib.sc_workspace_size.argtypes = [i32, i32, i32, i32, i32, C.POINTER(sz)]
     lib.sc_build_prior.restype = i32
@@ -100,7 +106,8 @@ lib = _load()
 EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
             "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched",
-            "sc_adamw_workspace_size", "sc_correct_adamw_batched")
+            "sc_adamw_workspace_size", "sc_correct_adamw_batched",
+            "ac_bern_mask", "ac_bern_pack", "ac_bern_unpack")
 
 
 def _check(rc: int):
@@ -201,6 +208,48 @@ def ac_unpack_scatter(vals: torch.Tensor, H: int, key: MaskKey, scale: float = 1
         raise AcscError(ACSC_EINVAL, "vals must be contiguous and y 2-D with unit column stride")
     _check(lib.ac_unpack_scatter(_ptr(vals), _ptr(idx), _dt(vals), rows, H, K, C.byref(key),
                                  float(scale), _ptr(y), y.stride(0), _stream(stream)))
+    return y
+
+
+def ac_bern_mask(rows: int, H: int, keep: float, key: MaskKey, device="cuda", stream=None):
+    """The Bernoulli mask of a [rows, H] tensor: (row_ptr int64 [rows + 1],
+    bits int32 [rows, ceil(H / 32)] holding uint32 patterns)."""
+    row_ptr = torch.empty(rows + 1, dtype=torch.int64, device=device)
+    bits = torch.empty(max(rows, 1), (H + 31) // 32, dtype=torch.int32, device=device)[:rows]
+    _check(lib.ac_bern_mask(rows, H, float(keep), C.byref(key), _ptr(row_ptr), _ptr(bits), _stream(stream)))
+    return row_ptr, bits
+
+
+def ac_bern_pack(x: torch.Tensor, row_ptr: torch.Tensor, bits: torch.Tensor, nnz: Optional[int] = None,
+                 with_idx: bool = True, stream=None):
+    """Packed values [nnz] (and uint16 indices as int16, or None) of x [rows, H]
+    under the mask (row_ptr, bits).  nnz defaults to row_ptr[-1] (a host
+    read, which synchronises)."""
+    _need_cuda(x, row_ptr, bits)
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise AcscError(ACSC_EINVAL, "x must be 2-D with unit column stride")
+    rows, H = x.shape
+    if nnz is None:
+        nnz = int(row_ptr[-1].item())
+    vals = torch.empty(max(nnz, 1), dtype=x.dtype, device=x.device)[:nnz]
+    idx = torch.empty(max(nnz, 1), dtype=torch.int16, device=x.device)[:nnz] if with_idx else None
+    _check(lib.ac_bern_pack(_ptr(x), _dt(x), rows, H, x.stride(0), _ptr(row_ptr), _ptr(bits), _ptr(vals),
+                            _ptr(idx), nnz, _stream(stream)))
+    return vals, idx
+
+
+def ac_bern_unpack(vals: torch.Tensor, H: int, row_ptr: torch.Tensor, bits: torch.Tensor, scale: float = 1.0,
+                   y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Dense [rows, H]: scale * value at the kept entries, +0 elsewhere."""
+    _need_cuda(vals, row_ptr, bits)
+    rows = row_ptr.numel() - 1
+    if y is None:
+        y = torch.empty(rows, H, dtype=vals.dtype, device=vals.device)
+    _need_cuda(y)
+    if y.dim() != 2 or y.stride(1) != 1 or not vals.is_contiguous():
+        raise AcscError(ACSC_EINVAL, "vals must be contiguous and y 2-D with unit column stride")
+    _check(lib.ac_bern_unpack(_ptr(vals), _dt(vals), rows, H, _ptr(row_ptr), _ptr(bits), vals.numel(),
+                              float(scale), _ptr(y), y.stride(0), _stream(stream)))
     return y
 
 

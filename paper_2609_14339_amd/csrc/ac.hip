@@ -639,6 +639,230 @@ __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ va
     }
 }
 
+// ---------------------------------------------------------------------------
+// Bernoulli variant (App. F: every entry kept independently with probability
+// 1 - p).  Rows keep a variable number of entries; the payload is laid out
+// by row_ptr (row r owns vals[row_ptr[r] .. row_ptr[r + 1]), ascending).
+// The draw (our specification, as the oracle): with k_r the row key, a and b
+// its low and high 32 bits, entries 2q and 2q + 1 take the low and the high
+// 16 bits of fmix32(fmix32(a ^ q) ^ b) and are kept when these are below T.
+// The hashing runs once per key, in bern_mask_kernel, which stores the row
+// bitmaps; pack and unpack read the bitmaps.
+// ---------------------------------------------------------------------------
+constexpr int kBernWaves = 4;
+
+// One wave per row: the row's bitmap (bit j % 32 of word j / 32 is entry j)
+// and its count, left at row_ptr[row + 1] for bern_scan_kernel.
+__global__ __launch_bounds__(64 * kBernWaves) void bern_mask_kernel(int64_t rows, int H, uint32_t T, uint64_t key,
+                                                                   int64_t *__restrict__ row_ptr,
+                                                                   uint32_t *__restrict__ bits)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * kBernWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (row >= rows)
+        return;
+    const uint64_t kr = mix64((key ^ static_cast<uint64_t>(row)) + kGamma);
+    const uint32_t a = static_cast<uint32_t>(kr), b = static_cast<uint32_t>(kr >> 32);
+    const int nw = (H + 31) >> 5;
+    uint32_t *br = bits + row * nw;
+    int cnt = 0;
+    for (int w = lane; w < nw; w += 64) {
+        uint32_t word = 0;
+#pragma unroll 4
+        for (int p = 0; p < 16; ++p) {
+            const uint32_t h = fmix32(fmix32(a ^ static_cast<uint32_t>(w * 16 + p)) ^ b);
+            word |= ((h & 0xFFFFu) < T ? 1u : 0u) << (2 * p);
+            word |= ((h >> 16) < T ? 1u : 0u) << (2 * p + 1);
+        }
+        const int left = H - w * 32;     // entries past H are never kept
+        if (left < 32)
+            word &= (1u << left) - 1u;
+        br[w] = word;
+        cnt += __popc(word);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        cnt += __shfl_xor(cnt, off, 64);
+    if (lane == 0)
+        row_ptr[row + 1] = cnt;
+}
+
+// One workgroup: row_ptr[1 ..] holds the row counts; it becomes their
+// inclusive prefix sum, row_ptr[0] = 0.  Tiles of 4096 rows: thread t loads
+// rows t, t + 1024, .. of the tile (coalesced), the tile is scanned in LDS in
+// a fixed order, and the running total carries to the next tile.
+__global__ __launch_bounds__(1024) void bern_scan_kernel(int64_t rows, int64_t *__restrict__ row_ptr)
+{
+    constexpr int kTile = 4096;
+    __shared__ int64_t v[kTile];
+    __shared__ int64_t part[1024];
+    const int t = threadIdx.x;
+    int64_t carry = 0;
+    for (int64_t r0 = 0; r0 < rows; r0 += kTile) {
+        const int n = static_cast<int>(min<int64_t>(kTile, rows - r0));
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = t + 1024 * k;
+            v[i] = i < n ? row_ptr[r0 + i + 1] : 0;
+        }
+        __syncthreads();
+        // thread t scans its run of four, then the 1024 run sums
+        int64_t s = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            s += v[4 * t + k];
+            v[4 * t + k] = s;
+        }
+        part[t] = s;
+        __syncthreads();
+        for (int off = 1; off < 1024; off <<= 1) {
+            const int64_t x = t >= off ? part[t - off] : 0;
+            __syncthreads();
+            part[t] += x;
+            __syncthreads();
+        }
+        const int64_t before = carry + (t ? part[t - 1] : 0);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            v[4 * t + k] += before;
+        carry += part[1023];
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = t + 1024 * k;
+            if (i < n)
+                row_ptr[r0 + i + 1] = v[i];
+        }
+        __syncthreads();
+    }
+    if (t == 0)
+        row_ptr[0] = 0;
+}
+
+// One wave per row, 64 bitmap words (2048 entries) at a time: the segment's
+// kept positions go to an LDS list in ascending order (word popcount prefix),
+// then the wave gathers them and stores the payload contiguously.  Payload
+// slots at or past cap are never written.
+template <typename E>
+__global__ __launch_bounds__(64 * kBernWaves) void bern_pack_kernel(const E *__restrict__ x, int64_t rows, int H,
+                                                                   int64_t ld_x, const int64_t *__restrict__ row_ptr,
+                                                                   const uint32_t *__restrict__ bits,
+                                                                   E *__restrict__ vals, uint16_t *__restrict__ idx,
+                                                                   int64_t cap)
+{
+    __shared__ uint16_t lists[kBernWaves][kSegWords * 32];
+    const int lane = threadIdx.x & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * kBernWaves + wid;
+    if (row >= rows)
+        return;
+    const int nw = (H + 31) >> 5;
+    const uint32_t *br = bits + row * nw;
+    const E *xr = x + row * ld_x;
+    uint16_t *L = lists[wid];
+    int64_t base = row_ptr[row];
+    for (int s0 = 0; s0 < nw; s0 += kSegWords) {
+        const int w = s0 + lane;
+        uint32_t word = w < nw ? br[w] : 0u;
+        const int left = H - w * 32;     // a bitmap never marks entries past H; do not trust it to
+        if (left < 32)
+            word &= left > 0 ? (1u << left) - 1u : 0u;
+        const int c = __popc(word);
+        const int pre = wave_exclusive_scan(c, lane);
+        const int total = __shfl(pre + c, 63, 64);
+        uint32_t bm = word;
+        int pos = pre;
+        while (bm) {
+            const int t = __ffs(bm) - 1;
+            bm &= bm - 1u;
+            L[pos++] = static_cast<uint16_t>(w * 32 + t);
+        }
+        wave_sync();
+        for (int i0 = 0; i0 < total; i0 += 256) {
+            // four gathers in flight before any store
+            E v[4];
+            uint16_t jj[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + lane + 64 * u;
+                jj[u] = i < total ? L[i] : uint16_t(0);
+                v[u] = i < total ? xr[jj[u]] : E(0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + lane + 64 * u;
+                const int64_t o = base + i;
+                if (i < total && o < cap) {
+                    vals[o] = v[u];
+                    if (idx)
+                        idx[o] = jj[u];
+                }
+            }
+        }
+        wave_sync();
+        base += total;
+    }
+}
+
+// One wave per row, a segment of the dense row at a time in LDS: zero it,
+// drop scale * (kept value) at the kept entries, write it out with 16-byte
+// non-temporal stores (element stores when the row is not 16-byte aligned).
+// Payload slots at or past cap read as zero.
+template <typename E, bool VEC>
+__global__ __launch_bounds__(64 * kBernWaves) void bern_unpack_kernel(const E *__restrict__ vals, int64_t rows, int H,
+                                                                     const int64_t *__restrict__ row_ptr,
+                                                                     const uint32_t *__restrict__ bits, float scale,
+                                                                     E *__restrict__ y, int64_t ld_y, int64_t cap)
+{
+    constexpr int N = Vec16<E>::N;
+    __shared__ __attribute__((aligned(16))) E segs[kBernWaves][kSegWords * 32];
+    const int lane = threadIdx.x & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * kBernWaves + wid;
+    if (row >= rows)
+        return;
+    const int nw = (H + 31) >> 5;
+    const uint32_t *br = bits + row * nw;
+    E *seg = segs[wid];
+    E *yr = y + row * ld_y;
+    int64_t base = row_ptr[row];
+    for (int s0 = 0; s0 < nw; s0 += kSegWords) {
+        const int e0 = s0 * 32;
+        const int len = min(kSegWords * 32, H - e0);
+#pragma unroll
+        for (int c = lane; c < kSegWords * 32 / N; c += 64)
+            reinterpret_cast<uint4 *>(seg)[c] = make_uint4(0u, 0u, 0u, 0u);
+        wave_sync();
+        const int w = s0 + lane;
+        const uint32_t word = w < nw ? br[w] : 0u;
+        const int c = __popc(word);
+        const int pre = wave_exclusive_scan(c, lane);
+        const int total = __shfl(pre + c, 63, 64);
+        uint32_t bm = word;
+        int rank = pre;
+        while (bm) {
+            const int t = __ffs(bm) - 1;
+            bm &= bm - 1u;
+            const int64_t o = base + rank++;
+            seg[lane * 32 + t] = o < cap ? scaled(vals[o], scale) : E(0);
+        }
+        wave_sync();
+        if (VEC) {
+            const int nch = len / N;
+            for (int q = lane; q < nch; q += 64)
+                __builtin_nontemporal_store(reinterpret_cast<const u32x4 *>(seg)[q],
+                                            reinterpret_cast<u32x4 *>(yr + e0 + q * N));
+            for (int j = nch * N + lane; j < len; j += 64)
+                yr[e0 + j] = seg[j];
+        } else {
+            for (int j = lane; j < len; j += 64)
+                yr[e0 + j] = seg[j];
+        }
+        wave_sync();
+        base += total;
+    }
+}
+
 int common_checks(acsc_dtype dt, int64_t rows, int H, int K, const ac_mask_key *key)
 {
     ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
@@ -841,4 +1065,124 @@ extern "C" int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dty
     }
 #undef ACSC_UNPACK
     return check_launch("ac_unpack_scatter");
+}
+
+// ---------------------------------------------------------------------------
+// Bernoulli variant entry points.
+// ---------------------------------------------------------------------------
+namespace acsc {
+namespace {
+
+int bern_threshold(double keep, uint32_t *T)
+{
+    ACSC_CHECK_ARG(keep > 0.0 && keep <= 1.0, ACSC_EINVAL, "keep=%g outside (0, 1]", keep);
+    const double t = std::floor(keep * 65536.0 + 0.5);
+    ACSC_CHECK_ARG(t >= 1.0, ACSC_EINVAL, "keep=%g rounds to a zero threshold (keep >= 2^-17)", keep);
+    *T = static_cast<uint32_t>(t > 65536.0 ? 65536.0 : t);
+    return ACSC_OK;
+}
+
+int bern_shape(int64_t rows, int H)
+{
+    ACSC_CHECK_ARG(rows >= 0, ACSC_EINVAL, "rows=%lld < 0", (long long)rows);
+    ACSC_CHECK_ARG(H >= 1 && H <= 65536, ACSC_EINVAL, "H=%d outside [1, 65536]", H);
+    return ACSC_OK;
+}
+
+unsigned bern_blocks(int64_t rows)
+{
+    return static_cast<unsigned>((rows + kBernWaves - 1) / kBernWaves);
+}
+
+}  // namespace
+}  // namespace acsc
+
+extern "C" int ac_bern_mask(int64_t rows, int H, double keep, const ac_mask_key *key, int64_t *row_ptr,
+                            uint32_t *bits, hipStream_t stream)
+{
+    clear_error();
+    int rc = bern_shape(rows, H);
+    if (rc)
+        return rc;
+    uint32_t T = 0;
+    if ((rc = bern_threshold(keep, &T)))
+        return rc;
+    ACSC_CHECK_ARG(key != nullptr, ACSC_EINVAL, "key is NULL");
+    ACSC_CHECK_ARG(key->H == static_cast<uint32_t>(H), ACSC_EINVAL, "key.H=%u != H=%d", key->H, H);
+    ACSC_CHECK_ARG(static_cast<int64_t>(key->B) * key->S == rows, ACSC_EINVAL,
+                   "rows=%lld != key.B*key.S=%llu", (long long)rows, (unsigned long long)key->B * key->S);
+    ACSC_CHECK_ARG(row_ptr != nullptr && (rows == 0 || bits != nullptr), ACSC_EINVAL, "row_ptr or bits is NULL");
+    ACSC_CHECK_ARG(aligned(row_ptr, 8) && aligned(bits, 4), ACSC_EALIGN, "row_ptr (8) or bits (4) misaligned");
+    const uint64_t k = chain_key(*key);
+    if (rows > 0)
+        ACSC_LAUNCH("ac_bern_mask", bern_mask_kernel, dim3(bern_blocks(rows)), dim3(64 * kBernWaves), 0, stream,
+                    rows, H, T, k, row_ptr, bits);
+    ACSC_LAUNCH("ac_bern_scan", bern_scan_kernel, dim3(1), dim3(1024), 0, stream, rows, row_ptr);
+    return check_launch("ac_bern_mask");
+}
+
+extern "C" int ac_bern_pack(const void *x, acsc_dtype dt, int64_t rows, int H, int64_t ld_x,
+                            const int64_t *row_ptr, const uint32_t *bits, void *vals, uint16_t *idx,
+                            int64_t cap, hipStream_t stream)
+{
+    clear_error();
+    int rc = bern_shape(rows, H);
+    if (rc)
+        return rc;
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(ld_x >= H, ACSC_EINVAL, "ld_x=%lld < H=%d", (long long)ld_x, H);
+    ACSC_CHECK_ARG(cap >= 0, ACSC_EINVAL, "cap=%lld < 0", (long long)cap);
+    if (rows == 0)
+        return ACSC_OK;
+    ACSC_CHECK_ARG(x && row_ptr && bits && (vals || cap == 0), ACSC_EINVAL, "null pointer argument");
+    const size_t es = dtype_size(dt);
+    ACSC_CHECK_ARG(aligned(x, es) && aligned(vals, es) && aligned(row_ptr, 8) && aligned(bits, 4) &&
+                       (!idx || aligned(idx, 2)),
+                   ACSC_EALIGN, "misaligned pointer argument");
+    if (dt == ACSC_BF16)
+        ACSC_LAUNCH("ac_bern_pack", bern_pack_kernel<uint16_t>, dim3(bern_blocks(rows)), dim3(64 * kBernWaves), 0,
+                    stream, static_cast<const uint16_t *>(x), rows, H, ld_x, row_ptr, bits,
+                    static_cast<uint16_t *>(vals), idx, cap);
+    else
+        ACSC_LAUNCH("ac_bern_pack", bern_pack_kernel<uint32_t>, dim3(bern_blocks(rows)), dim3(64 * kBernWaves), 0,
+                    stream, static_cast<const uint32_t *>(x), rows, H, ld_x, row_ptr, bits,
+                    static_cast<uint32_t *>(vals), idx, cap);
+    return check_launch("ac_bern_pack");
+}
+
+extern "C" int ac_bern_unpack(const void *vals, acsc_dtype dt, int64_t rows, int H, const int64_t *row_ptr,
+                              const uint32_t *bits, int64_t cap, float scale, void *y, int64_t ld_y,
+                              hipStream_t stream)
+{
+    clear_error();
+    int rc = bern_shape(rows, H);
+    if (rc)
+        return rc;
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(ld_y >= H, ACSC_EINVAL, "ld_y=%lld < H=%d", (long long)ld_y, H);
+    ACSC_CHECK_ARG(cap >= 0, ACSC_EINVAL, "cap=%lld < 0", (long long)cap);
+    ACSC_CHECK_ARG(std::isfinite(scale), ACSC_EINVAL, "scale must be finite");
+    if (rows == 0)
+        return ACSC_OK;
+    ACSC_CHECK_ARG(y && row_ptr && bits && (vals || cap == 0), ACSC_EINVAL, "null pointer argument");
+    const size_t es = dtype_size(dt);
+    ACSC_CHECK_ARG(aligned(y, es) && aligned(vals, es) && aligned(row_ptr, 8) && aligned(bits, 4), ACSC_EALIGN,
+                   "misaligned pointer argument");
+    const bool vec = aligned(y, 16) && (static_cast<size_t>(ld_y) * es) % 16 == 0;
+#define ACSC_BERN_UNPACK(E, V)                                                                                   \
+    ACSC_LAUNCH("ac_bern_unpack", (bern_unpack_kernel<E, V>), dim3(bern_blocks(rows)), dim3(64 * kBernWaves), 0, \
+                stream, static_cast<const E *>(vals), rows, H, row_ptr, bits, scale, static_cast<E *>(y), ld_y, cap)
+    if (dt == ACSC_BF16) {
+        if (vec)
+            ACSC_BERN_UNPACK(uint16_t, true);
+        else
+            ACSC_BERN_UNPACK(uint16_t, false);
+    } else {
+        if (vec)
+            ACSC_BERN_UNPACK(uint32_t, true);
+        else
+            ACSC_BERN_UNPACK(uint32_t, false);
+    }
+#undef ACSC_BERN_UNPACK
+    return check_launch("ac_bern_unpack");
 }
