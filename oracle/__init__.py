@@ -23,4 +23,11 @@ Pins (tests run without a GPU) and their status:
                float64 (independent library routines), the closed form of the
                first step from zero moments, clipping invariants, the norm
                identity the library clips with, planted-mistake checks.
+  powersgd.*   pinned: numpy's Householder QR for the Gram-Schmidt step,
+               dropped dependent columns (exact small case), exact
+               reconstruction at rank <= r, least squares and Pythagoras for
+               the output and memory, the rank-1 closed form, Eckart-Young
+               (SVD) reached by the warm-started iteration, telescoping error
+               feedback, brute-force rank for a compression ratio,
+               planted-mistake checks.
 """
