@@ -51,6 +51,8 @@ def parse():
                     help="skip the separate measurement of the corrected AdamW step")
     ap.add_argument("--no-bernoulli", action="store_true",
                     help="skip the separate measurement of the Bernoulli mask variant")
+    ap.add_argument("--no-powersgd", action="store_true",
+                    help="skip the separate measurement of the PowerSGD compressor")
     return ap.parse_args()
 
 
@@ -299,6 +301,9 @@ def main():
         comp["ac_bernoulli"] = bernoulli_component(pk, xs, gxs, keys, act, keep, esz, max(1, min(args.steps, 5)),
                                                    stream)
 
+    if not args.no_powersgd:
+        comp["psgd"] = psgd_component(pk, mats, gs, max(1, min(args.steps, 5)), stream)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, args.cpu_seconds)
@@ -420,6 +425,57 @@ def bernoulli_component(pk, xs, gxs, keys, act, keep, esz, calls, stream):
         n, ms = st["ac_bern_scan"]
         out["ac_bern_scan"] = {"avg_us": round(1e3 * ms / n, 2)}
     del bufs, idxs, ys
+    return out
+
+
+def psgd_component(pk, mats, gs, calls, stream):
+    """The data-parallel compressor the method is paired with: one PowerSGD
+    step with error feedback on every gradient of the step (x64 ranks; equal
+    ranks share a call), timed on its own after the step loop.  Algorithmic
+    bytes per element: the first sweep reads G and the fp32 memory and writes
+    the memory and its bf16 copy (12 with bf16 G), the second projection
+    reads the copy (2), the decompression reads and writes the memory and
+    writes the output (10)."""
+    import torch
+    from paper_2609_14339_amd.powersgd import PowerSGDState
+    dev = mats[0]["G_mask"].device
+    grads = [mt["G_mask"] for mt in mats]
+    state = PowerSGDState([(mt["m"], mt["n"]) for mt in mats], 64.0, gs.dtype, dev, seed=3)
+    outs = [torch.empty_like(g) for g in grads]
+    state.step(grads, outs, stream)
+    torch.cuda.synchronize()
+    pk.acsc_stats_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(calls):
+        state.step(grads, outs, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    st = pk.acsc_stats_read()
+    pk.acsc_stats_enable(False)
+    ms = e0.elapsed_time(e1) / calls
+    elems = float(sum(mt["m"] * mt["n"] for mt in mats))
+    gsz = 2 if gs.dtype == torch.bfloat16 else 4
+    algo = elems * ((gsz + 8 + 2) + 2 + 10)
+    full = elems * gsz
+    out = {"ms_per_call": round(ms, 4), "GB/s": round(algo / (ms * 1e-3) / 1e9, 1),
+           "frac_hbm": round(algo / (ms * 1e-3) / 1e9 / PEAK_HBM, 4), "bytes_per_call": algo,
+           "ranks": sorted(set(state.ranks)), "compression": round(full / gsz / state.sent_elements(), 2)}
+    # per sweep, each covering every element once per call: the first sweep
+    # (fused with P = M Q where the group's row blocks fill the GPU, else the
+    # sweep and a pass over the copy), the second projection, the decompression
+    sweeps = (("first_sweep", ("psgd_feedback_mq", "psgd_feedback", "psgd_pass_mq"), gsz + 10),
+              ("psgd_pass_mtp", ("psgd_pass_mtp",), 2), ("psgd_decompress", ("psgd_decompress",), 10))
+    for name, tags, per_elem in sweeps:
+        kms = sum(st[t][1] for t in tags if t in st)
+        if kms > 0:
+            rate = elems * per_elem * calls / (kms * 1e-3) / 1e9
+            out[name] = {"ms_per_call": round(kms / calls, 4), "GB/s": round(rate, 1),
+                         "frac_hbm": round(rate / PEAK_HBM, 4), "bytes_per_elem": per_elem}
+    out["kernels"] = {k: {"launches_per_call": n / calls, "ms_per_call": round(v / calls, 4)}
+                      for k, (n, v) in sorted(st.items())}
+    del state, outs
+    torch.cuda.empty_cache()
     return out
 
 

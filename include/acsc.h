@@ -294,6 +294,57 @@ int sc_correct_adamw_batched(int count, const sc_matrix *mats, const sc_adamw_st
                              acsc_dtype dt, int r, float alpha, const sc_adamw_hparams *hp,
                              float *norm_out, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * PowerSGD compressor with error feedback, one worker's share (the
+ * data-parallel side the method is paired with: Sec. 3.3, Sec. 5 setup,
+ * App. J family F3; Vogels, Karimireddy & Jaggi 2019, rank-r compression
+ * and error-feedback SGD).  One step on a matrix:
+ *   psgd_project:      M = G + E (stored in E);  P = M Q
+ *   (across workers:   P <- mean of P over the workers)
+ *   psgd_orthogonalize: P <- orth(P) (Gram-Schmidt order, here CholeskyQR2);
+ *                      Q <- M^T P
+ *   (across workers:   Q <- mean of Q over the workers)
+ *   psgd_decompress:   out = P Q^T (in dt);  E <- M - out
+ * On one worker the means are the identity and psgd_step runs the three
+ * phases.  Q carries over to the next step (warm start); the caller draws
+ * the first Q (e.g. Gaussian) and zeroes E once.  The factors of a matrix
+ * are m r + n r numbers against m n: rank r = floor(m n / (64 (m + n)))
+ * compresses by at least x64.
+ * ---------------------------------------------------------------------- */
+typedef struct psgd_matrix {
+    const void *G;    /* [m, n] gradient of dt, row-major; 16-byte aligned       */
+    float *E;         /* [m, n] fp32 memory, in/out; 16-byte aligned; holds M
+                         from psgd_project until psgd_decompress                 */
+    float *P;         /* [m, r] fp32: P = M Q (project), then P_hat (orthogonalize) */
+    float *Q;         /* [n, r] fp32: previous Q (project), then M^T P_hat          */
+    void *out;        /* [m, n] of dt: the decompressed gradient; may equal G      */
+    int m, n;
+    void *ws;         /* device workspace (256-byte aligned); carries the bf16
+                         copy of M from psgd_project to psgd_orthogonalize: keep
+                         it for this matrix in between                            */
+    size_t ws_bytes;  /* >= psgd_workspace_size(m, n, r, dt)                      */
+} psgd_matrix;
+
+/* Bytes of workspace a psgd call needs for one m x n matrix at rank r.
+ * Requires 1 <= r <= min(m, n, SC_KMAX). */
+int psgd_workspace_size(int m, int n, int r, acsc_dtype dt, size_t *bytes);
+
+/* The phases and the whole step over mats[0 .. count-1] (shared dt and r).
+ * Arithmetic: fp32 memory and accumulation; for bf16 G the two projections
+ * run on bf16 matrix cores from a bf16 copy of M and of the thin factor, the
+ * Gram matrices of CholeskyQR2 in fp64, and out = bf16(P Q^T) from bf16 P
+ * and Q; for fp32 G everything stays fp32.  E is taken against out as
+ * stored, so what out loses to rounding is carried to the next step.  A
+ * column of P that is numerically dependent on the earlier ones (Cholesky
+ * pivot at or below 1e-15 r times the largest diagonal of P^T P) becomes
+ * zero, as does the matching column of Q.  Matrices must not share any
+ * buffer or workspace; all arguments are checked before anything is
+ * enqueued; errors as elsewhere. */
+int psgd_project(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream);
+int psgd_orthogonalize(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream);
+int psgd_decompress(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream);
+int psgd_step(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -56,6 +56,13 @@ class AdamwHparams(C.Structure):
                 ("weight_decay", C.c_float), ("step", C.c_int64), ("max_norm", C.c_float)]
 
 
+class PsgdMatrix(C.Structure):
+    """psgd_matrix: one matrix of a PowerSGD call."""
+    _fields_ = [("G", C.c_void_p), ("E", C.c_void_p), ("P", C.c_void_p), ("Q", C.c_void_p),
+                ("out", C.c_void_p), ("m", C.c_int), ("n", C.c_int), ("ws", C.c_void_p),
+                ("ws_bytes", C.c_size_t)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -94,6 +101,12 @@ def _load():
     lib.sc_correct_adamw_batched.restype = i32
     lib.sc_correct_adamw_batched.argtypes = [i32, C.POINTER(ScMatrix), C.POINTER(AdamwState), i32, i32, f32,
                                              C.POINTER(AdamwHparams), vp, vp]
+    lib.psgd_workspace_size.restype = i32
+    lib.psgd_workspace_size.argtypes = [i32, i32, i32, i32, C.POINTER(sz)]
+    for name in ("psgd_project", "psgd_orthogonalize", "psgd_decompress", "psgd_step"):
+        fn = getattr(lib, name)
+        fn.restype = i32
+        fn.argtypes = [i32, C.POINTER(PsgdMatrix), i32, i32, vp]
     lib.acsc_stats_enable.restype = i32
     lib.acsc_stats_enable.argtypes = [i32]
     lib.acsc_stats_read.restype = i32
@@ -107,7 +120,8 @@ EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
             "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched",
             "sc_adamw_workspace_size", "sc_correct_adamw_batched",
-            "ac_bern_mask", "ac_bern_pack", "ac_bern_unpack")
+            "ac_bern_mask", "ac_bern_pack", "ac_bern_unpack",
+            "psgd_workspace_size", "psgd_project", "psgd_orthogonalize", "psgd_decompress", "psgd_step")
 
 
 def _check(rc: int):
@@ -384,3 +398,51 @@ def sc_correct_adamw_batched(items, r: int, alpha: float, lr: float, beta1: floa
     code = BF16 if dtype == torch.bfloat16 else F32
     _check(lib.sc_correct_adamw_batched(len(items), arr, st, code, r, float(alpha), C.byref(hp),
                                         _ptr(norm_out), _stream(stream)))
+
+
+def psgd_workspace_size(m: int, n: int, r: int, dtype: torch.dtype) -> int:
+    b = C.c_size_t(0)
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(lib.psgd_workspace_size(m, n, r, code, C.byref(b)))
+    return b.value
+
+
+def psgd_workspace(m: int, n: int, r: int, dtype: torch.dtype, device="cuda"):
+    return torch.empty(max(psgd_workspace_size(m, n, r, dtype), 256), dtype=torch.uint8, device=device)
+
+
+def _psgd(name: str, items, r: int, dtype: torch.dtype, stream):
+    arr = (PsgdMatrix * max(len(items), 1))()
+    keep = []
+    for i, it in enumerate(items):
+        G, E, P, Q, out, ws = _in(it.get("G")), it["E"], it["P"], it["Q"], it.get("out"), it["ws"]
+        _need_cuda(G, E, P, Q, out, ws)
+        _out(E, P, Q, out)
+        for t, shape in ((E, None), (P, (E.shape[0], r)), (Q, (E.shape[1], r))):
+            if t.dtype != torch.float32 or (shape is not None and tuple(t.shape) != shape):
+                raise AcscError(ACSC_EINVAL, "E [m, n], P [m, r], Q [n, r] must be fp32")
+        keep.append(G)
+        m, n = E.shape
+        arr[i] = PsgdMatrix(_p(G), _p(E), _p(P), _p(Q), _p(out), m, n, _p(ws), ws.numel())
+    code = BF16 if dtype == torch.bfloat16 else F32
+    _check(getattr(lib, name)(len(items), arr, code, r, _stream(stream)))
+
+
+def psgd_project(items, r: int, dtype: torch.dtype = torch.bfloat16, stream=None):
+    """items: dicts with G, E, P, Q, ws (out unused): E <- E + G, P <- E Q."""
+    _psgd("psgd_project", items, r, dtype, stream)
+
+
+def psgd_orthogonalize(items, r: int, dtype: torch.dtype = torch.bfloat16, stream=None):
+    """P <- orth(P), Q <- M^T P (M held in E and in the workspace)."""
+    _psgd("psgd_orthogonalize", items, r, dtype, stream)
+
+
+def psgd_decompress(items, r: int, dtype: torch.dtype = torch.bfloat16, stream=None):
+    """out <- P Q^T (in dtype), E <- M - out."""
+    _psgd("psgd_decompress", items, r, dtype, stream)
+
+
+def psgd_step(items, r: int, dtype: torch.dtype = torch.bfloat16, stream=None):
+    """The three phases on one worker (items: dicts with G, E, P, Q, out, ws)."""
+    _psgd("psgd_step", items, r, dtype, stream)

@@ -38,6 +38,7 @@ struct Job {
     int m, n;
     const uint16_t *P, *V;
     float *W, *m1, *m2;
+    float *E;
     int vec;
 };
 struct Batch {
@@ -58,11 +59,14 @@ __device__ __forceinline__ void sync_lds()
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// ADAM: the blended values are not stored; they are the gradient of the
-// AdamW step applied to the tile's weights and moments (fp32, in place).
-template <int RP, bool VEC, bool ADAM>
+// MODE kAdam: the blended values are not stored; they are the gradient of
+// the AdamW step applied to the tile's weights and moments (fp32, in place).
+// MODE kFeedback: no G; out = P V^T, and the fp32 memory E (holding M) takes
+// M - out, with out as stored (bf16).
+template <int RP, bool VEC, int MODE>
 __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha, const AdamArgs ad)
 {
+    constexpr bool ADAM = MODE == kAdam, EF = MODE == kFeedback;
     constexpr int RB = RP * 2;                  // bytes per P / V row
     constexpr int SLICE = kT * RB;              // bytes of one 128-row slice
     constexpr int NI = 2 * SLICE / 1024;        // DMA instructions for P and V
@@ -109,10 +113,25 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
     // VEC: exactly eight 16-byte loads per thread (row and column clamped into
     // G; what lies outside is never stored), so that "at most eight loads
     // outstanding" below means every slice DMA has landed.  Otherwise element
-    // loads, and the wait is for everything.
+    // loads, and the wait is for everything.  kFeedback: the same for the
+    // fp32 memory, sixteen 16-byte loads per thread.
     uint4 g[8];
+    nf4 ev[16];
+    if constexpr (EF) {
+        if (VEC) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < 8; ++u) {
+                const int q = tid + 256 * u;
+                const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
+                const nf4 *src = reinterpret_cast<const nf4 *>(J.E + static_cast<int64_t>(min(gi, m - 1)) * n +
+                                                               min(gj, n - 8));
+                ev[2 * u] = __builtin_nontemporal_load(src);
+                ev[2 * u + 1] = __builtin_nontemporal_load(src + 1);
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 8 && !EF; ++u) {
         const int q = tid + 256 * u;
         const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
         if (VEC) {
@@ -133,7 +152,9 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
             g[u] = v;
         }
     }
-    if (VEC)
+    if (VEC && EF)
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    else if (VEC)
         asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     else
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -186,6 +207,48 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
             }
     sync_lds();
     const float oma = 1.0f - alpha;
+    if constexpr (EF) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int q = tid + 256 * u;
+            const int rr = q >> 4, c8 = (q & 15) * 8;
+            const int gi = row0 + rr, gj = col0 + c8;
+            if (gi >= m)
+                continue;
+            const float4 p0 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8]);
+            const float4 p1 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8 + 4]);
+            const float pf[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+            uint16_t ob[8];
+            float of[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                ob[e] = f32_to_bf16(pf[e]);
+                of[e] = __uint_as_float(static_cast<uint32_t>(ob[e]) << 16);
+            }
+            const int64_t o = static_cast<int64_t>(gi) * n + gj;
+            if (VEC && gj + 8 <= n) {
+                nf4 e0 = ev[2 * u], e1 = ev[2 * u + 1];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    e0[e] = e0[e] - of[e];
+                    e1[e] = e1[e] - of[4 + e];
+                }
+                const nu4 ov{static_cast<uint32_t>(ob[0]) | (static_cast<uint32_t>(ob[1]) << 16),
+                             static_cast<uint32_t>(ob[2]) | (static_cast<uint32_t>(ob[3]) << 16),
+                             static_cast<uint32_t>(ob[4]) | (static_cast<uint32_t>(ob[5]) << 16),
+                             static_cast<uint32_t>(ob[6]) | (static_cast<uint32_t>(ob[7]) << 16)};
+                __builtin_nontemporal_store(ov, reinterpret_cast<nu4 *>(J.out + o));
+                __builtin_nontemporal_store(e0, reinterpret_cast<nf4 *>(J.E + o));
+                __builtin_nontemporal_store(e1, reinterpret_cast<nf4 *>(J.E + o) + 1);
+            } else {
+                for (int e = 0; e < 8 && gj + e < n; ++e) {
+                    J.out[o + e] = ob[e];
+                    J.E[o + e] = J.E[o + e] - of[e];
+                }
+            }
+        }
+        return;
+    }
     if constexpr (ADAM) {
         const float cf = *ad.coef;
 #pragma unroll
@@ -272,7 +335,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
     }
 }
 
-template <int RP, bool ADAM>
+template <int RP, int MODE>
 void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float alpha, const AdamArgs &ad,
                hipStream_t st)
 {
@@ -286,13 +349,50 @@ void launch_rp(const char *tag, const std::vector<Job> &jobs, int tiles, float a
             for (int i = 0; i < b.count; ++i)
                 b.j[i] = part[v][c0 + i];
             if (v) {
-                auto kern = blend_kernel<RP, true, ADAM>;
+                auto kern = blend_kernel<RP, true, MODE>;
                 ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha, ad);
             } else {
-                auto kern = blend_kernel<RP, false, ADAM>;
+                auto kern = blend_kernel<RP, false, MODE>;
                 ACSC_LAUNCH(tag, kern, dim3(tiles, 1, b.count), dim3(256), 0, st, b, alpha, ad);
             }
         }
+}
+
+template <int MODE>
+void launch_mode(const char *tag, int RP, const std::vector<Job> &jobs, int tiles, float alpha, const AdamArgs &ad,
+                 hipStream_t st)
+{
+    switch (RP) {
+    case 64: launch_rp<64, MODE>(tag, jobs, tiles, alpha, ad, st); break;
+    case 128: launch_rp<128, MODE>(tag, jobs, tiles, alpha, ad, st); break;
+    default: launch_rp<192, MODE>(tag, jobs, tiles, alpha, ad, st); break;
+    }
+}
+
+int launch_all(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st,
+               const AdamArgs *adam, bool feedback)
+{
+    if (!supported(RP))
+        return set_error(ACSC_EINVAL, "blend: padded rank %d not handled by the streamed-tile kernel", RP);
+    std::vector<Job> jobs;
+    int tiles = 1;
+    auto a16 = [](const void *p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+    for (const Req &q : reqs) {
+        bool vec = q.n % 8 == 0 && q.n >= 8 && (feedback ? a16(q.E) : a16(q.G));
+        vec = vec && (adam ? a16(q.W) && a16(q.m1) && a16(q.m2) : a16(q.out));
+        jobs.push_back(Job{q.G, q.out, q.m, q.n, q.P, q.V, q.W, q.m1, q.m2, q.E, vec ? 1 : 0});
+        const int64_t rbn = cdiv(q.m, kT), cbn = cdiv(q.n, kT);
+        tiles = std::max<int>(tiles, static_cast<int>(cdiv(rbn, 8) * 8 * cbn));
+    }
+    const AdamArgs none{};
+    const AdamArgs &ad = adam ? *adam : none;
+    if (feedback)
+        launch_mode<kFeedback>(tag, RP, jobs, tiles, alpha, ad, st);
+    else if (adam)
+        launch_mode<kAdam>(tag, RP, jobs, tiles, alpha, ad, st);
+    else
+        launch_mode<kPlain>(tag, RP, jobs, tiles, alpha, ad, st);
+    return ACSC_OK;
 }
 
 }  // namespace
@@ -301,26 +401,12 @@ bool supported(int RP) { return RP == 64 || RP == 128 || RP == 192; }
 
 int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st, const AdamArgs *adam)
 {
-    if (!supported(RP))
-        return set_error(ACSC_EINVAL, "blend: padded rank %d not handled by the streamed-tile kernel", RP);
-    std::vector<Job> jobs;
-    int tiles = 1;
-    auto a16 = [](const void *p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
-    for (const Req &q : reqs) {
-        bool vec = q.n % 8 == 0 && q.n >= 8 && a16(q.G);
-        vec = vec && (adam ? a16(q.W) && a16(q.m1) && a16(q.m2) : a16(q.out));
-        jobs.push_back(Job{q.G, q.out, q.m, q.n, q.P, q.V, q.W, q.m1, q.m2, vec ? 1 : 0});
-        const int64_t rbn = cdiv(q.m, kT), cbn = cdiv(q.n, kT);
-        tiles = std::max<int>(tiles, static_cast<int>(cdiv(rbn, 8) * 8 * cbn));
-    }
-    const AdamArgs none{};
-    const AdamArgs &ad = adam ? *adam : none;
-    switch (RP) {
-    case 64: adam ? launch_rp<64, true>(tag, jobs, tiles, alpha, ad, st) : launch_rp<64, false>(tag, jobs, tiles, alpha, ad, st); break;
-    case 128: adam ? launch_rp<128, true>(tag, jobs, tiles, alpha, ad, st) : launch_rp<128, false>(tag, jobs, tiles, alpha, ad, st); break;
-    default: adam ? launch_rp<192, true>(tag, jobs, tiles, alpha, ad, st) : launch_rp<192, false>(tag, jobs, tiles, alpha, ad, st); break;
-    }
-    return ACSC_OK;
+    return launch_all(tag, reqs, RP, alpha, st, adam, false);
+}
+
+int run_feedback(const char *tag, const std::vector<Req> &reqs, int RP, hipStream_t st)
+{
+    return launch_all(tag, reqs, RP, 0.0f, st, nullptr, true);
 }
 
 }  // namespace blend

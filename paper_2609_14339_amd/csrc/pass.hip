@@ -806,14 +806,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 template <int NT>
-void ema_launch(const char *tag, const std::vector<EmaJob> &jobs, int gx, int np, float beta, hipStream_t st)
+void ema_launch(const char *tag, const std::vector<EmaJob> &jobs, int gx, int np, float a, float b_coef, hipStream_t st)
 {
     for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
         EmaBatch b{};
         b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
         for (int i = 0; i < b.count; ++i)
             b.j[i] = jobs[c0 + i];
-        ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(gx, 1, b.count), dim3(512), 0, st, b, np, beta, 1.0f - beta);
+        ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(gx, 1, b.count), dim3(512), 0, st, b, np, a, b_coef);
     }
 }
 
@@ -906,7 +906,7 @@ bool ema_fusable(const std::vector<EmaReq> &reqs)
     return blocks >= 256;
 }
 
-int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float beta, hipStream_t st)
+int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, hipStream_t st)
 {
     if (!ema_fusable(reqs))
         return set_error(ACSC_EINVAL, "fused EMA pass: operands not aligned or batch too small");
@@ -925,12 +925,12 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float beta, hipStr
         gx = std::max(gx, nb);
     }
     switch ((NP / 16 + 1) / 2) {   // column tiles in pairs; tiles past NP read zeros
-    case 1: ema_launch<2>(tag, jobs, gx, NP, beta, st); break;
-    case 2: ema_launch<4>(tag, jobs, gx, NP, beta, st); break;
-    case 3: ema_launch<6>(tag, jobs, gx, NP, beta, st); break;
-    case 4: ema_launch<8>(tag, jobs, gx, NP, beta, st); break;
-    case 5: ema_launch<10>(tag, jobs, gx, NP, beta, st); break;
-    default: ema_launch<12>(tag, jobs, gx, NP, beta, st); break;
+    case 1: ema_launch<2>(tag, jobs, gx, NP, a, b, st); break;
+    case 2: ema_launch<4>(tag, jobs, gx, NP, a, b, st); break;
+    case 3: ema_launch<6>(tag, jobs, gx, NP, a, b, st); break;
+    case 4: ema_launch<8>(tag, jobs, gx, NP, a, b, st); break;
+    case 5: ema_launch<10>(tag, jobs, gx, NP, a, b, st); break;
+    default: ema_launch<12>(tag, jobs, gx, NP, a, b, st); break;
     }
     return ACSC_OK;
 }

@@ -1114,6 +1114,7 @@ struct BlendJob {
     int m, n;
     const GT *P, *Vc;
     float *W, *m1, *m2;   // corrected AdamW: fp32 weights and moments, in place
+    float *E;             // error feedback: fp32 memory (holds M), takes M - out
 };
 
 // Element (row, col) of G_proj = gp: stored, or (ADAM) the gradient of the
@@ -1133,10 +1134,11 @@ __device__ __forceinline__ void blend_out(const BlendJob<GT> &J, int64_t o, floa
     }
 }
 
-template <typename GT, bool ADAM>
+template <typename GT, int MODE>
 __global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb, int RP, float alpha,
                                                     const blend::AdamArgs ad)
 {
+    constexpr bool ADAM = MODE == blend::kAdam;
     const BlendJob<GT> &J = jb.j[blockIdx.z];
     const GT *G = J.G;
     const int m = J.m, n = J.n;
@@ -1207,8 +1209,15 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb
                 const int row = row0 + wr * 32 + a * 16 + (lane >> 4) * 4 + e;
                 if (row < m && col < n) {
                     const int64_t o = static_cast<int64_t>(row) * n + col;
-                    const float g = to_f32<GT>(G[o]);
-                    blend_out<ADAM>(J, o, alpha * g + oma * acc[a][b][e], cf, ad);
+                    if constexpr (MODE == blend::kFeedback) {
+                        // out = P V^T as stored; the memory takes M - out
+                        const GT ov = from_f32<GT>(acc[a][b][e]);
+                        J.out[o] = ov;
+                        J.E[o] = J.E[o] - to_f32<GT>(ov);
+                    } else {
+                        const float g = to_f32<GT>(G[o]);
+                        blend_out<ADAM>(J, o, alpha * g + oma * acc[a][b][e], cf, ad);
+                    }
                 }
             }
         }
@@ -1808,7 +1817,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
             return ACSC_OK;
         }
     };
-    int rc = fused ? pass::ema_run("sc_ema", er, beta, st) : pass(true);
+    int rc = fused ? pass::ema_run("sc_ema", er, beta, omb, st) : pass(true);
     if (rc)
         return rc;
     if ((rc = orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st)))
@@ -1992,7 +2001,7 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st, cons
             bj.push_back(BlendJob<GT>{static_cast<const GT *>(m.in->G), static_cast<GT *>(m.in->G_proj), m.D.m, m.D.n,
                                       static_cast<const GT *>(m.cw.Pc), static_cast<const GT *>(m.cw.Vc),
                                       m.ad ? m.ad->W : nullptr, m.ad ? m.ad->m1 : nullptr,
-                                      m.ad ? m.ad->m2 : nullptr});
+                                      m.ad ? m.ad->m2 : nullptr, nullptr});
             gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, 64)));
             gy = std::max<int>(gy, static_cast<int>(cdiv(m.D.m, 64)));
         }
@@ -2003,7 +2012,7 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st, cons
                     q.push_back(blend::Req{static_cast<const uint16_t *>(m.in->G), static_cast<uint16_t *>(m.in->G_proj),
                                            m.D.m, m.D.n, static_cast<const uint16_t *>(m.cw.Pc),
                                            static_cast<const uint16_t *>(m.cw.Vc), m.ad ? m.ad->W : nullptr,
-                                           m.ad ? m.ad->m1 : nullptr, m.ad ? m.ad->m2 : nullptr});
+                                           m.ad ? m.ad->m1 : nullptr, m.ad ? m.ad->m2 : nullptr, nullptr});
                 return blend::run(btag, q, RP, alpha, st, adam ? &ad : nullptr);
             }
             // 128 x 128 tiles, XCD-aware order (see blend16_kernel)
@@ -2030,9 +2039,9 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st, cons
             const size_t pitch = RP + 1;
             const size_t blds = 2 * 64 * pitch * sizeof(GT);
             if (adam)
-                launch_jobs(btag, blend_kernel<GT, true>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha, ad);
+                launch_jobs(btag, blend_kernel<GT, blend::kAdam>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha, ad);
             else
-                launch_jobs(btag, blend_kernel<GT, false>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha, ad);
+                launch_jobs(btag, blend_kernel<GT, blend::kPlain>, bj, dim3(gx, gy), dim3(256), blds, st, RP, alpha, ad);
         }
     }
     return ACSC_OK;
@@ -2062,6 +2071,292 @@ int check_matrix(const sc_matrix &a, int r, int oversample, acsc_dtype dt, bool 
                        "G, G_proj must be element-aligned");
     }
     return ACSC_OK;
+}
+
+// ---------------------------------------------------------------------------
+// PowerSGD compressor with error feedback (the data-parallel compressor the
+// method is paired with; rank-r step of Vogels et al. 2019):
+//   project:        M = G + E (into E) and P = M Q, one sweep over M (the
+//                   fused EMA pass with coefficients 1, 1, which also writes
+//                   the bf16 copy of M the second projection reads)
+//   orthogonalize:  P_hat = CholeskyQR2(P), Q' = M^T P_hat
+//   decompress:     out = P_hat Q'^T and E = M - out, one sweep over E (the
+//                   streamed-tile product with the feedback epilogue)
+// The phases meet through the caller's P [m, r] and Q [n, r], so that a
+// data-parallel caller can average them between the phases.
+// ---------------------------------------------------------------------------
+
+// dst [rows, cols] (row stride cols) = the first cols columns of src (row stride lds).
+struct CropJob {
+    const float *src;
+    int64_t lds;
+    float *dst;
+    int rows, cols;
+};
+
+__global__ __launch_bounds__(256) void crop_kernel(const Batch<CropJob> jb)
+{
+    const CropJob &J = jb.j[blockIdx.z];
+    const int64_t total = static_cast<int64_t>(J.rows) * J.cols;
+    for (int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+         idx += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t i = idx / J.cols;
+        const int c = static_cast<int>(idx - i * J.cols);
+        J.dst[idx] = J.src[i * J.lds + c];
+    }
+}
+
+// Padded rank of the decompression: the streamed-tile widths for bf16.
+int psgd_rp(int r, bool use16)
+{
+    if (!use16)
+        return static_cast<int>(round_up(r, 32));
+    return r <= 64 ? 64 : (r <= 128 ? 128 : 192);
+}
+
+struct PsgdWs {
+    PriorWs pw;     // M16, Zt16 (Q^T bf16), Y (P, P_hat), Yt16 (P_hat^T bf16), Z (Q'), part, T, gram
+    void *Pc, *Vc;  // decompression factors [m, RPd], [n, RPd] in the compute type
+    int RPd;
+};
+
+size_t carve_psgd(const Dims &d, acsc_dtype dt, void *base, PsgdWs *w)
+{
+    const bool use16 = dt == ACSC_BF16;
+    PsgdWs t;
+    Carve c(base);
+    c.off = carve_prior(d, use16, base, &t.pw);
+    t.RPd = psgd_rp(d.r, use16);
+    const size_t es = dtype_size(dt);
+    t.Pc = c.take<unsigned char>(static_cast<size_t>(d.m) * t.RPd * es);
+    t.Vc = c.take<unsigned char>(static_cast<size_t>(d.n) * t.RPd * es);
+    if (w)
+        *w = t;
+    return c.off;
+}
+
+struct PsgdItem {
+    const psgd_matrix *in;
+    Mat mat;   // dims and the CholeskyQR2 buffers (mat.pw == w.pw)
+    PsgdWs w;
+};
+
+void crop(const char *tag, const std::vector<CropJob> &jobs, hipStream_t st)
+{
+    int64_t tot = 1;
+    for (const CropJob &j : jobs)
+        tot = std::max<int64_t>(tot, static_cast<int64_t>(j.rows) * j.cols);
+    launch_jobs(tag, crop_kernel, jobs, dim3(grid1d(tot)), dim3(256), 0, st);
+}
+
+int psgd_project_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStream_t st)
+{
+    const int KP = it[0].mat.D.KP;
+    if (use16) {
+        // Q^T in bf16, rows r .. KP-1 zero: the thin factor of the pass
+        std::vector<TileJob> tj;
+        int gx = 1;
+        for (auto &x : it) {
+            tj.push_back(TileJob{x.in->Q, r, x.in->n, r, KP, x.w.pw.Zt16, x.w.pw.ldz16, nullptr, nullptr, 0, 0});
+            gx = std::max<int>(gx, static_cast<int>(cdiv(x.in->n, kTileRows)));
+        }
+        launch_jobs("psgd_qconvert", tile_bf16_kernel, tj, dim3(gx), dim3(256), 0, st);
+        std::vector<pass::EmaReq> er;
+        for (auto &x : it)
+            er.push_back(pass::EmaReq{x.in->E, static_cast<const uint16_t *>(x.in->G), x.w.pw.M16, x.w.pw.Zt16,
+                                      x.w.pw.ldz16, x.w.pw.Y, KP, x.in->m, x.in->n, KP});
+        if (pass::ema_fusable(er)) {
+            if (int rc = pass::ema_run("psgd_feedback_mq", er, 1.0f, 1.0f, st))
+                return rc;
+        } else {
+            std::vector<EmaJob<uint16_t>> j;
+            std::vector<pass::Req> q;
+            int64_t tot = 1;
+            for (auto &x : it) {
+                j.push_back(EmaJob<uint16_t>{x.in->E, static_cast<const uint16_t *>(x.in->G), x.in->m, x.in->n,
+                                             (x.in->n % 8) == 0 ? 1 : 0, x.w.pw.M16, x.w.pw.ld16});
+                tot = std::max<int64_t>(tot, static_cast<int64_t>(x.in->m) * cdiv(x.in->n, 8));
+                q.push_back(pass::Req{x.w.pw.M16, x.w.pw.ld16, true, x.w.pw.Zt16, x.w.pw.ldz16, x.w.pw.Y, KP,
+                                      x.in->m, x.in->n, KP, x.w.pw.part});
+            }
+            launch_jobs("psgd_feedback", ema_shadow_kernel<uint16_t>, j, dim3(grid1d(tot)), dim3(256), 0, st, 1.0f,
+                        1.0f);
+            if (int rc = pass::run("psgd_pass_mq", false, q, st))
+                return rc;
+        }
+    } else {
+        std::vector<PadJob<float>> pj;
+        std::vector<Ema32Job<float>> ej;
+        std::vector<GemmReq<float, float>> q;
+        int64_t tp = 1, te = 1;
+        for (auto &x : it) {
+            pj.push_back(PadJob<float>{x.in->Q, x.in->n, x.w.pw.Z});
+            tp = std::max<int64_t>(tp, static_cast<int64_t>(x.in->n) * KP);
+            const int64_t c = static_cast<int64_t>(x.in->m) * x.in->n;
+            ej.push_back(Ema32Job<float>{x.in->E, static_cast<const float *>(x.in->G), c});
+            te = std::max(te, cdiv(c, 4));
+            q.push_back(GemmReq<float, float>{x.in->E, x.in->n, x.w.pw.Z, KP, x.w.pw.Y, KP, x.in->m, x.in->n, r, KP,
+                                              x.w.pw.part, nullptr, 0});
+        }
+        launch_jobs("psgd_qconvert", pad_convert_kernel<float>, pj, dim3(grid1d(tp)), dim3(256), 0, st, r, KP);
+        launch_jobs("psgd_feedback", ema_kernel<float>, ej, dim3(grid1d(te)), dim3(256), 0, st, 1.0f, 1.0f);
+        tall_gemm<float, false, float>("psgd_pass_mq", q, st);
+    }
+    std::vector<CropJob> cj;
+    for (auto &x : it)
+        cj.push_back(CropJob{x.w.pw.Y, KP, x.in->P, x.in->m, r});
+    crop("psgd_crop", cj, st);
+    return ACSC_OK;
+}
+
+int psgd_orthogonalize_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStream_t st)
+{
+    const int KP = it[0].mat.D.KP;
+    {
+        std::vector<PadJob<float>> pj;
+        int64_t tp = 1;
+        for (auto &x : it) {
+            pj.push_back(PadJob<float>{x.in->P, x.in->m, x.w.pw.Y});
+            tp = std::max<int64_t>(tp, static_cast<int64_t>(x.in->m) * KP);
+        }
+        launch_jobs("psgd_pconvert", pad_convert_kernel<float>, pj, dim3(grid1d(tp)), dim3(256), 0, st, r, KP);
+    }
+    std::vector<Mat> ms;
+    for (auto &x : it)
+        ms.push_back(x.mat);
+    // CholeskyQR2: Y <- P_hat (fp32), and its bf16 transposed copy for the pass
+    if (int rc = orthonormalise(ms, true, 2, use16, st))
+        return rc;
+    std::vector<CropJob> cj;
+    for (auto &x : it)
+        cj.push_back(CropJob{x.w.pw.Y, KP, x.in->P, x.in->m, r});
+    crop("psgd_crop", cj, st);
+    if (use16) {
+        std::vector<pass::Req> q;
+        for (auto &x : it)
+            q.push_back(pass::Req{x.w.pw.M16, x.w.pw.ld16, true, x.w.pw.Yt16, x.w.pw.ldy16, x.w.pw.Z, KP, x.in->n,
+                                  x.in->m, KP, x.w.pw.part});
+        if (int rc = pass::run("psgd_pass_mtp", true, q, st))
+            return rc;
+    } else {
+        std::vector<GemmReq<float, float>> q;
+        for (auto &x : it)
+            q.push_back(GemmReq<float, float>{x.in->E, x.in->n, x.w.pw.Y, KP, x.w.pw.Z, KP, x.in->n, x.in->m, r, KP,
+                                              x.w.pw.part, nullptr, 0});
+        tall_gemm<float, true, float>("psgd_pass_mtp", q, st);
+    }
+    cj.clear();
+    for (auto &x : it)
+        cj.push_back(CropJob{x.w.pw.Z, KP, x.in->Q, x.in->n, r});
+    crop("psgd_crop", cj, st);
+    return ACSC_OK;
+}
+
+int psgd_decompress_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStream_t st)
+{
+    const int RPd = it[0].w.RPd;
+    if (use16) {
+        std::vector<TileJob> tj;
+        std::vector<blend::Req> q;
+        int gx = 1;
+        for (auto &x : it) {
+            tj.push_back(TileJob{x.in->P, r, x.in->m, r, RPd, nullptr, 0, static_cast<uint16_t *>(x.w.Pc), nullptr, 0,
+                                 0});
+            tj.push_back(TileJob{x.in->Q, r, x.in->n, r, RPd, nullptr, 0, static_cast<uint16_t *>(x.w.Vc), nullptr, 0,
+                                 0});
+            gx = std::max<int>(gx, static_cast<int>(cdiv(std::max(x.in->m, x.in->n), kTileRows)));
+            q.push_back(blend::Req{nullptr, static_cast<uint16_t *>(x.in->out), x.in->m, x.in->n,
+                                   static_cast<const uint16_t *>(x.w.Pc), static_cast<const uint16_t *>(x.w.Vc),
+                                   nullptr, nullptr, nullptr, x.in->E});
+        }
+        launch_jobs("psgd_fconvert", tile_bf16_kernel, tj, dim3(gx), dim3(256), 0, st);
+        return blend::run_feedback("psgd_decompress", q, RPd, st);
+    }
+    std::vector<PadJob<float>> pj;
+    std::vector<BlendJob<float>> bj;
+    int64_t tp = 1;
+    int gx = 1, gy = 1;
+    for (auto &x : it) {
+        pj.push_back(PadJob<float>{x.in->P, x.in->m, static_cast<float *>(x.w.Pc)});
+        pj.push_back(PadJob<float>{x.in->Q, x.in->n, static_cast<float *>(x.w.Vc)});
+        tp = std::max<int64_t>(tp, static_cast<int64_t>(std::max(x.in->m, x.in->n)) * RPd);
+        bj.push_back(BlendJob<float>{nullptr, static_cast<float *>(x.in->out), x.in->m, x.in->n,
+                                     static_cast<const float *>(x.w.Pc), static_cast<const float *>(x.w.Vc), nullptr,
+                                     nullptr, nullptr, x.in->E});
+        gx = std::max<int>(gx, static_cast<int>(cdiv(x.in->n, 64)));
+        gy = std::max<int>(gy, static_cast<int>(cdiv(x.in->m, 64)));
+    }
+    launch_jobs("psgd_fconvert", pad_convert_kernel<float>, pj, dim3(grid1d(tp)), dim3(256), 0, st, r, RPd);
+    const size_t blds = 2 * 64 * static_cast<size_t>(RPd + 1) * sizeof(float);
+    launch_jobs("psgd_decompress", blend_kernel<float, blend::kFeedback>, bj, dim3(gx, gy), dim3(256), blds, st, RPd,
+                0.0f, blend::AdamArgs{});
+    return ACSC_OK;
+}
+
+int check_psgd(const psgd_matrix &a, int i, int r, acsc_dtype dt, int phase)
+{
+    ACSC_CHECK_ARG(a.m >= 1 && a.n >= 1, ACSC_EINVAL, "matrix %d: m=%d, n=%d must be >= 1", i, a.m, a.n);
+    ACSC_CHECK_ARG(r >= 1 && r <= std::min(std::min(a.m, a.n), kKMax), ACSC_EINVAL,
+                   "matrix %d: r=%d outside [1, min(m, n, %d)] for a %d x %d matrix", i, r, kKMax, a.m, a.n);
+    const Dims d = dims_of(a.m, a.n, r, 0);
+    const size_t need = carve_psgd(d, dt, nullptr, nullptr);
+    ACSC_CHECK_ARG(a.ws != nullptr && a.E && a.P && a.Q, ACSC_EINVAL, "matrix %d: null ws, E, P or Q", i);
+    ACSC_CHECK_ARG(a.ws_bytes >= need, ACSC_ENOSPC, "matrix %d: workspace %zu bytes < %zu needed", i, a.ws_bytes,
+                   need);
+    ACSC_CHECK_ARG(aligned(a.ws, 256), ACSC_EALIGN, "matrix %d: workspace must be 256-byte aligned", i);
+    ACSC_CHECK_ARG(aligned(a.E, 16), ACSC_EALIGN, "matrix %d: E must be 16-byte aligned", i);
+    ACSC_CHECK_ARG(aligned(a.P, 4) && aligned(a.Q, 4), ACSC_EALIGN, "matrix %d: P, Q must be 4-byte aligned", i);
+    if (phase == 0 || phase == 3) {
+        ACSC_CHECK_ARG(a.G != nullptr, ACSC_EINVAL, "matrix %d: G is NULL", i);
+        ACSC_CHECK_ARG(aligned(a.G, 16), ACSC_EALIGN, "matrix %d: G must be 16-byte aligned", i);
+    }
+    if (phase == 2 || phase == 3) {
+        ACSC_CHECK_ARG(a.out != nullptr, ACSC_EINVAL, "matrix %d: out is NULL", i);
+        ACSC_CHECK_ARG(aligned(a.out, dtype_size(dt)), ACSC_EALIGN, "matrix %d: out must be element-aligned", i);
+    }
+    return ACSC_OK;
+}
+
+// phase 0 project, 1 orthogonalize, 2 decompress, 3 all three
+int psgd_run(int count, const psgd_matrix *mats, acsc_dtype dt, int r, int phase, hipStream_t st)
+{
+    clear_error();
+    ACSC_CHECK_ARG(count >= 0, ACSC_EINVAL, "count=%d < 0", count);
+    ACSC_CHECK_ARG(count == 0 || mats != nullptr, ACSC_EINVAL, "mats is NULL");
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    std::vector<PsgdItem> it;
+    for (int i = 0; i < count; ++i) {
+        if (int rc = check_psgd(mats[i], i, r, dt, phase))
+            return rc;
+        PsgdItem x;
+        x.in = &mats[i];
+        x.mat.in = nullptr;
+        x.mat.D = dims_of(mats[i].m, mats[i].n, r, 0);
+        carve_psgd(x.mat.D, dt, mats[i].ws, &x.w);
+        x.mat.pw = x.w.pw;
+        x.mat.seed = 0;
+        it.push_back(x);
+    }
+    if (it.empty())
+        return ACSC_OK;
+    const bool use16 = dt == ACSC_BF16;
+    if (int rc = chol::prepare(it[0].mat.D.KP))
+        return rc;
+    if (!use16) {
+        const size_t blds = 2 * 64 * static_cast<size_t>(it[0].w.RPd + 1) * sizeof(float);
+        if (int rc = allow_lds(blend_kernel<float, blend::kFeedback>, blds))
+            return rc;
+    }
+    int rc = ACSC_OK;
+    if (phase == 0 || phase == 3)
+        rc = psgd_project_phase(it, use16, r, st);
+    if (!rc && (phase == 1 || phase == 3))
+        rc = psgd_orthogonalize_phase(it, use16, r, st);
+    if (!rc && (phase == 2 || phase == 3))
+        rc = psgd_decompress_phase(it, use16, r, st);
+    if (rc)
+        return rc;
+    return check_launch("psgd");
 }
 
 }  // namespace
@@ -2164,7 +2459,7 @@ extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype d
         return ACSC_OK;
     const size_t es = dtype_size(dt);
     const size_t blds = 2 * 64 * (all[0].D.RP + (dt == ACSC_BF16 ? 8 : 1)) * es;
-    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t, false>, blds) : allow_lds(blend_kernel<float, false>, blds);
+    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t, blend::kPlain>, blds) : allow_lds(blend_kernel<float, blend::kPlain>, blds);
     if (rc)
         return rc;
     if (dt == ACSC_BF16)
@@ -2229,7 +2524,7 @@ extern "C" int sc_correct_adamw_batched(int count, const sc_matrix *mats, const 
         return ACSC_OK;
     const size_t es = dtype_size(dt);
     const size_t blds = 2 * 64 * (all[0].D.RP + (dt == ACSC_BF16 ? 8 : 1)) * es;
-    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t, true>, blds) : allow_lds(blend_kernel<float, true>, blds);
+    int rc = dt == ACSC_BF16 ? allow_lds(blend_kernel<uint16_t, blend::kAdam>, blds) : allow_lds(blend_kernel<float, blend::kAdam>, blds);
     if (rc)
         return rc;
     // bias corrections and the step size in double on the host, then fp32
@@ -2294,4 +2589,36 @@ extern "C" int sc_correct(const void *G, acsc_dtype dt, int m, int n, const floa
     a.ws = ws;
     a.ws_bytes = ws_bytes;
     return sc_correct_batched(1, &a, dt, r, alpha, stream);
+}
+
+extern "C" int psgd_workspace_size(int m, int n, int r, acsc_dtype dt, size_t *bytes)
+{
+    clear_error();
+    ACSC_CHECK_ARG(bytes != nullptr, ACSC_EINVAL, "bytes is NULL");
+    ACSC_CHECK_ARG(dt == ACSC_F32 || dt == ACSC_BF16, ACSC_EDTYPE, "unknown dtype %d", (int)dt);
+    ACSC_CHECK_ARG(m >= 1 && n >= 1, ACSC_EINVAL, "m=%d, n=%d must be >= 1", m, n);
+    ACSC_CHECK_ARG(r >= 1 && r <= std::min(std::min(m, n), kKMax), ACSC_EINVAL,
+                   "r=%d outside [1, min(m, n, %d)]", r, kKMax);
+    *bytes = carve_psgd(dims_of(m, n, r, 0), dt, nullptr, nullptr);
+    return ACSC_OK;
+}
+
+extern "C" int psgd_project(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream)
+{
+    return psgd_run(count, mats, dt, r, 0, stream);
+}
+
+extern "C" int psgd_orthogonalize(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream)
+{
+    return psgd_run(count, mats, dt, r, 1, stream);
+}
+
+extern "C" int psgd_decompress(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream)
+{
+    return psgd_run(count, mats, dt, r, 2, stream);
+}
+
+extern "C" int psgd_step(int count, const psgd_matrix *mats, acsc_dtype dt, int r, hipStream_t stream)
+{
+    return psgd_run(count, mats, dt, r, 3, stream);
 }

@@ -1,7 +1,9 @@
 // Fused blend of the spectral correction (internal; not part of the ABI):
 //   out = alpha * G + (1 - alpha) * P V^T
 // with P = U X_f [m, RP] and V [n, RP] in bf16 (Sec. 3.2: G_proj = alpha G +
-// (1 - alpha) U X_f V^T, the filtered gradient never materialised).
+// (1 - alpha) U X_f V^T, the filtered gradient never materialised).  The same
+// streamed tiles serve the decompression of the data-parallel compressor
+// (out = P_hat Q^T with error feedback; see run_feedback).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -19,7 +21,12 @@ struct Req {
     const uint16_t *P;   // [m, RP] bf16
     const uint16_t *V;   // [n, RP] bf16
     float *W, *m1, *m2;  // AdamW epilogue: fp32 [m, n] weights and moments, in place
+    float *E;            // feedback epilogue: fp32 [m, n] memory, holds M, takes M - out
 };
+
+// What a tile's product feeds: the stored blend, the AdamW step, or the
+// decompression with error feedback.
+enum Epilogue { kPlain = 0, kAdam = 1, kFeedback = 2 };
 
 // Constants of the AdamW epilogue (Alg. 1 update; the optimiser of App. I):
 // with g = coef * G_proj,
@@ -50,6 +57,11 @@ bool supported(int RP);
 // G_proj is not stored and the requests' W, m1, m2 take the AdamW step.
 int run(const char *tag, const std::vector<Req> &reqs, int RP, float alpha, hipStream_t st,
         const AdamArgs *adam = nullptr);
+
+// Decompression with error feedback (the data-parallel compressor):
+//   out = bf16(P V^T),  E <- E - out  (E holds M on entry, fp32),
+// for every request (G unused; all share RP) on `st`.
+int run_feedback(const char *tag, const std::vector<Req> &reqs, int RP, hipStream_t st);
 
 }  // namespace blend
 }  // namespace acsc

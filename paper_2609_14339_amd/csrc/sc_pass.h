@@ -37,9 +37,10 @@ int max_splits(int64_t M, int64_t K);
 int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t st);
 
 // The anchor EMA fused with the first pass of the subspace iteration
-// (Sec. 3.2): M <- beta M + (1 - beta) G (G may be null: M is kept), the bf16
-// shadow M16 = bf16(M) written for the later passes, and C = M16 * B in the
-// same sweep over M, so that the first pass does not read the shadow back.
+// (Sec. 3.2): M <- a M + b G (the EMA: a = beta, b = 1 - beta; error
+// feedback: a = b = 1; G may be null: M is kept), the bf16 shadow
+// M16 = bf16(M) written for the later passes, and C = M16 * B in the same
+// sweep over M, so that the first pass does not read the shadow back.
 struct EmaReq {
     float *M;             // [m, n] fp32, row stride n
     const uint16_t *G;    // [m, n] bf16, or nullptr
@@ -56,7 +57,7 @@ struct EmaReq {
 // GPU without splitting K.
 bool ema_fusable(const std::vector<EmaReq> &reqs);
 
-int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float beta, hipStream_t st);
+int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, hipStream_t st);
 
 }  // namespace pass
 }  // namespace acsc

@@ -95,3 +95,45 @@ def test_pack_and_unpack_reject_bad_arguments_before_launch(lib):
     key0 = Key(seed=1, step=1, layer=0, microbatch=0, B=0, S=4, H=64)
     assert lib.ac_mask_pack(None, 1, 0, 64, 64, 4, C.byref(key0), None, None, None) == 0
     assert lib.ac_unpack_scatter(None, None, 1, 0, 64, 4, C.byref(key0), 1.0, None, 64, None) == 0
+
+
+def test_psgd_workspace_and_rejects_bad_arguments_before_launch(lib):
+    import paper_2609_14339_amd as pk
+    vp = C.c_void_p
+    b = C.c_size_t(0)
+    assert lib.psgd_workspace_size(8192, 28672, 99, 1, C.byref(b)) == 0
+    big = b.value
+    # the bf16 copy of M dominates: at least m * n * 2 bytes
+    assert big >= 8192 * 28672 * 2
+    assert lib.psgd_workspace_size(256, 256, 8, 0, C.byref(b)) == 0 and b.value < big
+    assert lib.psgd_workspace_size(64, 64, 65, 1, C.byref(b)) == -1 and "r=65" in _err(lib)
+    assert lib.psgd_workspace_size(64, 64, 8, 5, C.byref(b)) == -2
+    fake = 0x10000
+
+    def mat(**kw):
+        d = dict(G=fake, E=fake, P=fake, Q=fake, out=fake, m=64, n=48, ws=fake, ws_bytes=1 << 30)
+        d.update(kw)
+        return pk.PsgdMatrix(**d)
+
+    def call(name, mats, r=4, dt=1):
+        arr = (pk.PsgdMatrix * len(mats))(*mats)
+        return getattr(lib, name)(len(mats), arr, dt, r, None)
+
+    for name in ("psgd_project", "psgd_orthogonalize", "psgd_decompress", "psgd_step"):
+        assert call(name, [mat()], r=0) == -1
+        assert call(name, [mat()], r=49) == -1            # r > min(m, n)
+        assert call(name, [mat()], dt=3) == -2
+        assert call(name, [mat(ws_bytes=1024)]) == -5      # ACSC_ENOSPC
+        assert call(name, [mat(ws=fake + 16)]) == -3       # workspace alignment
+        assert call(name, [mat(E=fake + 4)]) == -3         # E 16-byte alignment
+        assert call(name, [mat(P=None)]) == -1
+        assert call(name, [mat(), mat(m=0)]) == -1         # every matrix checked first
+        assert "matrix 1" in _err(lib)
+    assert call("psgd_project", [mat(G=None)]) == -1
+    assert call("psgd_project", [mat(G=fake + 2)]) == -3
+    assert call("psgd_decompress", [mat(out=None)]) == -1
+    assert call("psgd_decompress", [mat(out=fake + 1)]) == -3
+    assert call("psgd_step", [mat(G=None)]) == -1
+    # an empty call succeeds without touching anything; a negative count is rejected
+    assert lib.psgd_project(0, None, 1, 4, None) == 0
+    assert lib.psgd_step(-1, None, 1, 4, None) == -1
