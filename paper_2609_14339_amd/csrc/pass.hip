@@ -633,6 +633,9 @@ struct EmaJob {
     float *C;
     int64_t ldc;
     int m, n, nblocks;
+    float *part;      // split k: partial products [splits][m][np]
+    int64_t ss;       // elements per split's partial
+    int kchunk, splits;
 };
 struct EmaBatch {
     int count;
@@ -668,8 +671,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int m = J.m, n = J.n;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int row0 = blockIdx.x * kBM;
-    const int nsteps = static_cast<int>(cdiv(n, kBK));
+    // block -> (row block, k split): the k range [kbeg, kend) of the rows
+    const int split = static_cast<int>(blockIdx.x) % J.splits;
+    const int row0 = (static_cast<int>(blockIdx.x) / J.splits) * kBM;
+    const int kbeg = split * J.kchunk;
+    const int kend = min(n, kbeg + J.kchunk);
+    const int nsteps = static_cast<int>(cdiv(kend - kbeg, kBK));
 
     f32x16 acc[RT][NC];
 #pragma unroll
@@ -687,14 +694,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     uint2 rg[PU];
     uint4 rb[BPT];
     auto load = [&](int s) {
-        const int k0 = s * kBK;
+        const int k0 = kbeg + s * kBK;
 #pragma unroll
         for (int u = 0; u < PU; ++u) {
             const int q = tid + NTH * u;
             const int gi = row0 + (q >> 4), gk = k0 + (q & 15) * 4;
             float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
             uint2 g = make_uint2(0u, 0u);
-            if (gi < m && gk < n) {
+            if (gi < m && gk < kend) {
                 const int64_t o = static_cast<int64_t>(gi) * n + gk;
                 a = *reinterpret_cast<const float4 *>(M + o);
                 if (G)
@@ -709,13 +716,13 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             const int c = min(q >> 3, np - 1);
             const int gk = k0 + (q & 7) * 8;
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (gk < n)
+            if (gk < kend)
                 v = *reinterpret_cast<const uint4 *>(Bt + static_cast<int64_t>(c) * ldbt + gk);
             rb[j] = v;
         }
     };
     auto store = [&](int buf, int s) {
-        const int k0 = s * kBK;
+        const int k0 = kbeg + s * kBK;
         unsigned char *base = smem + buf * STAGE;
 #pragma unroll
         for (int u = 0; u < PU; ++u) {
@@ -724,7 +731,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             const int gi = row0 + row, gk = k0 + f * 4;
             float v[4] = {rm[u].x, rm[u].y, rm[u].z, rm[u].w};
             uint2 h = make_uint2(0u, 0u);
-            if (gi < m && gk < n) {
+            if (gi < m && gk < kend) {
                 const int64_t o = static_cast<int64_t>(gi) * n + gk;
                 if (G) {
                     v[0] = beta * v[0] + omb * __uint_as_float(rg[u].x << 16);
@@ -789,7 +796,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         lds_barrier();
     }
 
-    // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
+    // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4;
+    // a split writes its partial (row stride np), added up by pass_reduce_kernel
+    float *Cout = J.splits > 1 ? J.part + split * J.ss : J.C;
+    const int64_t ldo = J.splits > 1 ? static_cast<int64_t>(np) : J.ldc;
     const int wrow0 = row0 + wave * (RT * 32);
 #pragma unroll
     for (int a = 0; a < RT; ++a)
@@ -800,7 +810,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             for (int e = 0; e < 16; ++e) {
                 const int row = wrow0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
                 if (row < m && col < np)
-                    J.C[static_cast<int64_t>(row) * J.ldc + col] = acc[a][t][e];
+                    Cout[static_cast<int64_t>(row) * ldo + col] = acc[a][t][e];
             }
         }
 }
@@ -916,12 +926,37 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
     for (size_t i = 0; i < order.size(); ++i)
         order[i] = i;
     std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return reqs[a].n > reqs[b].n; });
+    // Balance: when the batch mixes long and short rows, every row is cut
+    // into k chunks of half the shortest row, so that all blocks do about
+    // the same work and the last round of blocks is not left half empty (a
+    // split writes an fp32 partial of np floats per row, ~1% of the bytes
+    // the sweep streams per row).
+    int64_t nmin = reqs[0].n, nmax = reqs[0].n;
+    for (const EmaReq &q : reqs) {
+        nmin = std::min<int64_t>(nmin, q.n);
+        nmax = std::max<int64_t>(nmax, q.n);
+    }
+    const int64_t kc = 2 * nmax >= 3 * nmin ? round_up(cdiv(nmin, 2), kBK) : nmax;
     std::vector<EmaJob> jobs;
+    std::vector<RedJob> red;
     int gx = 1;
+    int64_t rtot = 1;
     for (size_t oi : order) {
         const EmaReq &q = reqs[oi];
-        const int nb = static_cast<int>(cdiv(q.m, kBM));
-        jobs.push_back(EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, nb});
+        int splits = static_cast<int>(std::min<int64_t>(cdiv(q.n, kc), max_splits(q.m, q.n)));
+        splits = std::max(1, splits);
+        const int64_t chunk = round_up(cdiv(q.n, splits), kBK);
+        splits = static_cast<int>(cdiv(q.n, chunk));
+        if (splits > 1 && !q.part)
+            splits = 1;
+        const int nb = static_cast<int>(cdiv(q.m, kBM)) * splits;
+        const int64_t ss = static_cast<int64_t>(q.m) * NP;
+        jobs.push_back(EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, nb, q.part, ss,
+                              static_cast<int>(splits > 1 ? chunk : q.n), splits});
+        if (splits > 1) {
+            red.push_back(RedJob{q.part, ss, q.C, q.ldc, q.m, NP, splits});
+            rtot = std::max<int64_t>(rtot, static_cast<int64_t>(q.m) * (NP / 4));
+        }
         gx = std::max(gx, nb);
     }
     switch ((NP / 16 + 1) / 2) {   // column tiles in pairs; tiles past NP read zeros
@@ -931,6 +966,14 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
     case 4: ema_launch<8>(tag, jobs, gx, NP, a, b, st); break;
     case 5: ema_launch<10>(tag, jobs, gx, NP, a, b, st); break;
     default: ema_launch<12>(tag, jobs, gx, NP, a, b, st); break;
+    }
+    for (size_t c0 = 0; c0 < red.size(); c0 += kMaxJobs) {
+        RedBatch rb{};
+        rb.count = static_cast<int>(std::min<size_t>(kMaxJobs, red.size() - c0));
+        for (int i = 0; i < rb.count; ++i)
+            rb.j[i] = red[c0 + i];
+        const unsigned g = static_cast<unsigned>(std::min<int64_t>(cdiv(rtot, 256), 8192));
+        ACSC_LAUNCH("sc_split_reduce", pass_reduce_kernel, dim3(g, 1, rb.count), dim3(256), 0, st, rb);
     }
     return ACSC_OK;
 }

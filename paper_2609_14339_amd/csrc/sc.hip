@@ -1739,7 +1739,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     std::vector<pass::EmaReq> er;
     for (auto &m : ms)
         er.push_back(pass::EmaReq{m.in->M, static_cast<const uint16_t *>(m.in->G), m.pw.M16, m.pw.Zt16, m.pw.ldz16,
-                                  m.pw.Y, KP, m.D.m, m.D.n, KP});
+                                  m.pw.Y, KP, m.D.m, m.D.n, KP, m.pw.part});
     const bool fused = use16 && pass::ema_fusable(er);
     if (!fused) {
         if (use16) {
@@ -2164,7 +2164,7 @@ int psgd_project_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStream_t
         std::vector<pass::EmaReq> er;
         for (auto &x : it)
             er.push_back(pass::EmaReq{x.in->E, static_cast<const uint16_t *>(x.in->G), x.w.pw.M16, x.w.pw.Zt16,
-                                      x.w.pw.ldz16, x.w.pw.Y, KP, x.in->m, x.in->n, KP});
+                                      x.w.pw.ldz16, x.w.pw.Y, KP, x.in->m, x.in->n, KP, x.w.pw.part});
         if (pass::ema_fusable(er)) {
             if (int rc = pass::ema_run("psgd_feedback_mq", er, 1.0f, 1.0f, st))
                 return rc;

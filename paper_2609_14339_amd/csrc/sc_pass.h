@@ -50,6 +50,7 @@ struct EmaReq {
     float *C;             // [m, NP] fp32, row stride ldc
     int64_t ldc;
     int m, n, NP;
+    float *part;          // split-k partials, >= max_splits(m, n) * m * NP floats, or nullptr (no split)
 };
 
 // Whether the fused kernel takes this batch: 16-byte aligned operands, n a
