@@ -317,7 +317,8 @@ typedef struct psgd_matrix {
                          from psgd_project until psgd_decompress                 */
     float *P;         /* [m, r] fp32: P = M Q (project), then P_hat (orthogonalize) */
     float *Q;         /* [n, r] fp32: previous Q (project), then M^T P_hat          */
-    void *out;        /* [m, n] of dt: the decompressed gradient; may equal G      */
+    void *out;        /* [m, n] of dt: the decompressed gradient; may equal G,
+                         must not overlap E, P, Q or the workspace                */
     int m, n;
     void *ws;         /* device workspace (256-byte aligned); carries the bf16
                          copy of M from psgd_project to psgd_orthogonalize: keep
