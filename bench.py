@@ -53,6 +53,9 @@ def parse():
                     help="skip the separate measurement of the Bernoulli mask variant")
     ap.add_argument("--no-powersgd", action="store_true",
                     help="skip the separate measurement of the PowerSGD compressor")
+    ap.add_argument("--no-async", action="store_true",
+                    help="skip the second timed loop in which the anchor-prior build runs on its own "
+                         "stream beside the masking and the correction")
     return ap.parse_args()
 
 
@@ -104,19 +107,25 @@ def main():
     idxs = [[torch.empty(rows, K, dtype=torch.int16, device=dev) for _ in range(2)] for _ in range(L)]
     ys = [[torch.empty(rows, H, dtype=act.dtype, device=dev) for _ in range(2)] for _ in range(L)]
     mats = []
+    nbuf = 2
     for l in range(L):
         for j, (m, n) in enumerate(gs.shapes):
             G_anc, G_mask = workloads.grad_pair_fast(gs, cfg.cid, l, j, dev)
+            priors = [(torch.empty(m, r, device=dev), torch.empty(r, device=dev),
+                       torch.empty(n, r, device=dev), torch.empty(r, device=dev)) for _ in range(nbuf)]
+            ws = pk.workspace(m, n, r, p, gs.dtype)
             mats.append(dict(m=m, n=n, G_anc=G_anc, G_mask=G_mask,
-                             M=torch.zeros(m, n, device=dev),
-                             out=(torch.empty(m, r, device=dev), torch.empty(r, device=dev),
-                                  torch.empty(n, r, device=dev), torch.empty(r, device=dev)),
-                             Gp=torch.empty_like(G_mask),
-                             ws=pk.workspace(m, n, r, p, gs.dtype)))
-    # one batched call per phase over every matrix of the stage
-    build_items = [dict(G_anc=mt["G_anc"], M=mt["M"], out=mt["out"], ws=mt["ws"]) for mt in mats]
-    corr_items = [dict(G=mt["G_mask"], prior=(mt["out"][0], mt["out"][3], mt["out"][2]), out=mt["Gp"],
-                       ws=mt["ws"]) for mt in mats]
+                             M=torch.zeros(m, n, device=dev), out=priors[0], priors=priors,
+                             Gp=torch.empty_like(G_mask), ws=ws,
+                             cws=pk.workspace(m, n, r, 0, gs.dtype)))
+    # one batched call per phase over every matrix of the stage; with the
+    # anchor prior built asynchronously (Sec. 3.2; Alg. 1 corrects with the
+    # basis of the last anchor arrival), build b writes prior buffer b % 2
+    # while the correction reads the other one
+    build_items = [[dict(G_anc=mt["G_anc"], M=mt["M"], out=mt["priors"][b], ws=mt["ws"]) for mt in mats]
+                   for b in range(nbuf)]
+    corr_items = [[dict(G=mt["G_mask"], prior=(mt["priors"][b][0], mt["priors"][b][3], mt["priors"][b][2]),
+                        out=mt["Gp"], ws=mt["cws"]) for mt in mats] for b in range(nbuf)]
     torch.cuda.synchronize()
     setup_s = time.time() - t0
     print(f"[bench] inputs ready in {setup_s:.1f} s; HBM in use "
@@ -133,22 +142,62 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
     phase_ms = {"ac": 0.0, "build": 0.0, "correct": 0.0}
+    # The timed step runs its parts in order on one stream: the masking, the
+    # anchor-prior build, the correction with that prior.  A second loop
+    # (components.async_step) runs the build on a stream of its own (default
+    # priority) beside the masking and a correction that uses the previous
+    # build's prior, as the method uses it (the prior is built asynchronously).
+    serial = [True]
+    astream = torch.cuda.Stream()
+    bstream_of = lambda: stream if serial[0] else astream
+    n_steps_run = [0]
+    built = {}      # step -> event after its build
+    corrected = {}  # step -> event after its correction
+
+    build_marks = []
+
+    def build(i):
+        bstream = bstream_of()
+        # correction i - 1 reads prior buffer (i - 2) % 2 = i % 2: it must be done
+        if not serial[0] and i - 1 in corrected:
+            bstream.wait_event(corrected[i - 1])
+        b0, b1 = ev(), ev()
+        b0.record(bstream)
+        with torch.cuda.stream(bstream):
+            pk.sc_build_prior_batched(build_items[i % nbuf], r, workloads.BETA, workloads.TAU, p, q, seed=1000,
+                                      dtype=gs.dtype)
+        b1.record(bstream)
+        build_marks.append((b0, b1))
+        built[i] = b1
 
     def step(record: bool):
+        i = n_steps_run[0]
+        n_steps_run[0] += 1
         e0, e1, e2, e3 = ev(), ev(), ev(), ev()
         e0.record(stream)
+        if not serial[0]:
+            bstream_of().wait_event(e0)
+            build(i)
         for l in range(L):
             for dirn, src in enumerate((xs[l], gxs[l])):      # forward, then backward
                 pk.ac_mask_pack(src, K, keys[l], vals=vals[l][dirn], idx=idxs[l][dirn])
                 pk.ac_unpack_scatter(vals[l][dirn], H, keys[l], scale, idx=idxs[l][dirn],
                                      y=ys[l][dirn])
         e1.record(stream)
-        pk.sc_build_prior_batched(build_items, r, workloads.BETA, workloads.TAU, p, q, seed=1000,
-                                  dtype=gs.dtype)
+        if serial[0]:
+            build(i)
+            b = i % nbuf
+        else:
+            stream.wait_event(built[i - 1])            # the last finished anchor prior
+            b = (i - 1) % nbuf
         e2.record(stream)
-        pk.sc_correct_batched(corr_items, r, workloads.ALPHA, dtype=gs.dtype)
+        pk.sc_correct_batched(corr_items[b], r, workloads.ALPHA, dtype=gs.dtype)
         e3.record(stream)
+        c = torch.cuda.Event()
+        c.record(stream)
+        corrected[i] = c
         return (e0, e1, e2, e3) if record else None
+
 
     for _ in range(args.warmup):
         step(False)
@@ -170,8 +219,10 @@ def main():
     ms_per_step = total_ms / args.steps
     for e0, e1, e2, e3 in marks:
         phase_ms["ac"] += e0.elapsed_time(e1) / args.steps
-        phase_ms["build"] += e1.elapsed_time(e2) / args.steps
         phase_ms["correct"] += e2.elapsed_time(e3) / args.steps
+    # the builds of the timed steps (the last args.steps recorded)
+    for b0, b1 in build_marks[-args.steps:]:
+        phase_ms["build"] += b0.elapsed_time(b1) / args.steps
     print(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     # ---------------- algorithmic work of one step ----------------
@@ -304,6 +355,26 @@ def main():
     if not args.no_powersgd:
         comp["psgd"] = psgd_component(pk, mats, gs, max(1, min(args.steps, 5)), stream)
 
+    if not args.no_async:
+        # the same steps with the build on its own stream (the correction uses the
+        # previous build's prior); the first such step corrects with the last
+        # in-order build's prior
+        serial[0] = False
+        for _ in range(args.warmup):
+            step(False)
+        torch.cuda.synchronize()
+        a0, a1 = ev(), ev()
+        a0.record(stream)
+        for _ in range(args.steps):
+            step(False)
+        stream.wait_stream(astream)                    # the last build is part of the timed work
+        a1.record(stream)
+        torch.cuda.synchronize()
+        serial[0] = True
+        ams = a0.elapsed_time(a1) / args.steps
+        comp["async_step"] = {"ms_per_step": round(ams, 4), "value": round(step_bytes / (ams * 1e-3) / 1e9, 1),
+                              "unit": "GB/s", "speedup": round(ms_per_step / ams, 4), "steps": args.steps}
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, args.cpu_seconds)
@@ -317,6 +388,7 @@ def main():
         "config": {"workload": f"{cfg.name}: activation [{act.B},{act.S},{H}] keep {keep} (K={K}) "
                                f"fwd+bwd x{L} layers; gradients {shapes} x{L} layers, rank-{gs.rank} "
                                f"signal + noise; r={r}, k={kk}, power_iters={q}",
+                   "step": "in order on one stream: mask, anchor-prior build, correction with that prior",
                    "step_bytes": step_bytes, "step_flops": step_flops,
                    "step_TFLOP/s": round(step_flops / (ms_per_step * 1e-3) / 1e12, 2)},
         "roofline": roof,
