@@ -117,7 +117,8 @@ def main():
             mats.append(dict(m=m, n=n, G_anc=G_anc, G_mask=G_mask,
                              M=torch.zeros(m, n, device=dev), out=priors[0], priors=priors,
                              Gp=torch.empty_like(G_mask), ws=ws,
-                             cws=pk.workspace(m, n, r, 0, gs.dtype)))
+                             cws=torch.empty(max(pk.sc_adamw_workspace_size(m, n, r, gs.dtype), 256),
+                                             dtype=torch.uint8, device=dev)))
     # one batched call per phase over every matrix of the stage; with the
     # anchor prior built asynchronously (Sec. 3.2; Alg. 1 corrects with the
     # basis of the last anchor arrival), build b writes prior buffer b % 2
