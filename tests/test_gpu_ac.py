@@ -149,6 +149,17 @@ def test_strided_rows_and_unaligned_output(pk, dtype):
     assert torch.all(ybig[:, H:] == 7.0)     # columns past H untouched
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("H,K,pad", [(301, 100, 3), (2045, 400, 3), (9000, 3000, 8)])
+def test_padded_rows_with_ragged_tail(pk, dtype, H, K, pad):
+    # 16-byte aligned row stride with H not a multiple of the 16-byte chunk:
+    # the whole-row pack reads the chunks, then the last few entries one by one
+    B, S = 2, 9
+    x = workloads.gaussian((B * S, H), seed=H + K, dtype=dtype)
+    _run_case(pk, x, B, S, H, K, dict(seed=11, layer=2, step=5, microbatch=1), ld_pad=pad,
+              scales=(1.0, H / K))
+
+
 def test_zero_rows_and_determinism(pk):
     key0 = pk.make_key(seed=1, layer=0, step=0, microbatch=0, B=0, S=4, H=64)
     x = torch.empty(0, 64, device="cuda")
