@@ -73,8 +73,8 @@ def touched_line_fraction(H: int, K: int, elem_bytes: int, line: int = 128) -> f
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
-              "multi-GPU path: every GPU box here has one GPU.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the library has no "
+              "multi-GPU path (no collectives, no sharding), so N must be 1.", file=sys.stderr)
         return 2
 
     import torch
