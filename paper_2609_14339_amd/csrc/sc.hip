@@ -539,11 +539,29 @@ __device__ __forceinline__ double group8_sum(double x)
 
 // Reciprocal and reciprocal square root of the rotation formulas: the fp32
 // path takes the hardware approximations (about 1 ulp; a rotation only has to
-// be orthogonal, and the next sweep corrects its angle), fp64 the rounded ops.
+// be orthogonal, and the next sweep corrects its angle).  fp64 refines the
+// hardware estimates (v_rsq_f64, v_rcp_f64) by two Newton steps each, to
+// within a few ulp: much shorter dependent chains than the correctly rounded
+// square root and division, which sit on every round's critical path, and c
+// and s = c t stay orthogonal to working precision.  The arguments are
+// positive and finite (the caller skips pairs with a zero norm or product).
 __device__ __forceinline__ float jac_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
-__device__ __forceinline__ double jac_rsqrt(double x) { return 1.0 / sqrt(x); }
+__device__ __forceinline__ double jac_rsqrt(double x)
+{
+    double y = __builtin_amdgcn_rsq(x);
+    const double hx = 0.5 * x;
+    y = __builtin_fma(y, __builtin_fma(-hx * y, y, 0.5), y);   // y + y (1 - x y^2) / 2
+    y = __builtin_fma(y, __builtin_fma(-hx * y, y, 0.5), y);
+    return y;
+}
 __device__ __forceinline__ float jac_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
-__device__ __forceinline__ double jac_rcp(double x) { return 1.0 / x; }
+__device__ __forceinline__ double jac_rcp(double x)
+{
+    double y = __builtin_amdgcn_rcp(x);
+    y = __builtin_fma(y, __builtin_fma(-x, y, 1.0), y);        // y + y (1 - x y)
+    y = __builtin_fma(y, __builtin_fma(-x, y, 1.0), y);
+    return y;
+}
 
 // ---------------------------------------------------------------------------
 // One-sided (Hestenes) Jacobi SVD of the k x k factor L in LDS, one
