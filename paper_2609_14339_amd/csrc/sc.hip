@@ -586,12 +586,15 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     float *Bu = J.Bu, *Bv = J.Bv, *s_out = J.s_out, *d_out = J.d_out;
     int *info = J.info;
     extern __shared__ __attribute__((aligned(16))) unsigned char jsm[];
-    // column c at A[c * kp]; kp = k rounded up to 32 (= 8 RC), rows k..kp-1
-    // are zero.  Lane gl of a pair's 8 lanes holds the R = kp / 8 consecutive
-    // rows gl R .. gl R + R - 1 of both columns (R a multiple of 4: 16-byte
-    // LDS accesses).
+    // column c at A[c * kp]; kp = k rounded up to 8 V (= 8 RC; 32 rows in
+    // fp32, 16 in fp64), rows k..kp-1 are zero.  Lane gl of a pair's 8 lanes
+    // holds the R = kp / 8 consecutive rows gl R .. gl R + R - 1 of both
+    // columns (R a multiple of V: 16-byte LDS accesses).  Every round reads
+    // and writes whole columns, so the padding is kept to what the 16-byte
+    // accesses need.
+    constexpr int V = 16 / sizeof(T);   // elements per 16-byte access
     T *A = reinterpret_cast<T *>(jsm);
-    const int kp = (k + 31) & ~31;
+    const int kp = (k + 8 * V - 1) / (8 * V) * (8 * V);
     T *nrm = A + static_cast<size_t>(k) * kp;   // squared column norms
     __shared__ unsigned int sh_off;
     __shared__ double sh_cut;
@@ -609,8 +612,7 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     const int slots = nwave * 8;
     constexpr int R = RC;
     constexpr int RMAX = RC;
-    constexpr int V = 16 / sizeof(T);   // elements per 16-byte access
-    static_assert(R % 4 == 0, "rows per lane");
+    static_assert(R % V == 0, "rows per lane");
     int sweeps_used = 0;
     float last_off = 0.f;
     __syncthreads();
@@ -1558,13 +1560,18 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
 template <typename T>
 using JacobiFn = void (*)(const Batch<JacJob>, int, int, int, int, float, T, int);
 
+// rows per lane: k rounded up to 8 V, divided by 8 (fp64: k <= 128)
 template <typename T>
 JacobiFn<T> jacobi_fn(int k)
 {
-    switch (((k + 31) & ~31) / 8) {
+    switch (((k + 15) & ~15) / 8) {
+    case 2: return jacobi_kernel<T, 2>;
     case 4: return jacobi_kernel<T, 4>;
+    case 6: return jacobi_kernel<T, 6>;
     case 8: return jacobi_kernel<T, 8>;
+    case 10: return jacobi_kernel<T, 10>;
     case 12: return jacobi_kernel<T, 12>;
+    case 14: return jacobi_kernel<T, 14>;
     default: return jacobi_kernel<T, 16>;
     }
 }
@@ -1588,8 +1595,8 @@ unsigned jacobi_threads(int k)
     return 64u * static_cast<unsigned>(std::min<int64_t>(16, std::max<int64_t>(4, cdiv(npairs, 8))));
 }
 
-// columns padded to a multiple of 32 rows, plus the squared norms
-size_t jacobi_lds(int k, size_t es) { return (static_cast<size_t>(k) * round_up(k, 32) + k) * es; }
+// columns padded to a multiple of 8 V rows (32 in fp32, 16 in fp64), plus the squared norms
+size_t jacobi_lds(int k, size_t es) { return (static_cast<size_t>(k) * round_up(k, es == 8 ? 16 : 32) + k) * es; }
 
 // One tall-skinny product per job (opA * B), split-K through the job's
 // partial buffer `part` (nullptr: one split, straight into C).
