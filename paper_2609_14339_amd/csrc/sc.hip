@@ -358,7 +358,7 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const Batch<ReduceJo
 // j + 16 k; the result D[i][j] sits in lane j + 16 (i % 4), element i / 4.
 // ---------------------------------------------------------------------------
 constexpr int kGT = 32;
-constexpr int kGRows = 64;
+constexpr int kGRows = 32;
 typedef double v4d __attribute__((ext_vector_type(4)));
 
 struct GramJob {
@@ -376,7 +376,7 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> 
         return;
     constexpr int NTILES = NT * (NT + 1) / 2;
     constexpr int TPW = (NTILES + 3) / 4;          // tiles per wave
-    constexpr int PITCH = NT * kGT + 4;            // floats per staged row
+    constexpr int PITCH = NT * kGT + 16;           // floats per staged row (rows 48 banks apart: conflict-free reads)
     __shared__ __attribute__((aligned(16))) float Ys[kGRows * PITCH];
     const float *A = J.A;
     const int64_t lda = J.lda;
@@ -433,13 +433,29 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> 
         __syncthreads();
         if (rb + kGRows < r1)
             load(rb + kGRows);
-#pragma unroll 2
-        for (int k0 = 0; k0 < kGRows; k0 += 4) {
+        // the next k-step's operands are read from LDS before this step's
+        // products are issued, so their latency hides under the MFMAs
+        float op[2][TPW][4];
+        auto read_ops = [&](int k0, float (&o)[TPW][4]) {
             const float *yr = &Ys[(k0 + (lane >> 4)) * PITCH + (lane & 15)];
 #pragma unroll
             for (int u = 0; u < TPW; ++u) {
-                const double a0 = yr[tri_[u] * kGT], a1 = yr[tri_[u] * kGT + 16];
-                const double b0 = yr[trj_[u] * kGT], b1 = yr[trj_[u] * kGT + 16];
+                o[u][0] = yr[tri_[u] * kGT];
+                o[u][1] = yr[tri_[u] * kGT + 16];
+                o[u][2] = yr[trj_[u] * kGT];
+                o[u][3] = yr[trj_[u] * kGT + 16];
+            }
+        };
+        read_ops(0, op[0]);
+#pragma unroll
+        for (int k0 = 0; k0 < kGRows; k0 += 4) {
+            const int cur = (k0 >> 2) & 1;
+            if (k0 + 4 < kGRows)
+                read_ops(k0 + 4, op[cur ^ 1]);
+#pragma unroll
+            for (int u = 0; u < TPW; ++u) {
+                const double a0 = op[cur][u][0], a1 = op[cur][u][1];
+                const double b0 = op[cur][u][2], b1 = op[cur][u][3];
                 acc[u][0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[u][0][0], 0, 0, 0);
                 acc[u][0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[u][0][1], 0, 0, 0);
                 acc[u][1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[u][1][0], 0, 0, 0);
