@@ -7,7 +7,12 @@ resident in HBM (70B-class slice, four layers):
   activation gradient (backward, same mask key);
   per weight matrix (3 per layer): anchor EMA + top-r SVD + filter
   (sc_build_prior), then the spectral correction of the masked gradient
-  (sc_correct).
+  (sc_correct) with that prior.
+The build's streaming phase (EMA and power passes) runs alone; the masking
+runs on a second stream beside the build's Rayleigh-Ritz step and the
+correction.  The same steps are also timed strictly one part after another
+(components.serial_step) and with the prior built asynchronously
+(components.async_step).
 
 Prints one JSON line.  `value` is the algorithmic HBM bytes of the step
 divided by the measured step time (GB/s); `roofline` reports the kernel that
@@ -143,61 +148,85 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
     phase_ms = {"ac": 0.0, "build": 0.0, "correct": 0.0}
-    # The timed step runs its parts in order on one stream: the masking, the
-    # anchor-prior build, the correction with that prior.  A second loop
-    # (components.async_step) runs the build on a stream of its own (default
-    # priority) beside the masking and a correction that uses the previous
-    # build's prior, as the method uses it (the prior is built asynchronously).
-    serial = [True]
-    astream = torch.cuda.Stream()
-    bstream_of = lambda: stream if serial[0] else astream
+    # The timed step does every part once, each build with this step's
+    # anchor gradient and each correction with the prior it built: the
+    # subspace iteration of the build (EMA, power passes), then its
+    # Rayleigh-Ritz step and the correction, with the masking (independent of
+    # both) on a second stream beside them, after the streaming passes.  Two
+    # more loops time the same work arranged otherwise:
+    #   components.serial_step: masking, build, correction one after another
+    #     on one stream;
+    #   components.async_step: the build on a stream of its own beside the
+    #     masking and a correction that uses the previous build's prior, as
+    #     the method uses it (the prior is built asynchronously).
+    # Every stream has the default priority.
+    mode = ["overlap"]
+    astream = torch.cuda.Stream()       # the asynchronous build
+    side = torch.cuda.Stream()          # the overlapped step's masking
     n_steps_run = [0]
     built = {}      # step -> event after its build
     corrected = {}  # step -> event after its correction
+    builders = {None: pk.sc_build_prior_batched, "sub": pk.sc_build_subspace_batched,
+                "ritz": pk.sc_build_ritz_batched}
 
-    build_marks = []
-
-    def build(i):
-        bstream = bstream_of()
+    def build(i, phase=None):
+        bstream = astream if mode[0] == "async" else stream
         # correction i - 1 reads prior buffer (i - 2) % 2 = i % 2: it must be done
-        if not serial[0] and i - 1 in corrected:
+        if mode[0] == "async" and i - 1 in corrected:
             bstream.wait_event(corrected[i - 1])
         b0, b1 = ev(), ev()
         b0.record(bstream)
         with torch.cuda.stream(bstream):
-            pk.sc_build_prior_batched(build_items[i % nbuf], r, workloads.BETA, workloads.TAU, p, q, seed=1000,
-                                      dtype=gs.dtype)
+            builders[phase](build_items[i % nbuf], r, workloads.BETA, workloads.TAU, p, q, seed=1000,
+                            dtype=gs.dtype)
         b1.record(bstream)
-        build_marks.append((b0, b1))
-        built[i] = b1
+        return b0, b1
 
-    def step(record: bool):
-        i = n_steps_run[0]
-        n_steps_run[0] += 1
-        e0, e1, e2, e3 = ev(), ev(), ev(), ev()
-        e0.record(stream)
-        if not serial[0]:
-            bstream_of().wait_event(e0)
-            build(i)
+    def masking():
         for l in range(L):
             for dirn, src in enumerate((xs[l], gxs[l])):      # forward, then backward
                 pk.ac_mask_pack(src, K, keys[l], vals=vals[l][dirn], idx=idxs[l][dirn])
                 pk.ac_unpack_scatter(vals[l][dirn], H, keys[l], scale, idx=idxs[l][dirn],
                                      y=ys[l][dirn])
-        e1.record(stream)
-        if serial[0]:
-            build(i)
-            b = i % nbuf
+
+    def step(record: bool):
+        i = n_steps_run[0]
+        n_steps_run[0] += 1
+        e0 = ev()
+        e0.record(stream)
+        if mode[0] == "overlap":
+            s0, s1 = build(i, "sub")
+            side.wait_event(s1)
+            a0, a1 = ev(), ev()
+            a0.record(side)
+            with torch.cuda.stream(side):
+                masking()
+            a1.record(side)
+            _, r1 = build(i, "ritz")
+            bmark, b = (s0, r1), i % nbuf
         else:
-            stream.wait_event(built[i - 1])            # the last finished anchor prior
-            b = (i - 1) % nbuf
-        e2.record(stream)
+            if mode[0] == "async":
+                astream.wait_event(e0)
+                bmark = build(i)
+            a0, a1 = e0, ev()
+            masking()
+            a1.record(stream)
+            if mode[0] == "serial":
+                bmark, b = build(i), i % nbuf
+            else:
+                stream.wait_event(built[i - 1])            # the last finished anchor prior
+                b = (i - 1) % nbuf
+        built[i] = bmark[1]
+        c0, c1 = ev(), ev()
+        c0.record(stream)
         pk.sc_correct_batched(corr_items[b], r, workloads.ALPHA, dtype=gs.dtype)
-        e3.record(stream)
+        c1.record(stream)
+        if mode[0] == "overlap":
+            stream.wait_event(a1)                      # the next build streams M alone
         c = torch.cuda.Event()
         c.record(stream)
         corrected[i] = c
-        return (e0, e1, e2, e3) if record else None
+        return dict(ac=(a0, a1), build=bmark, correct=(c0, c1)) if record else None
 
 
     for _ in range(args.warmup):
@@ -218,12 +247,9 @@ def main():
     pk.acsc_stats_enable(False)
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
-    for e0, e1, e2, e3 in marks:
-        phase_ms["ac"] += e0.elapsed_time(e1) / args.steps
-        phase_ms["correct"] += e2.elapsed_time(e3) / args.steps
-    # the builds of the timed steps (the last args.steps recorded)
-    for b0, b1 in build_marks[-args.steps:]:
-        phase_ms["build"] += b0.elapsed_time(b1) / args.steps
+    for mk in marks:
+        for ph, (x0, x1) in mk.items():
+            phase_ms[ph] += x0.elapsed_time(x1) / args.steps
     print(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     # ---------------- algorithmic work of one step ----------------
@@ -356,14 +382,14 @@ def main():
     if not args.no_powersgd:
         comp["psgd"] = psgd_component(pk, mats, gs, max(1, min(args.steps, 5)), stream)
 
-    if not args.no_async:
-        # the same steps with the build on its own stream (the correction uses the
-        # previous build's prior); the first such step corrects with the last
-        # in-order build's prior
-        serial[0] = False
+    def other_arrangement(name, kernel_stats=False):
+        mode[0] = name
         for _ in range(args.warmup):
             step(False)
         torch.cuda.synchronize()
+        if kernel_stats:
+            pk.acsc_stats_enable(True)
+            torch.cuda.synchronize()
         a0, a1 = ev(), ev()
         a0.record(stream)
         for _ in range(args.steps):
@@ -371,10 +397,30 @@ def main():
         stream.wait_stream(astream)                    # the last build is part of the timed work
         a1.record(stream)
         torch.cuda.synchronize()
-        serial[0] = True
+        mode[0] = "overlap"
         ams = a0.elapsed_time(a1) / args.steps
-        comp["async_step"] = {"ms_per_step": round(ams, 4), "value": round(step_bytes / (ams * 1e-3) / 1e9, 1),
-                              "unit": "GB/s", "speedup": round(ms_per_step / ams, 4), "steps": args.steps}
+        out = {"ms_per_step": round(ams, 4), "value": round(step_bytes / (ams * 1e-3) / 1e9, 1),
+               "unit": "GB/s", "speedup": round(ms_per_step / ams, 4), "steps": args.steps}
+        if kernel_stats:
+            st = pk.acsc_stats_read()
+            pk.acsc_stats_enable(False)
+            # the masking kernels on their own (in the timed step they share
+            # the GPU with the Rayleigh-Ritz step)
+            for tag in ("ac_pack", "ac_unpack"):
+                if tag in st:
+                    kms = st[tag][1] / args.steps
+                    gbs = work[tag]["bytes"] / (kms * 1e-3) / 1e9
+                    out[tag] = {"GB/s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM, 4),
+                                "ms_per_step": round(kms, 4), "avg_us": round(1e3 * kms / work[tag]["calls"], 2)}
+        return out
+
+    # the same steps in one stream, one part after another
+    comp["serial_step"] = other_arrangement("serial", kernel_stats=True)
+    if not args.no_async:
+        # the same steps with the build on its own stream (the correction uses the
+        # previous build's prior); the first such step corrects with the last
+        # serial step's prior
+        comp["async_step"] = other_arrangement("async")
 
     cpu = None
     if not args.no_cpu_baseline:

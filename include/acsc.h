@@ -238,6 +238,29 @@ int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dtype dt, floa
                            int oversample, int power_iters, float tau, uint64_t seed,
                            hipStream_t stream);
 
+/* The same batched build in its two phases, for a caller that wants other
+ * work beside the second (App. E's top-r SVD as a randomised subspace
+ * iteration followed by a Rayleigh-Ritz step):
+ *   sc_build_subspace_batched: the EMA of Sec. 3.2, the power passes and
+ *     the last product Z = M^T Q, all streaming M; it leaves Q and Z in each
+ *     matrix's workspace and writes no output;
+ *   sc_build_ritz_batched: the Rayleigh-Ritz step on Z (a k x k Gram, its
+ *     Cholesky factor and that factor's SVD on a few workgroups, then the
+ *     basis U, V, s and the filter d); it does not touch M.
+ * Both take exactly the arguments of sc_build_prior_batched, and the ritz
+ * call must follow the subspace call with the same arguments and
+ * workspaces, in stream order, with nothing writing those workspaces in
+ * between.  The ritz call reads neither G_anc nor beta, power_iters or seed.
+ * The pair enqueues the same kernels in the same order as one
+ * sc_build_prior_batched call, so the results are bit-identical.  Errors as
+ * for sc_build_prior_batched. */
+int sc_build_subspace_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                              int oversample, int power_iters, float tau, uint64_t seed,
+                              hipStream_t stream);
+int sc_build_ritz_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                          int oversample, int power_iters, float tau, uint64_t seed,
+                          hipStream_t stream);
+
 /* sc_correct on each of mats[0 .. count-1] with shared dt, r and alpha. */
 int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,
                        hipStream_t stream);

@@ -92,8 +92,9 @@ def _load():
                                    vp, vp, vp, vp, vp, sz, vp]
     lib.sc_correct.restype = i32
     lib.sc_correct.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, f32, vp, vp, sz, vp]
-    lib.sc_build_prior_batched.restype = i32
-    lib.sc_build_prior_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, f32, i32, i32, i32, f32, u64, vp]
+    for fn in (lib.sc_build_prior_batched, lib.sc_build_subspace_batched, lib.sc_build_ritz_batched):
+        fn.restype = i32
+        fn.argtypes = [i32, C.POINTER(ScMatrix), i32, f32, i32, i32, i32, f32, u64, vp]
     lib.sc_correct_batched.restype = i32
     lib.sc_correct_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, i32, f32, vp]
     lib.sc_adamw_workspace_size.restype = i32
@@ -119,6 +120,7 @@ lib = _load()
 EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
             "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched",
+            "sc_build_subspace_batched", "sc_build_ritz_batched",
             "sc_adamw_workspace_size", "sc_correct_adamw_batched",
             "ac_bern_mask", "ac_bern_pack", "ac_bern_unpack",
             "psgd_workspace_size", "psgd_project", "psgd_orthogonalize", "psgd_decompress", "psgd_step")
@@ -330,6 +332,28 @@ def sc_build_prior_batched(items, r: int, beta: float, tau: float, oversample: i
                            stream=None):
     """items: list of dicts with G_anc (or None), M, out=(U, s, V, d), ws, and
     optionally V_warm.  Matrix i starts from the random block of seed + i."""
+    _build_batched(lib.sc_build_prior_batched, items, r, beta, tau, oversample, power_iters, seed, dtype, stream)
+
+
+def sc_build_subspace_batched(items, r: int, beta: float, tau: float, oversample: int,
+                              power_iters: int, seed: int = 0, dtype: torch.dtype = torch.bfloat16,
+                              stream=None):
+    """First phase of sc_build_prior_batched (EMA, power passes, Z = M^T Q);
+    the same arguments.  Follow it with sc_build_ritz_batched."""
+    _build_batched(lib.sc_build_subspace_batched, items, r, beta, tau, oversample, power_iters, seed, dtype,
+                   stream)
+
+
+def sc_build_ritz_batched(items, r: int, beta: float, tau: float, oversample: int,
+                          power_iters: int, seed: int = 0, dtype: torch.dtype = torch.bfloat16,
+                          stream=None):
+    """Second phase of sc_build_prior_batched (Rayleigh-Ritz on Z: U, s, V, d);
+    the same arguments and workspaces as the sc_build_subspace_batched call
+    it follows."""
+    _build_batched(lib.sc_build_ritz_batched, items, r, beta, tau, oversample, power_iters, seed, dtype, stream)
+
+
+def _build_batched(fn, items, r, beta, tau, oversample, power_iters, seed, dtype, stream):
     arr = (ScMatrix * max(len(items), 1))()
     keep = []
     for i, it in enumerate(items):
@@ -342,8 +366,7 @@ def sc_build_prior_batched(items, r: int, beta: float, tau: float, oversample: i
         arr[i] = ScMatrix(_p(G), _p(M), m, n, _p(U), _p(s), _p(V), _p(d), _p(Vw), None, _p(ws),
                           ws.numel())
     code = BF16 if dtype == torch.bfloat16 else F32
-    _check(lib.sc_build_prior_batched(len(items), arr, code, float(beta), r, oversample, power_iters,
-                                      float(tau), seed, _stream(stream)))
+    _check(fn(len(items), arr, code, float(beta), r, oversample, power_iters, float(tau), seed, _stream(stream)))
 
 
 def sc_correct_batched(items, r: int, alpha: float, dtype: torch.dtype = torch.bfloat16,

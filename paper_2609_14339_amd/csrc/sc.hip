@@ -1768,8 +1768,13 @@ int orthonormalise(std::vector<Mat> &ms, bool onY, int passes, bool use16, hipSt
 }
 
 // EMA + top-r SVD + filter for a group of matrices with the same k.
+// Phases of the build: the subspace iteration (EMA, power passes, the final
+// Z = M^T Q) and the Rayleigh-Ritz step on Z (Gram, Cholesky, Jacobi, basis,
+// filter).  The second reads only what the first left in the workspace.
+constexpr int kPhaseSubspace = 1, kPhaseRitz = 2;
+
 int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int power_iters, float tau,
-                 hipStream_t st)
+                int phases, hipStream_t st)
 {
     const Dims &d0 = ms[0].D;
     const int k = d0.k, KP = d0.KP, RP = d0.RP;
@@ -1782,7 +1787,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         er.push_back(pass::EmaReq{m.in->M, static_cast<const uint16_t *>(m.in->G), m.pw.M16, m.pw.Zt16, m.pw.ldz16,
                                   m.pw.Y, KP, m.D.m, m.D.n, KP, m.pw.part});
     const bool fused = use16 && pass::ema_fusable(er);
-    if (!fused) {
+    if ((phases & kPhaseSubspace) && !fused) {
         if (use16) {
             std::vector<EmaJob<uint16_t>> j;
             int64_t tot = 1;
@@ -1807,7 +1812,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
                 launch_jobs("sc_ema", ema_kernel<float>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
         }
     }
-    {
+    if (phases & kPhaseSubspace) {
         std::vector<InitJob> j;
         int64_t tot = 1;
         for (auto &m : ms) {
@@ -1858,24 +1863,29 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
             return ACSC_OK;
         }
     };
-    int rc = fused ? pass::ema_run("sc_ema", er, beta, omb, st) : pass(true);
-    if (rc)
-        return rc;
-    if ((rc = orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st)))
-        return rc;
-    for (int it = 0; it < power_iters; ++it) {
+    int rc = ACSC_OK;
+    if (phases & kPhaseSubspace) {
+        rc = fused ? pass::ema_run("sc_ema", er, beta, omb, st) : pass(true);
+        if (rc)
+            return rc;
+        if ((rc = orthonormalise(ms, true, power_iters == 0 ? 2 : 1, use16, st)))
+            return rc;
+        for (int it = 0; it < power_iters; ++it) {
+            if ((rc = pass(false)))
+                return rc;
+            if ((rc = orthonormalise(ms, false, 1, use16, st)))
+                return rc;
+            if ((rc = pass(true)))
+                return rc;
+            if ((rc = orthonormalise(ms, true, it + 1 == power_iters ? 2 : 1, use16, st)))
+                return rc;
+        }
+        // Z = M^T Q (= B^T) for the Rayleigh-Ritz step: B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
         if ((rc = pass(false)))
             return rc;
-        if ((rc = orthonormalise(ms, false, 1, use16, st)))
-            return rc;
-        if ((rc = pass(true)))
-            return rc;
-        if ((rc = orthonormalise(ms, true, it + 1 == power_iters ? 2 : 1, use16, st)))
-            return rc;
     }
-    // Rayleigh-Ritz: Z = M^T Q (= B^T), B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
-    if ((rc = pass(false)))
-        return rc;
+    if (!(phases & kPhaseRitz))
+        return ACSC_OK;
     {
         std::vector<const float *> A;
         std::vector<int> rows;
@@ -2420,9 +2430,10 @@ extern "C" int sc_workspace_size(int m, int n, int r, int oversample, acsc_dtype
     return ACSC_OK;
 }
 
-extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
-                                      int oversample, int power_iters, float tau, uint64_t seed,
-                                      hipStream_t stream)
+namespace {
+
+int build_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r, int oversample,
+                  int power_iters, float tau, uint64_t seed, int phases, hipStream_t stream)
 {
     clear_error();
     ACSC_CHECK_ARG(count >= 0, ACSC_EINVAL, "count=%d < 0", count);
@@ -2468,11 +2479,35 @@ extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dty
                 group.push_back(all[j]);
                 done[j] = true;
             }
-        const int rc = build_group(group, dt, beta, r, power_iters, tau, stream);
+        const int rc = build_group(group, dt, beta, r, power_iters, tau, phases, stream);
         if (rc)
             return rc;
     }
     return check_launch("sc_build_prior");
+}
+
+}  // namespace
+
+extern "C" int sc_build_prior_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                                      int oversample, int power_iters, float tau, uint64_t seed,
+                                      hipStream_t stream)
+{
+    return build_batched(count, mats, dt, beta, r, oversample, power_iters, tau, seed,
+                         kPhaseSubspace | kPhaseRitz, stream);
+}
+
+extern "C" int sc_build_subspace_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                                         int oversample, int power_iters, float tau, uint64_t seed,
+                                         hipStream_t stream)
+{
+    return build_batched(count, mats, dt, beta, r, oversample, power_iters, tau, seed, kPhaseSubspace, stream);
+}
+
+extern "C" int sc_build_ritz_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
+                                     int oversample, int power_iters, float tau, uint64_t seed,
+                                     hipStream_t stream)
+{
+    return build_batched(count, mats, dt, beta, r, oversample, power_iters, tau, seed, kPhaseRitz, stream);
 }
 
 extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,

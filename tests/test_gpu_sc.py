@@ -247,6 +247,47 @@ def test_batched_calls_equal_single_calls(pk):
             assert torch.equal(x, y)
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_build_in_two_phases_equals_one_call(pk, fused):
+    """sc_build_subspace_batched then sc_build_ritz_batched (the same
+    arguments and workspaces) give bit-identical EMA state and prior to one
+    sc_build_prior_batched call, with the unfused EMA (a small mixed batch)
+    and with the EMA fused with the first pass (8 x 8192 x 512, 256 row
+    blocks); the ritz phase leaves M alone."""
+    if fused:
+        shapes, r, p = [(8192, 512)] * 8, 32, 16
+    else:
+        shapes, r, p = [(256, 384), (384, 256), (200, 328)], 16, 8
+    q = 2
+    runs = []
+    for split in (False, True):
+        items = []
+        for i, (m, n) in enumerate(shapes):
+            gp = workloads.grad_pair(workloads.GradSpec(((m, n),), r, (1.0, 100.0), (r,), torch.bfloat16,
+                                                        None, None), 9, i, 0, "cpu")
+            outs = (torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
+                    torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda"))
+            items.append(dict(G_anc=gp.G_anc.cuda(), M=torch.zeros(m, n, device="cuda"), out=outs,
+                              ws=pk.workspace(m, n, r, p, torch.bfloat16)))
+        args = (r, workloads.BETA, workloads.TAU, p, q)
+        if split:
+            pk.sc_build_subspace_batched(items, *args, seed=70)
+            torch.cuda.synchronize()
+            M_mid = [it["M"].clone() for it in items]
+            pk.sc_build_ritz_batched(items, *args, seed=70)
+            torch.cuda.synchronize()
+            for it, Mm in zip(items, M_mid):
+                assert torch.equal(it["M"], Mm)
+        else:
+            pk.sc_build_prior_batched(items, *args, seed=70)
+            torch.cuda.synchronize()
+        runs.append(items)
+    for a, b in zip(*runs):
+        assert torch.equal(a["M"], b["M"])
+        for x, y in zip(a["out"], b["out"]):
+            assert torch.equal(x, y)
+
+
 def test_large_batch_takes_the_fused_ema_pass(pk):
     """A batch with enough row blocks to fill the GPU (8 matrices of 8192 x 512:
     256 row blocks of 256 rows) runs the anchor EMA fused with the first pass
