@@ -435,7 +435,7 @@ def main():
         "config": {"workload": f"{cfg.name}: activation [{act.B},{act.S},{H}] keep {keep} (K={K}) "
                                f"fwd+bwd x{L} layers; gradients {shapes} x{L} layers, rank-{gs.rank} "
                                f"signal + noise; r={r}, k={kk}, power_iters={q}",
-                   "step": "in order on one stream: mask, anchor-prior build, correction with that prior",
+                   "step": "anchor-prior subspace iteration alone; then its Rayleigh-Ritz step and the correction with that prior, the masking beside them on a second stream",
                    "step_bytes": step_bytes, "step_flops": step_flops,
                    "step_TFLOP/s": round(step_flops / (ms_per_step * 1e-3) / 1e12, 2)},
         "roofline": roof,
