@@ -253,3 +253,118 @@ def test_correct_rows_equals_the_rows_of_the_whole_correction():
     assert np.allclose(got, whole[rows], rtol=1e-12, atol=1e-12)
     got2 = osp.correct_rows(lambda a, b: G[a:b], U, d, V, 0.3, rows)
     assert np.allclose(got2, whole[rows], rtol=1e-12, atol=1e-12)
+
+
+def _orthonormal_columns(rows, cols, seed):
+    q, r = np.linalg.qr(np.random.default_rng(seed).standard_normal((rows, cols)))
+    return q * np.sign(np.diag(r))
+
+
+def test_projector_distance_is_the_sine_of_the_principal_angles():
+    """||P1 - P2||_F^2 = 2 sum_i sin^2(theta_i) for r-dimensional subspaces at
+    principal angles theta_i, so the distance over sqrt(2 r) is sin(eps) when
+    every angle is eps, 1 for orthogonal subspaces and 0 for a rotation of the
+    basis inside its span (the diagnostic the parity tests report)."""
+    m, r = 50, 4
+    B = _orthonormal_columns(m, 2 * r, 31)
+    Q, W = B[:, :r], B[:, r:]
+    for eps in (0.0, 0.05, 0.2, 0.7, np.pi / 2):
+        Q2 = Q * np.cos(eps) + W * np.sin(eps)
+        assert abs(osp.projector_distance(Q, Q2) - np.sin(eps)) < 1e-13, eps
+    assert abs(osp.projector_distance(Q, W) - 1.0) < 1e-13
+    R = _orthonormal_columns(r, r, 32)
+    assert osp.projector_distance(Q, Q @ R) < 1e-13
+    # unequal angles a, b on two of the columns (the other two shared)
+    a, b = 0.3, 1.1
+    Q3 = Q.copy()
+    Q3[:, 0] = Q[:, 0] * np.cos(a) + W[:, 0] * np.sin(a)
+    Q3[:, 1] = Q[:, 1] * np.cos(b) + W[:, 1] * np.sin(b)
+    expect = np.sqrt((np.sin(a) ** 2 + np.sin(b) ** 2) / r)
+    assert abs(osp.projector_distance(Q, Q3) - expect) < 1e-13
+
+
+def test_rel_fro_on_hand_computed_pairs():
+    """||a - b||_F / ||b||_F: the reference b is the denominator."""
+    a = np.array([[1.0, 0.0], [0.0, 0.0]])
+    b = np.array([[0.0, 2.0], [0.0, 0.0]])
+    assert abs(osp.rel_fro(a, b) - np.sqrt(5.0) / 2.0) < 1e-15      # ||b|| = 2, ||a|| = 1
+    assert abs(osp.rel_fro(b, a) - np.sqrt(5.0)) < 1e-15
+    c = np.array([3.0, 4.0])
+    assert abs(osp.rel_fro(1.1 * c, c) - 0.1) < 1e-14                # a relative scale error
+    assert osp.rel_fro(c, c) == 0.0
+    assert osp.rel_fro(c, np.zeros(2)) == 5.0                        # zero reference: absolute error
+
+
+def test_alignment_splits_a_gradient_into_its_in_and_out_of_subspace_energy():
+    """eta_r = ||U^T g V||^2 / ||g||^2 (App. G): for g = U C V^T + g_out with
+    U^T g_out V = 0, eta = ||C||^2 / (||C||^2 + ||g_out||^2)."""
+    m, n, r = 30, 22, 3
+    U = _orthonormal_columns(m, r, 41)
+    V = _orthonormal_columns(n, r, 42)
+    C = np.array([[2.0, 0.5, 0.0], [0.0, 1.0, -1.0], [0.25, 0.0, 3.0]])
+    g_in = U @ C @ V.T
+    N = np.random.default_rng(43).standard_normal((m, n))
+    g_out = N - U @ (U.T @ N)                    # U^T g_out = 0
+    for scale in (0.5, 1.0, 3.0):
+        g = g_in + scale * g_out
+        a = np.sum(C ** 2)
+        b = scale ** 2 * np.sum(g_out ** 2)
+        assert abs(osp.alignment(g, U, V) - a / (a + b)) < 1e-13, scale
+    assert abs(osp.alignment(g_in, U, V) - 1.0) < 1e-13
+    assert osp.alignment(g_out, U, V) < 1e-28
+    assert osp.alignment(np.zeros((m, n)), U, V) == 0.0
+
+
+def test_planted_mistakes_in_the_comparison_helpers_are_caught(monkeypatch):
+    """Plausible slips in the helpers that gate every parity assertion each
+    fail one of the pins above."""
+    mutants = {
+        "projector_distance": [
+            lambda U1, U2: 0.0,
+            lambda U1, U2: float(np.linalg.norm(U1 @ U1.T - U2 @ U2.T)),
+            lambda U1, U2: float(np.linalg.norm(U1 @ U1.T - U2 @ U2.T) / np.sqrt(U1.shape[1])),
+            lambda U1, U2: float(np.linalg.norm(U1 - U2) / np.sqrt(2.0 * U1.shape[1])),
+        ],
+        "rel_fro": [
+            lambda a, b: float(np.linalg.norm(np.subtract(a, b)) / np.linalg.norm(a)),
+            lambda a, b: float(np.linalg.norm(np.subtract(a, b))),
+            lambda a, b: float(np.linalg.norm(np.subtract(a, b)) ** 2 / np.linalg.norm(b) ** 2),
+        ],
+        "alignment": [
+            lambda g, U, V: float(np.linalg.norm(U.T @ g @ V) / np.linalg.norm(g)),
+            lambda g, U, V: float(np.linalg.norm(U.T @ g) ** 2 / np.linalg.norm(g) ** 2),
+            lambda g, U, V: float(np.linalg.norm(U.T @ g @ V) ** 2),
+        ],
+    }
+    pins = {
+        "projector_distance": test_projector_distance_is_the_sine_of_the_principal_angles,
+        "rel_fro": test_rel_fro_on_hand_computed_pairs,
+        "alignment": test_alignment_splits_a_gradient_into_its_in_and_out_of_subspace_energy,
+    }
+    for name, fns in mutants.items():
+        orig = getattr(osp, name)
+        for k, fn in enumerate(fns):
+            monkeypatch.setattr(osp, name, fn)
+            with pytest.raises(AssertionError), np.errstate(all="ignore"):
+                pins[name]()
+            monkeypatch.setattr(osp, name, orig)
+        pins[name]()
+
+
+def test_transposed_filter_operand_is_caught_by_idempotence():
+    """A transposed inner operand (U X^T V^T in place of U X V^T, which the
+    closed form cannot see because X is diagonal there) breaks the projector
+    identity at tau = 0."""
+    U, s, V = _basis(26, 19, 5, 4)
+    d = osp.filter_weights(s, 0.0)
+    A = np.random.default_rng(5).standard_normal((26, 19))
+
+    def transposed(G, U_, d_, V_):
+        X = U_.T @ np.asarray(G, dtype=np.float64) @ V_
+        Xf = d_[:, None] * X.T * d_[None, :]
+        return U_ @ Xf @ V_.T
+
+    P = lambda X: transposed(X, U, d, V)
+    assert not np.allclose(P(P(A)), P(A), atol=1e-12)
+    Q = lambda X: osp.two_sided_filter(X, U, d, V)
+    assert np.allclose(Q(Q(A)), Q(A), atol=1e-12)
