@@ -4,7 +4,11 @@
 One step = every row of the hot path once, over one batch of synthetic input
 resident in HBM (70B-class slice, four layers):
   per layer: pack + unpack of the boundary activation (forward) and of the
-  activation gradient (backward, same mask key);
+  activation gradient (backward, same mask key), each a batched launch over
+  the four boundaries.  Each side evaluates the mask once: the sender packs
+  from the key and keeps the kept positions, the receiver unpacks the
+  values-only payload from the key and keeps its own; the backward pack and
+  unpack read those lists;
   per weight matrix (3 per layer): anchor EMA + top-r SVD + filter
   (sc_build_prior), then the spectral correction of the masked gradient
   (sc_correct) with that prior.
@@ -103,14 +107,20 @@ def main():
     t0 = time.time()
 
     # ---------------- inputs, resident in HBM ----------------
-    xs, gxs, keys = [], [], []
+    # the L boundaries' activations (and gradients) stacked [L, rows, H];
+    # boundary l is keyed with layer l
+    x_all = torch.empty(L, rows, H, dtype=act.dtype, device=dev)
+    gx_all = torch.empty_like(x_all)
+    keys = []
     for l in range(L):
-        xs.append(workloads.activation(act, cfg.cid, l, 0, dev))
-        gxs.append(workloads.activation(act, cfg.cid, l, 1, dev))
+        x_all[l] = workloads.activation(act, cfg.cid, l, 0, dev)
+        gx_all[l] = workloads.activation(act, cfg.cid, l, 1, dev)
         keys.append(pk.make_key(B=act.B, S=act.S, H=H, **workloads.mask_key_fields(cfg.cid, layer=l)))
-    vals = [[torch.empty(rows, K, dtype=act.dtype, device=dev) for _ in range(2)] for _ in range(L)]
-    idxs = [[torch.empty(rows, K, dtype=torch.int16, device=dev) for _ in range(2)] for _ in range(L)]
-    ys = [[torch.empty(rows, H, dtype=act.dtype, device=dev) for _ in range(2)] for _ in range(L)]
+    xs, gxs = [x_all[l] for l in range(L)], [gx_all[l] for l in range(L)]
+    vals = [torch.empty(L, rows, K, dtype=act.dtype, device=dev) for _ in range(2)]
+    idx_s = torch.empty(L, rows, K, dtype=torch.int16, device=dev)      # the sender's kept positions
+    idx_r = torch.empty_like(idx_s)                                      # the receiver's
+    ys = [torch.empty(L, rows, H, dtype=act.dtype, device=dev) for _ in range(2)]
     mats = []
     nbuf = 2
     for l in range(L):
@@ -183,11 +193,14 @@ def main():
         return b0, b1
 
     def masking():
-        for l in range(L):
-            for dirn, src in enumerate((xs[l], gxs[l])):      # forward, then backward
-                pk.ac_mask_pack(src, K, keys[l], vals=vals[l][dirn], idx=idxs[l][dirn])
-                pk.ac_unpack_scatter(vals[l][dirn], H, keys[l], scale, idx=idxs[l][dirn],
-                                     y=ys[l][dirn])
+        # forward: the sender packs from the key (keeping its index lists), the
+        # receiver unpacks the values-only payload from the key (keeping its
+        # own); backward: the receiver packs the gradient from its lists, the
+        # sender unpacks it from its lists
+        pk.ac_mask_pack_batched(x_all, K, keys[0], vals=vals[0], idx_out=idx_s)
+        pk.ac_unpack_scatter_batched(vals[0], H, keys[0], scale, idx_out=idx_r, y=ys[0])
+        pk.ac_mask_pack_batched(gx_all, K, keys[0], vals=vals[1], idx_in=idx_r)
+        pk.ac_unpack_scatter_batched(vals[1], H, keys[0], scale, idx_in=idx_s, y=ys[1])
 
     def step(record: bool):
         i = n_steps_run[0]
@@ -264,8 +277,11 @@ def main():
     fused_first = int(round(pass_launches)) == passes - 1
     shadow_passes = passes - 1 if fused_first else passes
     kk = min(r + p, min(gs.shapes[0]))
-    work = {"ac_pack": dict(bytes=2 * L * pack_bytes, calls=2 * L),
-            "ac_unpack": dict(bytes=2 * L * unpack_bytes, calls=2 * L),
+    # every form moves the same bytes per row: the key-driven pack writes the
+    # index lists the index-driven one reads, and likewise for the unpack
+    work = {"ac_pack": dict(bytes=L * pack_bytes, calls=1), "ac_pack_idx": dict(bytes=L * pack_bytes, calls=1),
+            "ac_unpack": dict(bytes=L * unpack_bytes, calls=1),
+            "ac_unpack_idx": dict(bytes=L * unpack_bytes, calls=1),
             "sc_ema": dict(bytes=0.0, calls=0), "sc_pass": dict(flops=0.0, bytes=0.0, calls=0),
             "sc_correct": dict(bytes=0.0, flops=0.0, calls=0),
             "sc_blend": dict(bytes=0.0, flops=0.0, calls=0), "sc_gv": dict(bytes=0.0, flops=0.0, calls=0)}
@@ -287,8 +303,9 @@ def main():
         work["sc_gv"]["bytes"] += 1.0 * m * n * gsz
         work["sc_gv"]["flops"] += 2.0 * m * n * r
         work["sc_gv"]["calls"] += 1
-    step_bytes = (work["ac_pack"]["bytes"] + work["ac_unpack"]["bytes"] + work["sc_ema"]["bytes"]
-                  + work["sc_pass"]["bytes"] + work["sc_correct"]["bytes"])
+    ac_tags = ("ac_pack", "ac_pack_idx", "ac_unpack", "ac_unpack_idx")
+    ac_bytes = sum(work[t]["bytes"] for t in ac_tags)
+    step_bytes = ac_bytes + work["sc_ema"]["bytes"] + work["sc_pass"]["bytes"] + work["sc_correct"]["bytes"]
     step_flops = work["sc_pass"]["flops"] + work["sc_ema"].get("flops", 0.0) + work["sc_correct"]["flops"]
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
 
@@ -300,7 +317,7 @@ def main():
         kern[name] = dict(launches_per_step=n, ms_per_step=ms, avg_us=1e3 * ms / max(n, 1e-9))
     # roofline models for the kernels whose work has a clean algorithmic count
     def model(name):
-        if name in ("ac_pack", "ac_unpack", "sc_ema"):
+        if name in ac_tags or name == "sc_ema":
             return "hbm", work[name]["bytes"], work[name]["calls"]
         if name == "sc_blend":
             return "hbm", work["sc_blend"]["bytes"], work["sc_blend"]["calls"]
@@ -352,7 +369,7 @@ def main():
                  "traffic": measured_traffic(dom, cfg.cid)})
 
     comp = {}
-    for name in ("ac_pack", "ac_unpack", "sc_ema", "sc_gv", "sc_blend"):
+    for name in ac_tags + ("sc_ema", "sc_gv", "sc_blend"):
         if name in per_step:
             n, ms = per_step[name]
             gbs = work[name]["bytes"] / (ms * 1e-3) / 1e9
@@ -368,8 +385,7 @@ def main():
     comp["phase_ms"] = {k: round(v, 4) for k, v in phase_ms.items()}
     comp["sc_correct_step"] = {"GB/s": round(work["sc_correct"]["bytes"] / (phase_ms["correct"] * 1e-3) / 1e9, 1),
                                "TFLOP/s": round(work["sc_correct"]["flops"] / (phase_ms["correct"] * 1e-3) / 1e12, 2)}
-    comp["ac_step"] = {"GB/s": round((work["ac_pack"]["bytes"] + work["ac_unpack"]["bytes"])
-                                     / (phase_ms["ac"] * 1e-3) / 1e9, 1)}
+    comp["ac_step"] = {"GB/s": round(ac_bytes / (phase_ms["ac"] * 1e-3) / 1e9, 1)}
     comp["kernels"] = {k: {kk_: round(v, 4) if isinstance(v, float) else v for kk_, v in d.items()}
                        for k, d in sorted(kern.items())}
 
@@ -406,7 +422,7 @@ def main():
             pk.acsc_stats_enable(False)
             # the masking kernels on their own (in the timed step they share
             # the GPU with the Rayleigh-Ritz step)
-            for tag in ("ac_pack", "ac_unpack"):
+            for tag in ac_tags:
                 if tag in st:
                     kms = st[tag][1] / args.steps
                     gbs = work[tag]["bytes"] / (kms * 1e-3) / 1e9

@@ -115,6 +115,44 @@ int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int6
                       int K, const ac_mask_key *key, float scale, void *y, int64_t ld_y,
                       hipStream_t stream);
 
+/* Batched forms over nlayers pipeline boundaries in one launch (Alg. 1: the
+ * boundary after layer l has its own mask M_l = g(l, t, B, S, H); Sec. 3.1).
+ * Boundary l (0 <= l < nlayers) is keyed exactly as the single call with
+ * key->layer + l, and its tensors start at base + l * stride, strides counted
+ * in elements of the array they step:
+ *   x / y      [rows, ld] of dt per boundary, stride x_stride / y_stride;
+ *   vals       [rows, K] contiguous per boundary, stride vals_stride;
+ *   idx_in, idx_out   [rows, K] uint16 per boundary, stride idx_stride.
+ * Each boundary's result is bit-identical to the single call on its tensors.
+ *
+ * Index lists let each stage evaluate a boundary's mask once (the paper's
+ * shared PRF: both stages rebuild it, neither sends it):
+ *   pack   idx_in == NULL: the mask comes from the key; idx_out (or NULL)
+ *          receives the kept positions (what ac_mask_pack writes to idx).
+ *          idx_in != NULL: vals[r, i] = x[r, idx_in[r, i]] (bit copies; an
+ *          entry >= H gives +0) and the key's fields other than layer are
+ *          only checked; idx_out must then be NULL.
+ *   unpack idx_in == NULL: positions from the key; idx_out (or NULL)
+ *          receives them.  idx_in != NULL: as ac_unpack_scatter with idx
+ *          (strictly ascending rows; entries >= H ignored); idx_out NULL.
+ * So the sender packs from the key writing idx_out and later unpacks the
+ * gradient from those lists, and the receiver unpacks from the key writing
+ * idx_out and packs the gradient from them: only the values cross the link.
+ * Requirements as the single calls, plus 0 <= nlayers <= 65535 (0 is a
+ * no-op), key->layer + nlayers - 1 < 2^32, non-negative input strides, and
+ * output strides that keep boundaries apart when nlayers > 1:
+ * vals_stride >= rows * K, idx_stride >= rows * K (with idx_out),
+ * y_stride >= (rows - 1) * ld_y + H.  16-byte stores are used only when
+ * every boundary's rows are 16-byte aligned. */
+int ac_mask_pack_batched(const void *x, acsc_dtype dt, int nlayers, int64_t rows, int H, int64_t ld_x,
+                         int64_t x_stride, int K, const ac_mask_key *key, void *vals, int64_t vals_stride,
+                         const uint16_t *idx_in, uint16_t *idx_out, int64_t idx_stride,
+                         hipStream_t stream);
+int ac_unpack_scatter_batched(const void *vals, int64_t vals_stride, acsc_dtype dt, int nlayers, int64_t rows,
+                              int H, int K, const ac_mask_key *key, const uint16_t *idx_in, uint16_t *idx_out,
+                              int64_t idx_stride, float scale, void *y, int64_t ld_y, int64_t y_stride,
+                              hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Bernoulli mask variant (App. F: every entry of the mask an independent
  * Bernoulli draw, kept with probability 1 - p; the receiver rescales by

@@ -15,11 +15,15 @@ Readings of the paper taken here (the paper does not fix them):
   * tau acts on the raw singular values of the EMA;
   * 0 / 0 in the filter (s_i = 0 with tau = 0) is taken as d_i = 0, so an
     empty prior (M = 0) gives G_proj = alpha * G.
-The SVD is LAPACK's (numpy.linalg.svd), a library primitive.
+The SVD is LAPACK's (numpy.linalg.svd), a library primitive.  For matrices
+whose full SVD would take minutes on the host, ``top_r_svd_gram`` reaches the
+same top-r triplets through the symmetric eigendecomposition of the smaller
+Gram matrix (LAPACK's dsyevr, also a library primitive).
 """
 from __future__ import annotations
 
 import numpy as np
+import scipy.linalg
 
 
 def ema(M_prev: np.ndarray, G_anc: np.ndarray, beta: float) -> np.ndarray:
@@ -34,6 +38,30 @@ def top_r_svd(M: np.ndarray, r: int):
     M = np.asarray(M, dtype=np.float64)
     U, s, Vt = np.linalg.svd(M, full_matrices=False)
     return U[:, :r].copy(), s[:r].copy(), Vt[:r, :].T.copy()
+
+
+def top_r_svd_gram(M: np.ndarray, r: int):
+    """Top-r singular triplets of M (Sec. 3.2; App. E truncation) from the
+    Gram matrix of its shorter side.
+
+    For m <= n, M M^T = U S^2 U^T: the r largest eigenpairs give U and s, and
+    V = M^T U S^-1 (column i is M^T u_i / s_i).  For m > n the roles swap
+    through M^T M = V S^2 V^T.  A zero singular value leaves a zero column on
+    the derived side.  Returns U [m, r], s [r] (descending), V [n, r]."""
+    M = np.asarray(M, dtype=np.float64)
+    m, n = M.shape
+    wide = m <= n
+    A = M @ M.T if wide else M.T @ M
+    k = A.shape[0]
+    w, X = scipy.linalg.eigh(A, subset_by_index=[k - r, k - 1], driver="evr")
+    order = np.argsort(w)[::-1]
+    w, X = np.maximum(w[order], 0.0), X[:, order]
+    s = np.sqrt(w)
+    Y = M.T @ X if wide else M @ X
+    inv = np.zeros_like(s)
+    inv[s > 0] = 1.0 / s[s > 0]
+    Y = Y * inv
+    return (X, s, Y) if wide else (Y, s, X)
 
 
 def filter_weights(s: np.ndarray, tau: float) -> np.ndarray:
@@ -102,12 +130,21 @@ def alignment(g: np.ndarray, U: np.ndarray, V: np.ndarray) -> float:
     return float(num / den) if den > 0 else 0.0
 
 
-def projector_distance(U1: np.ndarray, U2: np.ndarray) -> float:
-    """||U1 U1^T - U2 U2^T||_F / sqrt(2 r): basis-free subspace distance."""
+def projector_distance(U1: np.ndarray, U2: np.ndarray, method: str = "auto") -> float:
+    """||U1 U1^T - U2 U2^T||_F / sqrt(2 r): basis-free subspace distance.
+
+    "projector" forms the two m x m projectors.  "residual" (the default past
+    m = 4096, where those would take gigabytes) uses, for orthonormal bases
+    of equal rank at principal angles theta_i,
+    ||P1 - P2||_F^2 = 2 sum sin^2 theta_i = 2 ||U1 - U2 (U2^T U1)||_F^2."""
     r = U1.shape[1]
-    P1 = U1 @ U1.T
-    P2 = U2 @ U2.T
-    return float(np.linalg.norm(P1 - P2) / np.sqrt(2.0 * r))
+    if method == "auto":
+        method = "projector" if U1.shape[0] <= 4096 else "residual"
+    if method == "projector":
+        P1 = U1 @ U1.T
+        P2 = U2 @ U2.T
+        return float(np.linalg.norm(P1 - P2) / np.sqrt(2.0 * r))
+    return float(np.linalg.norm(U1 - U2 @ (U2.T @ U1)) / np.sqrt(r))
 
 
 def rel_fro(a, b) -> float:

@@ -79,6 +79,12 @@ def _load():
     lib.ac_unpack_scatter.restype = i32
     lib.ac_unpack_scatter.argtypes = [vp, vp, i32, i64, i32, i32, C.POINTER(MaskKey), f32, vp,
                                       i64, vp]
+    lib.ac_mask_pack_batched.restype = i32
+    lib.ac_mask_pack_batched.argtypes = [vp, i32, i32, i64, i32, i64, i64, i32, C.POINTER(MaskKey), vp, i64,
+                                         vp, vp, i64, vp]
+    lib.ac_unpack_scatter_batched.restype = i32
+    lib.ac_unpack_scatter_batched.argtypes = [vp, i64, i32, i32, i64, i32, i32, C.POINTER(MaskKey), vp, vp, i64,
+                                              f32, vp, i64, i64, vp]
     lib.ac_bern_mask.restype = i32
     lib.ac_bern_mask.argtypes = [i64, i32, C.c_double, C.POINTER(MaskKey), vp, vp, vp]
     lib.ac_bern_pack.restype = i32
@@ -118,7 +124,8 @@ def _load():
 lib = _load()
 
 EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
-            "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "sc_workspace_size",
+            "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "ac_mask_pack_batched",
+            "ac_unpack_scatter_batched", "sc_workspace_size",
             "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched",
             "sc_build_subspace_batched", "sc_build_ritz_batched",
             "sc_adamw_workspace_size", "sc_correct_adamw_batched",
@@ -224,6 +231,66 @@ def ac_unpack_scatter(vals: torch.Tensor, H: int, key: MaskKey, scale: float = 1
         raise AcscError(ACSC_EINVAL, "vals must be contiguous and y 2-D with unit column stride")
     _check(lib.ac_unpack_scatter(_ptr(vals), _ptr(idx), _dt(vals), rows, H, K, C.byref(key),
                                  float(scale), _ptr(y), y.stride(0), _stream(stream)))
+    return y
+
+
+def _layer_stride(t: torch.Tensor) -> int:
+    return t.stride(0) if t.shape[0] > 1 else 0
+
+
+def ac_mask_pack_batched(x: torch.Tensor, K: int, key: MaskKey, vals: Optional[torch.Tensor] = None,
+                         idx_in: Optional[torch.Tensor] = None, idx_out: Optional[torch.Tensor] = None,
+                         stream=None) -> torch.Tensor:
+    """x: [nlayers, rows, H] (unit column stride; row and layer strides taken
+    from the tensor).  Boundary l is keyed with key.layer + l.  Returns vals
+    [nlayers, rows, K].  idx_in: [nlayers, rows, K] index lists to pack at
+    (no mask evaluated); idx_out: receives the kept positions (int16 holding
+    uint16 patterns)."""
+    _need_cuda(x, vals, idx_in, idx_out)
+    if x.dim() != 3 or x.stride(2) != 1:
+        raise AcscError(ACSC_EINVAL, "x must be [nlayers, rows, H] with unit column stride")
+    nl, rows, H = x.shape
+    if vals is None:
+        vals = torch.empty(nl, rows, K, dtype=x.dtype, device=x.device)
+    _need_cuda(vals)
+    idx_stride = 0
+    for t in (idx_in, idx_out):
+        if t is not None:
+            if tuple(t.shape) != (nl, rows, K) or t.stride(2) != 1 or t.stride(1) != K:
+                raise AcscError(ACSC_EINVAL, "index lists must be [nlayers, rows, K] with contiguous rows")
+            idx_stride = _layer_stride(t)
+    if tuple(vals.shape) != (nl, rows, K) or vals.stride(2) != 1 or vals.stride(1) != K:
+        raise AcscError(ACSC_EINVAL, "vals must be [nlayers, rows, K] with contiguous rows")
+    _check(lib.ac_mask_pack_batched(_ptr(x), _dt(x), nl, rows, H, x.stride(1), _layer_stride(x), K, C.byref(key),
+                                    _ptr(vals), _layer_stride(vals), _ptr(idx_in), _ptr(idx_out), idx_stride,
+                                    _stream(stream)))
+    return vals
+
+
+def ac_unpack_scatter_batched(vals: torch.Tensor, H: int, key: MaskKey, scale: float = 1.0,
+                              idx_in: Optional[torch.Tensor] = None, idx_out: Optional[torch.Tensor] = None,
+                              y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """vals: [nlayers, rows, K].  Returns (or fills) y [nlayers, rows, H].
+    idx_in: transmitted or kept index lists; idx_out: receives the positions
+    rebuilt from the key."""
+    _need_cuda(vals, idx_in, idx_out)
+    if vals.dim() != 3 or vals.stride(2) != 1 or vals.stride(1) != vals.shape[2]:
+        raise AcscError(ACSC_EINVAL, "vals must be [nlayers, rows, K] with contiguous rows")
+    nl, rows, K = vals.shape
+    if y is None:
+        y = torch.empty(nl, rows, H, dtype=vals.dtype, device=vals.device)
+    _need_cuda(y)
+    if y.dim() != 3 or y.stride(2) != 1 or tuple(y.shape) != (nl, rows, H):
+        raise AcscError(ACSC_EINVAL, "y must be [nlayers, rows, H] with unit column stride")
+    idx_stride = 0
+    for t in (idx_in, idx_out):
+        if t is not None:
+            if tuple(t.shape) != (nl, rows, K) or t.stride(2) != 1 or t.stride(1) != K:
+                raise AcscError(ACSC_EINVAL, "index lists must be [nlayers, rows, K] with contiguous rows")
+            idx_stride = _layer_stride(t)
+    _check(lib.ac_unpack_scatter_batched(_ptr(vals), _layer_stride(vals), _dt(vals), nl, rows, H, K, C.byref(key),
+                                         _ptr(idx_in), _ptr(idx_out), idx_stride, float(scale), _ptr(y), y.stride(1),
+                                         _layer_stride(y), _stream(stream)))
     return y
 
 

@@ -40,14 +40,39 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t h)
 }
 
 // Key chain over the fields of g(layer, step, B, S, H), plus seed and microbatch.
+__host__ __device__ __forceinline__ uint64_t chain_fields(uint64_t seed, uint64_t layer, uint64_t step,
+                                                          uint64_t microbatch, uint64_t B, uint64_t S, uint64_t H)
+{
+    uint64_t z = seed;
+    z = mix64((z ^ layer) + kGamma);
+    z = mix64((z ^ step) + kGamma);
+    z = mix64((z ^ microbatch) + kGamma);
+    z = mix64((z ^ B) + kGamma);
+    z = mix64((z ^ S) + kGamma);
+    return mix64((z ^ H) + kGamma);
+}
+
 uint64_t chain_key(const ac_mask_key &k)
 {
-    const uint64_t f[6] = {k.layer, k.step, k.microbatch, k.B, k.S, k.H};
-    uint64_t z = k.seed;
-    for (int i = 0; i < 6; ++i)
-        z = mix64((z ^ f[i]) + kGamma);
-    return z;
+    return chain_fields(k.seed, k.layer, k.step, k.microbatch, k.B, k.S, k.H);
 }
+
+// What a launch over several boundaries needs besides the row data: the key
+// of the first boundary (boundary l of the launch, blockIdx.y, is keyed with
+// layer + l, Alg. 1's per-boundary mask) and the element strides between
+// consecutive boundaries' tensors.
+struct MaskBatch {
+    uint64_t seed, step;
+    uint32_t layer, microbatch, B, S, H;
+    int64_t dense_stride;   // x (pack) or y (unpack)
+    int64_t vals_stride;
+    int64_t idx_stride;     // idx_in and idx_out
+
+    __device__ __forceinline__ uint64_t key(uint32_t l) const
+    {
+        return chain_fields(seed, static_cast<uint64_t>(layer) + l, step, microbatch, B, S, H);
+    }
+};
 
 int domain_bits(int H)
 {
@@ -214,9 +239,50 @@ __host__ __device__ __forceinline__ int pack_wave_bytes(int nw, int K)
     return 4 * pack_wave_words(nw, K) + (TABLE ? table_bytes<ROUNDS>() : 0);
 }
 
+// Pack by given index lists (FROM_IDX): the row's K indices are read from
+// idx_in, entries >= H give +0, and nothing of the mask is evaluated.  This is
+// the pack of the direction that did not compute the mask: the receiving
+// stage's backward pack reuses the index lists its key-driven unpack wrote.
+template <typename E>
+__global__ __launch_bounds__(256) void ac_pack_idx_kernel(const E *__restrict__ x, int64_t rows, int H,
+                                                          int64_t ld_x, int K, MaskBatch mb,
+                                                          const uint16_t *__restrict__ idx_in,
+                                                          E *__restrict__ vals)
+{
+    const int lane = threadIdx.x & 63;
+    const int wpb = blockDim.x >> 6;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (row >= rows)
+        return;
+    const uint32_t layer = blockIdx.y;
+    const E *xr = x + layer * mb.dense_stride + row * ld_x;
+    const uint16_t *ir = idx_in + layer * mb.idx_stride + row * K;
+    E *vr = vals + layer * mb.vals_stride + row * K;
+    for (int base = 0; base < K; base += 256) {
+        uint16_t jj[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + lane + 64 * u;
+            jj[u] = i < K ? ir[i] : uint16_t(0);
+        }
+        E v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + lane + 64 * u;
+            v[u] = (i < K && jj[u] < H) ? xr[jj[u]] : E(0);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + lane + 64 * u;
+            if (i < K)
+                vr[i] = v[u];
+        }
+    }
+}
+
 template <typename E, int ROUNDS, bool TABLE>
 __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, int64_t rows, int H,
-                                                      int64_t ld_x, int K, uint64_t key, int w,
+                                                      int64_t ld_x, int K, MaskBatch mb, int w,
                                                       E *__restrict__ vals,
                                                       uint16_t *__restrict__ idx)
 {
@@ -233,6 +299,12 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
 
     if (!active)
         return;
+    const uint32_t layer = blockIdx.y;
+    const uint64_t key = mb.key(layer);
+    x += layer * mb.dense_stride;
+    vals += layer * mb.vals_stride;
+    if (idx)
+        idx += layer * mb.idx_stride;
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
     {
@@ -405,7 +477,7 @@ __device__ __forceinline__ void row_bitmap(uint32_t *bm, uint32_t *pre, int nw, 
 // the packed row (and its indices) leaves with coalesced stores.
 template <typename E, int ROUNDS, bool TABLE>
 __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict__ x, int64_t rows, int H,
-                                                             int64_t ld_x, int K, uint64_t key, int w,
+                                                             int64_t ld_x, int K, MaskBatch mb, int w,
                                                              E *__restrict__ vals,
                                                              uint16_t *__restrict__ idx)
 {
@@ -424,6 +496,12 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
     uint16_t *ki = reinterpret_cast<uint16_t *>(kv + K);
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
+    const uint32_t layer = blockIdx.y;
+    const uint64_t key = mb.key(layer);
+    x += layer * mb.dense_stride;
+    vals += layer * mb.vals_stride;
+    if (idx)
+        idx += layer * mb.idx_stride;
     row_bitmap<ROUNDS, TABLE>(bm, pre, nw, active, key, row, w, H, K, lane, nullptr,
                               reinterpret_cast<uint8_t *>(bm) + staged);
     if (active) {
@@ -476,12 +554,28 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
 // Every lane's work is uniform (zeroing and copying) except the drop of the
 // few kept entries, where writing each 16-byte chunk with its kept entries in
 // place made every lane of the wave pay for the chunks that hold one.
+// The kept positions of a row, ascending, from its bitmap and word prefix:
+// every lane walks its words and stores each set bit's position at its rank.
+__device__ __forceinline__ void store_index_list(const uint32_t *bm, const uint32_t *pre, int nw, int lane,
+                                                 uint16_t *__restrict__ out)
+{
+    for (int wd = lane; wd < nw; wd += 64) {
+        uint32_t bits = bm[wd];
+        int rank = static_cast<int>(pre[wd]);
+        while (bits) {
+            const int t = __ffs(bits) - 1;
+            bits &= bits - 1u;
+            out[rank++] = static_cast<uint16_t>((wd << 5) + t);
+        }
+    }
+}
+
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC, bool TABLE>
 __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restrict__ vals,
                                                                const uint16_t *__restrict__ idx,
-                                                               int64_t rows, int H, int K, uint64_t key,
+                                                               int64_t rows, int H, int K, MaskBatch mb,
                                                                int w, float scale, E *__restrict__ y,
-                                                               int64_t ld_y)
+                                                               int64_t ld_y, uint16_t *__restrict__ idx_out)
 {
     extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
     const int lane = threadIdx.x & 63;
@@ -495,6 +589,12 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
     E *kv = reinterpret_cast<E *>(pre + nw);
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
+    const uint32_t layer = blockIdx.y;
+    const uint64_t key = FROM_IDX ? 0 : mb.key(layer);
+    vals += layer * mb.vals_stride;
+    y += layer * mb.dense_stride;
+    if (FROM_IDX)
+        idx += layer * mb.idx_stride;
     if (active) {
         const E *vr = vals + row * K;
         for (int i = lane; i < K; i += 64)
@@ -505,6 +605,8 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
                               reinterpret_cast<uint8_t *>(bm) + staged);
     if (!active)
         return;
+    if (!FROM_IDX && idx_out)
+        store_index_list(bm, pre, nw, lane, idx_out + layer * mb.idx_stride + row * K);
     // The dense row is assembled in LDS one segment (64 bitmap words) at a
     // time: zero the segment, drop the kept entries into it, then write it out
     // with whole 16-byte stores.  Global memory only sees full lines.
@@ -550,9 +652,9 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
 __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ vals,
                                                         const uint16_t *__restrict__ idx,
-                                                        int64_t rows, int H, int K, uint64_t key,
+                                                        int64_t rows, int H, int K, MaskBatch mb,
                                                         int w, float scale, E *__restrict__ y,
-                                                        int64_t ld_y)
+                                                        int64_t ld_y, uint16_t *__restrict__ idx_out)
 {
     extern __shared__ uint32_t smem[];
     const int lane = threadIdx.x & 63;
@@ -563,6 +665,12 @@ __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ va
     uint32_t *pre = bm + nw;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
+    const uint32_t layer = blockIdx.y;
+    const uint64_t key = FROM_IDX ? 0 : mb.key(layer);
+    vals += layer * mb.vals_stride;
+    y += layer * mb.dense_stride;
+    if (FROM_IDX)
+        idx += layer * mb.idx_stride;
 
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
@@ -600,6 +708,8 @@ __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ va
     wave_sync();
     if (!active)
         return;
+    if (!FROM_IDX && idx_out)
+        store_index_list(bm, pre, nw, lane, idx_out + layer * mb.idx_stride + row * K);
     const E *vr = vals + row * K;
     E *yr = y + row * ld_y;
     int jtail = 0;
@@ -886,9 +996,25 @@ int waves_for(size_t per_wave_bytes)
     return wpb;
 }
 
+MaskBatch make_batch(const ac_mask_key &k, int64_t dense_stride, int64_t vals_stride, int64_t idx_stride)
+{
+    MaskBatch mb;
+    mb.seed = k.seed;
+    mb.step = k.step;
+    mb.layer = k.layer;
+    mb.microbatch = k.microbatch;
+    mb.B = k.B;
+    mb.S = k.S;
+    mb.H = k.H;
+    mb.dense_stride = dense_stride;
+    mb.vals_stride = vals_stride;
+    mb.idx_stride = idx_stride;
+    return mb;
+}
+
 template <typename E, int ROUNDS, bool TABLE>
-void launch_pack_t(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
-                   void *vals, uint16_t *idx, hipStream_t st)
+void launch_pack_t(const void *x, int nl, int64_t rows, int H, int64_t ld_x, bool vec, int K, const MaskBatch &mb,
+                   int w, void *vals, uint16_t *idx, hipStream_t st)
 {
     // The streaming form (whole 16-byte chunks) measured slower on MI355X than
     // the gather below at every keep fraction of the workloads; it stays
@@ -896,14 +1022,13 @@ void launch_pack_t(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint
     const int nw = (H + 31) / 32;
     const size_t tab = TABLE ? table_bytes<ROUNDS>() : 0;
     const size_t sper = staged_wave_bytes(nw, K, sizeof(E), true) + tab;
-    const bool vec = aligned(x, 16) && (static_cast<size_t>(ld_x) * sizeof(E)) % 16 == 0;
     const bool dense = 4 * static_cast<int64_t>(K) >= H;
     if (dense && vec && sper <= kLdsBudget &&
         allow_lds(ac_pack_stream_kernel<E, ROUNDS, TABLE>, sper * waves_for(sper)) == ACSC_OK) {
         const int wpb = waves_for(sper);
         const int64_t blocks = (rows + wpb - 1) / wpb;
-        ACSC_LAUNCH("ac_pack", (ac_pack_stream_kernel<E, ROUNDS, TABLE>), dim3(static_cast<unsigned>(blocks)),
-                    dim3(64 * wpb), sper * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K, key, w,
+        ACSC_LAUNCH("ac_pack", (ac_pack_stream_kernel<E, ROUNDS, TABLE>), dim3(static_cast<unsigned>(blocks), nl),
+                    dim3(64 * wpb), sper * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K, mb, w,
                     static_cast<E *>(vals), idx);
         return;
     }
@@ -911,24 +1036,35 @@ void launch_pack_t(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint
     const int wpb = waves_for(per);
     allow_lds(ac_pack_kernel<E, ROUNDS, TABLE>, per * wpb);
     const int64_t blocks = (rows + wpb - 1) / wpb;
-    ACSC_LAUNCH("ac_pack", (ac_pack_kernel<E, ROUNDS, TABLE>), dim3(static_cast<unsigned>(blocks)),
+    ACSC_LAUNCH("ac_pack", (ac_pack_kernel<E, ROUNDS, TABLE>), dim3(static_cast<unsigned>(blocks), nl),
                 dim3(64 * wpb), per * wpb, st, static_cast<const E *>(x), rows, H, ld_x, K,
-                key, w, static_cast<E *>(vals), idx);
+                mb, w, static_cast<E *>(vals), idx);
 }
 
 template <typename E, int ROUNDS>
-void launch_pack(const void *x, int64_t rows, int H, int64_t ld_x, int K, uint64_t key, int w,
-                 void *vals, uint16_t *idx, hipStream_t st)
+void launch_pack(const void *x, int nl, int64_t rows, int H, int64_t ld_x, bool vec, int K, const MaskBatch &mb,
+                 int w, void *vals, uint16_t *idx, hipStream_t st)
 {
     if (use_table(H, K, w))
-        launch_pack_t<E, ROUNDS, true>(x, rows, H, ld_x, K, key, w, vals, idx, st);
+        launch_pack_t<E, ROUNDS, true>(x, nl, rows, H, ld_x, vec, K, mb, w, vals, idx, st);
     else
-        launch_pack_t<E, ROUNDS, false>(x, rows, H, ld_x, K, key, w, vals, idx, st);
+        launch_pack_t<E, ROUNDS, false>(x, nl, rows, H, ld_x, vec, K, mb, w, vals, idx, st);
+}
+
+template <typename E>
+void launch_pack_idx(const void *x, int nl, int64_t rows, int H, int64_t ld_x, int K, const MaskBatch &mb,
+                     const uint16_t *idx_in, void *vals, hipStream_t st)
+{
+    const int64_t blocks = (rows + kMaxWavesPerBlock - 1) / kMaxWavesPerBlock;
+    ACSC_LAUNCH("ac_pack_idx", ac_pack_idx_kernel<E>, dim3(static_cast<unsigned>(blocks), nl),
+                dim3(64 * kMaxWavesPerBlock), 0, st, static_cast<const E *>(x), rows, H, ld_x, K, mb, idx_in,
+                static_cast<E *>(vals));
 }
 
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC, bool TABLE>
-bool launch_unpack_stream(const void *vals, const uint16_t *idx, int64_t rows, int H, int K, uint64_t key,
-                          int w, float scale, void *y, int64_t ld_y, hipStream_t st)
+bool launch_unpack_stream(const void *vals, const uint16_t *idx, int nl, int64_t rows, int H, int K,
+                          const MaskBatch &mb, int w, float scale, void *y, int64_t ld_y, uint16_t *idx_out,
+                          hipStream_t st)
 {
     const int nw = (H + 31) / 32;
     const size_t sper = staged_wave_bytes(nw, K, sizeof(E), false) + (TABLE ? table_bytes<ROUNDS>() : 0);
@@ -937,25 +1073,25 @@ bool launch_unpack_stream(const void *vals, const uint16_t *idx, int64_t rows, i
         return false;
     const int wpb = waves_for(sper);
     const int64_t blocks = (rows + wpb - 1) / wpb;
-    ACSC_LAUNCH("ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, VEC, TABLE>),
-                dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), sper * wpb, st,
-                static_cast<const E *>(vals), idx, rows, H, K, key, w, scale, static_cast<E *>(y), ld_y);
+    ACSC_LAUNCH(FROM_IDX ? "ac_unpack_idx" : "ac_unpack", (ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, VEC, TABLE>),
+                dim3(static_cast<unsigned>(blocks), nl), dim3(64 * wpb), sper * wpb, st,
+                static_cast<const E *>(vals), idx, rows, H, K, mb, w, scale, static_cast<E *>(y), ld_y, idx_out);
     return true;
 }
 
 template <typename E, int ROUNDS, bool FROM_IDX>
-void launch_unpack(const void *vals, const uint16_t *idx, int64_t rows, int H, int K, uint64_t key,
-                   int w, float scale, void *y, int64_t ld_y, bool vec, hipStream_t st)
+void launch_unpack(const void *vals, const uint16_t *idx, int nl, int64_t rows, int H, int K, const MaskBatch &mb,
+                   int w, float scale, void *y, int64_t ld_y, bool vec, uint16_t *idx_out, hipStream_t st)
 {
     // transmitted indices need no permutation, so no round table either
     const bool table = !FROM_IDX && use_table(H, K, w);
     bool done;
     if (vec)
-        done = table ? launch_unpack_stream<E, ROUNDS, FROM_IDX, true, true>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st)
-                     : launch_unpack_stream<E, ROUNDS, FROM_IDX, true, false>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st);
+        done = table ? launch_unpack_stream<E, ROUNDS, FROM_IDX, true, true>(vals, idx, nl, rows, H, K, mb, w, scale, y, ld_y, idx_out, st)
+                     : launch_unpack_stream<E, ROUNDS, FROM_IDX, true, false>(vals, idx, nl, rows, H, K, mb, w, scale, y, ld_y, idx_out, st);
     else
-        done = table ? launch_unpack_stream<E, ROUNDS, FROM_IDX, false, true>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st)
-                     : launch_unpack_stream<E, ROUNDS, FROM_IDX, false, false>(vals, idx, rows, H, K, key, w, scale, y, ld_y, st);
+        done = table ? launch_unpack_stream<E, ROUNDS, FROM_IDX, false, true>(vals, idx, nl, rows, H, K, mb, w, scale, y, ld_y, idx_out, st)
+                     : launch_unpack_stream<E, ROUNDS, FROM_IDX, false, false>(vals, idx, nl, rows, H, K, mb, w, scale, y, ld_y, idx_out, st);
     if (done)
         return;
     const int nw = (H + 31) / 32;
@@ -965,15 +1101,129 @@ void launch_unpack(const void *vals, const uint16_t *idx, int64_t rows, int H, i
     allow_lds(ac_unpack_kernel<E, ROUNDS, FROM_IDX, false>, per * wpb);
     const int64_t blocks = (rows + wpb - 1) / wpb;
     if (vec)
-        ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, true>),
-                    dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
-                    static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
-                    static_cast<E *>(y), ld_y);
+        ACSC_LAUNCH(FROM_IDX ? "ac_unpack_idx" : "ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, true>),
+                    dim3(static_cast<unsigned>(blocks), nl), dim3(64 * wpb), per * wpb, st,
+                    static_cast<const E *>(vals), idx, rows, H, K, mb, w, scale,
+                    static_cast<E *>(y), ld_y, idx_out);
     else
-        ACSC_LAUNCH("ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, false>),
-                    dim3(static_cast<unsigned>(blocks)), dim3(64 * wpb), per * wpb, st,
-                    static_cast<const E *>(vals), idx, rows, H, K, key, w, scale,
-                    static_cast<E *>(y), ld_y);
+        ACSC_LAUNCH(FROM_IDX ? "ac_unpack_idx" : "ac_unpack", (ac_unpack_kernel<E, ROUNDS, FROM_IDX, false>),
+                    dim3(static_cast<unsigned>(blocks), nl), dim3(64 * wpb), per * wpb, st,
+                    static_cast<const E *>(vals), idx, rows, H, K, mb, w, scale,
+                    static_cast<E *>(y), ld_y, idx_out);
+}
+
+// Checks shared by the batched mask calls: the boundary count, the layer ids
+// it implies, and strides that keep every boundary's outputs apart.
+int batch_checks(int nlayers, const ac_mask_key *key, int64_t rows, int64_t out_extent, int64_t out_stride,
+                 const char *out_name)
+{
+    ACSC_CHECK_ARG(nlayers >= 0 && nlayers <= 65535, ACSC_EINVAL, "nlayers=%d outside [0, 65535]", nlayers);
+    if (nlayers > 1) {
+        ACSC_CHECK_ARG(static_cast<uint64_t>(key->layer) + static_cast<uint64_t>(nlayers - 1) <= 0xFFFFFFFFull,
+                       ACSC_EINVAL, "key.layer + nlayers - 1 exceeds the 32-bit layer field");
+        ACSC_CHECK_ARG(rows == 0 || out_stride >= out_extent, ACSC_EINVAL,
+                       "%s layer stride %lld < %lld elements: boundaries would overlap", out_name,
+                       (long long)out_stride, (long long)out_extent);
+    }
+    return ACSC_OK;
+}
+
+int mask_pack_impl(const void *x, acsc_dtype dt, int nlayers, int64_t rows, int H, int64_t ld_x, int64_t x_stride,
+                   int K, const ac_mask_key *key, void *vals, int64_t vals_stride, const uint16_t *idx_in,
+                   uint16_t *idx_out, int64_t idx_stride, hipStream_t stream)
+{
+    int rc = common_checks(dt, rows, H, K, key);
+    if (rc)
+        return rc;
+    ACSC_CHECK_ARG(ld_x >= H, ACSC_EINVAL, "ld_x=%lld < H=%d", (long long)ld_x, H);
+    if ((rc = batch_checks(nlayers, key, rows, rows * K, vals_stride, "vals")))
+        return rc;
+    if (idx_out && (rc = batch_checks(nlayers, key, rows, rows * K, idx_stride, "idx_out")))
+        return rc;
+    ACSC_CHECK_ARG(!(idx_in && idx_out), ACSC_EINVAL, "idx_in and idx_out are exclusive");
+    ACSC_CHECK_ARG(nlayers <= 1 || (x_stride >= 0 && (!idx_in || idx_stride >= 0)), ACSC_EINVAL,
+                   "negative layer stride");
+    if (rows == 0 || nlayers == 0)
+        return ACSC_OK;
+    ACSC_CHECK_ARG(x && vals, ACSC_EINVAL, "x or vals is NULL");
+    const size_t es = dtype_size(dt);
+    ACSC_CHECK_ARG(aligned(x, es) && aligned(vals, es), ACSC_EALIGN,
+                   "x and vals must be %zu-byte aligned", es);
+    ACSC_CHECK_ARG((!idx_in || aligned(idx_in, 2)) && (!idx_out || aligned(idx_out, 2)), ACSC_EALIGN,
+                   "idx must be 2-byte aligned");
+    const bool vec = aligned(x, 16) && (static_cast<size_t>(ld_x) * es) % 16 == 0 &&
+                     (nlayers <= 1 || (static_cast<size_t>(x_stride) * es) % 16 == 0);
+    const MaskBatch mb = make_batch(*key, nlayers > 1 ? x_stride : 0, nlayers > 1 ? vals_stride : 0,
+                                    nlayers > 1 ? idx_stride : 0);
+    const int w = domain_bits(H);
+    if (idx_in) {
+        if (dt == ACSC_BF16)
+            launch_pack_idx<uint16_t>(x, nlayers, rows, H, ld_x, K, mb, idx_in, vals, stream);
+        else
+            launch_pack_idx<uint32_t>(x, nlayers, rows, H, ld_x, K, mb, idx_in, vals, stream);
+    } else if (dt == ACSC_BF16) {
+        if (w <= 4)
+            launch_pack<uint16_t, 12>(x, nlayers, rows, H, ld_x, vec, K, mb, w, vals, idx_out, stream);
+        else
+            launch_pack<uint16_t, 8>(x, nlayers, rows, H, ld_x, vec, K, mb, w, vals, idx_out, stream);
+    } else {
+        if (w <= 4)
+            launch_pack<uint32_t, 12>(x, nlayers, rows, H, ld_x, vec, K, mb, w, vals, idx_out, stream);
+        else
+            launch_pack<uint32_t, 8>(x, nlayers, rows, H, ld_x, vec, K, mb, w, vals, idx_out, stream);
+    }
+    return check_launch("ac_mask_pack");
+}
+
+int unpack_impl(const void *vals, int64_t vals_stride, acsc_dtype dt, int nlayers, int64_t rows, int H, int K,
+                const ac_mask_key *key, const uint16_t *idx_in, uint16_t *idx_out, int64_t idx_stride, float scale,
+                void *y, int64_t ld_y, int64_t y_stride, hipStream_t stream)
+{
+    int rc = common_checks(dt, rows, H, K, key);
+    if (rc)
+        return rc;
+    ACSC_CHECK_ARG(ld_y >= H, ACSC_EINVAL, "ld_y=%lld < H=%d", (long long)ld_y, H);
+    ACSC_CHECK_ARG(std::isfinite(scale), ACSC_EINVAL, "scale must be finite");
+    if ((rc = batch_checks(nlayers, key, rows, rows > 0 ? (rows - 1) * ld_y + H : 0, y_stride, "y")))
+        return rc;
+    if (idx_out && (rc = batch_checks(nlayers, key, rows, rows * K, idx_stride, "idx_out")))
+        return rc;
+    ACSC_CHECK_ARG(!(idx_in && idx_out), ACSC_EINVAL, "idx_in and idx_out are exclusive");
+    ACSC_CHECK_ARG(nlayers <= 1 || (vals_stride >= 0 && (!idx_in || idx_stride >= 0)), ACSC_EINVAL,
+                   "negative layer stride");
+    if (rows == 0 || nlayers == 0)
+        return ACSC_OK;
+    ACSC_CHECK_ARG(vals && y, ACSC_EINVAL, "vals or y is NULL");
+    const size_t es = dtype_size(dt);
+    ACSC_CHECK_ARG(aligned(vals, es) && aligned(y, es), ACSC_EALIGN,
+                   "vals and y must be %zu-byte aligned", es);
+    ACSC_CHECK_ARG((!idx_in || aligned(idx_in, 2)) && (!idx_out || aligned(idx_out, 2)), ACSC_EALIGN,
+                   "idx must be 2-byte aligned");
+    const bool vec = aligned(y, 16) && (static_cast<size_t>(ld_y) * es) % 16 == 0 &&
+                     (nlayers <= 1 || (static_cast<size_t>(y_stride) * es) % 16 == 0);
+    const MaskBatch mb = make_batch(*key, nlayers > 1 ? y_stride : 0, nlayers > 1 ? vals_stride : 0,
+                                    nlayers > 1 ? idx_stride : 0);
+    const int w = domain_bits(H);
+#define ACSC_UNPACK(E, R)                                                                                         \
+    do {                                                                                                          \
+        if (idx_in)                                                                                               \
+            launch_unpack<E, R, true>(vals, idx_in, nlayers, rows, H, K, mb, w, scale, y, ld_y, vec, nullptr, stream); \
+        else                                                                                                      \
+            launch_unpack<E, R, false>(vals, nullptr, nlayers, rows, H, K, mb, w, scale, y, ld_y, vec, idx_out, stream); \
+    } while (0)
+    if (dt == ACSC_BF16) {
+        if (w <= 4)
+            ACSC_UNPACK(uint16_t, 12);
+        else
+            ACSC_UNPACK(uint16_t, 8);
+    } else {
+        if (w <= 4)
+            ACSC_UNPACK(uint32_t, 12);
+        else
+            ACSC_UNPACK(uint32_t, 8);
+    }
+#undef ACSC_UNPACK
+    return check_launch("ac_unpack_scatter");
 }
 
 }  // namespace
@@ -998,31 +1248,7 @@ extern "C" int ac_mask_pack(const void *x, acsc_dtype dt, int64_t rows, int H, i
                             const ac_mask_key *key, void *vals, uint16_t *idx, hipStream_t stream)
 {
     clear_error();
-    int rc = common_checks(dt, rows, H, K, key);
-    if (rc)
-        return rc;
-    ACSC_CHECK_ARG(ld_x >= H, ACSC_EINVAL, "ld_x=%lld < H=%d", (long long)ld_x, H);
-    if (rows == 0)
-        return ACSC_OK;
-    ACSC_CHECK_ARG(x && vals, ACSC_EINVAL, "x or vals is NULL");
-    const size_t es = dtype_size(dt);
-    ACSC_CHECK_ARG(aligned(x, es) && aligned(vals, es), ACSC_EALIGN,
-                   "x and vals must be %zu-byte aligned", es);
-    ACSC_CHECK_ARG(!idx || aligned(idx, 2), ACSC_EALIGN, "idx must be 2-byte aligned");
-    const uint64_t k = chain_key(*key);
-    const int w = domain_bits(H);
-    if (dt == ACSC_BF16) {
-        if (w <= 4)
-            launch_pack<uint16_t, 12>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
-        else
-            launch_pack<uint16_t, 8>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
-    } else {
-        if (w <= 4)
-            launch_pack<uint32_t, 12>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
-        else
-            launch_pack<uint32_t, 8>(x, rows, H, ld_x, K, k, w, vals, idx, stream);
-    }
-    return check_launch("ac_mask_pack");
+    return mask_pack_impl(x, dt, 1, rows, H, ld_x, 0, K, key, vals, 0, nullptr, idx, 0, stream);
 }
 
 extern "C" int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dtype dt, int64_t rows,
@@ -1030,41 +1256,28 @@ extern "C" int ac_unpack_scatter(const void *vals, const uint16_t *idx, acsc_dty
                                  int64_t ld_y, hipStream_t stream)
 {
     clear_error();
-    int rc = common_checks(dt, rows, H, K, key);
-    if (rc)
-        return rc;
-    ACSC_CHECK_ARG(ld_y >= H, ACSC_EINVAL, "ld_y=%lld < H=%d", (long long)ld_y, H);
-    ACSC_CHECK_ARG(std::isfinite(scale), ACSC_EINVAL, "scale must be finite");
-    if (rows == 0)
-        return ACSC_OK;
-    ACSC_CHECK_ARG(vals && y, ACSC_EINVAL, "vals or y is NULL");
-    const size_t es = dtype_size(dt);
-    ACSC_CHECK_ARG(aligned(vals, es) && aligned(y, es), ACSC_EALIGN,
-                   "vals and y must be %zu-byte aligned", es);
-    ACSC_CHECK_ARG(!idx || aligned(idx, 2), ACSC_EALIGN, "idx must be 2-byte aligned");
-    const bool vec = aligned(y, 16) && (static_cast<size_t>(ld_y) * es) % 16 == 0;
-    const uint64_t k = chain_key(*key);
-    const int w = domain_bits(H);
-#define ACSC_UNPACK(E, R)                                                                        \
-    do {                                                                                         \
-        if (idx)                                                                                 \
-            launch_unpack<E, R, true>(vals, idx, rows, H, K, k, w, scale, y, ld_y, vec, stream); \
-        else                                                                                     \
-            launch_unpack<E, R, false>(vals, idx, rows, H, K, k, w, scale, y, ld_y, vec, stream); \
-    } while (0)
-    if (dt == ACSC_BF16) {
-        if (w <= 4)
-            ACSC_UNPACK(uint16_t, 12);
-        else
-            ACSC_UNPACK(uint16_t, 8);
-    } else {
-        if (w <= 4)
-            ACSC_UNPACK(uint32_t, 12);
-        else
-            ACSC_UNPACK(uint32_t, 8);
-    }
-#undef ACSC_UNPACK
-    return check_launch("ac_unpack_scatter");
+    return unpack_impl(vals, 0, dt, 1, rows, H, K, key, idx, nullptr, 0, scale, y, ld_y, 0, stream);
+}
+
+extern "C" int ac_mask_pack_batched(const void *x, acsc_dtype dt, int nlayers, int64_t rows, int H, int64_t ld_x,
+                                    int64_t x_stride, int K, const ac_mask_key *key, void *vals,
+                                    int64_t vals_stride, const uint16_t *idx_in, uint16_t *idx_out,
+                                    int64_t idx_stride, hipStream_t stream)
+{
+    clear_error();
+    return mask_pack_impl(x, dt, nlayers, rows, H, ld_x, x_stride, K, key, vals, vals_stride, idx_in, idx_out,
+                          idx_stride, stream);
+}
+
+extern "C" int ac_unpack_scatter_batched(const void *vals, int64_t vals_stride, acsc_dtype dt, int nlayers,
+                                         int64_t rows, int H, int K, const ac_mask_key *key,
+                                         const uint16_t *idx_in, uint16_t *idx_out, int64_t idx_stride,
+                                         float scale, void *y, int64_t ld_y, int64_t y_stride,
+                                         hipStream_t stream)
+{
+    clear_error();
+    return unpack_impl(vals, vals_stride, dt, nlayers, rows, H, K, key, idx_in, idx_out, idx_stride, scale, y,
+                       ld_y, y_stride, stream);
 }
 
 // ---------------------------------------------------------------------------

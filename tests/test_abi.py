@@ -137,3 +137,36 @@ def test_psgd_workspace_and_rejects_bad_arguments_before_launch(lib):
     # an empty call succeeds without touching anything; a negative count is rejected
     assert lib.psgd_project(0, None, 1, 4, None) == 0
     assert lib.psgd_step(-1, None, 1, 4, None) == -1
+
+
+def test_batched_mask_calls_reject_bad_arguments_before_launch(lib):
+    vp, i64 = C.c_void_p, C.c_int64
+    lib.ac_mask_pack_batched.argtypes = [vp, C.c_int, C.c_int, i64, C.c_int, i64, i64, C.c_int, C.POINTER(Key),
+                                         vp, i64, vp, vp, i64, vp]
+    lib.ac_unpack_scatter_batched.argtypes = [vp, i64, C.c_int, C.c_int, i64, C.c_int, C.c_int, C.POINTER(Key),
+                                              vp, vp, i64, C.c_float, vp, i64, i64, vp]
+    key = Key(seed=1, step=1, layer=0, microbatch=0, B=2, S=4, H=64)
+    f = vp(0x10000)
+    rows, H, K = 8, 64, 4
+    pack = lambda nl, xs, vs, ii, io, istr, k=key: lib.ac_mask_pack_batched(
+        f, 1, nl, rows, H, H, xs, K, C.byref(k), f, vs, ii, io, istr, None)
+    unpack = lambda nl, vs, ii, io, istr, ys, k=key: lib.ac_unpack_scatter_batched(
+        f, vs, 1, nl, rows, H, K, C.byref(k), ii, io, istr, 1.0, f, H, ys, None)
+    assert pack(-1, 0, 0, None, None, 0) == -1
+    assert pack(65536, 0, 0, None, None, 0) == -1
+    assert pack(3, rows * H, rows * K - 1, None, None, 0) == -1 and "overlap" in _err(lib)
+    assert pack(3, rows * H, rows * K, None, f, rows * K - 1) == -1
+    assert pack(3, -1, rows * K, None, None, 0) == -1
+    assert pack(1, 0, 0, f, f, 0) == -1 and "exclusive" in _err(lib)
+    big = Key(seed=1, step=1, layer=0xFFFFFFFF, microbatch=0, B=2, S=4, H=64)
+    assert pack(2, rows * H, rows * K, None, None, 0, big) == -1 and "layer" in _err(lib)
+    assert pack(1, 0, 0, vp(0x10001), None, 0) == -3
+    assert unpack(3, rows * K, None, None, 0, rows * H - 1) == -1 and "overlap" in _err(lib)
+    assert unpack(3, rows * K, None, f, rows * K - 1, rows * H) == -1
+    assert unpack(2, rows * K, f, f, rows * K, rows * H) == -1
+    assert unpack(1, 0, None, vp(0x10001), 0, 0) == -3
+    # no boundaries, or no rows: a no-op that touches no pointer
+    assert lib.ac_mask_pack_batched(None, 1, 0, rows, H, H, 0, K, C.byref(key), None, 0, None, None, 0, None) == 0
+    key0 = Key(seed=1, step=1, layer=0, microbatch=0, B=0, S=4, H=64)
+    assert lib.ac_unpack_scatter_batched(None, 0, 1, 5, 0, H, K, C.byref(key0), None, None, 0, 1.0, None, H, 0,
+                                         None) == 0

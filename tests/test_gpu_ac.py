@@ -187,3 +187,108 @@ def test_errors_raise_without_side_effects(pk):
     assert e.value.code == pk.ACSC_EINVAL
     torch.cuda.synchronize()
     assert torch.all(vals == 3.0)
+
+
+def _oracle_key(fields, B, S, H, layer):
+    return om.mask_key(fields["seed"], layer, fields["step"], fields["microbatch"], B, S, H)
+
+
+def test_70b_slice_all_rows_batched_index_list_flow(pk):
+    """C5, every row of all four boundaries, both directions, in the batched
+    launch configuration the benchmark times: the sender packs the activation
+    from the key and keeps the index lists; the receiver unpacks from the key
+    (values-only wire) and keeps its own lists; the receiver packs the
+    activation gradient from its lists; the sender unpacks that payload from
+    its lists.  Every array bit-exact against the oracle, both sides' lists
+    equal, and boundary 2 equal to the single calls."""
+    spec = workloads.CONFIGS[5].act
+    H, rows, nl = spec.H, spec.B * spec.S, 4
+    K = om.keep_count(H, spec.keep[0])
+    fields = workloads.mask_key_fields(5, layer=0)
+    key = pk.make_key(B=spec.B, S=spec.S, H=H, **fields)
+    x = torch.stack([workloads.activation(spec, 5, 0, 2 * l, "cuda") for l in range(nl)])
+    gx = torch.stack([workloads.activation(spec, 5, 0, 2 * l + 1, "cuda") for l in range(nl)])
+    scale = H / K
+    idx_s = torch.empty(nl, rows, K, dtype=torch.int16, device="cuda")
+    idx_r = torch.empty_like(idx_s)
+    vals = pk.ac_mask_pack_batched(x, K, key, idx_out=idx_s)
+    y = pk.ac_unpack_scatter_batched(vals, H, key, scale, idx_out=idx_r)
+    gvals = pk.ac_mask_pack_batched(gx, K, key, idx_in=idx_r)
+    gy = pk.ac_unpack_scatter_batched(gvals, H, key, scale, idx_in=idx_s)
+    torch.cuda.synchronize()
+    assert torch.equal(idx_s, idx_r)
+    for l in range(nl):
+        okey = _oracle_key(fields, spec.B, spec.S, H, l)
+        ov, oi = om.pack(_bits(x[l]), K, okey)
+        assert np.array_equal(_bits(idx_s[l]), oi), l
+        assert np.array_equal(_bits(vals[l]), ov), l
+        assert np.array_equal(_bits(y[l]), om.unpack(ov, H, okey, scale)), l
+        gov, goi = om.pack(_bits(gx[l]), K, okey)
+        assert np.array_equal(goi, oi), l                         # backward inherits the mask
+        assert np.array_equal(_bits(gvals[l]), gov), l
+        assert np.array_equal(_bits(gy[l]), om.unpack(gov, H, okey, scale)), l
+    k2 = pk.make_key(B=spec.B, S=spec.S, H=H, **workloads.mask_key_fields(5, layer=2))
+    v2, i2 = pk.ac_mask_pack(x[2], K, k2)
+    y2 = pk.ac_unpack_scatter(v2, H, k2, scale)
+    torch.cuda.synchronize()
+    assert torch.equal(v2, vals[2]) and torch.equal(i2, idx_s[2]) and torch.equal(y2, y[2])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("nl,B,S,H,K,pad", [(3, 2, 33, 333, 50, 0), (2, 1, 9, 1000, 1000, 8), (3, 5, 13, 17, 3, 3),
+                                            (2, 1, 65, 4097, 410, 8), (1, 2, 3, 65536, 40000, 0),
+                                            (2, 2, 40, 300, 300, 0), (4, 1, 1, 1, 1, 0)])
+def test_batched_ragged_shapes_match_single_calls_and_oracle(pk, dtype, nl, B, S, H, K, pad):
+    """Ragged rows, padded row strides, a dense keep (K = H, the whole-row
+    pack), K > H / 4, and an unpack too large for its staged form (H = 65536,
+    K = 40000): each boundary of a batched call bit-exact against the oracle
+    and the single call, through both the key-driven and the index-driven
+    forms, with layer strides wider than the tensors."""
+    rows = B * S
+    fields = dict(seed=77, layer=5, step=3, microbatch=1)
+    key = pk.make_key(B=B, S=S, H=H, **fields)
+    gap = 24                                    # spare rows between boundaries
+    x_all = workloads.gaussian((nl * (rows + gap), H + pad), seed=H + K + nl, dtype=dtype).cuda()
+    x = x_all.view(nl, rows + gap, H + pad)[:, :rows, :H]
+    vals = torch.full((nl, rows + 1, K), 9, dtype=dtype, device="cuda")[:, :rows]
+    idx_s = torch.empty(nl, rows + 2, K, dtype=torch.int16, device="cuda")[:, :rows]
+    idx_r = torch.empty_like(idx_s)
+    ybuf = torch.full((nl, rows + 3, H + pad), 7, dtype=dtype, device="cuda")
+    y = ybuf[:, :rows, :H]
+    pk.ac_mask_pack_batched(x, K, key, vals=vals, idx_out=idx_s)
+    pk.ac_unpack_scatter_batched(vals, H, key, -0.75, idx_out=idx_r, y=y)
+    vals_i = pk.ac_mask_pack_batched(x, K, key, idx_in=idx_r)
+    y_i = pk.ac_unpack_scatter_batched(vals_i, H, key, -0.75, idx_in=idx_s)
+    torch.cuda.synchronize()
+    assert torch.all(ybuf[:, rows:] == 7) and (pad == 0 or torch.all(ybuf[:, :, H:] == 7))
+    assert torch.equal(idx_s, idx_r) and torch.equal(vals_i, vals) and torch.equal(y_i, y)
+    for l in range(nl):
+        okey = _oracle_key(fields, B, S, H, l + 5)
+        xl = x[l].cpu()
+        ov, oi = om.pack(_host_x(xl), K, okey)
+        assert np.array_equal(_bits(idx_s[l]), oi)
+        assert np.array_equal(_bits(vals[l]).view(np.uint8), ov.view(np.uint8))
+        vh = _bits(vals[l])
+        if dtype == torch.float32:
+            vh = vh.view(np.float32)
+        oy = om.unpack(vh, H, okey, -0.75)
+        assert np.array_equal(_bits(y[l]).view(np.uint8), oy.view(np.uint8))
+        kl = pk.make_key(B=B, S=S, H=H, **dict(fields, layer=5 + l))
+        v1, i1 = pk.ac_mask_pack(x[l], K, kl)
+        y1 = pk.ac_unpack_scatter(v1, H, kl, -0.75)
+        torch.cuda.synchronize()
+        assert torch.equal(v1, vals[l]) and torch.equal(i1, idx_s[l]) and torch.equal(y1, y[l])
+
+
+def test_index_driven_pack_reads_nothing_past_H(pk):
+    """An index entry >= H packs +0 (the row is never read there)."""
+    B, S, H, K = 1, 4, 100, 5
+    key = pk.make_key(seed=1, layer=0, step=1, microbatch=0, B=B, S=S, H=H)
+    x = (torch.arange(B * S * H, dtype=torch.float32, device="cuda") + 1).view(1, B * S, H)
+    idx = torch.tensor([[0, 7, 99, 100, 32767]] * (B * S), dtype=torch.int16, device="cuda").view(1, B * S, K)
+    v = pk.ac_mask_pack_batched(x, K, key, idx_in=idx)
+    torch.cuda.synchronize()
+    row0 = torch.arange(B * S, device="cuda").view(-1, 1) * H
+    expect = torch.stack([row0[:, 0] + 1, row0[:, 0] + 8, row0[:, 0] + 100,
+                          torch.zeros_like(row0[:, 0]), torch.zeros_like(row0[:, 0])], 1).float()
+    assert torch.equal(v[0], expect)

@@ -265,22 +265,24 @@ def test_projector_distance_is_the_sine_of_the_principal_angles():
     principal angles theta_i, so the distance over sqrt(2 r) is sin(eps) when
     every angle is eps, 1 for orthogonal subspaces and 0 for a rotation of the
     basis inside its span (the diagnostic the parity tests report)."""
-    m, r = 50, 4
-    B = _orthonormal_columns(m, 2 * r, 31)
-    Q, W = B[:, :r], B[:, r:]
-    for eps in (0.0, 0.05, 0.2, 0.7, np.pi / 2):
-        Q2 = Q * np.cos(eps) + W * np.sin(eps)
-        assert abs(osp.projector_distance(Q, Q2) - np.sin(eps)) < 1e-13, eps
-    assert abs(osp.projector_distance(Q, W) - 1.0) < 1e-13
-    R = _orthonormal_columns(r, r, 32)
-    assert osp.projector_distance(Q, Q @ R) < 1e-13
-    # unequal angles a, b on two of the columns (the other two shared)
-    a, b = 0.3, 1.1
-    Q3 = Q.copy()
-    Q3[:, 0] = Q[:, 0] * np.cos(a) + W[:, 0] * np.sin(a)
-    Q3[:, 1] = Q[:, 1] * np.cos(b) + W[:, 1] * np.sin(b)
-    expect = np.sqrt((np.sin(a) ** 2 + np.sin(b) ** 2) / r)
-    assert abs(osp.projector_distance(Q, Q3) - expect) < 1e-13
+    for m, method in ((50, "projector"), (50, "residual"), (5000, "auto")):
+        r = 4
+        B = _orthonormal_columns(m, 2 * r, 31)
+        Q, W = B[:, :r], B[:, r:]
+        dist = lambda A, C: osp.projector_distance(A, C, method=method)
+        for eps in (0.0, 0.05, 0.2, 0.7, np.pi / 2):
+            Q2 = Q * np.cos(eps) + W * np.sin(eps)
+            assert abs(dist(Q, Q2) - np.sin(eps)) < 1e-13, (m, method, eps)
+        assert abs(dist(Q, W) - 1.0) < 1e-13
+        R = _orthonormal_columns(r, r, 32)
+        assert dist(Q, Q @ R) < 1e-13
+        # unequal angles a, b on two of the columns (the other two shared)
+        a, b = 0.3, 1.1
+        Q3 = Q.copy()
+        Q3[:, 0] = Q[:, 0] * np.cos(a) + W[:, 0] * np.sin(a)
+        Q3[:, 1] = Q[:, 1] * np.cos(b) + W[:, 1] * np.sin(b)
+        expect = np.sqrt((np.sin(a) ** 2 + np.sin(b) ** 2) / r)
+        assert abs(dist(Q, Q3) - expect) < 1e-13
 
 
 def test_rel_fro_on_hand_computed_pairs():
@@ -320,10 +322,11 @@ def test_planted_mistakes_in_the_comparison_helpers_are_caught(monkeypatch):
     fail one of the pins above."""
     mutants = {
         "projector_distance": [
-            lambda U1, U2: 0.0,
-            lambda U1, U2: float(np.linalg.norm(U1 @ U1.T - U2 @ U2.T)),
-            lambda U1, U2: float(np.linalg.norm(U1 @ U1.T - U2 @ U2.T) / np.sqrt(U1.shape[1])),
-            lambda U1, U2: float(np.linalg.norm(U1 - U2) / np.sqrt(2.0 * U1.shape[1])),
+            lambda U1, U2, method="auto": 0.0,
+            lambda U1, U2, method="auto": float(np.linalg.norm(U1 @ U1.T - U2 @ U2.T)),
+            lambda U1, U2, method="auto": float(np.linalg.norm(U1 @ U1.T - U2 @ U2.T) / np.sqrt(U1.shape[1])),
+            lambda U1, U2, method="auto": float(np.linalg.norm(U1 - U2) / np.sqrt(2.0 * U1.shape[1])),
+            lambda U1, U2, method="auto": float(np.linalg.norm(U1 - U2 @ (U2.T @ U1)) / np.sqrt(2.0 * U1.shape[1])),
         ],
         "rel_fro": [
             lambda a, b: float(np.linalg.norm(np.subtract(a, b)) / np.linalg.norm(a)),
@@ -368,3 +371,37 @@ def test_transposed_filter_operand_is_caught_by_idempotence():
     assert not np.allclose(P(P(A)), P(A), atol=1e-12)
     Q = lambda X: osp.two_sided_filter(X, U, d, V)
     assert np.allclose(Q(Q(A)), Q(A), atol=1e-12)
+
+
+@pytest.mark.parametrize("m,n,r", [(60, 90, 7), (90, 60, 7), (50, 50, 50), (33, 80, 1)])
+def test_gram_route_gives_the_svd_triplets(m, n, r):
+    """The Gram route to the top-r triplets against LAPACK's SVD (a different
+    routine): singular values, projectors, and the triplet relations
+    M v = s u, M^T u = s v, on a spectrum with distinct values."""
+    rng = np.random.default_rng(m + 3 * n + r)
+    U, s, V = _basis(m, n, min(m, n), m * n)
+    s = np.geomspace(50.0, 0.5, min(m, n))
+    M = (U * s) @ V.T + 1e-3 * rng.standard_normal((m, n))
+    Ug, sg, Vg = osp.top_r_svd_gram(M, r)
+    Uo, so, Vo = osp.top_r_svd(M, r)
+    assert np.allclose(sg, so, rtol=1e-10, atol=1e-12 * so[0])
+    assert np.all(np.diff(sg) <= 0)
+    assert osp.projector_distance(Ug, Uo) < 1e-9
+    assert osp.projector_distance(Vg, Vo) < 1e-9
+    assert np.allclose(M @ Vg, Ug * sg, atol=1e-9 * so[0])
+    assert np.allclose(M.T @ Ug, Vg * sg, atol=1e-9 * so[0])
+    assert np.allclose(Ug.T @ Ug, np.eye(r), atol=1e-9)
+    assert np.allclose(Vg.T @ Vg, np.eye(r), atol=1e-9)
+
+
+def test_gram_route_on_a_rank_deficient_matrix():
+    """Rank 3 asked for r = 5: the constructed values, then zeros with zero
+    columns on the derived side (the filter then gives d = 0 there)."""
+    M, U, s, V = _closed_form_case(40, 28, 3, 8)
+    Ug, sg, Vg = osp.top_r_svd_gram(M, 5)
+    assert np.allclose(sg[:3], s, rtol=1e-12)
+    assert np.all(sg[3:] < 1e-6)
+    assert osp.projector_distance(Ug[:, :3], U) < 1e-10
+    assert osp.projector_distance(Vg[:, :3], V) < 1e-6
+    d = osp.filter_weights(np.where(sg < 1e-6, 0.0, sg), 1e-3)
+    assert np.all(d[3:] == 0)

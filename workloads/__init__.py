@@ -81,7 +81,7 @@ CONFIGS = {
               ActSpec(4, 4096, 4096, torch.bfloat16, (0.02, 0.05, 0.1), "student_t4"),
               GradSpec(((4096, 4096), (4096, 1024), (4096, 14336), (14336, 4096)), 64,
                        (1.0, 100.0), (64,), torch.bfloat16, None, None),
-              oversample=16, power_iters=2),
+              oversample=16, power_iters=3),
     4: Config(4, "8b-staleness",
               ActSpec(4, 4096, 4096, torch.bfloat16, (0.05,), "student_t4"),
               GradSpec(((4096, 4096), (4096, 1024), (4096, 14336), (14336, 4096)), 64,
@@ -217,6 +217,42 @@ def grad_pair(spec: GradSpec, cid: int, layer: int, mat: int, device="cpu",
     G_mask = (S2 + sm * Nm).to(spec.dtype)
     del Nm, S, S2
     return GradPair(G_anc, G_mask, s, U if keep_basis else U[:, :0], V if keep_basis else V[:, :0])
+
+
+def anchor_arrival(spec: GradSpec, cid: int, layer: int, mat: int, arrival: int, drift: float,
+                   device="cpu") -> Tuple[torch.Tensor, torch.Tensor]:
+    """(G_anc, G_mask) of anchor arrival ``arrival`` (0, 1, ..) of a signal
+    whose subspaces drift along one fixed geodesic.
+
+    The signal basis of ``grad_pair`` (same seed) is rotated by
+    arrival * drift for the anchor gradient and by (arrival + 1) * drift for
+    the masked gradient that the arrival's prior will correct (one arrival
+    ahead), always toward the same orthonormal directions, so the subspaces
+    of consecutive arrivals sit ``drift`` apart.  Each arrival draws fresh
+    noise at the spec's level.  float64 on ``device``, cast to spec.dtype."""
+    m, n = spec.shapes[mat]
+    rho = spec.rank
+    g = _gen(device, cid, layer, mat)
+    U = orthonormal(m, rho, g, device)
+    V = orthonormal(n, rho, g, device)
+    s = log_spaced(spec.s_range[0], spec.s_range[1], rho, device=device)
+    fro = float(torch.sqrt(torch.sum(s * s)))
+    auto = 0.05 * fro / math.sqrt(m * n)
+    sa = spec.anc_noise if spec.anc_noise is not None else auto
+    sm = spec.mask_noise if spec.mask_noise is not None else auto
+
+    def signal(angle: float) -> torch.Tensor:
+        gu = _gen(device, cid, layer, 500 + mat)      # the same directions at every angle
+        Ua = rotate_columns(U, angle, gu)
+        Va = rotate_columns(V, angle, gu)
+        return (Ua * s) @ Va.T
+
+    gn = _gen(device, cid, layer, 600 + 16 * mat + arrival)
+    Na = torch.randn(m, n, generator=gn, device=device, dtype=torch.float32).double()
+    G_anc = (signal(arrival * drift) + sa * Na).to(spec.dtype)
+    Nm = torch.randn(m, n, generator=gn, device=device, dtype=torch.float32).double()
+    G_mask = (signal((arrival + 1) * drift) + sm * Nm).to(spec.dtype)
+    return G_anc, G_mask
 
 
 def grad_pair_fast(spec: GradSpec, cid: int, layer: int, mat: int, device="cuda",
