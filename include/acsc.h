@@ -249,6 +249,24 @@ int sc_correct(const void *G, acsc_dtype dt, int m, int n, const float *U, const
                const float *V, int r, float alpha, void *G_proj, void *ws, size_t ws_bytes,
                hipStream_t stream);
 
+/* sc_correct without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops that forbid
+ * allocation).  Its scratch is a device array of SC_STATIC_SCRATCH_BYTES
+ * inside the library: each device that runs this call holds its own copy
+ * until the process ends, and its address is looked up once per device on
+ * the first call there.  The call allocates no device memory.  Every call on
+ * one device shares that device's array and leaves its contents behind (the
+ * correction writes every scratch byte it reads first, so nothing carries
+ * from one call to the next): calls that may overlap on one device, on
+ * different streams or threads, race and must be ordered by the caller.
+ * Arguments, results and errors as sc_correct; a shape whose scratch
+ * (sc_adamw_workspace_size) exceeds SC_STATIC_SCRATCH_BYTES returns
+ * ACSC_ENOSPC before anything is enqueued.  96 MiB covers a 28672 x 8192
+ * bf16 matrix at r = 128 (88 MiB). */
+#define SC_STATIC_SCRATCH_BYTES (96u * 1024u * 1024u)
+int sc_correct_static(const void *G, acsc_dtype dt, int m, int n, const float *U, const float *d,
+                      const float *V, int r, float alpha, void *G_proj, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Batched forms: the same operations on several weight matrices (e.g. all
  * targeted matrices of the layers a pipeline stage holds) in one call.  Every

@@ -98,6 +98,8 @@ def _load():
                                    vp, vp, vp, vp, vp, sz, vp]
     lib.sc_correct.restype = i32
     lib.sc_correct.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, f32, vp, vp, sz, vp]
+    lib.sc_correct_static.restype = i32
+    lib.sc_correct_static.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, f32, vp, vp]
     for fn in (lib.sc_build_prior_batched, lib.sc_build_subspace_batched, lib.sc_build_ritz_batched):
         fn.restype = i32
         fn.argtypes = [i32, C.POINTER(ScMatrix), i32, f32, i32, i32, i32, f32, u64, vp]
@@ -126,7 +128,7 @@ lib = _load()
 EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "ac_mask_pack_batched",
             "ac_unpack_scatter_batched", "sc_workspace_size",
-            "sc_build_prior", "sc_correct", "sc_build_prior_batched", "sc_correct_batched",
+            "sc_build_prior", "sc_correct", "sc_correct_static", "sc_build_prior_batched", "sc_correct_batched",
             "sc_build_subspace_batched", "sc_build_ritz_batched",
             "sc_adamw_workspace_size", "sc_correct_adamw_batched",
             "ac_bern_mask", "ac_bern_pack", "ac_bern_unpack",
@@ -387,6 +389,28 @@ def sc_correct(G: torch.Tensor, U: torch.Tensor, d: torch.Tensor, V: torch.Tenso
         ws = workspace(m, n, r, 0, G.dtype, G.device)
     _check(lib.sc_correct(_ptr(G), _dt(G), m, n, _ptr(U), _ptr(d), _ptr(V), r, float(alpha),
                           _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+SC_STATIC_SCRATCH_BYTES = 96 * 1024 * 1024
+
+
+def sc_correct_static(G: torch.Tensor, U: torch.Tensor, d: torch.Tensor, V: torch.Tensor, alpha: float,
+                      out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """sc_correct on the library's own device scratch (no workspace; for
+    callers that cannot allocate).  ``out`` must be given by a caller that
+    cannot allocate; calls that overlap on one GPU race."""
+    _need_cuda(G, U, d, V, out)
+    for t in (G, U, d, V):
+        if not t.is_contiguous():
+            raise AcscError(ACSC_EINVAL, "G, U, d, V must be contiguous (no copies are made)")
+    _out(out)
+    m, n = G.shape
+    r = U.shape[1]
+    if out is None:
+        out = torch.empty_like(G)
+    _check(lib.sc_correct_static(_ptr(G), _dt(G), m, n, _ptr(U), _ptr(d), _ptr(V), r, float(alpha), _ptr(out),
+                                 _stream(stream)))
     return out
 
 

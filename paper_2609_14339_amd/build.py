@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libacsc.so")
 OBJDIR = os.path.join(HERE, "_build")
-SOURCES = ["common.hip", "ac.hip", "sc.hip", "pass.hip", "blend.hip", "chol.hip", "orth.hip"]
+SOURCES = ["common.hip", "ac.hip", "sc.hip", "pass.hip", "blend.hip", "chol.hip", "orth.hip",
+           "static_scratch.hip"]
 ARCH = "gfx950"
 
 

@@ -170,3 +170,14 @@ def test_batched_mask_calls_reject_bad_arguments_before_launch(lib):
     key0 = Key(seed=1, step=1, layer=0, microbatch=0, B=0, S=4, H=64)
     assert lib.ac_unpack_scatter_batched(None, 0, 1, 5, 0, H, K, C.byref(key0), None, None, 0, 1.0, None, H, 0,
                                          None) == 0
+
+
+def test_static_correction_rejects_bad_arguments_before_launch(lib):
+    vp = C.c_void_p
+    lib.sc_correct_static.argtypes = [vp, C.c_int, C.c_int, C.c_int, vp, vp, vp, C.c_int, C.c_float, vp, vp]
+    f = vp(0x10000)
+    assert lib.sc_correct_static(f, 1, 64, 64, f, f, f, 0, 0.3, f, None) == -1
+    assert lib.sc_correct_static(f, 9, 64, 64, f, f, f, 4, 0.3, f, None) == -2
+    # beyond the static scratch: refused on the host with ACSC_ENOSPC
+    assert lib.sc_correct_static(f, 1, 65536, 8192, f, f, f, 128, 0.3, f, None) == -5
+    assert "scratch" in _err(lib)
