@@ -39,6 +39,8 @@ typedef enum acsc_dtype { ACSC_F32 = 0, ACSC_BF16 = 1 } acsc_dtype;
 #define ACSC_EALIGN (-3)  /* pointer or stride not aligned as required      */
 #define ACSC_EHIP (-4)    /* HIP launch or runtime failure                  */
 #define ACSC_ENOSPC (-5)  /* workspace too small                            */
+#define ACSC_ENOCONV (-6) /* sc_build_status: a build did not converge, or its
+                             two phases did not meet on its workspace       */
 
 /* Text of the last error raised on the calling thread ("" if none). */
 const char *acsc_last_error(void);
@@ -316,6 +318,23 @@ int sc_build_subspace_batched(int count, const sc_matrix *mats, acsc_dtype dt, f
 int sc_build_ritz_batched(int count, const sc_matrix *mats, acsc_dtype dt, float beta, int r,
                           int oversample, int power_iters, float tau, uint64_t seed,
                           hipStream_t stream);
+
+/* Status of the last build on each matrix's workspace (App. E's top-r SVD:
+ * the Rayleigh-Ritz step ends with a one-sided Jacobi SVD run to a
+ * tolerance, at most 40 sweeps).  Synchronises `stream`, then reads the
+ * status words the build left at the head of each workspace (mats[i].ws;
+ * the other fields are not read).  Returns ACSC_OK when every matrix's
+ * Jacobi met its tolerance; ACSC_ENOCONV when one stopped at the sweep cap
+ * above it, or when a Rayleigh-Ritz phase ran without a subspace phase
+ * having stamped that workspace since the last Rayleigh-Ritz phase (e.g.
+ * sc_build_ritz_batched alone, or after a correction that reused the
+ * workspace); acsc_last_error() names the first such matrix.  sweeps and
+ * residual (arrays of count, or NULL) receive each matrix's sweeps used and
+ * its last sweep's largest off-diagonal ratio.  A workspace that never held
+ * a build gives unspecified values.  The environment variable
+ * ACSC_JACOBI_MAX_SWEEPS, read by each build call, lowers the sweep cap
+ * (1..40), so that a non-converged build can be produced on purpose. */
+int sc_build_status(int count, const sc_matrix *mats, int *sweeps, float *residual, hipStream_t stream);
 
 /* sc_correct on each of mats[0 .. count-1] with shared dt, r and alpha. */
 int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,

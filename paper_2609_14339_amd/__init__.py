@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libacsc.so")
 F32, BF16 = 0, 1
 SC_KMAX = 192
 
-ACSC_OK, ACSC_EINVAL, ACSC_EDTYPE, ACSC_EALIGN, ACSC_EHIP, ACSC_ENOSPC = 0, -1, -2, -3, -4, -5
+ACSC_OK, ACSC_EINVAL, ACSC_EDTYPE, ACSC_EALIGN, ACSC_EHIP, ACSC_ENOSPC, ACSC_ENOCONV = 0, -1, -2, -3, -4, -5, -6
 
 
 class AcscError(RuntimeError):
@@ -103,6 +103,8 @@ def _load():
     for fn in (lib.sc_build_prior_batched, lib.sc_build_subspace_batched, lib.sc_build_ritz_batched):
         fn.restype = i32
         fn.argtypes = [i32, C.POINTER(ScMatrix), i32, f32, i32, i32, i32, f32, u64, vp]
+    lib.sc_build_status.restype = i32
+    lib.sc_build_status.argtypes = [i32, C.POINTER(ScMatrix), vp, vp, vp]
     lib.sc_correct_batched.restype = i32
     lib.sc_correct_batched.argtypes = [i32, C.POINTER(ScMatrix), i32, i32, f32, vp]
     lib.sc_adamw_workspace_size.restype = i32
@@ -129,7 +131,7 @@ EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "ac_mask_pack_batched",
             "ac_unpack_scatter_batched", "sc_workspace_size",
             "sc_build_prior", "sc_correct", "sc_correct_static", "sc_build_prior_batched", "sc_correct_batched",
-            "sc_build_subspace_batched", "sc_build_ritz_batched",
+            "sc_build_subspace_batched", "sc_build_ritz_batched", "sc_build_status",
             "sc_adamw_workspace_size", "sc_correct_adamw_batched",
             "ac_bern_mask", "ac_bern_pack", "ac_bern_unpack",
             "psgd_workspace_size", "psgd_project", "psgd_orthogonalize", "psgd_decompress", "psgd_step")
@@ -458,6 +460,27 @@ def _build_batched(fn, items, r, beta, tau, oversample, power_iters, seed, dtype
                           ws.numel())
     code = BF16 if dtype == torch.bfloat16 else F32
     _check(fn(len(items), arr, code, float(beta), r, oversample, power_iters, float(tau), seed, _stream(stream)))
+
+
+def sc_build_status(workspaces, stream=None):
+    """Synchronise and read the status the last build left in each workspace:
+    a list of (sweeps, residual) per workspace.  Raises AcscError with code
+    ACSC_ENOCONV when a build stopped at its sweep cap above tolerance or ran
+    its Rayleigh-Ritz phase without a subspace phase."""
+    n = len(workspaces)
+    arr = (ScMatrix * max(n, 1))()
+    for i, ws in enumerate(workspaces):
+        _need_cuda(ws)
+        arr[i] = ScMatrix(None, None, 0, 0, None, None, None, None, None, None, _p(ws), ws.numel())
+    sweeps = (C.c_int * max(n, 1))()
+    res = (C.c_float * max(n, 1))()
+    rc = lib.sc_build_status(n, arr, sweeps, res, _stream(stream))
+    out = [(sweeps[i], res[i]) for i in range(n)]
+    if rc != 0:
+        err = AcscError(rc, lib.acsc_last_error().decode())
+        err.status = out
+        raise err
+    return out
 
 
 def sc_correct_batched(items, r: int, alpha: float, dtype: torch.dtype = torch.bfloat16,

@@ -48,15 +48,45 @@ struct Batch {
 
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row & 8) >> 1); }
 
+// global_load_lds_dwordx4 takes its wave-uniform LDS address in M0.  The asm
+// saves M0 in a scratch SGPR and restores it, so M0 holds, after the
+// statement, whatever the compiler may have kept there; an LDS DMA needs one
+// wait state after a scalar write of M0 (the GFX9-family hazard), hence the
+// s_nop after each write (the compiler's hazard tracking does not see inside
+// the statement).  (The compiler's own builtin for this instruction counts
+// it in its LDS wait model and then waits for all fragment reads before the
+// first MFMA of a step; kept opaque here, the explicit vmcnt waits of the
+// kernel order the DMA.)
 __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
 {
-    // M0 is not otherwise used by this kernel
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr) : "memory");
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, off\n\t"
+                 "s_mov_b32 m0, %0\n\t"
+                 "s_nop 0"
+                 : "=&s"(saved)
+                 : "v"(gptr), "s"(lds_addr)
+                 : "memory");
 }
 
 __device__ __forceinline__ void sync_lds()
 {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Wait until at most N vector-memory instructions of this wave are in
+// flight (every older one has completed: they complete in issue order);
+// N < 0 waits for all of them.
+template <int N>
+__device__ __forceinline__ void wait_vm()
+{
+    static_assert(N < 64, "vmcnt range");
+    if constexpr (N < 0)
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // MODE kAdam: the blended values are not stored; they are the gradient of
@@ -110,17 +140,21 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         dma16(src + c * 8, lds0 + ins * 1024);
     }
     // the G tile into registers: thread q holds row q / 16, columns 8 (q % 16) ..
-    // VEC: exactly eight 16-byte loads per thread (row and column clamped into
-    // G; what lies outside is never stored), so that "at most eight loads
-    // outstanding" below means every slice DMA has landed.  Otherwise element
-    // loads, and the wait is for everything.  kFeedback: the same for the
-    // fp32 memory, sixteen 16-byte loads per thread.
-    uint4 g[8];
-    nf4 ev[16];
+    // VEC: kRowLoads unconditional 16-byte loads per thread of kLoadsPerRow
+    // instructions each (row and column clamped into G; what lies outside is
+    // never stored), so that "at most kTail loads outstanding" below means
+    // every slice DMA has landed.  Otherwise element loads, and the wait is
+    // for everything.  kFeedback: the fp32 memory, two 16-byte loads a row.
+    constexpr int kRowLoads = 8;
+    constexpr int kLoadsPerRow = EF ? 2 : 1;
+    constexpr int kTail = VEC ? kRowLoads * kLoadsPerRow : -1;
+    static_assert(kT * kT / (256 * 8) == kRowLoads, "one 16-byte chunk of 8 elements per thread and load");
+    uint4 g[kRowLoads];
+    nf4 ev[kRowLoads * 2];
     if constexpr (EF) {
         if (VEC) {
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < kRowLoads; ++u) {
                 const int q = tid + 256 * u;
                 const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
                 const nf4 *src = reinterpret_cast<const nf4 *>(J.E + static_cast<int64_t>(min(gi, m - 1)) * n +
@@ -131,7 +165,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         }
     }
 #pragma unroll
-    for (int u = 0; u < 8 && !EF; ++u) {
+    for (int u = 0; u < kRowLoads && !EF; ++u) {
         const int q = tid + 256 * u;
         const int gi = row0 + (q >> 4), gj = col0 + (q & 15) * 8;
         if (VEC) {
@@ -152,12 +186,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
             g[u] = v;
         }
     }
-    if (VEC && EF)
-        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    else if (VEC)
-        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_vm<kTail>();
     sync_lds();
 
     // P V^T: wave w computes rows 64 (w / 2) .., columns 64 (w % 2) .. as 2 x 2

@@ -320,10 +320,27 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int swz(int line) { return (line & 7) ^ ((line & 8) >> 1); }
 
+// global_load_lds_dwordx4 takes its wave-uniform LDS address in M0.  The asm
+// saves M0 in a scratch SGPR and restores it, so M0 holds, after the
+// statement, whatever the compiler may have kept there; an LDS DMA needs one
+// wait state after a scalar write of M0 (the GFX9-family hazard), hence the
+// s_nop after each write (the compiler's hazard tracking does not see inside
+// the statement).  (The compiler's own builtin for this instruction counts
+// it in its LDS wait model and then waits for all fragment reads before the
+// first MFMA of a step; kept opaque here, the explicit vmcnt waits of the
+// kernel order the DMA.)
 __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
 {
-    // M0 is not otherwise used by these kernels (no GWS, no indirect register moves)
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr) : "memory");
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, off\n\t"
+                 "s_mov_b32 m0, %0\n\t"
+                 "s_nop 0"
+                 : "=&s"(saved)
+                 : "v"(gptr), "s"(lds_addr)
+                 : "memory");
 }
 
 template <int N>

@@ -7,6 +7,9 @@
 // sc_correct: T = G V (MFMA, split-K), X = U^T T, X_f = d X d, P = U X_f, then
 // one fused pass G_proj = alpha G + (1 - alpha) P V^T.
 #include "common.h"
+
+#include <cstdlib>
+#include <cstring>
 #include "sc_pass.h"
 #include "sc_blend.h"
 #include "sc_chol.h"
@@ -593,6 +596,22 @@ struct JacJob {
     int *info;
 };
 
+// Status words at the head of a build workspace: the Jacobi sweeps used, the
+// last sweep's largest off-diagonal ratio and the tolerance (float bits), a
+// status (bit 0: the sweep cap was reached above the tolerance; bit 1: the
+// Rayleigh-Ritz phase found no stamp of a subspace phase), and the stamp the
+// subspace phase leaves for the Rayleigh-Ritz phase, which clears it.
+constexpr int kInfoSweeps = 0, kInfoResidual = 1, kInfoTol = 2, kInfoStatus = 3, kInfoStamp = 4;
+constexpr int kStatusNoConv = 1, kStatusNoSubspace = 2;
+constexpr int kSubspaceStamp = 0x5B5D7A11;
+constexpr int kJacobiMaxSweeps = 40;
+
+__global__ __launch_bounds__(64) void stamp_kernel(const Batch<JacJob> jb)
+{
+    if (threadIdx.x == 0)
+        jb.j[blockIdx.z].info[kInfoStamp] = kSubspaceStamp;
+}
+
 template <typename T, int RC>
 __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, int k, int KP, int r,
                                                       int RP, float tau, T tol, int max_sweeps)
@@ -631,6 +650,9 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
     static_assert(R % V == 0, "rows per lane");
     int sweeps_used = 0;
     float last_off = 0.f;
+    // the subspace phase that produced Lf stamps the workspace (read before
+    // this kernel clears the stamp, by the same thread)
+    const int stamp = (tid == 0 && info) ? info[kInfoStamp] : 0;
     __syncthreads();
     for (int sweep = 0; sweep < max_sweeps; ++sweep) {
         // exact squared norms at the start of every sweep (the rotations
@@ -738,8 +760,12 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
             break;
     }
     if (tid == 0 && info) {
-        info[0] = sweeps_used;
-        info[1] = __float_as_int(last_off);
+        info[kInfoSweeps] = sweeps_used;
+        info[kInfoResidual] = __float_as_int(last_off);
+        info[kInfoTol] = __float_as_int(static_cast<float>(tol));
+        info[kInfoStatus] = (last_off > static_cast<float>(tol) ? kStatusNoConv : 0) |
+                            (stamp != kSubspaceStamp ? kStatusNoSubspace : 0);
+        info[kInfoStamp] = 0;
     }
     // norms (one wave per column)
     for (int c = wave; c < k; c += nwave) {
@@ -1480,7 +1506,7 @@ Dims dims_of(int m, int n, int r, int oversample)
 
 // Buffers of sc_build_prior (carved in this order).
 struct PriorWs {
-    int *info;   // [0] Jacobi sweeps used, [1] last sweep's largest off-diagonal ratio (float bits)
+    int *info;   // status words (kInfo*): Jacobi sweeps, residual, tolerance, status, phase stamp
     float *Y, *Z, *part, *T, *Bu, *Bv;
     double *gpart, *gram;
     uint16_t *M16, *Yt16, *Zt16;   // bf16 path: shadow of M, transposed thin factors
@@ -1883,6 +1909,10 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         // Z = M^T Q (= B^T) for the Rayleigh-Ritz step: B B^T = Z^T Z = L L^T, SVD of L by Jacobi.
         if ((rc = pass(false)))
             return rc;
+        std::vector<JacJob> sj;
+        for (auto &m : ms)
+            sj.push_back(JacJob{nullptr, nullptr, nullptr, nullptr, nullptr, m.pw.info});
+        launch_jobs("sc_stamp", stamp_kernel, sj, dim3(1), dim3(64), 0, st);
     }
     if (!(phases & kPhaseRitz))
         return ACSC_OK;
@@ -1900,14 +1930,19 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         gram(ms, A, rows, st);
         if ((rc = chol::run("sc_chol", cj, k, KP, false, st)))
             return rc;
+        // the sweep cap can be lowered (not raised) through the environment, so
+        // that the non-convergence report can be exercised
+        int max_sweeps = kJacobiMaxSweeps;
+        if (const char *e = std::getenv("ACSC_JACOBI_MAX_SWEEPS"))
+            max_sweeps = std::max(1, std::min(kJacobiMaxSweeps, std::atoi(e)));
         if (k <= kJacobiF64MaxK)
             launch_jobs("sc_jacobi", jacobi_fn<double>(k), jj, dim3(1), dim3(jacobi_threads(k)),
                         jacobi_lds(k, sizeof(double)), st,
-                        k, KP, r, RP, tau, 1e-13, 40);
+                        k, KP, r, RP, tau, 1e-13, max_sweeps);
         else
             launch_jobs("sc_jacobi", jacobi_fn<float>(k), jj, dim3(1), dim3(jacobi_threads(k)),
                         jacobi_lds(k, sizeof(float)), st,
-                        k, KP, r, RP, tau, 1e-5f, 40);
+                        k, KP, r, RP, tau, 1e-5f, max_sweeps);
     }
     // U = Q Bu, V = Z Bv (first r columns)
     std::vector<orth::GemmReq> og;
@@ -2508,6 +2543,50 @@ extern "C" int sc_build_ritz_batched(int count, const sc_matrix *mats, acsc_dtyp
                                      hipStream_t stream)
 {
     return build_batched(count, mats, dt, beta, r, oversample, power_iters, tau, seed, kPhaseRitz, stream);
+}
+
+extern "C" int sc_build_status(int count, const sc_matrix *mats, int *sweeps, float *residual, hipStream_t stream)
+{
+    clear_error();
+    ACSC_CHECK_ARG(count >= 0, ACSC_EINVAL, "count=%d < 0", count);
+    ACSC_CHECK_ARG(count == 0 || mats != nullptr, ACSC_EINVAL, "mats is NULL");
+    for (int i = 0; i < count; ++i) {
+        ACSC_CHECK_ARG(mats[i].ws != nullptr, ACSC_EINVAL, "matrix %d: workspace is NULL", i);
+        ACSC_CHECK_ARG(aligned(mats[i].ws, 256), ACSC_EALIGN, "matrix %d: workspace must be 256-byte aligned", i);
+        ACSC_CHECK_ARG(mats[i].ws_bytes >= 5 * sizeof(int), ACSC_ENOSPC, "matrix %d: workspace too small", i);
+    }
+    std::vector<int> words(static_cast<size_t>(count) * 5, 0);
+    for (int i = 0; i < count; ++i) {
+        const hipError_t e = hipMemcpyAsync(words.data() + 5 * i, mats[i].ws, 5 * sizeof(int), hipMemcpyDeviceToHost,
+                                            stream);
+        if (e != hipSuccess)
+            return set_error(ACSC_EHIP, "reading the status of matrix %d: %s", i, hipGetErrorString(e));
+    }
+    const hipError_t e = hipStreamSynchronize(stream);
+    if (e != hipSuccess)
+        return set_error(ACSC_EHIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
+    int rc = ACSC_OK;
+    for (int i = 0; i < count; ++i) {
+        const int *w = words.data() + 5 * i;
+        float res, tol;
+        std::memcpy(&res, &w[kInfoResidual], sizeof(float));
+        std::memcpy(&tol, &w[kInfoTol], sizeof(float));
+        if (sweeps)
+            sweeps[i] = w[kInfoSweeps];
+        if (residual)
+            residual[i] = res;
+        if (rc)
+            continue;   // report the first failing matrix
+        if (w[kInfoStatus] & kStatusNoSubspace)
+            rc = set_error(ACSC_ENOCONV, "matrix %d: the Rayleigh-Ritz phase ran without a subspace phase on its "
+                                         "workspace before it", i);
+        else if (w[kInfoStatus] & kStatusNoConv)
+            rc = set_error(ACSC_ENOCONV, "matrix %d: the Rayleigh-Ritz Jacobi stopped after %d sweeps with an "
+                                         "off-diagonal ratio %g above its tolerance %g", i, w[kInfoSweeps], res, tol);
+        else if (w[kInfoStatus] != 0)
+            rc = set_error(ACSC_ENOCONV, "matrix %d: no status of a build (word %d)", i, w[kInfoStatus]);
+    }
+    return rc;
 }
 
 extern "C" int sc_correct_batched(int count, const sc_matrix *mats, acsc_dtype dt, int r, float alpha,

@@ -168,3 +168,44 @@ def test_empty_prior_gives_alpha_g(pk):
     out = ap.correct([G], 0.3)[0]
     torch.cuda.synchronize()
     assert torch.allclose(out, 0.3 * G, rtol=1e-6, atol=0)
+
+
+def test_anchor_prior_built_on_a_side_stream_equals_the_serial_order(pk):
+    """Builds on a stream of their own (from temporaries freed as soon as the
+    call returns) and corrections on the current stream: with publish=False
+    the correction right after an arrival still uses the previous basis (the
+    asynchronous prior of Alg. 1), after publish() the new one, and both are
+    bit-identical to the corrections of the serial order."""
+    from paper_2609_14339_amd.prior import AnchorPrior
+    cfg = workloads.CONFIGS[2]
+    gs = cfg.grad
+    r = gs.r[0]
+    mats = (0, 4)
+    shapes = [gs.shapes[j] for j in mats]
+    dev = torch.device("cuda")
+    pairs = [workloads.grad_pair(gs, 2, 0, j, "cpu") for j in mats]
+    anc = [[(p.G_anc.float() + 0.001 * a * workloads.gaussian(p.G_anc.shape, seed=50 * a + j)).to(torch.bfloat16)
+            .to(dev) for j, p in enumerate(pairs)] for a in range(3)]
+    gm = [p.G_mask.to(dev) for p in pairs]
+    args = (shapes, r, workloads.BETA, workloads.TAU, cfg.oversample, cfg.power_iters)
+    serial = AnchorPrior(*args, dtype=torch.bfloat16, device=dev, seed=9)
+    empty = [o.clone() for o in serial.correct(gm, workloads.ALPHA)]
+    ref = []
+    for a in range(3):
+        serial.arrive(anc[a])
+        ref.append([o.clone() for o in serial.correct(gm, workloads.ALPHA)])
+    side = torch.cuda.Stream()
+    ap = AnchorPrior(*args, dtype=torch.bfloat16, device=dev, seed=9)
+    before, after = [], []
+    for a in range(3):
+        ap.arrive([g.clone() for g in anc[a]], stream=side, publish=False)
+        before.append(ap.correct(gm, workloads.ALPHA))
+        ap.publish()
+        after.append(ap.correct(gm, workloads.ALPHA))
+    torch.cuda.synchronize()
+    for a in range(3):
+        for j in range(len(mats)):
+            assert torch.equal(after[a][j], ref[a][j]), (a, j)
+            assert torch.equal(before[a][j], (ref[a - 1] if a else empty)[j]), (a, j)
+    for j in range(len(mats)):
+        assert torch.equal(ap.M[j], serial.M[j])

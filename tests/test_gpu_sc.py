@@ -247,13 +247,14 @@ def test_batched_calls_equal_single_calls(pk):
             assert torch.equal(x, y)
 
 
-@pytest.mark.parametrize("fused", [False, True])
-def test_build_in_two_phases_equals_one_call(pk, fused):
+@pytest.mark.parametrize("fused,dtype", [(False, torch.bfloat16), (True, torch.bfloat16), (False, torch.float32)])
+def test_build_in_two_phases_equals_one_call(pk, fused, dtype):
     """sc_build_subspace_batched then sc_build_ritz_batched (the same
     arguments and workspaces) give bit-identical EMA state and prior to one
-    sc_build_prior_batched call, with the unfused EMA (a small mixed batch)
-    and with the EMA fused with the first pass (8 x 8192 x 512, 256 row
-    blocks); the ritz phase leaves M alone."""
+    sc_build_prior_batched call, with the unfused EMA (a small mixed batch,
+    bf16 and fp32) and with the EMA fused with the first pass (8 x 8192 x 512,
+    256 row blocks); the ritz phase leaves M alone, and both arrangements
+    report a converged build."""
     if fused:
         shapes, r, p = [(8192, 512)] * 8, 32, 16
     else:
@@ -263,29 +264,77 @@ def test_build_in_two_phases_equals_one_call(pk, fused):
     for split in (False, True):
         items = []
         for i, (m, n) in enumerate(shapes):
-            gp = workloads.grad_pair(workloads.GradSpec(((m, n),), r, (1.0, 100.0), (r,), torch.bfloat16,
+            gp = workloads.grad_pair(workloads.GradSpec(((m, n),), r, (1.0, 100.0), (r,), dtype,
                                                         None, None), 9, i, 0, "cpu")
             outs = (torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
                     torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda"))
             items.append(dict(G_anc=gp.G_anc.cuda(), M=torch.zeros(m, n, device="cuda"), out=outs,
-                              ws=pk.workspace(m, n, r, p, torch.bfloat16)))
+                              ws=pk.workspace(m, n, r, p, dtype)))
         args = (r, workloads.BETA, workloads.TAU, p, q)
         if split:
-            pk.sc_build_subspace_batched(items, *args, seed=70)
+            pk.sc_build_subspace_batched(items, *args, seed=70, dtype=dtype)
             torch.cuda.synchronize()
             M_mid = [it["M"].clone() for it in items]
-            pk.sc_build_ritz_batched(items, *args, seed=70)
+            pk.sc_build_ritz_batched(items, *args, seed=70, dtype=dtype)
             torch.cuda.synchronize()
             for it, Mm in zip(items, M_mid):
                 assert torch.equal(it["M"], Mm)
         else:
-            pk.sc_build_prior_batched(items, *args, seed=70)
+            pk.sc_build_prior_batched(items, *args, seed=70, dtype=dtype)
             torch.cuda.synchronize()
+        status = pk.sc_build_status([it["ws"] for it in items])
+        assert all(1 <= sw <= 40 for sw, _ in status), status
         runs.append(items)
     for a, b in zip(*runs):
         assert torch.equal(a["M"], b["M"])
         for x, y in zip(a["out"], b["out"]):
             assert torch.equal(x, y)
+
+
+@pytest.mark.parametrize("r,p", [(16, 8), (130, 16)])
+def test_build_status_reports_a_sweep_cap_and_a_missing_subspace_phase(pk, r, p, monkeypatch):
+    """The Rayleigh-Ritz Jacobi (fp64 for k <= 128, fp32 above) reports its
+    sweeps and residual; capped at one sweep through ACSC_JACOBI_MAX_SWEEPS
+    it stops above its tolerance and sc_build_status returns ACSC_ENOCONV.
+    A Rayleigh-Ritz phase run alone after a complete build, or after a
+    correction reused the workspace, finds no subspace stamp and is reported
+    too; a new subspace phase clears the report."""
+    m, n = 512, 384
+    spec = workloads.GradSpec(((m, n),), 64, (1.0, 100.0), (r,), torch.bfloat16, None, None)
+    gp = workloads.grad_pair(spec, 9, 0, 0, "cpu")
+    outs = (torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
+            torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda"))
+    item = dict(G_anc=gp.G_anc.cuda(), M=torch.zeros(m, n, device="cuda"), out=outs,
+                ws=pk.workspace(m, n, r, p, torch.bfloat16))
+    args = (r, workloads.BETA, workloads.TAU, p, 2)
+    pk.sc_build_prior_batched([item], *args, seed=3)
+    [(sw, res)] = pk.sc_build_status([item["ws"]])
+    assert 2 <= sw <= 40 and res <= (1e-5 if r + p > 128 else 1e-13), (sw, res)
+    monkeypatch.setenv("ACSC_JACOBI_MAX_SWEEPS", "1")
+    pk.sc_build_prior_batched([item], *args, seed=3)
+    with pytest.raises(pk.AcscError) as e:
+        pk.sc_build_status([item["ws"]])
+    assert e.value.code == pk.ACSC_ENOCONV and "1 sweeps" in str(e.value)
+    assert e.value.status[0][0] == 1
+    monkeypatch.delenv("ACSC_JACOBI_MAX_SWEEPS")
+    # a complete build, then the Rayleigh-Ritz phase alone on the same workspace
+    pk.sc_build_prior_batched([item], *args, seed=3)
+    pk.sc_build_status([item["ws"]])
+    pk.sc_build_ritz_batched([item], *args, seed=3)
+    with pytest.raises(pk.AcscError) as e:
+        pk.sc_build_status([item["ws"]])
+    assert e.value.code == pk.ACSC_ENOCONV and "without a subspace phase" in str(e.value)
+    # the subspace phase, a correction reusing the workspace, then the ritz phase
+    pk.sc_build_subspace_batched([item], *args, seed=3)
+    U, s, V, d = outs
+    pk.sc_correct(gp.G_mask.cuda(), U, d, V, workloads.ALPHA, ws=item["ws"])
+    pk.sc_build_ritz_batched([item], *args, seed=3)
+    with pytest.raises(pk.AcscError) as e:
+        pk.sc_build_status([item["ws"]])
+    assert e.value.code == pk.ACSC_ENOCONV
+    pk.sc_build_subspace_batched([item], *args, seed=3)
+    pk.sc_build_ritz_batched([item], *args, seed=3)
+    pk.sc_build_status([item["ws"]])
 
 
 def test_large_batch_takes_the_fused_ema_pass(pk):
