@@ -389,6 +389,23 @@ def main():
     comp["kernels"] = {k: {kk_: round(v, 4) if isinstance(v, float) else v for kk_, v in d.items()}
                        for k, d in sorted(kern.items())}
 
+    # the method's cadence (Table 2: an anchor arrives every K = 20 fast
+    # steps): every step masks and corrects, one step in 20 also builds the
+    # prior; device time from the summed kernel times of each part
+    corr_tags = ("sc_vconvert", "sc_gv", "sc_utt", "sc_inner_reduce", "sc_filter", "sc_ux", "sc_blend")
+    part_ms = {"masking": 0.0, "correction": 0.0, "build": 0.0}
+    for name, (n, ms) in per_step.items():
+        part = "masking" if name.startswith("ac_") else "correction" if name in corr_tags else "build"
+        part_ms[part] += ms
+    staleness = 20
+    cyc_ms = part_ms["masking"] + part_ms["correction"] + part_ms["build"] / staleness
+    cyc_bytes = ac_bytes + work["sc_correct"]["bytes"] + (work["sc_ema"]["bytes"] + work["sc_pass"]["bytes"]) / staleness
+    comp["per_cycle"] = {"builds_per_step": f"1/{staleness}", "kernel_ms": {k: round(v, 4) for k, v in part_ms.items()},
+                         "ms_per_step": round(cyc_ms, 4), "GB/s": round(cyc_bytes / (cyc_ms * 1e-3) / 1e9, 1),
+                         "frac_hbm": round(cyc_bytes / (cyc_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
+                         "basis": "summed kernel times of the timed steps (library events), one build per "
+                                  f"{staleness} masked and corrected steps"}
+
     if not args.no_adamw:
         comp["sc_correct_adamw"] = adamw_component(pk, mats, r, gs, max(1, min(args.steps, 5)), stream)
     if not args.no_bernoulli:
@@ -649,66 +666,128 @@ def measured_traffic(tag: str, cid: int):
     return table[tag]
 
 
+def _lscpu() -> dict:
+    """Model, sockets, cores and hardware threads of the host (lscpu), and the
+    CPUs this process may run on."""
+    info = {"model": platform.processor() or "unknown"}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
+        kv = {l.split(":", 1)[0].strip(): l.split(":", 1)[1].strip() for l in out.splitlines() if ":" in l}
+        sockets = int(kv.get("Socket(s)", "1"))
+        cores = int(kv.get("Core(s) per socket", "0")) * sockets
+        info = {"model": kv.get("Model name", info["model"]), "sockets": sockets, "cores": cores,
+                "threads": int(kv.get("CPU(s)", "0")), "threads_per_core": int(kv.get("Thread(s) per core", "1"))}
+    except Exception:
+        pass
+    info["affinity"] = len(os.sched_getaffinity(0))
+    return info
+
+
+def _timed(fn, repeat_below_s: float = 10.0):
+    """Wall time of fn(): the median of three runs when one run takes less
+    than repeat_below_s, else that one run.  Returns (seconds, runs)."""
+    t = time.time()
+    fn()
+    first = time.time() - t
+    if first >= repeat_below_s:
+        return first, 1
+    times = [first]
+    for _ in range(2):
+        t = time.time()
+        fn()
+        times.append(time.time() - t)
+    return sorted(times)[1], 3
+
+
 def cpu_baseline(cfg, budget_s: float):
     """The oracle as it stands, on host cores, on a bounded sample of the same
-    workload: pack + unpack of a slice of layer-0 rows (C oracle, one thread),
-    and build_prior + correct of one gradient block (float64 numpy/LAPACK)."""
+    workload, and single-thread figures of the two small configurations:
+      mask leg      the C oracle's pack + unpack of 2048 rows of layer 0 (one
+                    thread: the C oracle is single-threaded);
+      spectral leg  the float64 oracle's EMA + LAPACK SVD + correction of a
+                    leading block of the first gradient (LAPACK/BLAS threads
+                    as reported by threadpoolctl);
+      C1 / C2       the same legs at the tiny and 1B-class configurations with
+                    BLAS held to one thread (C1 whole; C2 the whole activation
+                    and the first 2048 x 2048 gradient).
+    `value` is the algorithmic bytes of the two sample legs over their summed
+    time; legs under 10 s are the median of three runs."""
     import numpy as np
     import torch
     import workloads
     from oracle import mask as om
     from oracle import spectral as osp
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
+        threadpool_limits = None
         blas_threads = 1
+
+    def mask_leg(c, rows):
+        act = c.act
+        H = act.H
+        K = om.keep_count(H, act.keep[0])
+        esz = 2 if act.dtype == torch.bfloat16 else 4
+        x = workloads.activation(act, c.cid, 0, 0, "cpu", rows=rows)
+        xh = x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
+        key = om.mask_key(**{k: v for k, v in workloads.mask_key_fields(c.cid).items()}, B=act.B, S=act.S, H=H)
+
+        def run():
+            vals, idx = om.pack(xh, K, key)
+            om.unpack(vals, H, key, H / K, idx=idx)
+        secs, runs = _timed(run)
+        nbytes = (touched_line_fraction(H, K, esz) * rows * H * esz + rows * K * (esz + 2)
+                  + rows * H * esz + rows * K * (esz + 2))
+        return secs, runs, nbytes
+
+    def spectral_leg(c, m, n):
+        gs = c.grad
+        gsz = 2 if gs.dtype == torch.bfloat16 else 4
+        spec = workloads.GradSpec(((m, n),), min(gs.rank, m, n), gs.s_range, (min(gs.r[0], m, n),),
+                                  gs.dtype, gs.anc_noise, gs.mask_noise)
+        gp = workloads.grad_pair(spec, c.cid, 0, 0, "cpu")
+        Ga, Gm = gp.G_anc.double().numpy(), gp.G_mask.double().numpy()
+
+        def run():
+            osp.corrected_step(np.zeros((m, n)), Ga, Gm, workloads.BETA, spec.r[0], workloads.TAU,
+                               workloads.ALPHA)
+        secs, runs = _timed(run)
+        # EMA (M and G read, M written), one read of M for the SVD, the correction's 3 mn
+        return secs, runs, m * n * (4 + 4 + gsz) + 4 * m * n + 3 * m * n * gsz
+
     act, gs = cfg.act, cfg.grad
-    H = act.H
-    K = om.keep_count(H, act.keep[0])
-    esz = 2 if act.dtype == torch.bfloat16 else 4
-    gsz = 2 if gs.dtype == torch.bfloat16 else 4
-    # mask sample: rows of layer 0
     rows = 2048
-    x = workloads.activation(act, cfg.cid, 0, 0, "cpu", rows=rows)
-    xh = x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
-    key = om.mask_key(**{k: v for k, v in workloads.mask_key_fields(cfg.cid).items()},
-                      B=act.B, S=act.S, H=H)
-    t = time.time()
-    vals, idx = om.pack(xh, K, key)
-    om.unpack(vals, H, key, H / K, idx=idx)
-    t_ac = time.time() - t
-    ac_bytes = (touched_line_fraction(H, K, esz) * rows * H * esz + rows * K * (esz + 2)
-                + rows * H * esz + rows * K * (esz + 2))
+    t_ac, r_ac, ac_bytes = mask_leg(cfg, rows)
     # spectral sample: leading block of the first gradient matrix, sized to the budget
     m0, n0 = gs.shapes[0]
     side = 1024
     while side * 2 <= min(m0, n0) and (side * 2) ** 3 * 4 / 2e10 < budget_s:
         side *= 2
     m, n = min(side, m0), min(side, n0)
-    spec = workloads.GradSpec(((m, n),), min(gs.rank, m), gs.s_range, (min(gs.r[0], m),),
-                              gs.dtype, gs.anc_noise, gs.mask_noise)
-    gp = workloads.grad_pair(spec, cfg.cid, 0, 0, "cpu")
-    Ga = gp.G_anc.double().numpy()
-    Gm = gp.G_mask.double().numpy()
-    t = time.time()
-    osp.corrected_step(np.zeros((m, n)), Ga, Gm, workloads.BETA, spec.r[0], workloads.TAU,
-                       workloads.ALPHA)
-    t_sc = time.time() - t
-    sc_bytes = m * n * (4 + 4 + gsz) + 4 * m * n + 3 * m * n * gsz   # EMA + one read of M + correction
+    t_sc, r_sc, sc_bytes = spectral_leg(cfg, m, n)
+    single = {}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            for cid in (1, 2):
+                c = workloads.CONFIGS[cid]
+                ta, ra, ba = mask_leg(c, c.act.B * c.act.S)
+                mm, nn = c.grad.shapes[0]
+                ts, rs, bs = spectral_leg(c, mm, nn)
+                single[f"C{cid}"] = {"threads": 1, "mask_s": round(ta, 4), "mask_runs": ra,
+                                     "mask_rows": c.act.B * c.act.S, "spectral_s": round(ts, 4),
+                                     "spectral_runs": rs, "spectral_block": f"{mm}x{nn}",
+                                     "GB/s": round((ba + bs) / (ta + ts) / 1e9, 4)}
     total = t_ac + t_sc
-    model = platform.processor()
-    try:
-        model = subprocess.run(["lscpu"], capture_output=True, text=True).stdout
-        model = [l.split(":", 1)[1].strip() for l in model.splitlines() if l.startswith("Model name")][0]
-    except Exception:
-        pass
     return {"value": round((ac_bytes + sc_bytes) / total / 1e9, 3), "unit": "GB/s",
             "cores": int(blas_threads), "kind": "oracle",
-            "sample": f"C oracle pack+unpack of {rows} rows x H={H} (1 thread, {t_ac:.2f} s); "
-                      f"float64 oracle EMA + LAPACK SVD + correction of a {m}x{n} block of the "
-                      f"{m0}x{n0} gradient ({blas_threads} BLAS threads, {t_sc:.2f} s)",
-            "cpu_model": model, "seconds": round(total, 2)}
+            "sample": f"C oracle pack+unpack of {rows} rows x H={act.H} (1 thread, {t_ac:.3f} s, "
+                      f"{'median of 3' if r_ac == 3 else 'one run'}); float64 oracle EMA + LAPACK SVD + "
+                      f"correction of a {m}x{n} block of the {m0}x{n0} gradient ({blas_threads} BLAS threads, "
+                      f"{t_sc:.2f} s, {'median of 3' if r_sc == 3 else 'one run'})",
+            "legs": {"mask": {"threads": 1, "seconds": round(t_ac, 4), "runs": r_ac},
+                     "spectral": {"threads": int(blas_threads), "seconds": round(t_sc, 3), "runs": r_sc}},
+            "single_thread": single, "host": _lscpu(), "seconds": round(total, 2)}
 
 
 if __name__ == "__main__":

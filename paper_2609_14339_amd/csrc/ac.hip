@@ -39,6 +39,21 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t h)
     return h;
 }
 
+// fmix32(h) & mask for masks of at most 8 bits (the Feistel round output,
+// hb <= 8): those bits of the result are bits 0..7 and 16..23 of the second
+// product, which depend only on the low 24 bits of its factors, so that
+// product is taken on the full-rate 24-bit multiplier.  Equal to
+// fmix32(h) & mask for every h.
+__device__ __forceinline__ uint32_t fmix32_low8(uint32_t h, uint32_t mask)
+{
+    h ^= h >> 16;
+    h *= 0x85EBCA6Bu;
+    h ^= h >> 13;
+    h = __umul24(h, 0xC2B2AE35u & 0xFFFFFFu);
+    h ^= h >> 16;
+    return h & mask;
+}
+
 // Key chain over the fields of g(layer, step, B, S, H), plus seed and microbatch.
 __host__ __device__ __forceinline__ uint64_t chain_fields(uint64_t seed, uint64_t layer, uint64_t step,
                                                           uint64_t microbatch, uint64_t B, uint64_t S, uint64_t H)
@@ -109,7 +124,7 @@ struct RowPerm {
         uint32_t L = x >> hb, R = x & mask;
 #pragma unroll
         for (int j = 0; j < ROUNDS; ++j) {
-            const uint32_t t = L ^ (fmix32(R ^ sk[j]) & mask);
+            const uint32_t t = L ^ fmix32_low8(R ^ sk[j], mask);
             L = R;
             R = t;
         }
@@ -159,7 +174,7 @@ struct TabPerm {
 #pragma unroll
         for (int j = 0; j < ROUNDS; ++j)
             for (int r = lane; r < n; r += 64)
-                t[j * kTabStride + r] = static_cast<uint8_t>(fmix32(static_cast<uint32_t>(r) ^ p.sk[j]) & p.mask);
+                t[j * kTabStride + r] = static_cast<uint8_t>(fmix32_low8(static_cast<uint32_t>(r) ^ p.sk[j], p.mask));
     }
 
     __device__ __forceinline__ uint32_t feistel(uint32_t x) const
@@ -402,25 +417,13 @@ struct Vec16<uint32_t> {
     static constexpr int N = 4;
 };
 
-// Per-wave LDS of the staged kernels: bitmap[nw], prefix[nw], then the packed
-// row (K values) and, for pack, its K indices.
-// Unpack: bitmap[nw], prefix[nw], the packed row (K values, padded to 8) and
-// a segment of kSegWords bitmap words of the dense row.
-constexpr int kSegWords = 64;
+// Per-wave LDS of the staged pack: bitmap[nw], prefix[nw], then the packed
+// row (K values) and its K indices.
+constexpr int kSegWords = 64;   // bitmap words per segment of the Bernoulli kernels
 
-// byte offset of the unpack segment in a wave's LDS (16-byte aligned)
-__host__ __device__ __forceinline__ size_t unpack_seg_offset(int nw, int K, int esize)
+__host__ __device__ __forceinline__ size_t staged_wave_bytes(int nw, int K, int esize)
 {
-    return (static_cast<size_t>(2 * nw) * 4 + static_cast<size_t>(K) * esize + 15) & ~static_cast<size_t>(15);
-}
-
-__host__ __device__ __forceinline__ size_t staged_wave_bytes(int nw, int K, int esize, bool with_idx)
-{
-    size_t b = static_cast<size_t>(2 * nw) * 4 + static_cast<size_t>(K) * esize;
-    if (with_idx)
-        b += static_cast<size_t>(K) * 2;
-    else
-        b = unpack_seg_offset(nw, K, esize) + static_cast<size_t>(kSegWords) * 32 * esize;
+    const size_t b = static_cast<size_t>(2 * nw) * 4 + static_cast<size_t>(K) * esize + static_cast<size_t>(K) * 2;
     return (b + 15) & ~static_cast<size_t>(15);
 }
 
@@ -488,7 +491,7 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
     const int wpb = blockDim.x >> 6;
     const int nw = (H + 31) >> 5;
     // the index slots are always reserved (they are written even when idx is NULL)
-    const size_t staged = staged_wave_bytes(nw, K, sizeof(E), true);
+    const size_t staged = staged_wave_bytes(nw, K, sizeof(E));
     const size_t per_wave = staged + (TABLE ? table_bytes<ROUNDS>() : 0);
     uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) + wid * per_wave);
     uint32_t *pre = bm + nw;
@@ -554,6 +557,121 @@ __global__ __launch_bounds__(256) void ac_pack_stream_kernel(const E *__restrict
 // Every lane's work is uniform (zeroing and copying) except the drop of the
 // few kept entries, where writing each 16-byte chunk with its kept entries in
 // place made every lane of the wave pay for the chunks that hold one.
+// Per wave the LDS holds the row bitmap, the packed row, one segment of
+// kUSegWords bitmap words of the dense row and (TABLE) the round table; the
+// rank of each kept entry comes from a wave scan of the segment's word
+// popcounts, so no per-word prefix is stored.  Small per-wave LDS keeps many
+// waves resident, which is what hides the mask's latency.
+constexpr int kUSegWords = 32;
+
+__host__ __device__ __forceinline__ size_t unpack_kv_offset(int nw) { return (static_cast<size_t>(nw) * 4 + 15) & ~static_cast<size_t>(15); }
+
+__host__ __device__ __forceinline__ size_t unpack_seg_offset(int nw, int K, int esize)
+{
+    return (unpack_kv_offset(nw) + static_cast<size_t>(K) * esize + 15) & ~static_cast<size_t>(15);
+}
+
+__host__ __device__ __forceinline__ size_t unpack_wave_bytes(int nw, int K, int esize)
+{
+    return unpack_seg_offset(nw, K, esize) + static_cast<size_t>(kUSegWords) * 32 * esize;
+}
+
+template <typename E, int ROUNDS, bool FROM_IDX, bool VEC, bool TABLE>
+__global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restrict__ vals,
+                                                               const uint16_t *__restrict__ idx,
+                                                               int64_t rows, int H, int K, MaskBatch mb,
+                                                               int w, float scale, E *__restrict__ y,
+                                                               int64_t ld_y, uint16_t *__restrict__ idx_out)
+{
+    extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
+    const int lane = threadIdx.x & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wpb = blockDim.x >> 6;
+    const int nw = (H + 31) >> 5;
+    const size_t staged = unpack_wave_bytes(nw, K, sizeof(E));
+    const size_t per_wave = staged + (TABLE ? table_bytes<ROUNDS>() : 0);
+    unsigned char *wbase = reinterpret_cast<unsigned char *>(smem) + wid * per_wave;
+    uint32_t *bm = reinterpret_cast<uint32_t *>(wbase);
+    E *kv = reinterpret_cast<E *>(wbase + unpack_kv_offset(nw));
+    E *seg = reinterpret_cast<E *>(wbase + unpack_seg_offset(nw, K, sizeof(E)));
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
+    if (row >= rows)
+        return;
+    const uint32_t layer = blockIdx.y;
+    vals += layer * mb.vals_stride + row * K;
+    y += layer * mb.dense_stride + row * ld_y;
+    for (int i = lane; i < K; i += 64)
+        kv[i] = vals[i];
+    for (int i = lane; i < nw; i += 64)
+        bm[i] = 0u;
+    if (FROM_IDX) {
+        wave_sync();
+        const uint16_t *ir = idx + layer * mb.idx_stride + row * K;
+        for (int i = lane; i < K; i += 64) {
+            const uint32_t j = ir[i];
+            if (j < static_cast<uint32_t>(H))
+                atomicOr(&bm[j >> 5], 1u << (j & 31));
+        }
+    } else {
+        const RowPerm<ROUNDS> perm(mb.key(layer), static_cast<uint64_t>(row), w, static_cast<uint32_t>(H));
+        if (TABLE) {
+            const TabPerm<ROUNDS> tp(perm, wbase + staged, lane);
+            wave_sync();
+            mark_kept(tp, K, static_cast<uint32_t>(H), bm, lane);
+        } else {
+            wave_sync();
+            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
+        }
+    }
+    wave_sync();
+    uint16_t *orow = (!FROM_IDX && idx_out) ? idx_out + layer * mb.idx_stride + row * K : nullptr;
+    // The dense row is assembled in LDS one segment at a time: zero the
+    // segment, drop the kept entries into it (lane l owns word l of the
+    // segment), then write it out with whole 16-byte stores.  Global memory
+    // only sees full lines.
+    constexpr int N = Vec16<E>::N;
+    int base = 0;   // kept entries before the segment
+    for (int s0 = 0; s0 < nw; s0 += kUSegWords) {
+        const int e0 = s0 * 32;                            // first element of the segment
+        const int len = min(kUSegWords * 32, H - e0);      // elements in it
+#pragma unroll
+        for (int c = lane; c < kUSegWords * 32 / N; c += 64)
+            reinterpret_cast<uint4 *>(seg)[c] = make_uint4(0u, 0u, 0u, 0u);
+        const int wd = s0 + lane;
+        uint32_t bits = (lane < kUSegWords && wd < nw) ? bm[wd] : 0u;
+        const int cnt = __popc(bits);
+        const int pre = wave_exclusive_scan(cnt, lane);
+        const int total = __shfl(pre + cnt, 63, 64);
+        wave_sync();
+        int rank = base + pre;
+        while (bits) {
+            const int t = __ffs(bits) - 1;
+            bits &= bits - 1u;
+            seg[lane * 32 + t] = scaled(kv[rank], scale);
+            if (orow)
+                orow[rank] = static_cast<uint16_t>((wd << 5) + t);
+            ++rank;
+        }
+        base += total;
+        wave_sync();
+        if (VEC) {
+            const int nch = len / N;
+            // non-temporal: the dense rows are not read again by this stage,
+            // and stores that stay dirty in the memory-side cache are only
+            // paid for by whichever kernel runs next
+            for (int c = lane; c < nch; c += 64)
+                __builtin_nontemporal_store(reinterpret_cast<const u32x4 *>(seg)[c],
+                                            reinterpret_cast<u32x4 *>(y + e0 + c * N));
+            for (int j = nch * N + lane; j < len; j += 64)
+                y[e0 + j] = seg[j];
+        } else {
+            for (int j = lane; j < len; j += 64)
+                y[e0 + j] = seg[j];
+        }
+        wave_sync();
+    }
+}
+
 // The kept positions of a row, ascending, from its bitmap and word prefix:
 // every lane walks its words and stores each set bit's position at its rank.
 __device__ __forceinline__ void store_index_list(const uint32_t *bm, const uint32_t *pre, int nw, int lane,
@@ -570,85 +688,8 @@ __device__ __forceinline__ void store_index_list(const uint32_t *bm, const uint3
     }
 }
 
-template <typename E, int ROUNDS, bool FROM_IDX, bool VEC, bool TABLE>
-__global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restrict__ vals,
-                                                               const uint16_t *__restrict__ idx,
-                                                               int64_t rows, int H, int K, MaskBatch mb,
-                                                               int w, float scale, E *__restrict__ y,
-                                                               int64_t ld_y, uint16_t *__restrict__ idx_out)
-{
-    extern __shared__ __attribute__((aligned(16))) uint32_t smem[];
-    const int lane = threadIdx.x & 63;
-    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int wpb = blockDim.x >> 6;
-    const int nw = (H + 31) >> 5;
-    const size_t staged = staged_wave_bytes(nw, K, sizeof(E), false);
-    const size_t per_wave = staged + (TABLE ? table_bytes<ROUNDS>() : 0);
-    uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) + wid * per_wave);
-    uint32_t *pre = bm + nw;
-    E *kv = reinterpret_cast<E *>(pre + nw);
-    const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
-    const bool active = row < rows;
-    const uint32_t layer = blockIdx.y;
-    const uint64_t key = FROM_IDX ? 0 : mb.key(layer);
-    vals += layer * mb.vals_stride;
-    y += layer * mb.dense_stride;
-    if (FROM_IDX)
-        idx += layer * mb.idx_stride;
-    if (active) {
-        const E *vr = vals + row * K;
-        for (int i = lane; i < K; i += 64)
-            kv[i] = vr[i];
-    }
-    row_bitmap<ROUNDS, TABLE>(bm, pre, nw, active, key, row, w, H, K, lane,
-                              (FROM_IDX && active) ? idx + row * K : nullptr,
-                              reinterpret_cast<uint8_t *>(bm) + staged);
-    if (!active)
-        return;
-    if (!FROM_IDX && idx_out)
-        store_index_list(bm, pre, nw, lane, idx_out + layer * mb.idx_stride + row * K);
-    // The dense row is assembled in LDS one segment (64 bitmap words) at a
-    // time: zero the segment, drop the kept entries into it, then write it out
-    // with whole 16-byte stores.  Global memory only sees full lines.
-    E *yr = y + row * ld_y;
-    E *seg = reinterpret_cast<E *>(reinterpret_cast<unsigned char *>(bm) + unpack_seg_offset(nw, K, sizeof(E)));
-    constexpr int N = Vec16<E>::N;
-    for (int s0 = 0; s0 < nw; s0 += kSegWords) {
-        const int e0 = s0 * 32;                            // first element of the segment
-        const int len = min(kSegWords * 32, H - e0);       // elements in it
-#pragma unroll
-        for (int c = lane; c < kSegWords * 32 / N; c += 64)
-            reinterpret_cast<uint4 *>(seg)[c] = make_uint4(0u, 0u, 0u, 0u);
-        wave_sync();
-        const int wd = s0 + lane;
-        if (wd < nw) {
-            uint32_t bits = bm[wd];
-            int rank = static_cast<int>(pre[wd]);
-            while (bits) {
-                const int t = __ffs(bits) - 1;
-                bits &= bits - 1u;
-                seg[lane * 32 + t] = scaled(kv[rank++], scale);
-            }
-        }
-        wave_sync();
-        if (VEC) {
-            const int nch = len / N;
-            // non-temporal: the dense rows are not read again by this stage,
-            // and stores that stay dirty in the memory-side cache are only
-            // paid for by whichever kernel runs next
-            for (int c = lane; c < nch; c += 64)
-                __builtin_nontemporal_store(reinterpret_cast<const u32x4 *>(seg)[c],
-                                            reinterpret_cast<u32x4 *>(yr + e0 + c * N));
-            for (int j = nch * N + lane; j < len; j += 64)
-                yr[e0 + j] = seg[j];
-        } else {
-            for (int j = lane; j < len; j += 64)
-                yr[e0 + j] = seg[j];
-        }
-        wave_sync();
-    }
-}
-
+// Unpack without LDS staging of the dense row (for rows whose staged form does
+// not fit the LDS budget).
 template <typename E, int ROUNDS, bool FROM_IDX, bool VEC>
 __global__ __launch_bounds__(256) void ac_unpack_kernel(const E *__restrict__ vals,
                                                         const uint16_t *__restrict__ idx,
@@ -1021,7 +1062,7 @@ void launch_pack_t(const void *x, int nl, int64_t rows, int H, int64_t ld_x, boo
     // available for rows whose kept entries are dense (keep >= 1/4).
     const int nw = (H + 31) / 32;
     const size_t tab = TABLE ? table_bytes<ROUNDS>() : 0;
-    const size_t sper = staged_wave_bytes(nw, K, sizeof(E), true) + tab;
+    const size_t sper = staged_wave_bytes(nw, K, sizeof(E)) + tab;
     const bool dense = 4 * static_cast<int64_t>(K) >= H;
     if (dense && vec && sper <= kLdsBudget &&
         allow_lds(ac_pack_stream_kernel<E, ROUNDS, TABLE>, sper * waves_for(sper)) == ACSC_OK) {
@@ -1067,7 +1108,7 @@ bool launch_unpack_stream(const void *vals, const uint16_t *idx, int nl, int64_t
                           hipStream_t st)
 {
     const int nw = (H + 31) / 32;
-    const size_t sper = staged_wave_bytes(nw, K, sizeof(E), false) + (TABLE ? table_bytes<ROUNDS>() : 0);
+    const size_t sper = unpack_wave_bytes(nw, K, sizeof(E)) + (TABLE ? table_bytes<ROUNDS>() : 0);
     if (sper > kLdsBudget ||
         allow_lds(ac_unpack_stream_kernel<E, ROUNDS, FROM_IDX, VEC, TABLE>, sper * waves_for(sper)) != ACSC_OK)
         return false;
