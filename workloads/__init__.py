@@ -92,7 +92,7 @@ CONFIGS = {
               ActSpec(2, 8192, 8192, torch.bfloat16, (0.02,), "normal"),
               GradSpec(((8192, 8192), (8192, 28672), (28672, 8192)), 128, (1.0, 100.0),
                        (128,), torch.bfloat16, None, None, layers=4),
-              oversample=32, power_iters=2),
+              oversample=16, power_iters=2),
 }
 
 
