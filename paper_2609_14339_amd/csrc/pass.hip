@@ -16,6 +16,9 @@
 #include "sc_pass.h"
 
 #include <algorithm>
+#include <functional>
+#include <map>
+#include <mutex>
 
 namespace acsc {
 namespace pass {
@@ -328,7 +331,8 @@ __device__ __forceinline__ int swz(int line) { return (line & 7) ^ ((line & 8) >
 // the statement).  (The compiler's own builtin for this instruction counts
 // it in its LDS wait model and then waits for all fragment reads before the
 // first MFMA of a step; kept opaque here, the explicit vmcnt waits of the
-// kernel order the DMA.)
+// kernel order the DMA.)  The LDS address is wave-uniform at every call;
+// readfirstlane hands it to the statement in an SGPR.
 __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
 {
     uint32_t saved;
@@ -339,7 +343,7 @@ __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
                  "s_mov_b32 m0, %0\n\t"
                  "s_nop 0"
                  : "=&s"(saved)
-                 : "v"(gptr), "s"(lds_addr)
+                 : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
                  : "memory");
 }
 
@@ -354,75 +358,118 @@ __device__ __forceinline__ void sync_lds()
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// One workgroup per CU (the LDS ring takes most of the 160 KiB), so the
-// register budget is that of one wave per SIMD.
+// A run of workgroups over one job: row blocks rb0 .. rb0 + nrb - 1, each cut
+// into `pieces` k ranges of kchunk (piece p of row block b is workgroup
+// wg0 + (b - rb0) * pieces + p).  A single piece writes C; several write
+// partials, which pass_reduce_kernel adds in piece order.
+struct Seg {
+    int job, wg0, rb0, nrb, pieces, kchunk;
+};
+struct DJob {
+    const uint16_t *A;
+    int64_t lda;
+    const uint16_t *Bt;
+    int64_t ldbt;
+    float *C;
+    int64_t ldc;
+    float *part;      // partial of piece p at part + p * ss, row stride np
+    int64_t ss;
+    int M, K;
+};
+struct SegBatch {
+    int njobs, nseg;
+    DJob j[kMaxJobs];
+    Seg s[2 * kMaxJobs];
+};
+
+// Eight waves, two per SIMD, one workgroup per CU (the LDS ring takes most of
+// the 160 KiB).  The stage's 256 lines of A form four 64-line groups; wave w
+// stages half (w / 4) of group (w % 4), 32 lines, and multiplies the 32
+// output rows of that half against all NP columns.  For opA = A those are
+// the lines it staged itself; for opA = A^T it also reads the other half's
+// k-lines, so the per-step barrier (needed anyway for the shared thin
+// factor) orders both.  With two waves per SIMD one wave's MFMAs overlap the
+// other's waits, which one wave per SIMD could not do.  Waves 0-3 also stage
+// the thin factor.
 template <bool TRANS, int NT, int S>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void pass_dma_kernel(const Batch jb, int np)
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void pass_dma_kernel(const SegBatch sb,
+                                                                                                  int np)
 {
-    const Job &J = jb.j[blockIdx.z];
-    if (static_cast<int>(blockIdx.x) >= J.nblocks)
-        return;
+    const int wg = static_cast<int>(blockIdx.x);
+    int si = 0;
+    while (si + 1 < sb.nseg && wg >= sb.s[si + 1].wg0)
+        ++si;
+    const Seg &G = sb.s[si];
+    const int rel = wg - G.wg0;
+    if (rel >= G.nrb * G.pieces)
+        return;   // padding between segments
+    const DJob &J = sb.j[G.job];
     constexpr int NP = NT * 16;
     constexpr int A_BYTES = 256 * 128;
     constexpr int STAGE = A_BYTES + NP * 128;
-    constexpr int BI = NT / 2;            // thin-factor DMA instructions per wave and step
-    constexpr int PER_STEP = 8 + BI;      // DMA instructions per wave and step
-    static_assert(S >= 2 && PER_STEP * (S - 2) < 64, "vmcnt range");
+    constexpr int BI = NT / 2;            // thin-factor DMA instructions of waves 0-3 per step
+    constexpr int PER_A = 4;              // A DMA instructions per wave and step
+    static_assert(S >= 2 && (PER_A + BI) * (S - 2) < 64, "vmcnt range");
     __shared__ __attribute__((aligned(1024))) unsigned char smem[S * STAGE];
 
     const uint16_t *__restrict__ A = J.A;
     const uint16_t *__restrict__ Bt = J.Bt;
     const int64_t lda = J.lda, ldbt = J.ldbt;
-    const int M = J.M, splits = J.splits;
+    const int M = J.M;
+    const int piece = rel % G.pieces;
+    const int row0 = (G.rb0 + rel / G.pieces) * kBM;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int split = static_cast<int>(blockIdx.x % splits);
-    const int row0 = static_cast<int>(blockIdx.x / splits) * kBM;
-    const int wrow0 = row0 + wave * 64;
-    const int kbeg = split * J.kchunk;
-    const int kend = min(J.K, kbeg + J.kchunk);
+    const int grp = wave & 3, half = wave >> 2;
+    const bool stages_b = wave < 4;
+    const int grow0 = row0 + grp * 64;     // first line of this wave's group (a row of A, or a column of A^T)
+    const int kbeg = piece * G.kchunk;
+    const int kend = min(J.K, kbeg + G.kchunk);
     const int nsteps = kend > kbeg ? static_cast<int>(cdiv(kend - kbeg, kBK)) : 0;
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_byte *)smem));
 
-    f32x16 acc[2][NT / 2];
+    constexpr int NC = NT / 2;
+    f32x16 acc[NC];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int t = 0; t < NC; ++t)
 #pragma unroll
-        for (int t = 0; t < NT / 2; ++t)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                acc[a][t][e] = 0.f;
+        for (int e = 0; e < 16; ++e)
+            acc[t][e] = 0.f;
 
-    // Issue one step's DMA into stage `st`: this wave's 64 lines of A (8
-    // instructions), then BI of the 2 NT instructions of the thin factor.
-    // Addresses are clamped into the operands: rows past M feed outputs that
-    // are never stored, thin-factor rows past np feed columns that are never
-    // stored, k past kend is zeroed in LDS before the tail step is used.
+    // Issue one step's DMA into stage `st`: this wave's 32 lines of A (4
+    // instructions), and for waves 0-3 BI of the 2 NT instructions of the
+    // thin factor.  Addresses are clamped into the operands: rows past M feed
+    // outputs that are never stored, thin-factor rows past np feed columns
+    // that are never stored, k past kend is zeroed in LDS before the tail
+    // step is used.
     auto issue = [&](int s, int st) {
         const int k0 = kbeg + s * kBK;
         const uint32_t sbase = lds0 + st * STAGE;
         const int sub = lane >> 3;            // line within the instruction
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int line = j * 8 + sub;     // line within this wave's 64
+        for (int jj = 0; jj < PER_A; ++jj) {
+            const int j = half * PER_A + jj;
+            const int line = j * 8 + sub;     // line within the group's 64
             const int c = (lane & 7) ^ swz(line);
             const uint16_t *src;
             if (!TRANS) {
                 const int gk = k0 + c * 8;
-                src = A + static_cast<int64_t>(min(wrow0 + line, M - 1)) * lda + (gk < kend ? gk : kbeg);
+                src = A + static_cast<int64_t>(min(grow0 + line, M - 1)) * lda + (gk < kend ? gk : kbeg);
             } else {
-                src = A + static_cast<int64_t>(min(k0 + line, kend - 1)) * lda + min(wrow0 + c * 8, (M - 1) & ~7);
+                src = A + static_cast<int64_t>(min(k0 + line, kend - 1)) * lda + min(grow0 + c * 8, (M - 1) & ~7);
             }
-            dma16(src, sbase + wave * 8192 + j * 1024);
+            dma16(src, sbase + grp * 8192 + j * 1024);
         }
+        if (stages_b) {
 #pragma unroll
-        for (int b = 0; b < BI; ++b) {
-            const int m = b * 4 + wave;       // instruction index within the thin-factor tile
-            const int line = m * 8 + sub;
-            const int c = (lane & 7) ^ swz(line);
-            const int gk = k0 + c * 8;
-            const uint16_t *src = Bt + static_cast<int64_t>(min(line, np - 1)) * ldbt + (gk < kend ? gk : kbeg);
-            dma16(src, sbase + A_BYTES + m * 1024);
+            for (int b = 0; b < BI; ++b) {
+                const int m = b * 4 + wave;   // instruction index within the thin-factor tile
+                const int line = m * 8 + sub;
+                const int c = (lane & 7) ^ swz(line);
+                const int gk = k0 + c * 8;
+                const uint16_t *src = Bt + static_cast<int64_t>(min(line, np - 1)) * ldbt + (gk < kend ? gk : kbeg);
+                dma16(src, sbase + A_BYTES + m * 1024);
+            }
         }
     };
     // Tail step: zero k >= kend in the thin factor (and in A when k runs
@@ -431,7 +478,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         unsigned char *base = smem + st * STAGE;
         const int kk = kend - k0;
         const int nlines = (TRANS ? 0 : 256) + NP;
-        for (int q = tid; q < nlines * 8; q += 256) {
+        for (int q = tid; q < nlines * 8; q += 512) {
             const int l = q >> 3, c = q & 7;
             if (c * 8 + 8 <= kk)
                 continue;
@@ -441,41 +488,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             *slot = keep_first(*slot, kk - c * 8);
         }
     };
-    // v_mfma_f32_32x32x16_bf16 (one wave per SIMD reaches its full rate with
-    // it, unlike 16x16x32): A[i][k] / B[k][j] in lane i (j) + 32 (k / 8),
-    // element k % 8.  The wave's 64 rows are two row tiles, the NP columns NC
+    // v_mfma_f32_32x32x16_bf16: A[i][k] / B[k][j] in lane i (j) + 32 (k / 8),
+    // element k % 8.  The wave's 32 rows are one row tile, the NP columns NC
     // column tiles; a 64-deep step is four 16-deep substeps.
-    constexpr int NC = NT / 2;
-    auto frags = [&](const unsigned char *aw, const unsigned char *bw, int kq, bf16x8 (&af)[2], bf16x8 (&bf)[NC]) {
+    auto frags = [&](const unsigned char *aw, const unsigned char *bw, int kq, bf16x8 &af, bf16x8 (&bf)[NC]) {
         const int c = kq * 2 + (lane >> 5);
-#pragma unroll
-        for (int a = 0; a < 2; ++a) {
-            if (!TRANS) {
-                const int line = a * 32 + (lane & 31);
-                af[a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
-            } else {
-                // ds_read_b64_tr_b16: in each group of 16 lanes, result lane
-                // L, element e = element L % 4 of what lane 4 e + L / 4 read.
-                // Source lane 4 e + q of the group reads columns 4 q .. 4 q + 3
-                // (of the group's 16) from k-line e, so lane L receives column
-                // L of four consecutive k-lines; two reads give the eight k of
-                // a fragment.
-                const int l16 = lane & 15;
-                const int col = a * 32 + ((lane >> 4) & 1) * 16 + (l16 & 3) * 4;
-                const int line0 = kq * 16 + (lane >> 5) * 8 + (l16 >> 2);
-                v4i16 h0, h1;
-                {
-                    const int line = line0;
-                    h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
-                        (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
-                }
-                {
-                    const int line = line0 + 4;
-                    h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
-                        (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
-                }
-                af[a] = bf16x8{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+        if (!TRANS) {
+            const int line = half * 32 + (lane & 31);
+            af = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
+        } else {
+            // ds_read_b64_tr_b16: in each group of 16 lanes, result lane
+            // L, element e = element L % 4 of what lane 4 e + L / 4 read.
+            // Source lane 4 e + q of the group reads columns 4 q .. 4 q + 3
+            // (of the group's 16) from k-line e, so lane L receives column
+            // L of four consecutive k-lines; two reads give the eight k of
+            // a fragment.
+            const int l16 = lane & 15;
+            const int col = half * 32 + ((lane >> 4) & 1) * 16 + (l16 & 3) * 4;
+            const int line0 = kq * 16 + (lane >> 5) * 8 + (l16 >> 2);
+            v4i16 h0, h1;
+            {
+                const int line = line0;
+                h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
+                    (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
             }
+            {
+                const int line = line0 + 4;
+                h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
+                    (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
+            }
+            af = bf16x8{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
         }
 #pragma unroll
         for (int t = 0; t < NC; ++t) {
@@ -485,9 +527,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     };
     auto compute = [&](int st) {
         const unsigned char *base = smem + st * STAGE;
-        const unsigned char *aw = base + wave * 8192;
+        const unsigned char *aw = base + grp * 8192;
         const unsigned char *bw = base + A_BYTES;
-        bf16x8 af[2][2], bf[2][NC];
+        bf16x8 af[2], bf[2][NC];
         frags(aw, bw, 0, af[0], bf[0]);
 #pragma unroll
         for (int kq = 0; kq < 4; ++kq) {
@@ -495,19 +537,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
                 frags(aw, bw, kq + 1, af[(kq + 1) & 1], bf[(kq + 1) & 1]);
 #pragma unroll
             for (int t = 0; t < NC; ++t)
-#pragma unroll
-                for (int a = 0; a < 2; ++a)
-                    acc[a][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kq & 1][a], bf[kq & 1][t], acc[a][t], 0, 0, 0);
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kq & 1], bf[kq & 1][t], acc[t], 0, 0, 0);
         }
         // keep each substep's fragment reads ahead of the previous substep's MFMAs
-        constexpr int DS = (TRANS ? 4 : 2) + NC;
+        constexpr int DS = (TRANS ? 2 : 1) + NC;
         __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
 #pragma unroll
         for (int kq = 0; kq < 3; ++kq) {
             __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * NC, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NC, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NC, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NC, 0);
     };
 
     if (nsteps > 0) {
@@ -517,7 +557,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             issue(min(p, last), p);
         int st = 0;   // stage of step s
         for (int s = 0; s < nsteps; ++s) {
-            wait_dma<PER_STEP * (S - 2)>();   // this wave's DMA for step s has landed
+            // this wave's DMA for step s has landed
+            if (stages_b)
+                wait_dma<(PER_A + BI) * (S - 2)>();
+            else
+                wait_dma<PER_A * (S - 2)>();
             sync_lds();                        // everyone's has; stage (s - 1) % S is free
             const int k0 = kbeg + s * kBK;
             if (k0 + kBK > kend) {
@@ -536,20 +580,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 
     // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
-    float *Cs = J.C + static_cast<int64_t>(split) * J.split_stride;
-    const int64_t ldc = J.ldc;
+    float *Cs = G.pieces > 1 ? J.part + static_cast<int64_t>(piece) * J.ss : J.C;
+    const int64_t ldo = G.pieces > 1 ? static_cast<int64_t>(np) : J.ldc;
+    const int wrow0 = grow0 + half * 32;
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int t = 0; t < NC; ++t) {
+        const int col = t * 32 + (lane & 31);
 #pragma unroll
-        for (int t = 0; t < NT / 2; ++t) {
-            const int col = t * 32 + (lane & 31);
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int row = wrow0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                if (row < M && col < np)
-                    Cs[static_cast<int64_t>(row) * ldc + col] = acc[a][t][e];
-            }
+        for (int e = 0; e < 16; ++e) {
+            const int row = wrow0 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            if (row < M && col < np)
+                Cs[static_cast<int64_t>(row) * ldo + col] = acc[t][e];
         }
+    }
 }
 
 // C[i, c] = sum over splits of part[s][i, c] (NP columns, float4 when aligned).
@@ -586,50 +629,170 @@ __global__ __launch_bounds__(256) void pass_reduce_kernel(const RedBatch jb)
     }
 }
 
-template <bool TRANS, int NTK, bool VEC>
-void launch_nt(const char *tag, const std::vector<Job> &jobs, int gx, int np, hipStream_t st)
+// Element-load passes (operands that are not 16-byte aligned): one z slice
+// of the grid per job.
+template <bool TRANS>
+void launch_scalar(const char *tag, const std::vector<Job> &jobs, int gx, int np, hipStream_t st)
 {
     for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
         Batch b{};
         b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
         for (int i = 0; i < b.count; ++i)
             b.j[i] = jobs[c0 + i];
-        if (VEC) {
-            // three LDS stages while they fit in 160 KiB, else two
-            constexpr int S = (3 * (256 * 128 + NTK * 16 * 128) <= 160 * 1024) ? 3 : 2;
-            auto kern = pass_dma_kernel<TRANS, NTK, S>;
-            ACSC_LAUNCH(tag, kern, dim3(gx, 1, b.count), dim3(256), 0, st, b, np);
-        } else {
-            auto kern = pass_kernel<TRANS, NTK, false>;
-            ACSC_LAUNCH(tag, kern, dim3(gx, 1, b.count), dim3(256), 0, st, b, np);
+        auto kern = pass_kernel<TRANS, kMaxNT, false>;
+        ACSC_LAUNCH(tag, kern, dim3(gx, 1, b.count), dim3(256), 0, st, b, np);
+    }
+}
+
+template <bool TRANS, int NTK>
+void launch_segs(const char *tag, const SegBatch &b, int grid, int np, hipStream_t st)
+{
+    // three LDS stages while they fit in 160 KiB, else two
+    constexpr int S = (3 * (256 * 128 + NTK * 16 * 128) <= 160 * 1024) ? 3 : 2;
+    auto kern = pass_dma_kernel<TRANS, NTK, S>;
+    ACSC_LAUNCH(tag, kern, dim3(grid), dim3(512), 0, st, b, np);
+}
+
+// Column tiles are computed in pairs (even NTK).
+template <bool TRANS>
+void launch_dma(const char *tag, const SegBatch &b, int grid, int np, hipStream_t st)
+{
+    switch ((np / 16 + 1) / 2) {
+    case 1: launch_segs<TRANS, 2>(tag, b, grid, np, st); break;
+    case 2: launch_segs<TRANS, 4>(tag, b, grid, np, st); break;
+    case 3: launch_segs<TRANS, 6>(tag, b, grid, np, st); break;
+    case 4: launch_segs<TRANS, 8>(tag, b, grid, np, st); break;
+    case 5: launch_segs<TRANS, 10>(tag, b, grid, np, st); break;
+    default: launch_segs<TRANS, 12>(tag, b, grid, np, st); break;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Workgroup order of the DMA passes.  Workgroups go to the XCDs in turn
+// (workgroup i to XCD i % X) and, within an XCD, to whichever CU frees up
+// first; one pass workgroup fills a CU.  A batch that mixes long and short
+// rows (the 70B-class build: 128 row blocks of 448 steps, 576 of 128) then
+// ends with a round in which only some CUs work.  The plan below simulates
+// that dispatch and, where it shortens the simulated makespan, moves the
+// last-dispatched row blocks to the end of the grid as two k halves each
+// (partials added by pass_reduce_kernel): for the 70B-class batch, 64 short
+// row blocks halved make the long blocks' CUs finish with the others.
+// ---------------------------------------------------------------------------
+struct JobShape {
+    int nrb, splits, kchunk, K;
+    bool halvable;
+};
+
+struct SegPlan {
+    std::vector<Seg> segs;
+    std::vector<int> halved;   // per job: trailing row blocks cut in two k halves
+    int grid = 0;
+    int64_t makespan = 0;
+};
+
+int64_t simulate_dispatch(const std::vector<int> &cost, int xcds, int cus_per_xcd)
+{
+    std::vector<std::vector<int64_t>> free_at(static_cast<size_t>(xcds),
+                                              std::vector<int64_t>(static_cast<size_t>(cus_per_xcd), 0));
+    int64_t end = 0;
+    for (size_t i = 0; i < cost.size(); ++i) {
+        if (cost[i] == 0)
+            continue;
+        std::vector<int64_t> &h = free_at[i % static_cast<size_t>(xcds)];
+        std::pop_heap(h.begin(), h.end(), std::greater<int64_t>());
+        h.back() += cost[i];
+        end = std::max(end, h.back());
+        std::push_heap(h.begin(), h.end(), std::greater<int64_t>());
+    }
+    return end;
+}
+
+SegPlan layout(const std::vector<JobShape> &js, const std::vector<int> &halved, int xcds, int cus_per_xcd)
+{
+    SegPlan p;
+    p.halved = halved;
+    std::vector<int> cost;
+    auto add = [&](int job, int rb0, int nrb, int pieces, int kc) {
+        if (nrb <= 0)
+            return;
+        const int wg0 = static_cast<int>(round_up(static_cast<int64_t>(cost.size()), 8));
+        cost.resize(static_cast<size_t>(wg0), 0);
+        p.segs.push_back(Seg{job, wg0, rb0, nrb, pieces, kc});
+        for (int b = 0; b < nrb; ++b)
+            for (int pc = 0; pc < pieces; ++pc) {
+                const int64_t kb = static_cast<int64_t>(pc) * kc;
+                const int64_t ke = std::min<int64_t>(js[job].K, kb + kc);
+                cost.push_back(ke > kb ? static_cast<int>(cdiv(ke - kb, kBK)) : 0);
+            }
+    };
+    for (size_t j = 0; j < js.size(); ++j)
+        add(static_cast<int>(j), 0, js[j].nrb - halved[j], js[j].splits, js[j].kchunk);
+    for (size_t j = 0; j < js.size(); ++j)
+        if (halved[j] > 0)
+            add(static_cast<int>(j), js[j].nrb - halved[j], halved[j], 2,
+                static_cast<int>(round_up(cdiv(js[j].K, 2), kBK)));
+    p.grid = static_cast<int>(cost.size());
+    p.makespan = simulate_dispatch(cost, xcds, cus_per_xcd);
+    return p;
+}
+
+void device_cus(int &xcds, int &cus_per_xcd)
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    xcds = std::max(1, cus / 32);   // 32 CUs per XCD on gfx950 (one XCD per partition in CPX mode)
+    cus_per_xcd = std::max(1, cus / xcds);
+}
+
+// The plan depends only on the batch's shapes and the device, so it is made
+// once per distinct batch and kept.
+SegPlan plan(const std::vector<JobShape> &js)
+{
+    int xcds = 8, cpx = 32;
+    device_cus(xcds, cpx);
+    std::vector<int64_t> key{xcds, cpx};
+    for (const JobShape &j : js)
+        key.insert(key.end(), {j.nrb, j.splits, j.kchunk, j.K, j.halvable ? 1 : 0});
+    static std::mutex mu;
+    static std::map<std::vector<int64_t>, SegPlan> cache;
+    {
+        std::lock_guard<std::mutex> g(mu);
+        auto it = cache.find(key);
+        if (it != cache.end())
+            return it->second;
+    }
+    std::vector<int> halved(js.size(), 0);
+    SegPlan best = layout(js, halved, xcds, cpx);
+    bool whole = true;
+    int64_t wgs = 0;
+    for (const JobShape &j : js) {
+        whole = whole && j.splits == 1;
+        wgs += static_cast<int64_t>(j.nrb) * j.splits;
+    }
+    if (whole && wgs >= static_cast<int64_t>(xcds) * cpx) {
+        // trailing row blocks (in dispatch order) that may be halved
+        int hmax = 0;
+        for (size_t j = js.size(); j-- > 0 && js[j].halvable;)
+            hmax += js[j].nrb;
+        hmax = std::min(hmax, 2 * xcds * cpx);
+        for (int h = 8; h <= hmax; h += 8) {
+            std::vector<int> hv(js.size(), 0);
+            int rest = h;
+            for (size_t j = js.size(); j-- > 0 && rest > 0;) {
+                hv[j] = std::min(rest, js[j].nrb);
+                rest -= hv[j];
+            }
+            SegPlan p = layout(js, hv, xcds, cpx);
+            if (p.makespan < best.makespan)
+                best = p;
         }
     }
+    std::lock_guard<std::mutex> g(mu);
+    cache.emplace(key, best);
+    return best;
 }
-
-// Column tiles are computed in pairs (even NTK); unaligned operands take the
-// element-load variant, which is built for the largest width only.
-template <bool TRANS>
-int launch(const char *tag, int np, bool vec, const std::vector<Job> &jobs, int gx, hipStream_t st)
-{
-    if (jobs.empty())
-        return ACSC_OK;
-    if (np < 16 || np % 16 != 0 || np > SC_KMAX)
-        return set_error(ACSC_EINVAL, "pass with %d thin-factor columns (a multiple of 16 up to %d)", np, SC_KMAX);
-    if (!vec) {
-        launch_nt<TRANS, kMaxNT, false>(tag, jobs, gx, np, st);
-        return ACSC_OK;
-    }
-    switch ((np / 16 + 1) / 2) {
-    case 1: launch_nt<TRANS, 2, true>(tag, jobs, gx, np, st); break;
-    case 2: launch_nt<TRANS, 4, true>(tag, jobs, gx, np, st); break;
-    case 3: launch_nt<TRANS, 6, true>(tag, jobs, gx, np, st); break;
-    case 4: launch_nt<TRANS, 8, true>(tag, jobs, gx, np, st); break;
-    case 5: launch_nt<TRANS, 10, true>(tag, jobs, gx, np, st); break;
-    default: launch_nt<TRANS, 12, true>(tag, jobs, gx, np, st); break;
-    }
-    return ACSC_OK;
-}
-
 
 // ---------------------------------------------------------------------------
 // Anchor EMA fused with the first pass (see sc_pass.h).  A workgroup of 512
@@ -860,6 +1023,8 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
     if (reqs.empty())
         return ACSC_OK;
     const int NP = reqs[0].NP;
+    if (NP < 16 || NP % 16 != 0 || NP > SC_KMAX)
+        return set_error(ACSC_EINVAL, "pass with %d thin-factor columns (a multiple of 16 up to %d)", NP, SC_KMAX);
     for (const auto &q : reqs)
         if (q.NP != NP)
             return set_error(ACSC_EINVAL, "pass: thin factors of one launch must have the same width");
@@ -876,7 +1041,9 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
     for (size_t i = 0; i < order.size(); ++i)
         order[i] = i;
     std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return reqs[a].K > reqs[b].K; });
-    std::vector<Job> jobs;
+    std::vector<Job> sj;                 // element-load jobs
+    std::vector<const Req *> vq;         // DMA jobs
+    std::vector<int> vsplits, vchunk;
     std::vector<RedJob> red;
     int gx = 1;
     int64_t rtot = 1;
@@ -885,28 +1052,61 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
         int splits = std::min(want, max_splits(q.M, q.K));
         const int64_t chunk = round_up(cdiv(q.K, splits), kBK);
         splits = static_cast<int>(std::max<int64_t>(1, cdiv(q.K, chunk)));
-        const int nb = static_cast<int>(cdiv(q.M, kBM) * splits);
-        gx = std::max(gx, nb);
-        if (splits == 1) {
-            jobs.push_back(Job{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, 0, q.M, q.K, static_cast<int>(chunk), 1,
-                               nb, q.avec ? 1 : 0});
-        } else {
-            const int64_t ss = static_cast<int64_t>(q.M) * NP;
-            jobs.push_back(Job{q.A, q.lda, q.Bt, q.ldbt, q.part, NP, ss, q.M, q.K, static_cast<int>(chunk),
-                               splits, nb, q.avec ? 1 : 0});
+        const int64_t ss = static_cast<int64_t>(q.M) * NP;
+        if (splits > 1) {
             red.push_back(RedJob{q.part, ss, q.C, q.ldc, q.M, NP, splits});
             rtot = std::max<int64_t>(rtot, static_cast<int64_t>(q.M) * (NP / 4));
         }
+        if (q.avec) {
+            vq.push_back(&q);
+            vsplits.push_back(splits);
+            vchunk.push_back(static_cast<int>(chunk));
+            continue;
+        }
+        const int nb = static_cast<int>(cdiv(q.M, kBM) * splits);
+        gx = std::max(gx, nb);
+        if (splits == 1)
+            sj.push_back(Job{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, 0, q.M, q.K, static_cast<int>(chunk), 1, nb, 0});
+        else
+            sj.push_back(Job{q.A, q.lda, q.Bt, q.ldbt, q.part, NP, ss, q.M, q.K, static_cast<int>(chunk), splits, nb,
+                             0});
     }
     gx = static_cast<int>(round_up(gx, 8));   // block -> XCD placement is the same for every job
-    std::vector<Job> vj, sj;
-    for (const Job &j : jobs)
-        (j.avec ? vj : sj).push_back(j);
-    for (int v = 0; v < 2; ++v) {
-        const std::vector<Job> &js = v == 0 ? vj : sj;
-        const int rc = trans ? launch<true>(tag, NP, v == 0, js, gx, st) : launch<false>(tag, NP, v == 0, js, gx, st);
-        if (rc != ACSC_OK)
-            return rc;
+    if (!sj.empty()) {
+        if (trans)
+            launch_scalar<true>(tag, sj, gx, NP, st);
+        else
+            launch_scalar<false>(tag, sj, gx, NP, st);
+    }
+    for (size_t c0 = 0; c0 < vq.size(); c0 += kMaxJobs) {
+        const size_t cnt = std::min<size_t>(kMaxJobs, vq.size() - c0);
+        std::vector<JobShape> js;
+        SegBatch b{};
+        b.njobs = static_cast<int>(cnt);
+        for (size_t i = 0; i < cnt; ++i) {
+            const Req &q = *vq[c0 + i];
+            b.j[i] = DJob{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, q.part, static_cast<int64_t>(q.M) * NP, q.M, q.K};
+            js.push_back(JobShape{static_cast<int>(cdiv(q.M, kBM)), vsplits[c0 + i], vchunk[c0 + i], q.K,
+                                  q.part != nullptr && max_splits(q.M, q.K) >= 2 && q.K >= 2 * kBK});
+        }
+        const SegPlan pl = plan(js);
+        b.nseg = static_cast<int>(pl.segs.size());
+        for (size_t i = 0; i < pl.segs.size(); ++i)
+            b.s[i] = pl.segs[i];
+        if (trans)
+            launch_dma<true>(tag, b, pl.grid, NP, st);
+        else
+            launch_dma<false>(tag, b, pl.grid, NP, st);
+        for (size_t i = 0; i < cnt; ++i) {
+            const int h = pl.halved[i];
+            if (h <= 0)
+                continue;
+            const Req &q = *vq[c0 + i];
+            const int64_t r0 = static_cast<int64_t>(js[i].nrb - h) * kBM;
+            red.push_back(RedJob{q.part + r0 * NP, static_cast<int64_t>(q.M) * NP, q.C + r0 * q.ldc, q.ldc,
+                                 static_cast<int>(q.M - r0), NP, 2});
+            rtot = std::max<int64_t>(rtot, (q.M - r0) * (NP / 4));
+        }
     }
     for (size_t c0 = 0; c0 < red.size(); c0 += kMaxJobs) {
         RedBatch b{};
