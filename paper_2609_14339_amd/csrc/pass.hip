@@ -26,7 +26,6 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) unsigned char lds_byte;
@@ -389,8 +388,14 @@ struct SegBatch {
 // the lines it staged itself; for opA = A^T it also reads the other half's
 // k-lines, so the per-step barrier (needed anyway for the shared thin
 // factor) orders both.  With two waves per SIMD one wave's MFMAs overlap the
-// other's waits, which one wave per SIMD could not do.  Waves 0-3 also stage
-// the thin factor.
+// other's waits, which one wave per SIMD could not do.  The 2 NT DMA
+// instructions of the thin factor go round the eight waves.
+//
+// The product runs on v_mfma_f32_16x16x32_bf16 over exactly NP = 16 NT
+// columns.  These passes run at a third of the MFMA peak, and with real data
+// the MFMA's power draw, not HBM, sets their pace: covering 144 columns with
+// 16-wide tiles (rather than padding to 160 for 32x32 tiles) takes 8% less
+// time, and needs fewer fragment reads than 32x32 tiles plus a 16-wide one.
 template <bool TRANS, int NT, int S>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void pass_dma_kernel(const SegBatch sb,
                                                                                                   int np)
@@ -407,9 +412,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     constexpr int NP = NT * 16;
     constexpr int A_BYTES = 256 * 128;
     constexpr int STAGE = A_BYTES + NP * 128;
-    constexpr int BI = NT / 2;            // thin-factor DMA instructions of waves 0-3 per step
-    constexpr int PER_A = 4;              // A DMA instructions per wave and step
-    static_assert(S >= 2 && (PER_A + BI) * (S - 2) < 64, "vmcnt range");
+    constexpr int BN = 2 * NT;                    // thin-factor DMA instructions per step
+    constexpr int BI_LO = BN / 8, BI_HI = (BN + 7) / 8;
+    constexpr int PER_A = 4;                      // A DMA instructions per wave and step
+    static_assert(S >= 2 && (PER_A + BI_HI) * (S - 2) < 64, "vmcnt range");
     __shared__ __attribute__((aligned(1024))) unsigned char smem[S * STAGE];
 
     const uint16_t *__restrict__ A = J.A;
@@ -421,24 +427,23 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave & 3, half = wave >> 2;
-    const bool stages_b = wave < 4;
+    const bool b_hi = wave < BN % 8;             // this wave issues BI_HI thin-factor instructions, else BI_LO
     const int grow0 = row0 + grp * 64;     // first line of this wave's group (a row of A, or a column of A^T)
     const int kbeg = piece * G.kchunk;
     const int kend = min(J.K, kbeg + G.kchunk);
     const int nsteps = kend > kbeg ? static_cast<int>(cdiv(kend - kbeg, kBK)) : 0;
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_byte *)smem));
 
-    constexpr int NC = NT / 2;
-    f32x16 acc[NC];
+    f32x4 acc[2][NT];
 #pragma unroll
-    for (int t = 0; t < NC; ++t)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-            acc[t][e] = 0.f;
+        for (int t = 0; t < NT; ++t)
+            acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // Issue one step's DMA into stage `st`: this wave's 32 lines of A (4
-    // instructions), and for waves 0-3 BI of the 2 NT instructions of the
-    // thin factor.  Addresses are clamped into the operands: rows past M feed
+    // instructions), and instructions w, w + 8, ... of the 2 NT of the thin
+    // factor.  Addresses are clamped into the operands: rows past M feed
     // outputs that are never stored, thin-factor rows past np feed columns
     // that are never stored, k past kend is zeroed in LDS before the tail
     // step is used.
@@ -460,10 +465,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             }
             dma16(src, sbase + grp * 8192 + j * 1024);
         }
-        if (stages_b) {
 #pragma unroll
-            for (int b = 0; b < BI; ++b) {
-                const int m = b * 4 + wave;   // instruction index within the thin-factor tile
+        for (int b = 0; b < BI_HI; ++b) {
+            if (b < BI_LO || b_hi) {
+                const int m = b * 8 + wave;   // instruction index within the thin-factor tile
                 const int line = m * 8 + sub;
                 const int c = (lane & 7) ^ swz(line);
                 const int gk = k0 + c * 8;
@@ -488,40 +493,43 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             *slot = keep_first(*slot, kk - c * 8);
         }
     };
-    // v_mfma_f32_32x32x16_bf16: A[i][k] / B[k][j] in lane i (j) + 32 (k / 8),
-    // element k % 8.  The wave's 32 rows are one row tile, the NP columns NC
-    // column tiles; a 64-deep step is four 16-deep substeps.
-    auto frags = [&](const unsigned char *aw, const unsigned char *bw, int kq, bf16x8 &af, bf16x8 (&bf)[NC]) {
-        const int c = kq * 2 + (lane >> 5);
-        if (!TRANS) {
-            const int line = half * 32 + (lane & 31);
-            af = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
-        } else {
-            // ds_read_b64_tr_b16: in each group of 16 lanes, result lane
-            // L, element e = element L % 4 of what lane 4 e + L / 4 read.
-            // Source lane 4 e + q of the group reads columns 4 q .. 4 q + 3
-            // (of the group's 16) from k-line e, so lane L receives column
-            // L of four consecutive k-lines; two reads give the eight k of
-            // a fragment.
-            const int l16 = lane & 15;
-            const int col = half * 32 + ((lane >> 4) & 1) * 16 + (l16 & 3) * 4;
-            const int line0 = kq * 16 + (lane >> 5) * 8 + (l16 >> 2);
-            v4i16 h0, h1;
-            {
-                const int line = line0;
-                h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
-                    (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
+    // v_mfma_f32_16x16x32_bf16: A[i][k] / B[k][j] in lane i (j) + 16 (k / 8),
+    // element k % 8.  The wave's 32 rows are two 16-row tiles, the NP columns
+    // NT 16-wide tiles; a 64-deep step is two 32-deep halves.
+    auto frags = [&](const unsigned char *aw, const unsigned char *bw, int kh, bf16x8 (&af)[2], bf16x8 (&bf)[NT]) {
+        const int c = kh * 4 + (lane >> 4);   // 16-byte chunk: k = 8 c .. 8 c + 7 of the step
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+            if (!TRANS) {
+                const int line = half * 32 + a * 16 + (lane & 15);
+                af[a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
+            } else {
+                // ds_read_b64_tr_b16: in each group of 16 lanes, result lane
+                // L, element e = element L % 4 of what lane 4 e + L / 4 read.
+                // Source lane 4 e + q of group g reads columns 4 q .. 4 q + 3
+                // (of the tile's 16) from k-line 8 g + e, so lane L receives
+                // column L of four consecutive k-lines; two reads give the
+                // eight k of a fragment.
+                const int l16 = lane & 15;
+                const int col = half * 32 + a * 16 + (l16 & 3) * 4;
+                const int line0 = kh * 32 + (lane >> 4) * 8 + (l16 >> 2);
+                v4i16 h0, h1;
+                {
+                    const int line = line0;
+                    h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
+                        (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
+                }
+                {
+                    const int line = line0 + 4;
+                    h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
+                        (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
+                }
+                af[a] = bf16x8{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
             }
-            {
-                const int line = line0 + 4;
-                h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16 *>(
-                    (lds_byte *)(aw + line * 128 + 16 * ((col >> 3) ^ swz(line)) + (col & 7) * 2)));
-            }
-            af = bf16x8{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
         }
 #pragma unroll
-        for (int t = 0; t < NC; ++t) {
-            const int line = t * 32 + (lane & 31);
+        for (int t = 0; t < NT; ++t) {
+            const int line = t * 16 + (lane & 15);
             bf[t] = *reinterpret_cast<const bf16x8 *>(bw + line * 128 + 16 * (c ^ swz(line)));
         }
     };
@@ -529,25 +537,22 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         const unsigned char *base = smem + st * STAGE;
         const unsigned char *aw = base + grp * 8192;
         const unsigned char *bw = base + A_BYTES;
-        bf16x8 af[2], bf[2][NC];
+        bf16x8 af[2][2], bf[2][NT];
         frags(aw, bw, 0, af[0], bf[0]);
+        frags(aw, bw, 1, af[1], bf[1]);
 #pragma unroll
-        for (int kq = 0; kq < 4; ++kq) {
-            if (kq + 1 < 4)
-                frags(aw, bw, kq + 1, af[(kq + 1) & 1], bf[(kq + 1) & 1]);
+        for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-            for (int t = 0; t < NC; ++t)
-                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kq & 1], bf[kq & 1][t], acc[t], 0, 0, 0);
-        }
-        // keep each substep's fragment reads ahead of the previous substep's MFMAs
-        constexpr int DS = (TRANS ? 2 : 1) + NC;
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[kh][a], bf[kh][t], acc[a][t], 0, 0, 0);
+        // the second half's fragment reads go out under the first half's MFMAs
+        constexpr int DS = (TRANS ? 4 : 2) + NT;
         __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
-#pragma unroll
-        for (int kq = 0; kq < 3; ++kq) {
-            __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, NC, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, NC, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NT, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NT, 0);
     };
 
     if (nsteps > 0) {
@@ -558,10 +563,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         int st = 0;   // stage of step s
         for (int s = 0; s < nsteps; ++s) {
             // this wave's DMA for step s has landed
-            if (stages_b)
-                wait_dma<(PER_A + BI) * (S - 2)>();
+            if (b_hi)
+                wait_dma<(PER_A + BI_HI) * (S - 2)>();
             else
-                wait_dma<PER_A * (S - 2)>();
+                wait_dma<(PER_A + BI_LO) * (S - 2)>();
             sync_lds();                        // everyone's has; stage (s - 1) % S is free
             const int k0 = kbeg + s * kBK;
             if (k0 + kBK > kend) {
@@ -579,20 +584,22 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         wait_dma<0>();
     }
 
-    // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
+    // D[i][j] of a 16 x 16 tile: lane j + 16 (i / 4), element i % 4
     float *Cs = G.pieces > 1 ? J.part + static_cast<int64_t>(piece) * J.ss : J.C;
     const int64_t ldo = G.pieces > 1 ? static_cast<int64_t>(np) : J.ldc;
     const int wrow0 = grow0 + half * 32;
 #pragma unroll
-    for (int t = 0; t < NC; ++t) {
-        const int col = t * 32 + (lane & 31);
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int row = wrow0 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-            if (row < M && col < np)
-                Cs[static_cast<int64_t>(row) * ldo + col] = acc[t][e];
+        for (int t = 0; t < NT; ++t) {
+            const int col = t * 16 + (lane & 15);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = wrow0 + a * 16 + 4 * (lane >> 4) + e;
+                if (row < M && col < np)
+                    Cs[static_cast<int64_t>(row) * ldo + col] = acc[a][t][e];
+            }
         }
-    }
 }
 
 // C[i, c] = sum over splits of part[s][i, c] (NP columns, float4 when aligned).
@@ -653,16 +660,21 @@ void launch_segs(const char *tag, const SegBatch &b, int grid, int np, hipStream
     ACSC_LAUNCH(tag, kern, dim3(grid), dim3(512), 0, st, b, np);
 }
 
-// Column tiles are computed in pairs (even NTK).
 template <bool TRANS>
 void launch_dma(const char *tag, const SegBatch &b, int grid, int np, hipStream_t st)
 {
-    switch ((np / 16 + 1) / 2) {
-    case 1: launch_segs<TRANS, 2>(tag, b, grid, np, st); break;
-    case 2: launch_segs<TRANS, 4>(tag, b, grid, np, st); break;
-    case 3: launch_segs<TRANS, 6>(tag, b, grid, np, st); break;
-    case 4: launch_segs<TRANS, 8>(tag, b, grid, np, st); break;
-    case 5: launch_segs<TRANS, 10>(tag, b, grid, np, st); break;
+    switch (np / 16) {
+    case 1: launch_segs<TRANS, 1>(tag, b, grid, np, st); break;
+    case 2: launch_segs<TRANS, 2>(tag, b, grid, np, st); break;
+    case 3: launch_segs<TRANS, 3>(tag, b, grid, np, st); break;
+    case 4: launch_segs<TRANS, 4>(tag, b, grid, np, st); break;
+    case 5: launch_segs<TRANS, 5>(tag, b, grid, np, st); break;
+    case 6: launch_segs<TRANS, 6>(tag, b, grid, np, st); break;
+    case 7: launch_segs<TRANS, 7>(tag, b, grid, np, st); break;
+    case 8: launch_segs<TRANS, 8>(tag, b, grid, np, st); break;
+    case 9: launch_segs<TRANS, 9>(tag, b, grid, np, st); break;
+    case 10: launch_segs<TRANS, 10>(tag, b, grid, np, st); break;
+    case 11: launch_segs<TRANS, 11>(tag, b, grid, np, st); break;
     default: launch_segs<TRANS, 12>(tag, b, grid, np, st); break;
     }
 }
@@ -800,7 +812,7 @@ SegPlan plan(const std::vector<JobShape> &js)
 // (16-byte loads, 16 lanes per row) and of G, forms the EMA, stores M
 // (non-temporal) and the bf16 shadow, and drops the bf16 piece into the
 // swizzled LDS layout of the streaming pass, where the step is multiplied on
-// 32x32x16 MFMA.  All loads go through registers (the next step's are
+// 16x16x32 MFMA.  All loads go through registers (the next step's are
 // issued before this step's product), so the compiler's own wait counts are
 // exact.
 // ---------------------------------------------------------------------------
@@ -832,14 +844,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     if (static_cast<int>(blockIdx.x) >= J.nblocks)
         return;
     constexpr int NP = NT * 16;
-    constexpr int NC = NT / 2;
     constexpr int A_BYTES = 256 * 128;
     constexpr int STAGE = A_BYTES + NP * 128;
     constexpr int BCH = NP * 8;                 // 16-byte chunks of one thin-factor step
     constexpr int W = 8;                        // waves
     constexpr int NTH = 64 * W;                 // threads
     constexpr int PU = 4096 / NTH;              // 4-element pieces of M per thread and step
-    constexpr int RT = 8 / W;                   // 32-row tiles per wave
     constexpr int BPT = (BCH + NTH - 1) / NTH;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE];
 
@@ -858,14 +868,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int kend = min(n, kbeg + J.kchunk);
     const int nsteps = static_cast<int>(cdiv(kend - kbeg, kBK));
 
-    f32x16 acc[RT][NC];
+    f32x4 acc[2][NT];
 #pragma unroll
-    for (int a = 0; a < RT; ++a)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int t = 0; t < NC; ++t)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                acc[a][t][e] = 0.f;
+        for (int t = 0; t < NT; ++t)
+            acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // piece u of this thread: row (tid + 512 u) / 16 of the block, 4 elements
     // at column 4 ((tid + 512 u) % 16) of the step, so that 16 lanes cover a
@@ -938,30 +946,35 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             }
         }
     };
-    // v_mfma_f32_32x32x16_bf16 on the step in LDS (the layout of pass_dma_kernel<false>)
+    // v_mfma_f32_16x16x32_bf16 on the step in LDS, in the layout and order of
+    // pass_dma_kernel<false> (the same products in the same order, so the
+    // result equals the separate EMA and pass bit for bit); this wave's 32
+    // rows are two 16-row tiles
     auto compute = [&](int buf) {
-        const unsigned char *aw = smem + buf * STAGE + wave * (RT * 4096);
+        const unsigned char *aw = smem + buf * STAGE + wave * 4096;
         const unsigned char *bw = smem + buf * STAGE + A_BYTES;
+        bf16x8 af[2][2], bf[2][NT];
 #pragma unroll
-        for (int kq = 0; kq < 4; ++kq) {
-            const int c = kq * 2 + (lane >> 5);
-            bf16x8 af[RT], bf[NC];
+        for (int kh = 0; kh < 2; ++kh) {
+            const int c = kh * 4 + (lane >> 4);
 #pragma unroll
-            for (int a = 0; a < RT; ++a) {
-                const int line = a * 32 + (lane & 31);
-                af[a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
+            for (int a = 0; a < 2; ++a) {
+                const int line = a * 16 + (lane & 15);
+                af[kh][a] = *reinterpret_cast<const bf16x8 *>(aw + line * 128 + 16 * (c ^ swz(line)));
             }
 #pragma unroll
-            for (int t = 0; t < NC; ++t) {
-                const int line = t * 32 + (lane & 31);
-                bf[t] = *reinterpret_cast<const bf16x8 *>(bw + line * 128 + 16 * (c ^ swz(line)));
+            for (int t = 0; t < NT; ++t) {
+                const int line = t * 16 + (lane & 15);
+                bf[kh][t] = *reinterpret_cast<const bf16x8 *>(bw + line * 128 + 16 * (c ^ swz(line)));
             }
-#pragma unroll
-            for (int t = 0; t < NC; ++t)
-#pragma unroll
-                for (int a = 0; a < RT; ++a)
-                    acc[a][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[t], acc[a][t], 0, 0, 0);
         }
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[kh][a], bf[kh][t], acc[a][t], 0, 0, 0);
     };
 
     load(0);
@@ -976,19 +989,19 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         lds_barrier();
     }
 
-    // D[i][j] of a 32 x 32 tile: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4;
+    // D[i][j] of a 16 x 16 tile: lane j + 16 (i / 4), element i % 4;
     // a split writes its partial (row stride np), added up by pass_reduce_kernel
     float *Cout = J.splits > 1 ? J.part + split * J.ss : J.C;
     const int64_t ldo = J.splits > 1 ? static_cast<int64_t>(np) : J.ldc;
-    const int wrow0 = row0 + wave * (RT * 32);
+    const int wrow0 = row0 + wave * 32;
 #pragma unroll
-    for (int a = 0; a < RT; ++a)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int t = 0; t < NC; ++t) {
-            const int col = t * 32 + (lane & 31);
+        for (int t = 0; t < NT; ++t) {
+            const int col = t * 16 + (lane & 15);
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int row = wrow0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            for (int e = 0; e < 4; ++e) {
+                const int row = wrow0 + a * 16 + 4 * (lane >> 4) + e;
                 if (row < m && col < np)
                     Cout[static_cast<int64_t>(row) * ldo + col] = acc[a][t][e];
             }
@@ -1176,12 +1189,18 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
         }
         gx = std::max(gx, nb);
     }
-    switch ((NP / 16 + 1) / 2) {   // column tiles in pairs; tiles past NP read zeros
-    case 1: ema_launch<2>(tag, jobs, gx, NP, a, b, st); break;
-    case 2: ema_launch<4>(tag, jobs, gx, NP, a, b, st); break;
-    case 3: ema_launch<6>(tag, jobs, gx, NP, a, b, st); break;
-    case 4: ema_launch<8>(tag, jobs, gx, NP, a, b, st); break;
-    case 5: ema_launch<10>(tag, jobs, gx, NP, a, b, st); break;
+    switch (NP / 16) {
+    case 1: ema_launch<1>(tag, jobs, gx, NP, a, b, st); break;
+    case 2: ema_launch<2>(tag, jobs, gx, NP, a, b, st); break;
+    case 3: ema_launch<3>(tag, jobs, gx, NP, a, b, st); break;
+    case 4: ema_launch<4>(tag, jobs, gx, NP, a, b, st); break;
+    case 5: ema_launch<5>(tag, jobs, gx, NP, a, b, st); break;
+    case 6: ema_launch<6>(tag, jobs, gx, NP, a, b, st); break;
+    case 7: ema_launch<7>(tag, jobs, gx, NP, a, b, st); break;
+    case 8: ema_launch<8>(tag, jobs, gx, NP, a, b, st); break;
+    case 9: ema_launch<9>(tag, jobs, gx, NP, a, b, st); break;
+    case 10: ema_launch<10>(tag, jobs, gx, NP, a, b, st); break;
+    case 11: ema_launch<11>(tag, jobs, gx, NP, a, b, st); break;
     default: ema_launch<12>(tag, jobs, gx, NP, a, b, st); break;
     }
     for (size_t c0 = 0; c0 < red.size(); c0 += kMaxJobs) {
