@@ -374,6 +374,7 @@ struct DJob {
     float *part;      // partial of piece p at part + p * ss, row stride np
     int64_t ss;
     int M, K;
+    int ntc;          // > 0: A is a tiled shadow (ntc tiles per tile row)
 };
 struct SegBatch {
     int njobs, nseg;
@@ -457,7 +458,20 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             const int line = j * 8 + sub;     // line within the group's 64
             const int c = (lane & 7) ^ swz(line);
             const uint16_t *src;
-            if (!TRANS) {
+            if (J.ntc > 0) {
+                // tiled shadow: this wave's 64 lines are one tile (opA = A: rows
+                // grow0.., k0..k0+63) or one tile's k-rows (opA = A^T: k-rows
+                // k0.., columns grow0..grow0+63).  Row blocks past M re-read the
+                // last tile row (outputs never stored); k-rows past kend are
+                // clamped to kend - 1, so the zero rows of the thin factor never
+                // meet the tile's unwritten padding.
+                const int tg = min(grow0 >> 6, (M - 1) >> 6);
+                if (!TRANS)
+                    src = A + (static_cast<int64_t>(tg) * J.ntc + (k0 >> 6)) * 4096 + line * 64 + c * 8;
+                else
+                    src = A + (static_cast<int64_t>(k0 >> 6) * J.ntc + tg) * 4096 + min(line, kend - 1 - k0) * 64 +
+                          c * 8;
+            } else if (!TRANS) {
                 const int gk = k0 + c * 8;
                 src = A + static_cast<int64_t>(min(grow0 + line, M - 1)) * lda + (gk < kend ? gk : kbeg);
             } else {
@@ -828,6 +842,7 @@ struct EmaJob {
     float *part;      // split k: partial products [splits][m][np]
     int64_t ss;       // elements per split's partial
     int kchunk, splits;
+    int ntc;          // tiles per tile row of the shadow
 };
 struct EmaBatch {
     int count;
@@ -930,7 +945,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                 }
                 h.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
                 h.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-                *reinterpret_cast<uint2 *>(M16 + o) = h;
+                *reinterpret_cast<uint2 *>(M16 + (static_cast<int64_t>(gi >> 6) * J.ntc + (gk >> 6)) * 4096 +
+                                           (gi & 63) * 64 + (gk & 63)) = h;
             }
             *reinterpret_cast<uint2 *>(base + row * 128 + 16 * ((f >> 1) ^ swz(row & 63)) + 8 * (f & 1)) = h;
         }
@@ -1038,9 +1054,13 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
     const int NP = reqs[0].NP;
     if (NP < 16 || NP % 16 != 0 || NP > SC_KMAX)
         return set_error(ACSC_EINVAL, "pass with %d thin-factor columns (a multiple of 16 up to %d)", NP, SC_KMAX);
-    for (const auto &q : reqs)
+    for (const auto &q : reqs) {
         if (q.NP != NP)
             return set_error(ACSC_EINVAL, "pass: thin factors of one launch must have the same width");
+        if (q.ntc > 0 && (!q.avec || q.ntc != tiles_per_row(trans ? q.M : q.K)))
+            return set_error(ACSC_EINVAL, "pass: a tiled operand must be aligned and have ceil(columns / 64) tiles "
+                                          "per tile row");
+    }
     // Split K only as far as needed for one workgroup per CU over the batch.
     int64_t blocks = 0;
     for (const auto &q : reqs)
@@ -1098,7 +1118,7 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
         b.njobs = static_cast<int>(cnt);
         for (size_t i = 0; i < cnt; ++i) {
             const Req &q = *vq[c0 + i];
-            b.j[i] = DJob{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, q.part, static_cast<int64_t>(q.M) * NP, q.M, q.K};
+            b.j[i] = DJob{q.A, q.lda, q.Bt, q.ldbt, q.C, q.ldc, q.part, static_cast<int64_t>(q.M) * NP, q.M, q.K, q.ntc};
             js.push_back(JobShape{static_cast<int>(cdiv(q.M, kBM)), vsplits[c0 + i], vchunk[c0 + i], q.K,
                                   q.part != nullptr && max_splits(q.M, q.K) >= 2 && q.K >= 2 * kBK});
         }
@@ -1182,7 +1202,8 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
         const int nb = static_cast<int>(cdiv(q.m, kBM)) * splits;
         const int64_t ss = static_cast<int64_t>(q.m) * NP;
         jobs.push_back(EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, nb, q.part, ss,
-                              static_cast<int>(splits > 1 ? chunk : q.n), splits});
+                              static_cast<int>(splits > 1 ? chunk : q.n), splits,
+                              static_cast<int>(tiles_per_row(q.n))});
         if (splits > 1) {
             red.push_back(RedJob{q.part, ss, q.C, q.ldc, q.m, NP, splits});
             rtot = std::max<int64_t>(rtot, static_cast<int64_t>(q.m) * (NP / 4));

@@ -225,15 +225,21 @@ __global__ __launch_bounds__(256) void gemm_tall_kernel(const Batch<GemmJob<TA, 
 // Anchor EMA with a bf16 shadow for the streaming passes (one thread per 8
 // consecutive elements of a row; 16-byte accesses when rows are aligned):
 //   M <- beta * M + (1 - beta) * G;  M16 <- bf16(M).   With G == NULL only the
-// shadow is written.
+// shadow is written.  The shadow is stored in 64 x 64 tiles (ntc tiles per
+// tile row; see sc_pass.h).
 template <typename GT>
 struct EmaJob {
     float *M;
     const GT *G;
     int m, n, vec;
     uint16_t *M16;
-    int64_t ld16;
+    int64_t ntc;
 };
+
+__device__ __forceinline__ int64_t tile_at(int64_t i, int64_t j, int64_t ntc)
+{
+    return ((i >> 6) * ntc + (j >> 6)) * 4096 + (i & 63) * 64 + (j & 63);
+}
 
 template <typename GT>
 __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>> jb, float beta, float omb)
@@ -244,7 +250,7 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
     const int m = J.m, n = J.n;
     const bool VEC = J.vec != 0;
     uint16_t *M16 = J.M16;
-    const int64_t ld16 = J.ld16;
+    const int64_t ntc = J.ntc;
     const int nch = (n + 7) / 8;
     const int64_t total = static_cast<int64_t>(m) * nch;
     for (int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; q < total;
@@ -285,7 +291,7 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 h[e] = f32_to_bf16(v[e]);
-            *reinterpret_cast<uint4 *>(M16 + i * ld16 + j0) = *reinterpret_cast<const uint4 *>(h);
+            *reinterpret_cast<uint4 *>(M16 + tile_at(i, j0, ntc)) = *reinterpret_cast<const uint4 *>(h);
         } else {
             for (int e = 0; e < 8 && j0 + e < n; ++e) {
                 float x = mr[e];
@@ -293,7 +299,7 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
                     x = beta * x + omb * to_f32<GT>(gr[e]);
                     mr[e] = x;
                 }
-                M16[i * ld16 + j0 + e] = f32_to_bf16(x);
+                M16[tile_at(i, j0 + e, ntc)] = f32_to_bf16(x);
             }
         }
     }
@@ -1509,8 +1515,8 @@ struct PriorWs {
     int *info;   // status words (kInfo*): Jacobi sweeps, residual, tolerance, status, phase stamp
     float *Y, *Z, *part, *T, *Bu, *Bv;
     double *gpart, *gram;
-    uint16_t *M16, *Yt16, *Zt16;   // bf16 path: shadow of M, transposed thin factors
-    int64_t ld16, ldy16, ldz16;
+    uint16_t *M16, *Yt16, *Zt16;   // bf16 path: shadow of M (64 x 64 tiles), transposed thin factors
+    int64_t ntc16, ldy16, ldz16;
 };
 
 size_t carve_prior(const Dims &d, bool use16, void *base, PriorWs *w)
@@ -1525,10 +1531,10 @@ size_t carve_prior(const Dims &d, bool use16, void *base, PriorWs *w)
     const int64_t part = std::max<int64_t>(s1 * d.m, s2 * d.n) * d.KP;
     PriorWs t;
     t.info = c.take<int>(64);
-    t.ld16 = round_up(d.n, 8);
+    t.ntc16 = pass::tiles_per_row(d.n);
     t.ldy16 = round_up(d.m, 8);
     t.ldz16 = round_up(d.n, 8);
-    t.M16 = use16 ? c.take<uint16_t>(static_cast<size_t>(d.m) * t.ld16) : nullptr;
+    t.M16 = use16 ? c.take<uint16_t>(static_cast<size_t>(pass::tiled_elems(d.m, d.n))) : nullptr;
     t.Yt16 = use16 ? c.take<uint16_t>(static_cast<size_t>(d.KP) * t.ldy16) : nullptr;
     t.Zt16 = use16 ? c.take<uint16_t>(static_cast<size_t>(d.KP) * t.ldz16) : nullptr;
     t.Y = c.take<float>(static_cast<size_t>(d.m) * d.KP);
@@ -1819,7 +1825,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
             int64_t tot = 1;
             for (auto &m : ms) {
                 j.push_back(EmaJob<uint16_t>{m.in->M, static_cast<const uint16_t *>(m.in->G), m.D.m, m.D.n,
-                                             (m.D.n % 8) == 0 ? 1 : 0, m.pw.M16, m.pw.ld16});
+                                             (m.D.n % 8) == 0 ? 1 : 0, m.pw.M16, m.pw.ntc16});
                 tot = std::max<int64_t>(tot, static_cast<int64_t>(m.D.m) * cdiv(m.D.n, 8));
             }
             launch_jobs("sc_ema", ema_shadow_kernel<uint16_t>, j, dim3(grid1d(tot)), dim3(256), 0, st, beta, omb);
@@ -1865,11 +1871,11 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
             std::vector<pass::Req> q;
             for (auto &m : ms) {
                 if (mz)
-                    q.push_back(pass::Req{m.pw.M16, m.pw.ld16, true, m.pw.Zt16, m.pw.ldz16, m.pw.Y, KP, m.D.m, m.D.n,
-                                        KP, m.pw.part});
+                    q.push_back(pass::Req{m.pw.M16, 0, true, m.pw.Zt16, m.pw.ldz16, m.pw.Y, KP, m.D.m, m.D.n,
+                                        KP, m.pw.part, static_cast<int>(m.pw.ntc16)});
                 else
-                    q.push_back(pass::Req{m.pw.M16, m.pw.ld16, true, m.pw.Yt16, m.pw.ldy16, m.pw.Z, KP, m.D.n, m.D.m,
-                                        KP, m.pw.part});
+                    q.push_back(pass::Req{m.pw.M16, 0, true, m.pw.Yt16, m.pw.ldy16, m.pw.Z, KP, m.D.n, m.D.m,
+                                        KP, m.pw.part, static_cast<int>(m.pw.ntc16)});
             }
             return mz ? pass::run("sc_pass_mz", false, q, st) : pass::run("sc_pass_mtq", true, q, st);
         } else {
@@ -2260,10 +2266,10 @@ int psgd_project_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStream_t
             int64_t tot = 1;
             for (auto &x : it) {
                 j.push_back(EmaJob<uint16_t>{x.in->E, static_cast<const uint16_t *>(x.in->G), x.in->m, x.in->n,
-                                             (x.in->n % 8) == 0 ? 1 : 0, x.w.pw.M16, x.w.pw.ld16});
+                                             (x.in->n % 8) == 0 ? 1 : 0, x.w.pw.M16, x.w.pw.ntc16});
                 tot = std::max<int64_t>(tot, static_cast<int64_t>(x.in->m) * cdiv(x.in->n, 8));
-                q.push_back(pass::Req{x.w.pw.M16, x.w.pw.ld16, true, x.w.pw.Zt16, x.w.pw.ldz16, x.w.pw.Y, KP,
-                                      x.in->m, x.in->n, KP, x.w.pw.part});
+                q.push_back(pass::Req{x.w.pw.M16, 0, true, x.w.pw.Zt16, x.w.pw.ldz16, x.w.pw.Y, KP,
+                                      x.in->m, x.in->n, KP, x.w.pw.part, static_cast<int>(x.w.pw.ntc16)});
             }
             launch_jobs("psgd_feedback", ema_shadow_kernel<uint16_t>, j, dim3(grid1d(tot)), dim3(256), 0, st, 1.0f,
                         1.0f);
@@ -2320,8 +2326,8 @@ int psgd_orthogonalize_phase(std::vector<PsgdItem> &it, bool use16, int r, hipSt
     if (use16) {
         std::vector<pass::Req> q;
         for (auto &x : it)
-            q.push_back(pass::Req{x.w.pw.M16, x.w.pw.ld16, true, x.w.pw.Yt16, x.w.pw.ldy16, x.w.pw.Z, KP, x.in->n,
-                                  x.in->m, KP, x.w.pw.part});
+            q.push_back(pass::Req{x.w.pw.M16, 0, true, x.w.pw.Yt16, x.w.pw.ldy16, x.w.pw.Z, KP, x.in->n,
+                                  x.in->m, KP, x.w.pw.part, static_cast<int>(x.w.pw.ntc16)});
         if (int rc = pass::run("psgd_pass_mtp", true, q, st))
             return rc;
     } else {

@@ -7,6 +7,12 @@
 // with B given transposed in bf16 (Bt[c][k], row stride ldbt, a multiple of 8).
 // These are the power passes Y = M Z and Z = M^T Y of the anchor SVD and the
 // product T = G V of the correction (Sec. 3.2).
+//
+// The bf16 shadow of the EMA is kept in 64 x 64 tiles: element (i, j) of an
+// [R x C] shadow sits at ((i / 64) * ntc + j / 64) * 4096 + (i % 64) * 64 + j % 64,
+// ntc = ceil(C / 64), in a buffer of tiled_elems(R, C) elements.  A pass step
+// then reads whole 8 KiB tiles (one per 64 rows of opA = A, four side by side
+// for opA = A^T) instead of 128-byte pieces of 256 rows.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -27,7 +33,12 @@ struct Req {
     int64_t ldc;
     int M, K, NP;       // NP = columns of the thin factor, a multiple of 16
     float *part;        // split-K partials, >= max_splits(M, K) * M * NP floats
+    int ntc;            // 0: A row-major with stride lda; > 0: A is a tiled shadow with ntc tiles per
+                        // tile row (lda unused; requires avec)
 };
+
+inline int64_t tiles_per_row(int64_t C) { return (C + 63) / 64; }
+inline int64_t tiled_elems(int64_t R, int64_t C) { return tiles_per_row(R) * tiles_per_row(C) * 4096; }
 
 // Largest number of K splits a pass over an [M x K] operand may use; the
 // caller sizes `part` for it.
@@ -44,7 +55,7 @@ int run(const char *tag, bool trans, const std::vector<Req> &reqs, hipStream_t s
 struct EmaReq {
     float *M;             // [m, n] fp32, row stride n
     const uint16_t *G;    // [m, n] bf16, or nullptr
-    uint16_t *M16;        // [m, n] bf16, row stride n
+    uint16_t *M16;        // [m, n] bf16 in 64 x 64 tiles (tiled_elems(m, n) elements)
     const uint16_t *Bt;   // thin factor transposed [NP, ldbt] bf16
     int64_t ldbt;
     float *C;             // [m, NP] fp32, row stride ldc
