@@ -72,6 +72,16 @@ inline int allow_lds(F kernel, size_t bytes)
 
 inline size_t dtype_size(acsc_dtype dt) { return dt == ACSC_BF16 ? 2 : 4; }
 
+// One step of the anchor EMA, M <- beta M + (1 - beta) G (Sec. 3.2), with the
+// contraction written out: every kernel that forms it rounds the same way
+// (the product (1 - beta) G, then one fused multiply-add), so the fused and
+// the separate EMA kernels agree bit for bit whatever the compiler would
+// otherwise contract.
+__device__ __forceinline__ float ema_step(float m, float g, float beta, float omb)
+{
+    return __builtin_fmaf(beta, m, omb * g);
+}
+
 // bf16 <-> fp32 on bit patterns.
 __device__ __forceinline__ float bf16_to_f32(uint16_t h)
 {

@@ -937,10 +937,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             if (gi < m && gk < kend) {
                 const int64_t o = static_cast<int64_t>(gi) * n + gk;
                 if (G) {
-                    v[0] = beta * v[0] + omb * __uint_as_float(rg[u].x << 16);
-                    v[1] = beta * v[1] + omb * __uint_as_float(rg[u].x & 0xFFFF0000u);
-                    v[2] = beta * v[2] + omb * __uint_as_float(rg[u].y << 16);
-                    v[3] = beta * v[3] + omb * __uint_as_float(rg[u].y & 0xFFFF0000u);
+                    v[0] = ema_step(v[0], __uint_as_float(rg[u].x << 16), beta, omb);
+                    v[1] = ema_step(v[1], __uint_as_float(rg[u].x & 0xFFFF0000u), beta, omb);
+                    v[2] = ema_step(v[2], __uint_as_float(rg[u].y << 16), beta, omb);
+                    v[3] = ema_step(v[3], __uint_as_float(rg[u].y & 0xFFFF0000u), beta, omb);
                     __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4 *>(M + o));
                 }
                 h.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);

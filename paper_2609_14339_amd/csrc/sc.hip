@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
                 }
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    v[e] = beta * v[e] + omb * g[e];
+                    v[e] = ema_step(v[e], g[e], beta, omb);
                 __builtin_nontemporal_store(nf4{v[0], v[1], v[2], v[3]}, reinterpret_cast<nf4 *>(mr));
                 __builtin_nontemporal_store(nf4{v[4], v[5], v[6], v[7]}, reinterpret_cast<nf4 *>(mr + 4));
             }
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(256) void ema_shadow_kernel(const Batch<EmaJob<GT>>
             for (int e = 0; e < 8 && j0 + e < n; ++e) {
                 float x = mr[e];
                 if (gr) {
-                    x = beta * x + omb * to_f32<GT>(gr[e]);
+                    x = ema_step(x, to_f32<GT>(gr[e]), beta, omb);
                     mr[e] = x;
                 }
                 M16[tile_at(i, j0 + e, ntc)] = f32_to_bf16(x);
@@ -871,14 +871,14 @@ __global__ __launch_bounds__(256) void ema_kernel(const Batch<Ema32Job<GT>> jb, 
                 g2 = gv.z;
                 g3 = gv.w;
             }
-            m.x = beta * m.x + omb * g0;
-            m.y = beta * m.y + omb * g1;
-            m.z = beta * m.z + omb * g2;
-            m.w = beta * m.w + omb * g3;
+            m.x = ema_step(m.x, g0, beta, omb);
+            m.y = ema_step(m.y, g1, beta, omb);
+            m.z = ema_step(m.z, g2, beta, omb);
+            m.w = ema_step(m.w, g3, beta, omb);
             *reinterpret_cast<float4 *>(M + i) = m;
         } else {
             for (int64_t j = i; j < count; ++j)
-                M[j] = beta * M[j] + omb * to_f32<GT>(G[j]);
+                M[j] = ema_step(M[j], to_f32<GT>(G[j]), beta, omb);
         }
     }
 }
