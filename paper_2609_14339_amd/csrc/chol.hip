@@ -67,6 +67,19 @@ __device__ __forceinline__ double row_bcast(double v)
     return __hiloint2double(hi, lo);
 }
 
+// 1 / sqrt(d) for d > 0 from the hardware estimate and two Newton steps
+// (y <- y + y (1 - d y^2) / 2; each step about doubles the correct bits), so
+// that a pivot costs a few dependent multiply-adds rather than a correctly
+// rounded square root and division; within an ulp or two of 1.0 / sqrt(d).
+__device__ __forceinline__ double rsqrt_refined(double d)
+{
+    double y = __builtin_amdgcn_rsq(d);
+    const double hd = 0.5 * d;
+    y = fma(y, fma(-hd * y, y, 0.5), y);
+    y = fma(y, fma(-hd * y, y, 0.5), y);
+    return y;
+}
+
 // One elimination step on the diagonal block.  Lane (i, h) = (lane % 16,
 // lane / 16) holds A[i][4h .. 4h+3] in a[] and X[i][4h .. 4h+3] in x[].
 // Rows below the pivot lose their multiple f_i = A[i][J] / d_J of pivot row
@@ -78,7 +91,7 @@ __device__ __forceinline__ void elim_step(double (&a)[4], double (&x)[4], double
 {
     constexpr int HJ = J >> 2, EJ = J & 3;
     const double d = readlane64(a[EJ], J + 16 * HJ);
-    const double rs = d > thresh ? 1.0 / sqrt(d) : 0.0;
+    const double rs = d > thresh ? rsqrt_refined(d) : 0.0;
     dsc[J] = rs;
     const double cij = bpermute64(a[EJ], i + 16 * HJ);
     const double f = i > J ? cij * (rs * rs) : 0.0;

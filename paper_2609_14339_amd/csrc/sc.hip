@@ -886,15 +886,22 @@ __global__ __launch_bounds__(256) void ema_kernel(const Batch<Ema32Job<GT>> jb, 
 // Starting block Z0 [n, KP]: V_warm columns first (if given), then uniform
 // random values in [-1, 1) from a counter-based hash of (seed, i, c); zero
 // beyond k.
-// Entry (i, c) of the seeded starting block: one SplitMix64 finalisation of
-// seed ^ (i * 0x100000001B3 + c), top 24 bits mapped to [-1, 1).
+// Entry (i, c) of the seeded starting block: the low 32 bits of the seed
+// added to a Weyl combination of row and column, then C. Wellons's lowbias32
+// integer hash (two 32-bit multiplies), the top 24 bits mapped to [-1, 1).
+// The subspace iteration only needs a seeded block of full rank with no
+// preferred direction; a 64-bit mixer here made the start block the most
+// expensive step of a cold build after the passes.
 __device__ __forceinline__ float start_uniform(uint64_t seed, int64_t i, int c)
 {
-    uint64_t z = seed ^ (static_cast<uint64_t>(i) * 0x100000001B3ull + c);
-    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-    z ^= z >> 31;
-    return static_cast<float>(z >> 40) * (2.0f / 16777216.0f) - 1.0f;
+    uint32_t h = static_cast<uint32_t>(i) * 0x9E3779B1u + static_cast<uint32_t>(c) * 0x632BE5ABu +
+                 static_cast<uint32_t>(seed) + static_cast<uint32_t>(seed >> 32) * 0x85EBCA6Bu;
+    h ^= h >> 16;
+    h *= 0x7FEB352Du;
+    h ^= h >> 15;
+    h *= 0x846CA68Bu;
+    h ^= h >> 16;
+    return static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f;
 }
 
 struct InitJob {
@@ -942,46 +949,56 @@ struct TileJob {
     const float *Vw;
     int rw;
     uint64_t seed;
+    int blk0;   // first workgroup of this job in the launch (set by launch_tiles)
 };
 
 constexpr int kTileRows = 64;
 
 __global__ __launch_bounds__(256) void tile_bf16_kernel(const Batch<TileJob> jb)
 {
-    const TileJob &J = jb.j[blockIdx.z];
-    const int row0 = blockIdx.x * kTileRows;
+    // one workgroup per 64-row tile of every job of the batch, jobs one after
+    // another along x
+    int ji = 0;
+    while (ji + 1 < jb.count && static_cast<int>(blockIdx.x) >= jb.j[ji + 1].blk0)
+        ++ji;
+    const TileJob &J = jb.j[ji];
+    const int row0 = (static_cast<int>(blockIdx.x) - J.blk0) * kTileRows;
     if (row0 >= J.rows)
         return;
-    __shared__ float Ts[kTileRows * (kKMax + 1)];
-    const int CP = J.CP, P = CP + 1;
-    for (int idx = threadIdx.x; idx < kTileRows * CP; idx += 256) {
-        const int r = idx / CP, c = idx - (idx / CP) * CP;
+    // The tile is staged already rounded to bf16 (both copies take bf16 of the
+    // same values): 25 KiB, six workgroups per CU.  Staged rows are 97 words
+    // apart, so the eight rows a transposed 16-byte store gathers sit in
+    // distinct banks.
+    constexpr int kPitch = kKMax + 2;
+    __shared__ __attribute__((aligned(16))) uint16_t Ts[kTileRows * kPitch];
+    const int CP = J.CP;
+    // wave w fills rows w, w + 4, ..., its lanes 64 consecutive columns
+    const int cl = threadIdx.x & 63, rg = threadIdx.x >> 6;
+    for (int r = rg; r < kTileRows; r += 4) {
         const int64_t i = row0 + r;
-        float v = 0.f;
-        if (i < J.rows && c < J.cols) {
-            if (J.X)
-                v = J.X[i * J.ldx + c];
-            else if (J.Vw && c < J.rw)
-                v = J.Vw[i * J.rw + c];
-            else
-                v = start_uniform(J.seed, i, c);
+        for (int c = cl; c < CP; c += 64) {
+            float v = 0.f;
+            if (i < J.rows && c < J.cols) {
+                if (J.X)
+                    v = J.X[i * J.ldx + c];
+                else if (J.Vw && c < J.rw)
+                    v = J.Vw[i * J.rw + c];
+                else
+                    v = start_uniform(J.seed, i, c);
+            }
+            Ts[r * kPitch + c] = f32_to_bf16(v);
         }
-        Ts[r * P + c] = v;
     }
     __syncthreads();
     if (J.Xc) {
-        const int c8n = CP / 8;
-        for (int idx = threadIdx.x; idx < kTileRows * c8n; idx += 256) {
-            const int r = idx / c8n, c8 = (idx - (idx / c8n) * c8n) * 8;
-            if (row0 + r >= J.rows)
-                continue;
-            uint32_t w[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                w[e] = static_cast<uint32_t>(f32_to_bf16(Ts[r * P + c8 + 2 * e])) |
-                       (static_cast<uint32_t>(f32_to_bf16(Ts[r * P + c8 + 2 * e + 1])) << 16);
-            *reinterpret_cast<uint4 *>(J.Xc + static_cast<int64_t>(row0 + r) * CP + c8) = make_uint4(w[0], w[1], w[2], w[3]);
-        }
+        // 32 lanes per row, lane q copies the 16-byte chunk q of the row (CP / 8 <= 24 chunks)
+        const int q = threadIdx.x & 31;
+        if (q < CP / 8)
+            for (int r = threadIdx.x >> 5; r < kTileRows && row0 + r < J.rows; r += 8) {
+                const uint32_t *src = reinterpret_cast<const uint32_t *>(&Ts[r * kPitch + 8 * q]);
+                *reinterpret_cast<uint4 *>(J.Xc + static_cast<int64_t>(row0 + r) * CP + 8 * q) =
+                    make_uint4(src[0], src[1], src[2], src[3]);
+            }
     }
     if (J.Xt) {
         for (int idx = threadIdx.x; idx < CP * (kTileRows / 8); idx += 256) {
@@ -991,8 +1008,8 @@ __global__ __launch_bounds__(256) void tile_bf16_kernel(const Batch<TileJob> jb)
             uint32_t w[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                w[e] = static_cast<uint32_t>(f32_to_bf16(Ts[(r8 + 2 * e) * P + c])) |
-                       (static_cast<uint32_t>(f32_to_bf16(Ts[(r8 + 2 * e + 1) * P + c])) << 16);
+                w[e] = static_cast<uint32_t>(Ts[(r8 + 2 * e) * kPitch + c]) |
+                       (static_cast<uint32_t>(Ts[(r8 + 2 * e + 1) * kPitch + c]) << 16);
             *reinterpret_cast<uint4 *>(J.Xt + static_cast<int64_t>(c) * J.ldt + row0 + r8) = make_uint4(w[0], w[1], w[2], w[3]);
         }
     }
@@ -1604,6 +1621,24 @@ void launch_jobs(const char *tag, K kernel, const std::vector<Job> &jobs, dim3 g
     }
 }
 
+// tile_bf16_kernel over a list of jobs: each launch takes up to kMaxBatch jobs
+// and exactly as many workgroups as they have 64-row tiles.
+void launch_tiles(const char *tag, std::vector<TileJob> jobs, hipStream_t st)
+{
+    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxBatch) {
+        Batch<TileJob> b{};
+        b.count = static_cast<int>(std::min<size_t>(kMaxBatch, jobs.size() - c0));
+        int blocks = 0;
+        for (int i = 0; i < b.count; ++i) {
+            b.j[i] = jobs[c0 + i];
+            b.j[i].blk0 = blocks;
+            blocks += static_cast<int>(cdiv(b.j[i].rows, kTileRows));
+        }
+        if (blocks > 0)
+            ACSC_LAUNCH(tag, tile_bf16_kernel, dim3(blocks), dim3(256), 0, st, b);
+    }
+}
+
 // The Jacobi kernel for order k, by rows per lane (k rounded up to 32, over 8).
 template <typename T>
 using JacobiFn = void (*)(const Batch<JacJob>, int, int, int, int, float, T, int);
@@ -1854,13 +1889,10 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
         if (use16) {
             // the bf16 passes read only the transposed copy of the starting block
             std::vector<TileJob> tj;
-            int gx = 1;
-            for (auto &m : ms) {
+            for (auto &m : ms)
                 tj.push_back(TileJob{nullptr, 0, m.D.n, k, KP, m.pw.Zt16, m.pw.ldz16, nullptr, m.in->V_warm,
                                      m.in->V_warm ? r : 0, m.seed});
-                gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, kTileRows)));
-            }
-            launch_jobs("sc_init", tile_bf16_kernel, tj, dim3(gx), dim3(256), 0, st);
+            launch_tiles("sc_init", tj, st);
         } else {
             launch_jobs("sc_init", init_block_kernel, j, dim3(grid1d(tot)), dim3(256), 0, st, k, KP, r);
         }
@@ -2008,16 +2040,14 @@ int correct_group(std::vector<Mat> &ms, int r, float alpha, hipStream_t st, cons
         // V to bf16 once: transposed for T = G V, row-major for the blend
         std::vector<TileJob> t;
         std::vector<pass::Req> q;
-        int gx = 1;
         for (auto &m : ms) {
             t.push_back(TileJob{m.in->V, r, m.D.n, r, RP, m.cw.Vt16, m.cw.ldv16, static_cast<uint16_t *>(m.cw.Vc),
                                 nullptr, 0, 0});
-            gx = std::max<int>(gx, static_cast<int>(cdiv(m.D.n, kTileRows)));
             const bool avec = aligned(m.in->G, 16) && (m.D.n % 8) == 0;
             q.push_back(pass::Req{static_cast<const uint16_t *>(m.in->G), m.D.n, avec, m.cw.Vt16, m.cw.ldv16, m.cw.Tm,
                                 RP, m.D.m, m.D.n, RP, m.cw.part});
         }
-        launch_jobs("sc_vconvert", tile_bf16_kernel, t, dim3(gx), dim3(256), 0, st);
+        launch_tiles("sc_vconvert", t, st);
         const int rc = pass::run("sc_gv", false, q, st);
         if (rc)
             return rc;
@@ -2247,12 +2277,9 @@ int psgd_project_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStream_t
     if (use16) {
         // Q^T in bf16, rows r .. KP-1 zero: the thin factor of the pass
         std::vector<TileJob> tj;
-        int gx = 1;
-        for (auto &x : it) {
+        for (auto &x : it)
             tj.push_back(TileJob{x.in->Q, r, x.in->n, r, KP, x.w.pw.Zt16, x.w.pw.ldz16, nullptr, nullptr, 0, 0});
-            gx = std::max<int>(gx, static_cast<int>(cdiv(x.in->n, kTileRows)));
-        }
-        launch_jobs("psgd_qconvert", tile_bf16_kernel, tj, dim3(gx), dim3(256), 0, st);
+        launch_tiles("psgd_qconvert", tj, st);
         std::vector<pass::EmaReq> er;
         for (auto &x : it)
             er.push_back(pass::EmaReq{x.in->E, static_cast<const uint16_t *>(x.in->G), x.w.pw.M16, x.w.pw.Zt16,
@@ -2350,18 +2377,16 @@ int psgd_decompress_phase(std::vector<PsgdItem> &it, bool use16, int r, hipStrea
     if (use16) {
         std::vector<TileJob> tj;
         std::vector<blend::Req> q;
-        int gx = 1;
         for (auto &x : it) {
             tj.push_back(TileJob{x.in->P, r, x.in->m, r, RPd, nullptr, 0, static_cast<uint16_t *>(x.w.Pc), nullptr, 0,
                                  0});
             tj.push_back(TileJob{x.in->Q, r, x.in->n, r, RPd, nullptr, 0, static_cast<uint16_t *>(x.w.Vc), nullptr, 0,
                                  0});
-            gx = std::max<int>(gx, static_cast<int>(cdiv(std::max(x.in->m, x.in->n), kTileRows)));
             q.push_back(blend::Req{nullptr, static_cast<uint16_t *>(x.in->out), x.in->m, x.in->n,
                                    static_cast<const uint16_t *>(x.w.Pc), static_cast<const uint16_t *>(x.w.Vc),
                                    nullptr, nullptr, nullptr, x.in->E});
         }
-        launch_jobs("psgd_fconvert", tile_bf16_kernel, tj, dim3(gx), dim3(256), 0, st);
+        launch_tiles("psgd_fconvert", tj, st);
         return blend::run_feedback("psgd_decompress", q, RPd, st);
     }
     std::vector<PadJob<float>> pj;

@@ -138,8 +138,11 @@ def test_ragged_bf16_build_ignores_workspace_padding(pk, m, n):
     multiples of 64 must still match the oracle (Sec. 3.2 EMA and SVD,
     App. E filter) to the bf16 bounds: no pass may multiply padding into a
     stored output."""
+    # singular values in [1, 10]: at these small shapes a [1, 100] range puts
+    # the noise edge above the smallest signal value and leaves the top-12
+    # subspace undetermined
     r, p, q = 12, 8, 3
-    spec = workloads.GradSpec(((m, n),), r, (1.0, 100.0), (r,), torch.bfloat16, None, None)
+    spec = workloads.GradSpec(((m, n),), r, (1.0, 10.0), (r,), torch.bfloat16, None, None)
     gp = workloads.grad_pair(spec, 9, 0, 0, "cpu")
     ws = pk.workspace(m, n, r, p, torch.bfloat16)
     ws.fill_(255)
