@@ -16,6 +16,7 @@
 #include "sc_orth.h"
 
 #include <algorithm>
+#include <utility>
 #include <vector>
 
 namespace acsc {
@@ -361,12 +362,16 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const Batch<ReduceJo
 // ---------------------------------------------------------------------------
 // fp64 Gram matrix of the first KP columns of A (rows x lda, fp32), on
 // v_mfma_f64_16x16x4_f64: one workgroup per block of rows computes every
-// upper 32 x 32 tile (ti <= tj) of that block's partial Gram; the partials
+// upper 16 x 16 tile (ti <= tj) of that block's partial Gram; the partials
 // are summed by gram_reduce_kernel, which also mirrors the lower triangle.
-// Operands (one fp64 per lane): A[i][k] in lane i + 16 k, B[k][j] in lane
-// j + 16 k; the result D[i][j] sits in lane j + 16 (i % 4), element i / 4.
+// The rows pass through LDS in 32-row chunks, converted to fp64 once and
+// double-buffered (one barrier per chunk).  Operands (one fp64 per lane):
+// A[i][k] in lane i + 16 k, B[k][j] in lane j + 16 k, so both come from the
+// same read of a chunk row group: lane l takes row k0 + l / 16, column
+// 16 b + l % 16, and every wave reads the KP / 16 column blocks once per
+// 4-row step.  The result D[i][j] sits in lane j + 16 (i % 4), element i / 4.
 // ---------------------------------------------------------------------------
-constexpr int kGT = 32;
+constexpr int kGT = 16;
 constexpr int kGRows = 32;
 typedef double v4d __attribute__((ext_vector_type(4)));
 
@@ -377,46 +382,59 @@ struct GramJob {
     double *part;
 };
 
-template <int NT>
-__global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> jb, int KP)
+// Staged row pitch in doubles: an odd multiple of 128 bytes, so that the two
+// rows of a 32-lane half of an operand read fall in different bank halves.
+__host__ __device__ constexpr int gram_pitch(int NB) { return NB * kGT + ((NB & 1) ? 0 : kGT); }
+
+// Upper tiles in row-major order: tile t of an NB x NB block grid.
+__host__ __device__ constexpr int gram_tile_row(int t, int NB)
 {
-    const GramJob &J = jb.j[blockIdx.z];
-    if (static_cast<int>(blockIdx.x) >= J.blocks)
-        return;
-    constexpr int NTILES = NT * (NT + 1) / 2;
-    constexpr int TPW = (NTILES + 3) / 4;          // tiles per wave
-    constexpr int PITCH = NT * kGT + 16;           // floats per staged row (rows 48 banks apart: conflict-free reads)
-    __shared__ __attribute__((aligned(16))) float Ys[kGRows * PITCH];
-    const float *A = J.A;
-    const int64_t lda = J.lda;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int r0 = blockIdx.x * J.rows_per_block;
-    const int r1 = min(J.rows, r0 + J.rows_per_block);
-    // this wave's tiles: t = wave + 4 u, upper tiles in row-major order
-    int tri_[TPW], trj_[TPW];
-#pragma unroll
-    for (int u = 0; u < TPW; ++u) {
-        int t = wave + 4 * u, ti = 0;
-        if (t >= NTILES)
-            t = 0;   // idle slot: recomputes tile 0, never stored
-        while (t >= NT - ti) {
-            t -= NT - ti;
-            ++ti;
-        }
-        tri_[u] = ti;
-        trj_[u] = ti + t;
+    int ti = 0;
+    while (t >= NB - ti) {
+        t -= NB - ti;
+        ++ti;
     }
-    v4d acc[TPW][2][2];
+    return ti;
+}
+__host__ __device__ constexpr int gram_tile_col(int t, int NB)
+{
+    int ti = 0;
+    while (t >= NB - ti) {
+        t -= NB - ti;
+        ++ti;
+    }
+    return ti + t;
+}
+
+// One 4-row step of wave W's tiles: tile T = W + 4 U takes block rows
+// ti(T) and tj(T) of the step's operands (indices fixed at compile time).
+template <int NB, int T>
+__device__ __forceinline__ v4d gram_mfma(const double (&op)[NB], v4d acc)
+{
+    constexpr int ti = gram_tile_row(T, NB), tj = gram_tile_col(T, NB);
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(op[ti], op[tj], acc, 0, 0, 0);
+}
+template <int NB, int W, int... U>
+__device__ __forceinline__ void gram_mfmas(v4d *acc, const double (&op)[NB], std::integer_sequence<int, U...>)
+{
+    ((acc[U] = gram_mfma<NB, W + 4 * U>(op, acc[U])), ...);
+}
+
+// Wave W's share of the upper tiles: t = W, W + 4, ...  (compile-time, so
+// that the operand registers are indexed by constants).
+template <int NB, int W>
+__device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, int nchunks,
+                                          const float *A, int64_t lda, int r0, int r1, int KP, double *pb, int tid)
+{
+    constexpr int NTILES = NB * (NB + 1) / 2;
+    constexpr int TPW = NTILES > W ? (NTILES - W + 3) / 4 : 0;
+    constexpr int PITCH = gram_pitch(NB);          // doubles per staged row
+    constexpr int q4 = NB * kGT / 4;               // float4 per staged row
+    constexpr int PF = (kGRows * q4 + 255) / 256;  // float4 per thread and chunk
+    v4d acc[TPW > 0 ? TPW : 1];
 #pragma unroll
     for (int u = 0; u < TPW; ++u)
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-                acc[u][a][c] = v4d{0.0, 0.0, 0.0, 0.0};
-    constexpr int q4 = NT * kGT / 4;               // float4 per staged row
-    constexpr int PF = (kGRows * q4 + 255) / 256;  // float4 per thread and chunk
-    // the next chunk is loaded into registers while this one is multiplied
+        acc[u] = v4d{0.0, 0.0, 0.0, 0.0};
     float4 pf[PF];
     auto load = [&](int rb) {
 #pragma unroll
@@ -431,63 +449,75 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> 
         }
     };
     load(r0);
-    for (int rb = r0; rb < r1; rb += kGRows) {
-        __syncthreads();
+    for (int c = 0; c < nchunks; ++c) {
+        double *Ys = (c & 1) ? Ys1 : Ys0;
+        // stage this chunk (loaded during the previous one) as fp64; the
+        // buffer was last read two chunks ago, before the previous barrier
 #pragma unroll
         for (int u = 0; u < PF; ++u) {
             const int idx = tid + 256 * u;
-            if (idx < kGRows * q4)
-                *reinterpret_cast<float4 *>(&Ys[(idx / q4) * PITCH + (idx % q4) * 4]) = pf[u];
+            if (idx < kGRows * q4) {
+                double *d = Ys + (idx / q4) * PITCH + (idx % q4) * 4;
+                *reinterpret_cast<double2 *>(d) = make_double2(pf[u].x, pf[u].y);
+                *reinterpret_cast<double2 *>(d + 2) = make_double2(pf[u].z, pf[u].w);
+            }
         }
         __syncthreads();
-        if (rb + kGRows < r1)
-            load(rb + kGRows);
-        // the next k-step's operands are read from LDS before this step's
-        // products are issued, so their latency hides under the MFMAs
-        float op[2][TPW][4];
-        auto read_ops = [&](int k0, float (&o)[TPW][4]) {
-            const float *yr = &Ys[(k0 + (lane >> 4)) * PITCH + (lane & 15)];
+        if (c + 1 < nchunks)
+            load(r0 + (c + 1) * kGRows);
+        if constexpr (TPW > 0) {
+            // the next step's operands are read before this step's products
+            // are issued, so their latency hides under the MFMAs
+            const double *yr = Ys + (lane >> 4) * PITCH + (lane & 15);
+            double opA[NB], opB[NB];
+            auto read = [&](double (&o)[NB], int k0) {
 #pragma unroll
-            for (int u = 0; u < TPW; ++u) {
-                o[u][0] = yr[tri_[u] * kGT];
-                o[u][1] = yr[tri_[u] * kGT + 16];
-                o[u][2] = yr[trj_[u] * kGT];
-                o[u][3] = yr[trj_[u] * kGT + 16];
-            }
-        };
-        read_ops(0, op[0]);
+                for (int b = 0; b < NB; ++b)
+                    o[b] = yr[k0 * PITCH + b * kGT];
+            };
+            read(opA, 0);
 #pragma unroll
-        for (int k0 = 0; k0 < kGRows; k0 += 4) {
-            const int cur = (k0 >> 2) & 1;
-            if (k0 + 4 < kGRows)
-                read_ops(k0 + 4, op[cur ^ 1]);
-#pragma unroll
-            for (int u = 0; u < TPW; ++u) {
-                const double a0 = op[cur][u][0], a1 = op[cur][u][1];
-                const double b0 = op[cur][u][2], b1 = op[cur][u][3];
-                acc[u][0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[u][0][0], 0, 0, 0);
-                acc[u][0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[u][0][1], 0, 0, 0);
-                acc[u][1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[u][1][0], 0, 0, 0);
-                acc[u][1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[u][1][1], 0, 0, 0);
+            for (int k0 = 0; k0 < kGRows; k0 += 8) {
+                read(opB, k0 + 4);
+                gram_mfmas<NB, W>(acc, opA, std::make_integer_sequence<int, TPW>{});
+                if (k0 + 8 < kGRows)
+                    read(opA, k0 + 8);
+                gram_mfmas<NB, W>(acc, opB, std::make_integer_sequence<int, TPW>{});
             }
         }
     }
-    double *pb = J.part + static_cast<int64_t>(blockIdx.x) * KP * KP;
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
-        if (wave + 4 * u >= NTILES)
-            continue;
+        const int t = W + 4 * u;
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int i = tri_[u] * kGT + a * 16 + (lane >> 4) + 4 * e;
-                    const int j = trj_[u] * kGT + c * 16 + (lane & 15);
-                    if (i < KP && j < KP)
-                        pb[static_cast<int64_t>(i) * KP + j] = acc[u][a][c][e];
-                }
+        for (int e = 0; e < 4; ++e) {
+            const int i = gram_tile_row(t, NB) * kGT + (lane >> 4) + 4 * e;
+            const int j = gram_tile_col(t, NB) * kGT + (lane & 15);
+            if (i < KP && j < KP)
+                pb[static_cast<int64_t>(i) * KP + j] = acc[u][e];
+        }
+    }
+}
+
+template <int NB>
+__global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> jb, int KP)
+{
+    const GramJob &J = jb.j[blockIdx.z];
+    if (static_cast<int>(blockIdx.x) >= J.blocks)
+        return;
+    constexpr int PITCH = gram_pitch(NB);
+    __shared__ __attribute__((aligned(16))) double Ys[2][kGRows * PITCH];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r0 = blockIdx.x * J.rows_per_block;
+    const int r1 = min(J.rows, r0 + J.rows_per_block);
+    const int nchunks = (r1 - r0 + kGRows - 1) / kGRows;
+    double *pb = J.part + static_cast<int64_t>(blockIdx.x) * KP * KP;
+    switch (wave) {
+    case 0: gram_wave<NB, 0>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    case 1: gram_wave<NB, 1>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    case 2: gram_wave<NB, 2>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    default: gram_wave<NB, 3>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
     }
 }
 
@@ -1790,7 +1820,13 @@ void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const
     case 3: launch_jobs("sc_gram", gram_partial_kernel<3>, gj, dim3(gy), dim3(256), 0, st, KP); break;
     case 4: launch_jobs("sc_gram", gram_partial_kernel<4>, gj, dim3(gy), dim3(256), 0, st, KP); break;
     case 5: launch_jobs("sc_gram", gram_partial_kernel<5>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    default: launch_jobs("sc_gram", gram_partial_kernel<6>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 6: launch_jobs("sc_gram", gram_partial_kernel<6>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 7: launch_jobs("sc_gram", gram_partial_kernel<7>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 8: launch_jobs("sc_gram", gram_partial_kernel<8>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 9: launch_jobs("sc_gram", gram_partial_kernel<9>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 10: launch_jobs("sc_gram", gram_partial_kernel<10>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 11: launch_jobs("sc_gram", gram_partial_kernel<11>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    default: launch_jobs("sc_gram", gram_partial_kernel<12>, gj, dim3(gy), dim3(256), 0, st, KP); break;
     }
     launch_jobs("sc_gram_reduce", gram_reduce_kernel, rj, dim3(static_cast<unsigned>(cdiv(int64_t(KP) * KP, 32))),
                 dim3(256), 0, st, KP);
