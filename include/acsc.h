@@ -56,8 +56,13 @@ int acsc_version(void);
  * the name (NUL-terminated, truncated to name_len), launch count and summed
  * milliseconds of the index-th kernel name (alphabetical); ACSC_EINVAL past
  * the last one.  Timing serialises nothing but adds two event records per
- * launch. */
+ * launch.  acsc_stats_only(tag) restricts timing to the launches of that
+ * kernel name (copied; NULL or "" times every launch again), so that one
+ * kernel can be timed inside a loop without the records of all the others;
+ * it keeps the counters.  Returns ACSC_EINVAL for a name of 64 or more
+ * characters. */
 int acsc_stats_enable(int on);
+int acsc_stats_only(const char *tag);
 int acsc_stats_read(int index, char *name, size_t name_len, int64_t *launches, double *total_ms);
 
 /* ------------------------------------------------------------------------

@@ -120,6 +120,8 @@ def _load():
         fn.argtypes = [i32, C.POINTER(PsgdMatrix), i32, i32, vp]
     lib.acsc_stats_enable.restype = i32
     lib.acsc_stats_enable.argtypes = [i32]
+    lib.acsc_stats_only.restype = i32
+    lib.acsc_stats_only.argtypes = [C.c_char_p]
     lib.acsc_stats_read.restype = i32
     lib.acsc_stats_read.argtypes = [i32, C.c_char_p, sz, C.POINTER(i64), C.POINTER(C.c_double)]
     return lib
@@ -127,7 +129,7 @@ def _load():
 
 lib = _load()
 
-EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_read",
+EXPORTED = ("acsc_last_error", "acsc_version", "acsc_stats_enable", "acsc_stats_only", "acsc_stats_read",
             "ac_keep_count", "ac_mask_pack", "ac_unpack_scatter", "ac_mask_pack_batched",
             "ac_unpack_scatter_batched", "sc_workspace_size",
             "sc_build_prior", "sc_correct", "sc_correct_static", "sc_build_prior_batched", "sc_correct_batched",
@@ -179,6 +181,11 @@ def _out(*ts):
 def acsc_stats_enable(on: bool = True) -> None:
     """Start (resetting the counters) or stop per-kernel event timing."""
     _check(lib.acsc_stats_enable(1 if on else 0))
+
+
+def acsc_stats_only(tag=None) -> None:
+    """Time only the launches of kernel name `tag` (None: every launch)."""
+    _check(lib.acsc_stats_only(tag.encode() if tag else None))
 
 
 def acsc_stats_read() -> dict:

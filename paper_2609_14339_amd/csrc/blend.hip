@@ -294,8 +294,8 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
             float gp[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                gp[2 * e] = cf * (alpha * __uint_as_float(w[e] << 16) + oma * pf[2 * e]);
-                gp[2 * e + 1] = cf * (alpha * __uint_as_float(w[e] & 0xFFFF0000u) + oma * pf[2 * e + 1]);
+                gp[2 * e] = cf * blend_step(__uint_as_float(w[e] << 16), pf[2 * e], alpha, oma);
+                gp[2 * e + 1] = cf * blend_step(__uint_as_float(w[e] & 0xFFFF0000u), pf[2 * e + 1], alpha, oma);
             }
             const int64_t o = static_cast<int64_t>(gi) * n + gj;
             if (VEC && gj + 8 <= n) {
@@ -349,8 +349,8 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         uint32_t o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float lo = alpha * __uint_as_float(w[e] << 16) + oma * pf[2 * e];
-            const float hi = alpha * __uint_as_float(w[e] & 0xFFFF0000u) + oma * pf[2 * e + 1];
+            const float lo = blend_step(__uint_as_float(w[e] << 16), pf[2 * e], alpha, oma);
+            const float hi = blend_step(__uint_as_float(w[e] & 0xFFFF0000u), pf[2 * e + 1], alpha, oma);
             o[e] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
         }
         uint16_t *dst = J.out + static_cast<int64_t>(gi) * n + gj;

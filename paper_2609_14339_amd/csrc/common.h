@@ -82,6 +82,14 @@ __device__ __forceinline__ float ema_step(float m, float g, float beta, float om
     return __builtin_fmaf(beta, m, omb * g);
 }
 
+// One element of the blend G_proj = alpha G + (1 - alpha) P V^T (Sec. 3.2),
+// p = (P V^T)[i, j] in fp32, oma = 1 - alpha: one product and one fused
+// multiply-add in a fixed order, so that every blend kernel rounds alike.
+__device__ __forceinline__ float blend_step(float g, float p, float alpha, float oma)
+{
+    return __builtin_fmaf(alpha, g, oma * p);
+}
+
 // bf16 <-> fp32 on bit patterns.
 __device__ __forceinline__ float bf16_to_f32(uint16_t h)
 {

@@ -24,6 +24,7 @@ struct Totals {
 };
 std::mutex g_mu;
 bool g_on = false;
+std::string g_only;   // time only the launches of this kernel name (empty: all)
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
 std::map<std::string, Totals> g_totals;
@@ -76,7 +77,7 @@ bool stats_on() { return g_on; }
 void *stats_begin(hipStream_t st, const char *tag)
 {
     std::lock_guard<std::mutex> lk(g_mu);
-    if (!g_on)
+    if (!g_on || (!g_only.empty() && g_only != tag))
         return nullptr;
     if (g_pending.size() >= 8192)
         drain_locked();
@@ -113,6 +114,17 @@ extern "C" int acsc_stats_enable(int on)
     acsc::g_on = on != 0;
     if (rc)
         return acsc::set_error(rc, "an event of a timed launch failed");
+    return ACSC_OK;
+}
+
+extern "C" int acsc_stats_only(const char *tag)
+{
+    acsc::clear_error();
+    const size_t len = tag ? std::strlen(tag) : 0;
+    if (len >= 64)
+        return acsc::set_error(ACSC_EINVAL, "kernel name of %zu characters", len);
+    std::lock_guard<std::mutex> lk(acsc::g_mu);
+    acsc::g_only.assign(tag ? tag : "");
     return ACSC_OK;
 }
 

@@ -1331,7 +1331,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch<BlendJob<GT>> jb
                         J.E[o] = J.E[o] - to_f32<GT>(ov);
                     } else {
                         const float g = to_f32<GT>(G[o]);
-                        blend_out<ADAM>(J, o, alpha * g + oma * acc[a][b][e], cf, ad);
+                        blend_out<ADAM>(J, o, blend_step(g, acc[a][b][e], alpha, oma), cf, ad);
                     }
                 }
             }
@@ -1474,7 +1474,7 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
                     const int gi = row0 + rr, gj = col0 + cc;
                     if (gi < m && gj < n)
                         blend_out<true>(J, static_cast<int64_t>(gi) * n + gj,
-                                        alpha * bf16_to_f32(Gs[rr * kGPitch + cc]) + oma * acc[a][c][e], cf, ad);
+                                        blend_step(bf16_to_f32(Gs[rr * kGPitch + cc]), acc[a][c][e], alpha, oma), cf, ad);
                 }
             }
         return;
@@ -1488,7 +1488,7 @@ __global__ __launch_bounds__(256) void blend16_kernel(const Batch<BlendJob<uint1
             for (int e = 0; e < 4; ++e) {
                 const int rr = wr * 64 + a * 16 + (lane >> 4) * 4 + e;
                 uint16_t &gv = Gs[rr * kGPitch + cc];
-                gv = f32_to_bf16(alpha * bf16_to_f32(gv) + oma * acc[a][c][e]);
+                gv = f32_to_bf16(blend_step(bf16_to_f32(gv), acc[a][c][e], alpha, oma));
             }
         }
     __syncthreads();

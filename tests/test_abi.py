@@ -181,3 +181,12 @@ def test_static_correction_rejects_bad_arguments_before_launch(lib):
     # beyond the static scratch: refused on the host with ACSC_ENOSPC
     assert lib.sc_correct_static(f, 1, 65536, 8192, f, f, f, 128, 0.3, f, None) == -5
     assert "scratch" in _err(lib)
+
+
+def test_stats_filter_takes_a_name_or_null_on_host(lib):
+    # no launch happens: the filter is host state only
+    lib.acsc_stats_only.argtypes = [C.c_char_p]
+    assert lib.acsc_stats_only(b"sc_ema") == 0
+    assert lib.acsc_stats_only(b"x" * 64) == -1 and "64" in _err(lib)
+    assert lib.acsc_stats_only(None) == 0
+    assert lib.acsc_stats_only(b"") == 0
