@@ -219,7 +219,8 @@ __device__ __forceinline__ void wave_sync()
 // unassigned index; the wave runs about 2 K / 64 steps for H about half the
 // Feistel domain.
 template <typename Perm>
-__device__ __forceinline__ void mark_kept(const Perm &perm, int K, uint32_t H, uint32_t *bm, int lane)
+__device__ __forceinline__ void mark_kept(const Perm &perm, int K, uint32_t H, uint32_t *bm, int lane,
+                                          uint16_t *order = nullptr)
 {
     int i = lane;
     bool live = i < K;
@@ -227,8 +228,11 @@ __device__ __forceinline__ void mark_kept(const Perm &perm, int K, uint32_t H, u
     int next = 64;
     while (__ballot(live)) {
         const bool done = live && y < H;
-        if (done)
+        if (done) {
             atomicOr(&bm[y >> 5], 1u << (y & 31));
+            if (order)
+                order[i] = static_cast<uint16_t>(y);   // pi(i), before sorting
+        }
         const unsigned long long fin = __ballot(done);
         const int before = __popcll(fin & ((1ull << lane) - 1ull));
         uint32_t src = y;
@@ -243,8 +247,10 @@ __device__ __forceinline__ void mark_kept(const Perm &perm, int K, uint32_t H, u
     }
 }
 
-// Per-wave LDS layout of the pack kernel: bitmap[nw] then uint16 kidx[K].
-__host__ __device__ __forceinline__ int pack_wave_words(int nw, int K) { return nw + (K + 1) / 2; }
+// Per-wave LDS layout of the pack kernel: bitmap[nw], uint16 order[K] (the
+// kept indices in the order they were drawn), uint16 prefix[nw] (kept
+// indices before each bitmap word).
+__host__ __device__ __forceinline__ int pack_wave_words(int nw, int K) { return nw + (K + 1) / 2 + (nw + 1) / 2; }
 
 // Per-wave LDS of the pack kernel in bytes: the words above, then (TABLE) the
 // row's round table.
@@ -308,7 +314,8 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
     const int nw = (H + 31) >> 5;
     uint32_t *bm = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(smem) +
                                                 wid * pack_wave_bytes<ROUNDS, TABLE>(nw, K));
-    uint16_t *kidx = reinterpret_cast<uint16_t *>(bm + nw);
+    uint16_t *order = reinterpret_cast<uint16_t *>(bm + nw);
+    uint16_t *wpre = order + 2 * ((K + 1) / 2);
     const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wid;
     const bool active = row < rows;
 
@@ -327,53 +334,53 @@ __global__ __launch_bounds__(256) void ac_pack_kernel(const E *__restrict__ x, i
         if (TABLE) {
             const TabPerm<ROUNDS> tp(perm, reinterpret_cast<uint8_t *>(bm + pack_wave_words(nw, K)), lane);
             wave_sync();
-            mark_kept(tp, K, static_cast<uint32_t>(H), bm, lane);
+            mark_kept(tp, K, static_cast<uint32_t>(H), bm, lane, order);
         } else {
             wave_sync();
-            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
+            mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane, order);
         }
     }
     wave_sync();
-    {
-        const int per = (nw + 63) >> 6;
-        const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
-        int cnt = 0;
-        for (int i = w0; i < w1; ++i)
-            cnt += __popc(bm[i]);
-        int pos = wave_exclusive_scan(cnt, lane);
-        for (int i = w0; i < w1; ++i) {
-            uint32_t b = bm[i];
-            while (b) {
-                const int t = __ffs(b) - 1;
-                b &= b - 1u;
-                kidx[pos++] = static_cast<uint16_t>((i << 5) + t);
-            }
+    // The kept values are gathered in the order they were drawn, right after
+    // the mask, and stored at their rank (the number of kept indices below
+    // them) once the bitmap's word prefixes are known: the gather's HBM
+    // latency overlaps the prefix scan instead of following the sorted list.
+    const E *xr = x + row * ld_x;
+    E *vr = vals + row * K;
+    uint16_t *ir = idx ? idx + row * K : nullptr;
+    bool scanned = false;
+    for (int base = 0; base < K; base += 256) {
+        E v[4];
+        uint16_t jj[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + lane + 64 * u;
+            jj[u] = i < K ? order[i] : uint16_t(0);
+            v[u] = i < K ? xr[jj[u]] : E(0);
         }
-    }
-    wave_sync();
-    {
-        // gather four kept values per lane before storing any, so that their
-        // HBM latencies overlap
-        const E *xr = x + row * ld_x;
-        E *vr = vals + row * K;
-        uint16_t *ir = idx ? idx + row * K : nullptr;
-        for (int base = 0; base < K; base += 256) {
-            E v[4];
-            uint16_t jj[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = base + lane + 64 * u;
-                jj[u] = i < K ? kidx[i] : uint16_t(0);
-                v[u] = i < K ? xr[jj[u]] : E(0);
+        if (!scanned) {
+            const int per = (nw + 63) >> 6;
+            const int w0 = min(lane * per, nw), w1 = min(w0 + per, nw);
+            int cnt = 0;
+            for (int i = w0; i < w1; ++i)
+                cnt += __popc(bm[i]);
+            int pos = wave_exclusive_scan(cnt, lane);
+            for (int i = w0; i < w1; ++i) {
+                wpre[i] = static_cast<uint16_t>(pos);
+                pos += __popc(bm[i]);
             }
+            wave_sync();
+            scanned = true;
+        }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = base + lane + 64 * u;
-                if (i < K) {
-                    vr[i] = v[u];
-                    if (ir)
-                        ir[i] = jj[u];
-                }
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + lane + 64 * u;
+            if (i < K) {
+                const uint32_t y = jj[u];
+                const int rank = wpre[y >> 5] + __popc(bm[y >> 5] & ((1u << (y & 31)) - 1u));
+                vr[rank] = v[u];
+                if (ir)
+                    ir[rank] = jj[u];
             }
         }
     }
@@ -600,8 +607,15 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
     const uint32_t layer = blockIdx.y;
     vals += layer * mb.vals_stride + row * K;
     y += layer * mb.dense_stride + row * ld_y;
-    for (int i = lane; i < K; i += 64)
-        kv[i] = vals[i];
+    // the row's first values are loaded into registers before the mask is
+    // built and reach LDS after it, so their latency overlaps the mask
+    constexpr int kPre = 4;
+    E pv[kPre];
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) {
+        const int i = lane + 64 * u;
+        pv[u] = i < K ? vals[i] : E(0);
+    }
     for (int i = lane; i < nw; i += 64)
         bm[i] = 0u;
     if (FROM_IDX) {
@@ -623,6 +637,14 @@ __global__ __launch_bounds__(256) void ac_unpack_stream_kernel(const E *__restri
             mark_kept(perm, K, static_cast<uint32_t>(H), bm, lane);
         }
     }
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) {
+        const int i = lane + 64 * u;
+        if (i < K)
+            kv[i] = pv[u];
+    }
+    for (int i = lane + 64 * kPre; i < K; i += 64)
+        kv[i] = vals[i];
     wave_sync();
     uint16_t *orow = (!FROM_IDX && idx_out) ? idx_out + layer * mb.idx_stride + row * K : nullptr;
     // The dense row is assembled in LDS one segment at a time: zero the
