@@ -373,6 +373,7 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const Batch<ReduceJo
 // ---------------------------------------------------------------------------
 constexpr int kGT = 16;
 constexpr int kGRows = 32;
+constexpr int kGWaves = 8;                         // waves per Gram workgroup
 typedef double v4d __attribute__((ext_vector_type(4)));
 
 struct GramJob {
@@ -406,7 +407,7 @@ __host__ __device__ constexpr int gram_tile_col(int t, int NB)
     return ti + t;
 }
 
-// One 4-row step of wave W's tiles: tile T = W + 4 U takes block rows
+// One 4-row step of wave W's tiles: tile T = W + kGWaves U takes block rows
 // ti(T) and tj(T) of the step's operands (indices fixed at compile time).
 template <int NB, int T>
 __device__ __forceinline__ v4d gram_mfma(const double (&op)[NB], v4d acc)
@@ -417,20 +418,21 @@ __device__ __forceinline__ v4d gram_mfma(const double (&op)[NB], v4d acc)
 template <int NB, int W, int... U>
 __device__ __forceinline__ void gram_mfmas(v4d *acc, const double (&op)[NB], std::integer_sequence<int, U...>)
 {
-    ((acc[U] = gram_mfma<NB, W + 4 * U>(op, acc[U])), ...);
+    ((acc[U] = gram_mfma<NB, W + kGWaves * U>(op, acc[U])), ...);
 }
 
-// Wave W's share of the upper tiles: t = W, W + 4, ...  (compile-time, so
+// Wave W's share of the upper tiles: t = W, W + kGWaves, ...  (compile-time, so
 // that the operand registers are indexed by constants).
 template <int NB, int W>
 __device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, int nchunks,
                                           const float *A, int64_t lda, int r0, int r1, int KP, double *pb, int tid)
 {
     constexpr int NTILES = NB * (NB + 1) / 2;
-    constexpr int TPW = NTILES > W ? (NTILES - W + 3) / 4 : 0;
+    constexpr int TPW = NTILES > W ? (NTILES - W + kGWaves - 1) / kGWaves : 0;
+    constexpr int NTH = 64 * kGWaves;              // threads
     constexpr int PITCH = gram_pitch(NB);          // doubles per staged row
     constexpr int q4 = NB * kGT / 4;               // float4 per staged row
-    constexpr int PF = (kGRows * q4 + 255) / 256;  // float4 per thread and chunk
+    constexpr int PF = (kGRows * q4 + NTH - 1) / NTH;  // float4 per thread and chunk
     v4d acc[TPW > 0 ? TPW : 1];
 #pragma unroll
     for (int u = 0; u < TPW; ++u)
@@ -439,7 +441,7 @@ __device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, in
     auto load = [&](int rb) {
 #pragma unroll
         for (int u = 0; u < PF; ++u) {
-            const int idx = tid + 256 * u;
+            const int idx = tid + NTH * u;
             const int rr = idx / q4, c4 = (idx % q4) * 4;
             const int gr = rb + rr;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -455,7 +457,7 @@ __device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, in
         // buffer was last read two chunks ago, before the previous barrier
 #pragma unroll
         for (int u = 0; u < PF; ++u) {
-            const int idx = tid + 256 * u;
+            const int idx = tid + NTH * u;
             if (idx < kGRows * q4) {
                 double *d = Ys + (idx / q4) * PITCH + (idx % q4) * 4;
                 *reinterpret_cast<double2 *>(d) = make_double2(pf[u].x, pf[u].y);
@@ -488,7 +490,7 @@ __device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, in
     }
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
-        const int t = W + 4 * u;
+        const int t = W + kGWaves * u;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int i = gram_tile_row(t, NB) * kGT + (lane >> 4) + 4 * e;
@@ -500,7 +502,7 @@ __device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, in
 }
 
 template <int NB>
-__global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> jb, int KP)
+__global__ __launch_bounds__(64 * kGWaves) void gram_partial_kernel(const Batch<GramJob> jb, int KP)
 {
     const GramJob &J = jb.j[blockIdx.z];
     if (static_cast<int>(blockIdx.x) >= J.blocks)
@@ -517,7 +519,11 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const Batch<GramJob> 
     case 0: gram_wave<NB, 0>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
     case 1: gram_wave<NB, 1>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
     case 2: gram_wave<NB, 2>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
-    default: gram_wave<NB, 3>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    case 3: gram_wave<NB, 3>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    case 4: gram_wave<NB, 4>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    case 5: gram_wave<NB, 5>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    case 6: gram_wave<NB, 6>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
+    default: gram_wave<NB, 7>(Ys[0], Ys[1], lane, nchunks, J.A, J.lda, r0, r1, KP, pb, tid); break;
     }
 }
 
@@ -1815,18 +1821,18 @@ void gram(const std::vector<Mat> &ms, const std::vector<const float *> &A, const
         gy = std::max(gy, gb);
     }
     switch (nt) {
-    case 1: launch_jobs("sc_gram", gram_partial_kernel<1>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 2: launch_jobs("sc_gram", gram_partial_kernel<2>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 3: launch_jobs("sc_gram", gram_partial_kernel<3>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 4: launch_jobs("sc_gram", gram_partial_kernel<4>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 5: launch_jobs("sc_gram", gram_partial_kernel<5>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 6: launch_jobs("sc_gram", gram_partial_kernel<6>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 7: launch_jobs("sc_gram", gram_partial_kernel<7>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 8: launch_jobs("sc_gram", gram_partial_kernel<8>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 9: launch_jobs("sc_gram", gram_partial_kernel<9>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 10: launch_jobs("sc_gram", gram_partial_kernel<10>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    case 11: launch_jobs("sc_gram", gram_partial_kernel<11>, gj, dim3(gy), dim3(256), 0, st, KP); break;
-    default: launch_jobs("sc_gram", gram_partial_kernel<12>, gj, dim3(gy), dim3(256), 0, st, KP); break;
+    case 1: launch_jobs("sc_gram", gram_partial_kernel<1>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 2: launch_jobs("sc_gram", gram_partial_kernel<2>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 3: launch_jobs("sc_gram", gram_partial_kernel<3>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 4: launch_jobs("sc_gram", gram_partial_kernel<4>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 5: launch_jobs("sc_gram", gram_partial_kernel<5>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 6: launch_jobs("sc_gram", gram_partial_kernel<6>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 7: launch_jobs("sc_gram", gram_partial_kernel<7>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 8: launch_jobs("sc_gram", gram_partial_kernel<8>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 9: launch_jobs("sc_gram", gram_partial_kernel<9>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 10: launch_jobs("sc_gram", gram_partial_kernel<10>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    case 11: launch_jobs("sc_gram", gram_partial_kernel<11>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
+    default: launch_jobs("sc_gram", gram_partial_kernel<12>, gj, dim3(gy), dim3(64 * kGWaves), 0, st, KP); break;
     }
     launch_jobs("sc_gram_reduce", gram_reduce_kernel, rj, dim3(static_cast<unsigned>(cdiv(int64_t(KP) * KP, 32))),
                 dim3(256), 0, st, KP);
