@@ -422,3 +422,30 @@ def test_large_batch_takes_the_fused_ema_pass(pk):
         assert torch.equal(it["M"], M0)
         for x, y in zip(it["out"], out0):
             assert torch.equal(x, y)
+
+
+def test_stats_filter_times_only_the_named_kernel(pk):
+    """acsc_stats_only: with a name set, only that kernel's launches are
+    timed; the build's result does not depend on the timing."""
+    cfg = workloads.CONFIGS[2]
+    gp = workloads.grad_pair(cfg.grad, 2, 0, 0, "cpu")
+    ref = _gpu_step(pk, gp.G_anc, gp.G_mask, 32, cfg)
+    try:
+        pk.acsc_stats_only("sc_gram")
+        pk.acsc_stats_enable(True)
+        out = _gpu_step(pk, gp.G_anc, gp.G_mask, 32, cfg)
+        torch.cuda.synchronize()
+        only = pk.acsc_stats_read()
+        pk.acsc_stats_only(None)
+        pk.acsc_stats_enable(True)
+        _gpu_step(pk, gp.G_anc, gp.G_mask, 32, cfg)
+        torch.cuda.synchronize()
+        every = pk.acsc_stats_read()
+    finally:
+        pk.acsc_stats_enable(False)
+        pk.acsc_stats_only(None)
+    assert set(only) == {"sc_gram"}
+    assert only["sc_gram"][0] == every["sc_gram"][0] > 0
+    assert {"sc_jacobi", "sc_chol_inv", "sc_gram"} <= set(every)
+    for x, y in zip(ref, out):
+        assert torch.equal(x, y)
