@@ -46,7 +46,20 @@ struct Batch {
     Job j[kMaxJobs];
 };
 
-__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row & 8) >> 1); }
+// LDS slot of 16-byte chunk c of P / V row r (rows of RB bytes; an XOR, so
+// the same map takes a slot back to its chunk).  Measured with the bank
+// conflict counter on MI355X: 256-byte rows need all four chunk bits mixed
+// with the row's low bits for the 16 rows a fragment read touches to spread
+// over every bank; other row widths mix the low three bits with
+// (r >> 1) ^ r.  Either way a fragment read runs without bank conflicts.
+template <int RB>
+__device__ __forceinline__ int slot_of(int c, int r)
+{
+    if constexpr (RB == 256)
+        return c ^ (r & 15);
+    else
+        return (c & ~7) | ((c & 7) ^ (((r >> 1) ^ r) & 7));
+}
 
 // global_load_lds_dwordx4 takes its wave-uniform LDS address in M0.  The asm
 // saves M0 in a scratch SGPR and restores it, so M0 holds, after the
@@ -134,7 +147,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         const bool isV = ins * 1024 >= SLICE;
         const int r = off / RB;
         const int cl = (off % RB) / 16;
-        const int c = (cl & ~7) | ((cl & 7) ^ swz(r));
+        const int c = slot_of<RB>(cl, r);
         const uint16_t *src = isV ? J.V + static_cast<int64_t>(min(col0 + r, n - 1)) * RP
                                   : J.P + static_cast<int64_t>(min(row0 + r, m - 1)) * RP;
         dma16(src + c * 8, lds0 + ins * 1024);
@@ -208,12 +221,12 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
 #pragma unroll
         for (int a = 0; a < 2; ++a) {
             const int r = wr + a * 32 + (lane & 31);
-            af[a] = *reinterpret_cast<const bf16x8 *>(Ps + r * RB + 16 * ((cs & ~7) | ((cs & 7) ^ swz(r))));
+            af[a] = *reinterpret_cast<const bf16x8 *>(Ps + r * RB + 16 * slot_of<RB>(cs, r));
         }
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int r = wc + c * 32 + (lane & 31);
-            bfr[c] = *reinterpret_cast<const bf16x8 *>(Vs + r * RB + 16 * ((cs & ~7) | ((cs & 7) ^ swz(r))));
+            bfr[c] = *reinterpret_cast<const bf16x8 *>(Vs + r * RB + 16 * slot_of<RB>(cs, r));
         }
 #pragma unroll
         for (int a = 0; a < 2; ++a)

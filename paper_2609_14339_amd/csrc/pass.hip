@@ -315,12 +315,16 @@ __global__ __launch_bounds__(256) void pass_kernel(const Batch jb, int np)
 // workgroup's 256 lines of A (a row of A, or a k-row of A^T: 128 bytes each)
 // and the NP lines of the thin factor (128 bytes of k each).  Each line's
 // eight 16-byte chunks are stored XOR-swizzled (slot = chunk ^ swz(line)) so
-// that fragment reads from consecutive lines hit distinct banks.  No
+// that fragment reads from consecutive lines hit distinct banks: with
+// swz = ((line >> 1) ^ line) & 7 neither the 16-byte reads of 16 lines nor
+// the transposed 8-byte reads of four lines conflict (measured with the
+// bank-conflict counter on MI355X; (line & 7) ^ ((line & 8) >> 1) cost four
+// conflict cycles per 16-byte read).  No
 // register staging: registers hold only the accumulators, and S - 1 steps of
 // the stream are in flight while one is multiplied.  Used for 16-byte
 // aligned operands (VEC); waits on the DMA counters are explicit.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int swz(int line) { return (line & 7) ^ ((line & 8) >> 1); }
+__device__ __forceinline__ int swz(int line) { return ((line >> 1) ^ line) & 7; }
 
 // global_load_lds_dwordx4 takes its wave-uniform LDS address in M0.  The asm
 // saves M0 in a scratch SGPR and restores it, so M0 holds, after the
