@@ -364,7 +364,7 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         for (int e = 0; e < 4; ++e) {
             const float lo = blend_step(__uint_as_float(w[e] << 16), pf[2 * e], alpha, oma);
             const float hi = blend_step(__uint_as_float(w[e] & 0xFFFF0000u), pf[2 * e + 1], alpha, oma);
-            o[e] = static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+            o[e] = f32x2_to_bf16x2(lo, hi);
         }
         uint16_t *dst = J.out + static_cast<int64_t>(gi) * n + gj;
         if (VEC && gj + 8 <= n) {

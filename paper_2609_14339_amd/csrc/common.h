@@ -96,14 +96,25 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h)
     return __uint_as_float(static_cast<uint32_t>(h) << 16);
 }
 
-// Round to nearest even; NaN stays a quiet NaN of the same sign.
+// Round to nearest even on gfx950's v_cvt_pk_bf16_f32 (fp32 denormals are
+// kept in the kernels' float mode, so they round like every other value); a
+// NaN gives a quiet NaN.
+typedef __bf16 acsc_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float acsc_f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint16_t f32_to_bf16(float f)
 {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
-        return static_cast<uint16_t>((u >> 16) | 0x0040u);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
+    const __bf16 b = static_cast<__bf16>(f);
+    uint16_t u;
+    __builtin_memcpy(&u, &b, 2);
+    return u;
+}
+// Two values in one instruction: lo in bits 0..15, hi in bits 16..31.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float lo, float hi)
+{
+    const acsc_bf16x2 b = __builtin_convertvector(acsc_f32x2{lo, hi}, acsc_bf16x2);
+    uint32_t u;
+    __builtin_memcpy(&u, &b, 4);
+    return u;
 }
 
 }  // namespace acsc

@@ -172,10 +172,8 @@ __global__ __launch_bounds__(256) void tall_small_kernel(const Batch jb)
         for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                uint32_t w0 = static_cast<uint32_t>(f32_to_bf16(acc[t][4 * q])) |
-                              (static_cast<uint32_t>(f32_to_bf16(acc[t][4 * q + 1])) << 16);
-                uint32_t w1 = static_cast<uint32_t>(f32_to_bf16(acc[t][4 * q + 2])) |
-                              (static_cast<uint32_t>(f32_to_bf16(acc[t][4 * q + 3])) << 16);
+                uint32_t w0 = f32x2_to_bf16x2(acc[t][4 * q], acc[t][4 * q + 1]);
+                uint32_t w1 = f32x2_to_bf16x2(acc[t][4 * q + 2], acc[t][4 * q + 3]);
                 *reinterpret_cast<uint2 *>(St + (32 * t + j) * kSP + 32 * wave + 8 * q + 4 * hi) = make_uint2(w0, w1);
             }
         __syncthreads();

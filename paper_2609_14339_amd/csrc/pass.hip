@@ -947,8 +947,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                     v[3] = ema_step(v[3], __uint_as_float(rg[u].y & 0xFFFF0000u), beta, omb);
                     __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, reinterpret_cast<f32x4 *>(M + o));
                 }
-                h.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-                h.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+                h.x = f32x2_to_bf16x2(v[0], v[1]);
+                h.y = f32x2_to_bf16x2(v[2], v[3]);
                 *reinterpret_cast<uint2 *>(M16 + (static_cast<int64_t>(gi >> 6) * J.ntc + (gk >> 6)) * 4096 +
                                            (gi & 63) * 64 + (gk & 63)) = h;
             }
