@@ -26,7 +26,7 @@ typedef unsigned int nu4 __attribute__((ext_vector_type(4)));
 typedef float nf4 __attribute__((ext_vector_type(4)));
 
 constexpr int kT = 128;          // tile edge
-constexpr int kStPitch = 132;    // floats per staged product row (conflict-free column writes)
+constexpr int kStPitch = 132;    // floats per staged product row (16-byte writes of 16 rows conflict-free)
 constexpr int kMaxJobs = 16;
 constexpr int kBand = 16;        // column blocks per band of the tile walk
 
@@ -228,24 +228,31 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
             const int r = wc + c * 32 + (lane & 31);
             bfr[c] = *reinterpret_cast<const bf16x8 *>(Vs + r * RB + 16 * slot_of<RB>(cs, r));
         }
+        // (P V^T)^T = V P^T: V's rows as the A operand put four consecutive
+        // columns of a G row in each lane's consecutive accumulators, so the
+        // product is staged with 16-byte writes
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
             for (int c = 0; c < 2; ++c)
-                acc[a][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[c], acc[a][c], 0, 0, 0);
+                acc[a][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[c], af[a], acc[a][c], 0, 0, 0);
     }
     sync_lds();
-    // stage the product (D[i][j]: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4)
+    // stage the product: D^T[j][i] sits in lane i + 32 ((j / 4) % 2), element
+    // 4 (j / 8) + j % 4, so elements 4 q .. 4 q + 3 are columns
+    // j0 + 8 q + 4 (lane / 32) .. + 3 of row i = lane % 32 (row pitch 132
+    // floats: the 16 rows a write touches fall on distinct banks)
     float *St = reinterpret_cast<float *>(smem);
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int i = wr + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                const int j = wc + c * 32 + (lane & 31);
-                St[i * kStPitch + j] = acc[a][c][e];
+            for (int q = 0; q < 4; ++q) {
+                const int i = wr + a * 32 + (lane & 31);
+                const int j = wc + c * 32 + 8 * q + 4 * (lane >> 5);
+                *reinterpret_cast<float4 *>(&St[i * kStPitch + j]) =
+                    make_float4(acc[a][c][4 * q], acc[a][c][4 * q + 1], acc[a][c][4 * q + 2], acc[a][c][4 * q + 3]);
             }
     sync_lds();
     const float oma = 1.0f - alpha;
