@@ -355,6 +355,33 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         }
         return;
     }
+    // chunk u of this thread: row q / 16, columns 8 (q % 16) .. of the tile
+    auto blended = [&](int u, int rr, int c8) {
+        const float4 p0 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8]);
+        const float4 p1 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8 + 4]);
+        const float pf[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+        const uint32_t w[4] = {g[u].x, g[u].y, g[u].z, g[u].w};
+        nu4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = blend_step(__uint_as_float(w[e] << 16), pf[2 * e], alpha, oma);
+            const float hi = blend_step(__uint_as_float(w[e] & 0xFFFF0000u), pf[2 * e + 1], alpha, oma);
+            o[e] = f32x2_to_bf16x2(lo, hi);
+        }
+        return o;
+    };
+    if (VEC && row0 + kT <= m && col0 + kT <= n) {
+        // a whole tile: every chunk is stored, with no bounds tests
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int q = tid + 256 * u;
+            const int rr = q >> 4, c8 = (q & 15) * 8;
+            const nu4 o = blended(u, rr, c8);
+            __builtin_nontemporal_store(o, reinterpret_cast<nu4 *>(J.out + static_cast<int64_t>(row0 + rr) * n +
+                                                                   col0 + c8));
+        }
+        return;
+    }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
         const int q = tid + 256 * u;
@@ -362,22 +389,13 @@ __global__ __launch_bounds__(256) void blend_kernel(const Batch jb, float alpha,
         const int gi = row0 + rr, gj = col0 + c8;
         if (gi >= m)
             continue;
-        const float4 p0 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8]);
-        const float4 p1 = *reinterpret_cast<const float4 *>(&St[rr * kStPitch + c8 + 4]);
-        const float pf[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-        const uint32_t w[4] = {g[u].x, g[u].y, g[u].z, g[u].w};
-        uint32_t o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float lo = blend_step(__uint_as_float(w[e] << 16), pf[2 * e], alpha, oma);
-            const float hi = blend_step(__uint_as_float(w[e] & 0xFFFF0000u), pf[2 * e + 1], alpha, oma);
-            o[e] = f32x2_to_bf16x2(lo, hi);
-        }
+        const nu4 o = blended(u, rr, c8);
         uint16_t *dst = J.out + static_cast<int64_t>(gi) * n + gj;
         if (VEC && gj + 8 <= n) {
-            __builtin_nontemporal_store(nu4{o[0], o[1], o[2], o[3]}, reinterpret_cast<nu4 *>(dst));
+            __builtin_nontemporal_store(o, reinterpret_cast<nu4 *>(dst));
         } else {
-            const uint16_t *e8 = reinterpret_cast<const uint16_t *>(o);
+            const uint32_t ow[4] = {o.x, o.y, o.z, o.w};
+            const uint16_t *e8 = reinterpret_cast<const uint16_t *>(ow);
             for (int e = 0; e < 8 && gj + e < n; ++e)
                 dst[e] = e8[e];
         }
