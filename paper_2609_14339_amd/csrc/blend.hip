@@ -9,7 +9,7 @@
 // LDS in G's row order, and each thread blends its own 16-byte chunks of G
 // and writes them out.  Tiles are dealt so that XCD x owns the row blocks
 // congruent to x mod 8 (each P slice stays in one L2) and walks them in bands
-// of columns (the band's V slices stay there too).
+// of 64 columns (the band's V slices stay there too).
 #include "common.h"
 #include "sc_blend.h"
 
@@ -28,7 +28,7 @@ typedef float nf4 __attribute__((ext_vector_type(4)));
 constexpr int kT = 128;          // tile edge
 constexpr int kStPitch = 132;    // floats per staged product row (16-byte writes of 16 rows conflict-free)
 constexpr int kMaxJobs = 16;
-constexpr int kBand = 16;        // column blocks per band of the tile walk
+constexpr int kBand = 64;        // column blocks per band of the tile walk (2 MiB of V slices per XCD)
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
