@@ -842,15 +842,19 @@ struct EmaJob {
     int64_t ldbt;
     float *C;
     int64_t ldc;
-    int m, n, nblocks;
-    float *part;      // split k: partial products [splits][m][np]
-    int64_t ss;       // elements per split's partial
-    int kchunk, splits;
+    int m, n;
+    float *part;      // pieces of a halved row block: partial p at part + p * ss, row stride np
+    int64_t ss;
     int ntc;          // tiles per tile row of the shadow
 };
+// Workgroups in the order of the streaming passes' dispatch plan (Seg runs
+// over the jobs; see plan()), so that a batch that mixes long and short rows
+// ends with every CU busy: whole rows, only the last-dispatched row blocks
+// cut into two k halves.
 struct EmaBatch {
-    int count;
+    int njobs, nseg;
     EmaJob j[kMaxJobs];
+    Seg s[2 * kMaxJobs];
 };
 
 // Eight waves per workgroup, two per SIMD (four waves left the stream with
@@ -859,9 +863,15 @@ template <int NT>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void ema_pass_kernel(const EmaBatch jb, int np,
                                                                                                  float beta, float omb)
 {
-    const EmaJob &J = jb.j[blockIdx.z];
-    if (static_cast<int>(blockIdx.x) >= J.nblocks)
-        return;
+    const int wg = static_cast<int>(blockIdx.x);
+    int si = 0;
+    while (si + 1 < jb.nseg && wg >= jb.s[si + 1].wg0)
+        ++si;
+    const Seg &SG = jb.s[si];
+    const int rel = wg - SG.wg0;
+    if (rel >= SG.nrb * SG.pieces)
+        return;   // padding between segments
+    const EmaJob &J = jb.j[SG.job];
     constexpr int NP = NT * 16;
     constexpr int A_BYTES = 256 * 128;
     constexpr int STAGE = A_BYTES + NP * 128;
@@ -880,11 +890,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int m = J.m, n = J.n;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // block -> (row block, k split): the k range [kbeg, kend) of the rows
-    const int split = static_cast<int>(blockIdx.x) % J.splits;
-    const int row0 = (static_cast<int>(blockIdx.x) / J.splits) * kBM;
-    const int kbeg = split * J.kchunk;
-    const int kend = min(n, kbeg + J.kchunk);
+    // workgroup -> (row block, piece): the k range [kbeg, kend) of the rows
+    const int piece = rel % SG.pieces;
+    const int row0 = (SG.rb0 + rel / SG.pieces) * kBM;
+    const int kbeg = piece * SG.kchunk;
+    const int kend = min(n, kbeg + SG.kchunk);
     const int nsteps = static_cast<int>(cdiv(kend - kbeg, kBK));
 
     f32x4 acc[2][NT];
@@ -1010,9 +1020,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
 
     // D[i][j] of a 16 x 16 tile: lane j + 16 (i / 4), element i % 4;
-    // a split writes its partial (row stride np), added up by pass_reduce_kernel
-    float *Cout = J.splits > 1 ? J.part + split * J.ss : J.C;
-    const int64_t ldo = J.splits > 1 ? static_cast<int64_t>(np) : J.ldc;
+    // a piece of a halved row block writes its partial (row stride np),
+    // added up by pass_reduce_kernel
+    float *Cout = SG.pieces > 1 ? J.part + piece * J.ss : J.C;
+    const int64_t ldo = SG.pieces > 1 ? static_cast<int64_t>(np) : J.ldc;
     const int wrow0 = row0 + wave * 32;
 #pragma unroll
     for (int a = 0; a < 2; ++a)
@@ -1029,15 +1040,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 template <int NT>
-void ema_launch(const char *tag, const std::vector<EmaJob> &jobs, int gx, int np, float a, float b_coef, hipStream_t st)
+void ema_launch(const char *tag, const EmaBatch &b, int grid, int np, float a, float b_coef, hipStream_t st)
 {
-    for (size_t c0 = 0; c0 < jobs.size(); c0 += kMaxJobs) {
-        EmaBatch b{};
-        b.count = static_cast<int>(std::min<size_t>(kMaxJobs, jobs.size() - c0));
-        for (int i = 0; i < b.count; ++i)
-            b.j[i] = jobs[c0 + i];
-        ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(gx, 1, b.count), dim3(512), 0, st, b, np, a, b_coef);
-    }
+    ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(grid), dim3(512), 0, st, b, np, a, b_coef);
 }
 
 }  // namespace
@@ -1175,58 +1180,55 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
     if (!ema_fusable(reqs))
         return set_error(ACSC_EINVAL, "fused EMA pass: operands not aligned or batch too small");
     const int NP = reqs[0].NP;
-    // longest rows first, as for the streaming passes
+    // longest rows first, as for the streaming passes, and the same dispatch
+    // plan: for a batch of the same shapes the fused kernel multiplies the
+    // same pieces in the same order as pass_dma_kernel<false>
     std::vector<size_t> order(reqs.size());
     for (size_t i = 0; i < order.size(); ++i)
         order[i] = i;
     std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return reqs[a].n > reqs[b].n; });
-    // Balance: when the batch mixes long and short rows, every row is cut
-    // into k chunks of half the shortest row, so that all blocks do about
-    // the same work and the last round of blocks is not left half empty (a
-    // split writes an fp32 partial of np floats per row, ~1% of the bytes
-    // the sweep streams per row).
-    int64_t nmin = reqs[0].n, nmax = reqs[0].n;
-    for (const EmaReq &q : reqs) {
-        nmin = std::min<int64_t>(nmin, q.n);
-        nmax = std::max<int64_t>(nmax, q.n);
-    }
-    const int64_t kc = 2 * nmax >= 3 * nmin ? round_up(cdiv(nmin, 2), kBK) : nmax;
-    std::vector<EmaJob> jobs;
     std::vector<RedJob> red;
-    int gx = 1;
     int64_t rtot = 1;
-    for (size_t oi : order) {
-        const EmaReq &q = reqs[oi];
-        int splits = static_cast<int>(std::min<int64_t>(cdiv(q.n, kc), max_splits(q.m, q.n)));
-        splits = std::max(1, splits);
-        const int64_t chunk = round_up(cdiv(q.n, splits), kBK);
-        splits = static_cast<int>(cdiv(q.n, chunk));
-        if (splits > 1 && !q.part)
-            splits = 1;
-        const int nb = static_cast<int>(cdiv(q.m, kBM)) * splits;
-        const int64_t ss = static_cast<int64_t>(q.m) * NP;
-        jobs.push_back(EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, nb, q.part, ss,
-                              static_cast<int>(splits > 1 ? chunk : q.n), splits,
-                              static_cast<int>(tiles_per_row(q.n))});
-        if (splits > 1) {
-            red.push_back(RedJob{q.part, ss, q.C, q.ldc, q.m, NP, splits});
-            rtot = std::max<int64_t>(rtot, static_cast<int64_t>(q.m) * (NP / 4));
+    for (size_t c0 = 0; c0 < order.size(); c0 += kMaxJobs) {
+        const size_t cnt = std::min<size_t>(kMaxJobs, order.size() - c0);
+        std::vector<JobShape> js;
+        EmaBatch eb{};
+        eb.njobs = static_cast<int>(cnt);
+        for (size_t i = 0; i < cnt; ++i) {
+            const EmaReq &q = reqs[order[c0 + i]];
+            eb.j[i] = EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, q.part,
+                             static_cast<int64_t>(q.m) * NP, static_cast<int>(tiles_per_row(q.n))};
+            js.push_back(JobShape{static_cast<int>(cdiv(q.m, kBM)), 1, static_cast<int>(round_up(q.n, kBK)), q.n,
+                                  q.part != nullptr && max_splits(q.m, q.n) >= 2 && q.n >= 2 * kBK});
         }
-        gx = std::max(gx, nb);
-    }
-    switch (NP / 16) {
-    case 1: ema_launch<1>(tag, jobs, gx, NP, a, b, st); break;
-    case 2: ema_launch<2>(tag, jobs, gx, NP, a, b, st); break;
-    case 3: ema_launch<3>(tag, jobs, gx, NP, a, b, st); break;
-    case 4: ema_launch<4>(tag, jobs, gx, NP, a, b, st); break;
-    case 5: ema_launch<5>(tag, jobs, gx, NP, a, b, st); break;
-    case 6: ema_launch<6>(tag, jobs, gx, NP, a, b, st); break;
-    case 7: ema_launch<7>(tag, jobs, gx, NP, a, b, st); break;
-    case 8: ema_launch<8>(tag, jobs, gx, NP, a, b, st); break;
-    case 9: ema_launch<9>(tag, jobs, gx, NP, a, b, st); break;
-    case 10: ema_launch<10>(tag, jobs, gx, NP, a, b, st); break;
-    case 11: ema_launch<11>(tag, jobs, gx, NP, a, b, st); break;
-    default: ema_launch<12>(tag, jobs, gx, NP, a, b, st); break;
+        const SegPlan pl = plan(js);
+        eb.nseg = static_cast<int>(pl.segs.size());
+        for (size_t i = 0; i < pl.segs.size(); ++i)
+            eb.s[i] = pl.segs[i];
+        switch (NP / 16) {
+        case 1: ema_launch<1>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 2: ema_launch<2>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 3: ema_launch<3>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 4: ema_launch<4>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 5: ema_launch<5>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 6: ema_launch<6>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 7: ema_launch<7>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 8: ema_launch<8>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 9: ema_launch<9>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 10: ema_launch<10>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 11: ema_launch<11>(tag, eb, pl.grid, NP, a, b, st); break;
+        default: ema_launch<12>(tag, eb, pl.grid, NP, a, b, st); break;
+        }
+        for (size_t i = 0; i < cnt; ++i) {
+            const int h = pl.halved[i];
+            if (h <= 0)
+                continue;
+            const EmaReq &q = reqs[order[c0 + i]];
+            const int64_t r0 = static_cast<int64_t>(js[i].nrb - h) * kBM;
+            red.push_back(RedJob{q.part + r0 * NP, static_cast<int64_t>(q.m) * NP, q.C + r0 * q.ldc, q.ldc,
+                                 static_cast<int>(q.m - r0), NP, 2});
+            rtot = std::max<int64_t>(rtot, (q.m - r0) * (NP / 4));
+        }
     }
     for (size_t c0 = 0; c0 < red.size(); c0 += kMaxJobs) {
         RedBatch rb{};
