@@ -51,7 +51,7 @@ struct Lds {
     static constexpr int FLOATS = MAIN > STAGE ? MAIN : STAGE;
 };
 
-template <int NT>
+template <int NT, bool TRI>
 __global__ __launch_bounds__(256) void tall_small_kernel(const Batch jb)
 {
     using L = Lds<NT>;
@@ -71,7 +71,6 @@ __global__ __launch_bounds__(256) void tall_small_kernel(const Batch jb)
     const float *B = J.B;
     const int64_t lda = J.lda, ldb = J.ldb;
     const int K = J.K, N = J.N;
-    const bool tri = J.tri != 0;
     const int nk = (K + kKC - 1) / kKC;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -130,16 +129,43 @@ __global__ __launch_bounds__(256) void tall_small_kernel(const Batch jb)
         __syncthreads();
         if (kc + 1 < nk)
             load(kc + 1);
-        // A[i][k] = A[32 wave + i][2 s + k] in lane i + 32 k; B[k][j] = B[2 s + k][32 t + j]
+        // A[i][k] = A[32 wave + i][2 s + k] in lane i + 32 k; B[k][j] = B[2 s + k][32 t + j].
+        // The chunk's 16 steps go in four groups of four; each group's
+        // operands are read before the previous group's products are issued
+        // (scheduling barriers: left alone, the compiler reads each operand
+        // just before its product and waits for it there).
+        constexpr int SG = 4;
         const float *ya = Ys + (32 * wave + (lane & 31)) * kYP + (lane >> 5);
         const float *tb = Ts + (lane >> 5) * TP + (lane & 31);
+        float ah[2][SG], bh[2][SG][NT];
+        auto rd = [&](int g) {
 #pragma unroll
-        for (int s = 0; s < kKC / 2; ++s) {
-            const float a = ya[2 * s];
+            for (int q = 0; q < SG; ++q) {
+                const int s = SG * g + q;
+                ah[g & 1][q] = ya[2 * s];
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    bh[g & 1][q][t] = tb[2 * s * TP + 32 * t];
+            }
+        };
+        auto mm = [&](int g) {
 #pragma unroll
             for (int t = 0; t < NT; ++t)
-                if (!tri || t >= kc)
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, tb[2 * s * TP + 32 * t], acc[t], 0, 0, 0);
+                if (!TRI || t >= kc) {
+#pragma unroll
+                    for (int q = 0; q < SG; ++q)
+                        acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(ah[g & 1][q], bh[g & 1][q][t], acc[t], 0, 0,
+                                                                      0);
+                }
+        };
+        rd(0);
+#pragma unroll
+        for (int g = 0; g < kKC / 2 / SG; ++g) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (g + 1 < kKC / 2 / SG)
+                rd(g + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            mm(g);
         }
     }
 
@@ -199,7 +225,11 @@ void launch(const char *tag, const std::vector<Job> &jobs, hipStream_t st)
             b.j[i] = jobs[c0 + i];
             gx = std::max(gx, (b.j[i].rows + kRows - 1) / kRows);
         }
-        ACSC_LAUNCH(tag, tall_small_kernel<NT>, dim3(gx, 1, b.count), dim3(256), 0, st, b);
+        // run() and gemm() each make jobs of one kind (triangular B or not)
+        if (b.j[0].tri)
+            ACSC_LAUNCH(tag, (tall_small_kernel<NT, true>), dim3(gx, 1, b.count), dim3(256), 0, st, b);
+        else
+            ACSC_LAUNCH(tag, (tall_small_kernel<NT, false>), dim3(gx, 1, b.count), dim3(256), 0, st, b);
     }
 }
 

@@ -477,14 +477,21 @@ __device__ __forceinline__ void gram_wave(double *Ys0, double *Ys1, int lane, in
                 for (int b = 0; b < NB; ++b)
                     o[b] = yr[k0 * PITCH + b * kGT];
             };
+            // (scheduling barriers keep each read ahead of the products before
+            // it: left alone, the compiler sinks the reads to just before
+            // their use and waits for them there)
             read(opA, 0);
 #pragma unroll
             for (int k0 = 0; k0 < kGRows; k0 += 8) {
                 read(opB, k0 + 4);
+                __builtin_amdgcn_sched_barrier(0);
                 gram_mfmas<NB, W>(acc, opA, std::make_integer_sequence<int, TPW>{});
+                __builtin_amdgcn_sched_barrier(0);
                 if (k0 + 8 < kGRows)
                     read(opA, k0 + 8);
+                __builtin_amdgcn_sched_barrier(0);
                 gram_mfmas<NB, W>(acc, opB, std::make_integer_sequence<int, TPW>{});
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     }
