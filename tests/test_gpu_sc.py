@@ -424,6 +424,31 @@ def test_large_batch_takes_the_fused_ema_pass(pk):
             assert torch.equal(x, y)
 
 
+def test_fused_ema_pass_over_more_matrices_than_one_launch_takes(pk):
+    """20 matrices of 4096 x 256 (320 row blocks: the fused EMA pass, in two
+    launches of at most 16 matrices, each with its own dispatch plan) give
+    the same M and prior, bit for bit, as single calls (separate EMA and
+    pass, the same products in the same order)."""
+    m, n, r, p, q = 4096, 256, 16, 16, 2
+    spec = workloads.GradSpec(((m, n),), 16, (1.0, 100.0), (r,), torch.bfloat16, None, None)
+    pairs = [workloads.grad_pair(spec, 11, layer, 0, "cpu") for layer in range(20)]
+    items = []
+    for gp in pairs:
+        outs = (torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
+                torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda"))
+        items.append(dict(G_anc=gp.G_anc.cuda(), M=torch.zeros(m, n, device="cuda"), out=outs,
+                          ws=pk.workspace(m, n, r, p, torch.bfloat16)))
+    pk.sc_build_prior_batched(items, r, workloads.BETA, workloads.TAU, p, q, seed=90)
+    torch.cuda.synchronize()
+    for i, (it, gp) in enumerate(zip(items, pairs)):
+        M = torch.zeros(m, n, device="cuda")
+        single = pk.sc_build_prior(gp.G_anc.cuda(), M, r, workloads.BETA, workloads.TAU, p, q, seed=90 + i)
+        torch.cuda.synchronize()
+        assert torch.equal(it["M"], M), i
+        for x, y in zip(it["out"], single):
+            assert torch.equal(x, y), i
+
+
 def test_stats_filter_times_only_the_named_kernel(pk):
     """acsc_stats_only: with a name set, only that kernel's launches are
     timed; the build's result does not depend on the timing."""
