@@ -857,8 +857,38 @@ struct EmaBatch {
     Seg s[2 * kMaxJobs];
 };
 
+// Workgroup-scope counters in LDS: a wave adds one when its part of a stage
+// is written (or its reads of it are done); waiting waves poll.  Release and
+// acquire order the stage's LDS accesses around the counters.
+__device__ __forceinline__ void stage_signal(unsigned int *c, int lane)
+{
+    if (lane == 0)
+        __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+// Every wave of the workgroup reaches each of its signals, so a wait ends
+// within a few steps' time; the poll count is bounded (about a second)
+// so that a fault elsewhere cannot turn into a hung GPU.
+__device__ __forceinline__ void stage_wait(unsigned int *c, unsigned int target)
+{
+    for (int i = 0; i < (1 << 24); ++i) {
+        if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target)
+            return;
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
 // Eight waves per workgroup, two per SIMD (four waves left the stream with
-// too few loads in flight); each wave multiplies 32 rows.
+// too few loads in flight).  Wave w loads, updates and multiplies rows
+// 32 w .. 32 w + 31 of the block, staging their bf16 copy in an LDS region of
+// its own, so the rows need no synchronisation between waves.  The thin
+// factor's step is shared: each wave stages an eighth of it into a ring of
+// kEmaStages buffers, and counters per buffer (parts written, readers done)
+// replace the workgroup barrier, so that a wave waits for the others only
+// when it is kEmaStages - 1 steps ahead (a barrier per step held the waves
+// in lockstep on the slowest one's HBM loads).  Every wave runs every step,
+// so every counter reaches its target.
+constexpr int kEmaStages = 3;
+
 template <int NT>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void ema_pass_kernel(const EmaBatch jb, int np,
                                                                                                  float beta, float omb)
@@ -873,14 +903,17 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         return;   // padding between segments
     const EmaJob &J = jb.j[SG.job];
     constexpr int NP = NT * 16;
-    constexpr int A_BYTES = 256 * 128;
-    constexpr int STAGE = A_BYTES + NP * 128;
-    constexpr int BCH = NP * 8;                 // 16-byte chunks of one thin-factor step
     constexpr int W = 8;                        // waves
-    constexpr int NTH = 64 * W;                 // threads
-    constexpr int PU = 4096 / NTH;              // 4-element pieces of M per thread and step
-    constexpr int BPT = (BCH + NTH - 1) / NTH;
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE];
+    constexpr int A_WAVE = 32 * 128;            // a wave's 32 rows of one step (bf16)
+    constexpr int A_BYTES = W * 2 * A_WAVE;     // two buffers per wave
+    constexpr int B_STAGE = NP * 128;
+    constexpr int NB = kEmaStages;
+    constexpr int BCH = NP * 8;                 // 16-byte chunks of one thin-factor step
+    constexpr int CPW = (BCH + W - 1) / W;      // chunks staged per wave
+    constexpr int BPL = (CPW + 63) / 64;        // chunks per lane
+    constexpr int PU = 8;                       // 4-element pieces of M per lane and step
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[A_BYTES + NB * B_STAGE];
+    __shared__ unsigned int ready[NB], done[NB];
 
     float *__restrict__ M = J.M;
     const uint16_t *__restrict__ G = J.G;
@@ -896,6 +929,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int kbeg = piece * SG.kchunk;
     const int kend = min(n, kbeg + SG.kchunk);
     const int nsteps = static_cast<int>(cdiv(kend - kbeg, kBK));
+    const int wrow0 = row0 + wave * 32;
+    if (tid < NB) {
+        ready[tid] = 0u;
+        done[tid] = 0u;
+    }
+    __syncthreads();
 
     f32x4 acc[2][NT];
 #pragma unroll
@@ -904,48 +943,63 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int t = 0; t < NT; ++t)
             acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // piece u of this thread: row (tid + 512 u) / 16 of the block, 4 elements
-    // at column 4 ((tid + 512 u) % 16) of the step, so that 16 lanes cover a
-    // row's 256 bytes of M (128 of G) with one instruction
+    // piece u of this lane: row 4 u + lane / 16 of the wave's 32, 4 elements at
+    // column 4 (lane % 16) of the step, so that 16 lanes cover a row's 256
+    // bytes of M (128 of G) with one instruction
     float4 rm[PU];
     uint2 rg[PU];
-    uint4 rb[BPT];
-    auto load = [&](int s) {
+    uint4 rb[BPL];
+    // the thin factor's part first, so that its wait leaves M and G in flight
+    // Loads are unconditional, from addresses clamped into the operands
+    // (k past the end reads the piece's first step, rows past m the last
+    // row; without a new gradient G is read from M's bytes), and what lies
+    // outside is zeroed or skipped when the registers are used: the wait
+    // for the thin factor's loads then counts exactly the M and G loads
+    // issued after them and leaves those in flight.
+    const uint16_t *__restrict__ Gs = G ? G : reinterpret_cast<const uint16_t *>(M);
+    auto load_b = [&](int s) {
         const int k0 = kbeg + s * kBK;
 #pragma unroll
-        for (int u = 0; u < PU; ++u) {
-            const int q = tid + NTH * u;
-            const int gi = row0 + (q >> 4), gk = k0 + (q & 15) * 4;
-            float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-            uint2 g = make_uint2(0u, 0u);
-            if (gi < m && gk < kend) {
-                const int64_t o = static_cast<int64_t>(gi) * n + gk;
-                a = *reinterpret_cast<const float4 *>(M + o);
-                if (G)
-                    g = *reinterpret_cast<const uint2 *>(G + o);
-            }
-            rm[u] = a;
-            rg[u] = g;
-        }
-#pragma unroll
-        for (int j = 0; j < BPT; ++j) {
-            const int q = min(tid + NTH * j, BCH - 1);
+        for (int j = 0; j < BPL; ++j) {
+            const int q = min(wave * CPW + lane + 64 * j, BCH - 1);
             const int c = min(q >> 3, np - 1);
             const int gk = k0 + (q & 7) * 8;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (gk < kend)
-                v = *reinterpret_cast<const uint4 *>(Bt + static_cast<int64_t>(c) * ldbt + gk);
-            rb[j] = v;
+            rb[j] = *reinterpret_cast<const uint4 *>(Bt + static_cast<int64_t>(c) * ldbt + (gk < kend ? gk : kbeg));
         }
     };
-    auto store = [&](int buf, int s) {
+    auto load_mg = [&](int s) {
         const int k0 = kbeg + s * kBK;
-        unsigned char *base = smem + buf * STAGE;
 #pragma unroll
         for (int u = 0; u < PU; ++u) {
-            const int q = tid + NTH * u;
-            const int row = q >> 4, f = q & 15;
-            const int gi = row0 + row, gk = k0 + f * 4;
+            const int gi = min(wrow0 + 4 * u + (lane >> 4), m - 1), gk = k0 + (lane & 15) * 4;
+            const int64_t o = static_cast<int64_t>(gi) * n + (gk < kend ? gk : kbeg);
+            rm[u] = *reinterpret_cast<const float4 *>(M + o);
+            rg[u] = *reinterpret_cast<const uint2 *>(Gs + o);
+        }
+    };
+    auto store_b = [&](int s) {
+        const int k0 = kbeg + s * kBK;
+        unsigned char *bw = smem + A_BYTES + (s % NB) * B_STAGE;
+#pragma unroll
+        for (int j = 0; j < BPL; ++j) {
+            const int qi = lane + 64 * j;
+            const int q = wave * CPW + qi;
+            if (qi < CPW && q < BCH) {
+                const int line = q >> 3, c = q & 7;
+                uint4 v = rb[j];
+                if (line >= np || k0 + c * 8 >= kend)
+                    v = make_uint4(0u, 0u, 0u, 0u);
+                *reinterpret_cast<uint4 *>(bw + line * 128 + 16 * (c ^ swz(line))) = v;
+            }
+        }
+    };
+    auto store_mg = [&](int s) {
+        const int k0 = kbeg + s * kBK;
+        unsigned char *aw = smem + (wave * 2 + (s & 1)) * A_WAVE;
+#pragma unroll
+        for (int u = 0; u < PU; ++u) {
+            const int row = 4 * u + (lane >> 4), f = lane & 15;
+            const int gi = wrow0 + row, gk = k0 + f * 4;
             float v[4] = {rm[u].x, rm[u].y, rm[u].z, rm[u].w};
             uint2 h = make_uint2(0u, 0u);
             if (gi < m && gk < kend) {
@@ -962,27 +1016,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                 *reinterpret_cast<uint2 *>(M16 + (static_cast<int64_t>(gi >> 6) * J.ntc + (gk >> 6)) * 4096 +
                                            (gi & 63) * 64 + (gk & 63)) = h;
             }
-            *reinterpret_cast<uint2 *>(base + row * 128 + 16 * ((f >> 1) ^ swz(row & 63)) + 8 * (f & 1)) = h;
-        }
-#pragma unroll
-        for (int j = 0; j < BPT; ++j) {
-            const int q = tid + NTH * j;
-            if (q < BCH) {
-                const int line = q >> 3, c = q & 7;
-                uint4 v = rb[j];
-                if (line >= np)
-                    v = make_uint4(0u, 0u, 0u, 0u);
-                *reinterpret_cast<uint4 *>(base + A_BYTES + line * 128 + 16 * (c ^ swz(line))) = v;
-            }
+            *reinterpret_cast<uint2 *>(aw + row * 128 + 16 * ((f >> 1) ^ swz(row)) + 8 * (f & 1)) = h;
         }
     };
     // v_mfma_f32_16x16x32_bf16 on the step in LDS, in the layout and order of
     // pass_dma_kernel<false> (the same products in the same order, so the
     // result equals the separate EMA and pass bit for bit); this wave's 32
     // rows are two 16-row tiles
-    auto compute = [&](int buf) {
-        const unsigned char *aw = smem + buf * STAGE + wave * 4096;
-        const unsigned char *bw = smem + buf * STAGE + A_BYTES;
+    auto compute = [&](int s) {
+        const unsigned char *aw = smem + (wave * 2 + (s & 1)) * A_WAVE;
+        const unsigned char *bw = smem + A_BYTES + (s % NB) * B_STAGE;
         bf16x8 af[2][2], bf[2][NT];
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh) {
@@ -1006,17 +1049,32 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                 for (int a = 0; a < 2; ++a)
                     acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[kh][a], bf[kh][t], acc[a][t], 0, 0, 0);
     };
+    // step s: its thin factor sits in buffer s % NB once ready[s % NB] has
+    // reached W (s / NB + 1); the buffer may take step s + NB once done[s % NB]
+    // has reached W (s / NB + 1)
+    auto put_b = [&](int s) {
+        if (s >= NB)
+            stage_wait(&done[s % NB], W * (s / NB));
+        store_b(s);
+        stage_signal(&ready[s % NB], lane);
+    };
 
-    load(0);
-    store(0, 0);
-    lds_barrier();
+    load_b(0);
+    load_mg(0);
+    put_b(0);
+    store_mg(0);
     for (int s = 0; s < nsteps; ++s) {
-        if (s + 1 < nsteps)
-            load(s + 1);
-        compute(s & 1);
-        if (s + 1 < nsteps)
-            store((s + 1) & 1, s + 1);
-        lds_barrier();
+        const bool more = s + 1 < nsteps;
+        if (more) {
+            load_b(s + 1);
+            load_mg(s + 1);
+            put_b(s + 1);
+        }
+        stage_wait(&ready[s % NB], W * (s / NB + 1));
+        compute(s);
+        stage_signal(&done[s % NB], lane);
+        if (more)
+            store_mg(s + 1);
     }
 
     // D[i][j] of a 16 x 16 tile: lane j + 16 (i / 4), element i % 4;
@@ -1024,7 +1082,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // added up by pass_reduce_kernel
     float *Cout = SG.pieces > 1 ? J.part + piece * J.ss : J.C;
     const int64_t ldo = SG.pieces > 1 ? static_cast<int64_t>(np) : J.ldc;
-    const int wrow0 = row0 + wave * 32;
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
