@@ -449,6 +449,37 @@ def test_fused_ema_pass_over_more_matrices_than_one_launch_takes(pk):
             assert torch.equal(x, y), i
 
 
+def test_fused_ema_pass_on_ragged_shapes(pk):
+    """10 matrices of 8000 x 1000 (320 row blocks: the fused EMA pass, with a
+    partial last row block and a 40-column last step) give the same M and
+    prior, bit for bit, as single calls (separate EMA and pass), with and
+    without a new gradient."""
+    m, n, r, p, q = 8000, 1000, 16, 16, 2
+    spec = workloads.GradSpec(((m, n),), 16, (1.0, 100.0), (r,), torch.bfloat16, None, None)
+    pairs = [workloads.grad_pair(spec, 12, layer, 0, "cpu") for layer in range(10)]
+    items = []
+    for gp in pairs:
+        outs = (torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
+                torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda"))
+        items.append(dict(G_anc=gp.G_anc.cuda(), M=torch.zeros(m, n, device="cuda"), out=outs,
+                          ws=pk.workspace(m, n, r, p, torch.bfloat16)))
+    singles = [torch.zeros(m, n, device="cuda") for _ in pairs]
+    for arrival in range(2):
+        if arrival == 1:
+            for it in items:
+                it["G_anc"] = None
+        pk.sc_build_prior_batched(items, r, workloads.BETA, workloads.TAU, p, q, seed=40, dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        for i, (it, gp) in enumerate(zip(items, pairs)):
+            G = gp.G_anc.cuda() if arrival == 0 else None
+            single = pk.sc_build_prior(G, singles[i], r, workloads.BETA, workloads.TAU, p, q, seed=40 + i,
+                                       dtype=torch.bfloat16)
+            torch.cuda.synchronize()
+            assert torch.equal(it["M"], singles[i]), (arrival, i)
+            for x, y in zip(it["out"], single):
+                assert torch.equal(x, y), (arrival, i)
+
+
 def test_stats_filter_times_only_the_named_kernel(pk):
     """acsc_stats_only: with a name set, only that kernel's launches are
     timed; the build's result does not depend on the timing."""
