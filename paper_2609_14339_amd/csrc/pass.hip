@@ -973,8 +973,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int u = 0; u < PU; ++u) {
             const int gi = min(wrow0 + 4 * u + (lane >> 4), m - 1), gk = k0 + (lane & 15) * 4;
             const int64_t o = static_cast<int64_t>(gi) * n + (gk < kend ? gk : kbeg);
-            rm[u] = *reinterpret_cast<const float4 *>(M + o);
-            rg[u] = *reinterpret_cast<const uint2 *>(Gs + o);
+            const f32x4 a = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(M + o));
+            rm[u] = make_float4(a[0], a[1], a[2], a[3]);
+            const unsigned long long gg = __builtin_nontemporal_load(reinterpret_cast<const unsigned long long *>(Gs + o));
+            rg[u] = make_uint2(static_cast<uint32_t>(gg), static_cast<uint32_t>(gg >> 32));
         }
     };
     auto store_b = [&](int s) {
@@ -1013,8 +1015,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                 }
                 h.x = f32x2_to_bf16x2(v[0], v[1]);
                 h.y = f32x2_to_bf16x2(v[2], v[3]);
-                *reinterpret_cast<uint2 *>(M16 + (static_cast<int64_t>(gi >> 6) * J.ntc + (gk >> 6)) * 4096 +
-                                           (gi & 63) * 64 + (gk & 63)) = h;
+                __builtin_nontemporal_store(static_cast<unsigned long long>(h.x) | (static_cast<unsigned long long>(h.y) << 32),
+                                            reinterpret_cast<unsigned long long *>(M16 + (static_cast<int64_t>(gi >> 6) * J.ntc + (gk >> 6)) * 4096 +
+                                                                                   (gi & 63) * 64 + (gk & 63)));
             }
             *reinterpret_cast<uint2 *>(aw + row * 128 + 16 * ((f >> 1) ^ swz(row)) + 8 * (f & 1)) = h;
         }
