@@ -349,6 +349,22 @@ __device__ __forceinline__ void dma16(const void *gptr, uint32_t lds_addr)
                  : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
                  : "memory");
 }
+// The same DMA with the non-temporal hint, for the streamed operand A: each
+// line of it is read once per pass, so it is not kept in L2 at the expense of
+// the thin factor, which every workgroup of an XCD re-reads.
+__device__ __forceinline__ void dma16_nt(const void *gptr, uint32_t lds_addr)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, off nt\n\t"
+                 "s_mov_b32 m0, %0\n\t"
+                 "s_nop 0"
+                 : "=&s"(saved)
+                 : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
+}
 
 template <int N>
 __device__ __forceinline__ void wait_dma()
@@ -481,7 +497,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             } else {
                 src = A + static_cast<int64_t>(min(k0 + line, kend - 1)) * lda + min(grow0 + c * 8, (M - 1) & ~7);
             }
-            dma16(src, sbase + grp * 8192 + j * 1024);
+            dma16_nt(src, sbase + grp * 8192 + j * 1024);
         }
 #pragma unroll
         for (int b = 0; b < BI_HI; ++b) {
