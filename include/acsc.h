@@ -39,8 +39,9 @@ typedef enum acsc_dtype { ACSC_F32 = 0, ACSC_BF16 = 1 } acsc_dtype;
 #define ACSC_EALIGN (-3)  /* pointer or stride not aligned as required      */
 #define ACSC_EHIP (-4)    /* HIP launch or runtime failure                  */
 #define ACSC_ENOSPC (-5)  /* workspace too small                            */
-#define ACSC_ENOCONV (-6) /* sc_build_status: a build did not converge, or its
-                             two phases did not meet on its workspace       */
+#define ACSC_ENOCONV (-6) /* sc_build_status: a build did not converge, its
+                             two phases did not meet on its workspace, or
+                             its fused EMA pass gave up a wait              */
 
 /* Text of the last error raised on the calling thread ("" if none). */
 const char *acsc_last_error(void);
@@ -335,10 +336,15 @@ int sc_build_ritz_batched(int count, const sc_matrix *mats, acsc_dtype dt, float
  * sc_build_ritz_batched alone, or after a correction that reused the
  * workspace); acsc_last_error() names the first such matrix.  sweeps and
  * residual (arrays of count, or NULL) receive each matrix's sweeps used and
- * its last sweep's largest off-diagonal ratio.  A workspace that never held
- * a build gives unspecified values.  The environment variable
- * ACSC_JACOBI_MAX_SWEEPS, read by each build call, lowers the sweep cap
- * (1..40), so that a non-converged build can be produced on purpose. */
+ * its last sweep's largest off-diagonal ratio.  ACSC_ENOCONV also reports
+ * a subspace phase whose fused EMA pass (bf16 shadow, large batches) gave up
+ * one of its bounded waits between the waves of a workgroup (the wait polls
+ * for about a second or more before it gives up; the kernel then finishes
+ * with a product that is not to be trusted).  A workspace that never held
+ * a build gives unspecified values.  The environment variables
+ * ACSC_JACOBI_MAX_SWEEPS and ACSC_EMA_SPIN_LIMIT, read by each build call,
+ * lower the sweep cap (1..40) and the polls of a wait (0 gives up at the
+ * first unmet check), so that both reports can be produced on purpose. */
 int sc_build_status(int count, const sc_matrix *mats, int *sweeps, float *residual, hipStream_t stream);
 
 /* sc_correct on each of mats[0 .. count-1] with shared dt, r and alpha. */

@@ -16,6 +16,7 @@
 #include "sc_pass.h"
 
 #include <algorithm>
+#include <cstdlib>
 #include <functional>
 #include <map>
 #include <mutex>
@@ -862,6 +863,7 @@ struct EmaJob {
     float *part;      // pieces of a halved row block: partial p at part + p * ss, row stride np
     int64_t ss;
     int ntc;          // tiles per tile row of the shadow
+    int *stall;       // EmaReq::stall
 };
 // Workgroups in the order of the streaming passes' dispatch plan (Seg runs
 // over the jobs; see plan()), so that a batch that mixes long and short rows
@@ -884,13 +886,18 @@ __device__ __forceinline__ void stage_signal(unsigned int *c, int lane)
 // Every wave of the workgroup reaches each of its signals, so a wait ends
 // within a few steps' time; the poll count is bounded (about a second)
 // so that a fault elsewhere cannot turn into a hung GPU.
-__device__ __forceinline__ void stage_wait(unsigned int *c, unsigned int target)
+// True once the counter has reached target; false if it had not after
+// `spin` polls (the caller reports it: the stage's data may be stale).
+__device__ __forceinline__ bool stage_wait(unsigned int *c, unsigned int target, int spin)
 {
-    for (int i = 0; i < (1 << 24); ++i) {
-        if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target)
-            return;
+    if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target)
+        return true;
+    for (int i = 0; i < spin; ++i) {
         __builtin_amdgcn_s_sleep(1);
+        if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target)
+            return true;
     }
+    return false;
 }
 
 // Eight waves per workgroup, two per SIMD (four waves left the stream with
@@ -907,7 +914,8 @@ constexpr int kEmaStages = 3;
 
 template <int NT>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void ema_pass_kernel(const EmaBatch jb, int np,
-                                                                                                 float beta, float omb)
+                                                                                                 float beta, float omb,
+                                                                                                 int spin)
 {
     const int wg = static_cast<int>(blockIdx.x);
     int si = 0;
@@ -1071,9 +1079,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // step s: its thin factor sits in buffer s % NB once ready[s % NB] has
     // reached W (s / NB + 1); the buffer may take step s + NB once done[s % NB]
     // has reached W (s / NB + 1)
+    bool waited = true;   // every wait of this wave met its count
     auto put_b = [&](int s) {
         if (s >= NB)
-            stage_wait(&done[s % NB], W * (s / NB));
+            waited &= stage_wait(&done[s % NB], W * (s / NB), spin);
         store_b(s);
         stage_signal(&ready[s % NB], lane);
     };
@@ -1089,7 +1098,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             load_mg(s + 1);
             put_b(s + 1);
         }
-        stage_wait(&ready[s % NB], W * (s / NB + 1));
+        waited &= stage_wait(&ready[s % NB], W * (s / NB + 1), spin);
         compute(s);
         stage_signal(&done[s % NB], lane);
         if (more)
@@ -1099,6 +1108,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // D[i][j] of a 16 x 16 tile: lane j + 16 (i / 4), element i % 4;
     // a piece of a halved row block writes its partial (row stride np),
     // added up by pass_reduce_kernel
+    if (!waited && lane == 0 && J.stall)
+        __hip_atomic_store(J.stall, kEmaStallMark, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     float *Cout = SG.pieces > 1 ? J.part + piece * J.ss : J.C;
     const int64_t ldo = SG.pieces > 1 ? static_cast<int64_t>(np) : J.ldc;
 #pragma unroll
@@ -1116,9 +1127,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 template <int NT>
-void ema_launch(const char *tag, const EmaBatch &b, int grid, int np, float a, float b_coef, hipStream_t st)
+void ema_launch(const char *tag, const EmaBatch &b, int grid, int np, float a, float b_coef, int spin,
+                hipStream_t st)
 {
-    ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(grid), dim3(512), 0, st, b, np, a, b_coef);
+    ACSC_LAUNCH(tag, ema_pass_kernel<NT>, dim3(grid), dim3(512), 0, st, b, np, a, b_coef, spin);
 }
 
 }  // namespace
@@ -1256,6 +1268,9 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
     if (!ema_fusable(reqs))
         return set_error(ACSC_EINVAL, "fused EMA pass: operands not aligned or batch too small");
     const int NP = reqs[0].NP;
+    int spin = kEmaSpinLimit;
+    if (const char *e = std::getenv("ACSC_EMA_SPIN_LIMIT"))
+        spin = std::max(0, std::min(kEmaSpinLimit, std::atoi(e)));
     // longest rows first, as for the streaming passes, and the same dispatch
     // plan: for a batch of the same shapes the fused kernel multiplies the
     // same pieces in the same order as pass_dma_kernel<false>
@@ -1273,7 +1288,7 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
         for (size_t i = 0; i < cnt; ++i) {
             const EmaReq &q = reqs[order[c0 + i]];
             eb.j[i] = EmaJob{q.M, q.G, q.M16, q.Bt, q.ldbt, q.C, q.ldc, q.m, q.n, q.part,
-                             static_cast<int64_t>(q.m) * NP, static_cast<int>(tiles_per_row(q.n))};
+                             static_cast<int64_t>(q.m) * NP, static_cast<int>(tiles_per_row(q.n)), q.stall};
             js.push_back(JobShape{static_cast<int>(cdiv(q.m, kBM)), 1, static_cast<int>(round_up(q.n, kBK)), q.n,
                                   q.part != nullptr && max_splits(q.m, q.n) >= 2 && q.n >= 2 * kBK});
         }
@@ -1282,18 +1297,18 @@ int ema_run(const char *tag, const std::vector<EmaReq> &reqs, float a, float b, 
         for (size_t i = 0; i < pl.segs.size(); ++i)
             eb.s[i] = pl.segs[i];
         switch (NP / 16) {
-        case 1: ema_launch<1>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 2: ema_launch<2>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 3: ema_launch<3>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 4: ema_launch<4>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 5: ema_launch<5>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 6: ema_launch<6>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 7: ema_launch<7>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 8: ema_launch<8>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 9: ema_launch<9>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 10: ema_launch<10>(tag, eb, pl.grid, NP, a, b, st); break;
-        case 11: ema_launch<11>(tag, eb, pl.grid, NP, a, b, st); break;
-        default: ema_launch<12>(tag, eb, pl.grid, NP, a, b, st); break;
+        case 1: ema_launch<1>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 2: ema_launch<2>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 3: ema_launch<3>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 4: ema_launch<4>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 5: ema_launch<5>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 6: ema_launch<6>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 7: ema_launch<7>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 8: ema_launch<8>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 9: ema_launch<9>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 10: ema_launch<10>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        case 11: ema_launch<11>(tag, eb, pl.grid, NP, a, b, spin, st); break;
+        default: ema_launch<12>(tag, eb, pl.grid, NP, a, b, spin, st); break;
         }
         for (size_t i = 0; i < cnt; ++i) {
             const int h = pl.halved[i];

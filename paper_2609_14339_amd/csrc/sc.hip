@@ -650,15 +650,23 @@ struct JacJob {
 // status (bit 0: the sweep cap was reached above the tolerance; bit 1: the
 // Rayleigh-Ritz phase found no stamp of a subspace phase), and the stamp the
 // subspace phase leaves for the Rayleigh-Ritz phase, which clears it.
-constexpr int kInfoSweeps = 0, kInfoResidual = 1, kInfoTol = 2, kInfoStatus = 3, kInfoStamp = 4;
-constexpr int kStatusNoConv = 1, kStatusNoSubspace = 2;
-constexpr int kSubspaceStamp = 0x5B5D7A11;
+constexpr int kInfoSweeps = 0, kInfoResidual = 1, kInfoTol = 2, kInfoStatus = 3, kInfoStamp = 4, kInfoStall = 5;
+constexpr int kStatusNoConv = 1, kStatusNoSubspace = 2, kStatusStalled = 4;
+// The stamp a subspace phase leaves for its Rayleigh-Ritz phase: the plain
+// one, or the one that also says its fused EMA pass gave up a wait.
+constexpr int kSubspaceStamp = 0x5B5D7A11, kSubspaceStalledStamp = 0x5B5D7A13;
 constexpr int kJacobiMaxSweeps = 40;
 
+// End of a subspace phase: fold the EMA pass's stall word into the stamp and
+// clear it for the next phase.
 __global__ __launch_bounds__(64) void stamp_kernel(const Batch<JacJob> jb)
 {
-    if (threadIdx.x == 0)
-        jb.j[blockIdx.z].info[kInfoStamp] = kSubspaceStamp;
+    if (threadIdx.x == 0) {
+        int *info = jb.j[blockIdx.z].info;
+        const bool stalled = info[kInfoStall] == pass::kEmaStallMark;
+        info[kInfoStall] = 0;
+        info[kInfoStamp] = stalled ? kSubspaceStalledStamp : kSubspaceStamp;
+    }
 }
 
 template <typename T, int RC>
@@ -813,7 +821,8 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(const Batch<JacJob> jb, in
         info[kInfoResidual] = __float_as_int(last_off);
         info[kInfoTol] = __float_as_int(static_cast<float>(tol));
         info[kInfoStatus] = (last_off > static_cast<float>(tol) ? kStatusNoConv : 0) |
-                            (stamp != kSubspaceStamp ? kStatusNoSubspace : 0);
+                            (stamp != kSubspaceStamp && stamp != kSubspaceStalledStamp ? kStatusNoSubspace : 0) |
+                            (stamp == kSubspaceStalledStamp ? kStatusStalled : 0);
         info[kInfoStamp] = 0;
     }
     // norms (one wave per column)
@@ -1901,7 +1910,7 @@ int build_group(std::vector<Mat> &ms, acsc_dtype dt, float beta, int r, int powe
     std::vector<pass::EmaReq> er;
     for (auto &m : ms)
         er.push_back(pass::EmaReq{m.in->M, static_cast<const uint16_t *>(m.in->G), m.pw.M16, m.pw.Zt16, m.pw.ldz16,
-                                  m.pw.Y, KP, m.D.m, m.D.n, KP, m.pw.part});
+                                  m.pw.Y, KP, m.D.m, m.D.n, KP, m.pw.part, m.pw.info + kInfoStall});
     const bool fused = use16 && pass::ema_fusable(er);
     if ((phases & kPhaseSubspace) && !fused) {
         if (use16) {
@@ -2660,6 +2669,9 @@ extern "C" int sc_build_status(int count, const sc_matrix *mats, int *sweeps, fl
         if (w[kInfoStatus] & kStatusNoSubspace)
             rc = set_error(ACSC_ENOCONV, "matrix %d: the Rayleigh-Ritz phase ran without a subspace phase on its "
                                          "workspace before it", i);
+        else if (w[kInfoStatus] & kStatusStalled)
+            rc = set_error(ACSC_ENOCONV, "matrix %d: a wait of the fused EMA pass ran out of polls (its "
+                                         "subspace and prior are not to be trusted)", i);
         else if (w[kInfoStatus] & kStatusNoConv)
             rc = set_error(ACSC_ENOCONV, "matrix %d: the Rayleigh-Ritz Jacobi stopped after %d sweeps with an "
                                          "off-diagonal ratio %g above its tolerance %g", i, w[kInfoSweeps], res, tol);

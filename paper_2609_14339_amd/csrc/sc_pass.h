@@ -62,7 +62,17 @@ struct EmaReq {
     int64_t ldc;
     int m, n, NP;
     float *part;          // split-k partials, >= max_splits(m, n) * m * NP floats, or nullptr (no split)
+    int *stall;           // set to kEmaStallMark if a wait of the kernel ran out of polls, or nullptr
 };
+
+// What the fused kernel writes to EmaReq::stall when one of its bounded waits
+// for the other waves of a workgroup gave up (that workgroup's products are
+// then not to be trusted); nothing is written otherwise.
+constexpr int kEmaStallMark = 0x57A11ED0;
+// Polls of a wait before it gives up (each about a microsecond or less).  The
+// environment variable ACSC_EMA_SPIN_LIMIT, read by each call, lowers it (0
+// gives up at the first unmet check), so that the report can be exercised.
+constexpr int kEmaSpinLimit = 1 << 24;
 
 // Whether the fused kernel takes this batch: 16-byte aligned operands, n a
 // multiple of 8, one NP, and enough row blocks over the batch to fill the

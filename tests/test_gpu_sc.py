@@ -371,6 +371,47 @@ def test_build_status_reports_a_sweep_cap_and_a_missing_subspace_phase(pk, r, p,
     pk.sc_build_status([item["ws"]])
 
 
+def test_build_status_reports_a_fused_ema_pass_that_gave_up_a_wait(pk, monkeypatch):
+    """The fused EMA pass bounds every wait for the other waves of its
+    workgroup.  With ACSC_EMA_SPIN_LIMIT=0 a wait gives up at its first unmet
+    check (the kernel still finishes, every access in bounds), and
+    sc_build_status reports the build as ACSC_ENOCONV.  The EMA of M is each
+    wave's own and stays exact; the next build with the default limit clears
+    the report and is bit-identical to a build that never gave up."""
+    m, n, r, p, q = 8192, 512, 32, 16, 2
+    spec = workloads.GradSpec(((m, n),), 32, (1.0, 100.0), (r,), torch.bfloat16, None, None)
+    pairs = [workloads.grad_pair(spec, 9, layer, 0, "cpu") for layer in range(8)]
+
+    def make():
+        return [dict(G_anc=gp.G_anc.cuda(), M=torch.zeros(m, n, device="cuda"),
+                     out=(torch.empty(m, r, device="cuda"), torch.empty(r, device="cuda"),
+                          torch.empty(n, r, device="cuda"), torch.empty(r, device="cuda")),
+                     ws=pk.workspace(m, n, r, p, torch.bfloat16)) for gp in pairs]
+
+    args = (r, workloads.BETA, workloads.TAU, p, q)
+    ref = make()
+    pk.sc_build_prior_batched(ref, *args, seed=70)
+    pk.sc_build_status([it["ws"] for it in ref])
+    items = make()
+    monkeypatch.setenv("ACSC_EMA_SPIN_LIMIT", "0")
+    pk.sc_build_prior_batched(items, *args, seed=70)
+    with pytest.raises(pk.AcscError) as e:
+        pk.sc_build_status([it["ws"] for it in items])
+    assert e.value.code == pk.ACSC_ENOCONV and "fused EMA pass" in str(e.value)
+    for it, rf in zip(items, ref):
+        assert torch.equal(it["M"], rf["M"])
+    monkeypatch.delenv("ACSC_EMA_SPIN_LIMIT")
+    for it in items:
+        it["M"].zero_()
+    pk.sc_build_prior_batched(items, *args, seed=70)
+    pk.sc_build_status([it["ws"] for it in items])
+    torch.cuda.synchronize()
+    for it, rf in zip(items, ref):
+        assert torch.equal(it["M"], rf["M"])
+        for x, y in zip(it["out"], rf["out"]):
+            assert torch.equal(x, y)
+
+
 def test_large_batch_takes_the_fused_ema_pass(pk):
     """A batch with enough row blocks to fill the GPU (8 matrices of 8192 x 512:
     256 row blocks of 256 rows) runs the anchor EMA fused with the first pass
