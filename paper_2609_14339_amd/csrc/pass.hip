@@ -611,7 +611,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             int nst = st + S - 1;
             if (nst >= S)
                 nst -= S;
+            __builtin_amdgcn_s_setprio(1);   // the DMA leaves ahead of other waves' products
             issue(min(s + S - 1, last), nst);
+            __builtin_amdgcn_s_setprio(0);
             compute(st);
             if (++st == S)
                 st = 0;
@@ -1094,8 +1096,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int s = 0; s < nsteps; ++s) {
         const bool more = s + 1 < nsteps;
         if (more) {
+            // the next step's HBM loads leave at a raised wave priority, ahead
+            // of the other wave of the SIMD's products
+            __builtin_amdgcn_s_setprio(1);
             load_b(s + 1);
             load_mg(s + 1);
+            __builtin_amdgcn_s_setprio(0);
             put_b(s + 1);
         }
         waited &= stage_wait(&ready[s % NB], W * (s / NB + 1), spin);
